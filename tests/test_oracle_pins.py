@@ -1,0 +1,385 @@
+"""Pins for the CPU oracle: each check ties the oracle to something other
+than itself (dense brute force, closed forms, exact special cases,
+invariants, an independent selection method, a hand-worked greedy example),
+so that a dropped term, a wrong sign or index, or a transposed operand fails
+at least one of them. CPU only."""
+import json
+import os
+import struct
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def dense(A, n_cols=None):
+    n_cols = A.n if n_cols is None else n_cols
+    M = np.zeros((A.n, n_cols), dtype=np.float64)
+    for i in range(A.n):
+        s, e = A.rowptr[i], A.rowptr[i + 1]
+        M[i, A.col[s:e]] = A.val[s:e]
+    return M
+
+
+def key_of(q):
+    """Key encoding written from its definition, independent of the oracle:
+    NaN -> 0, else IEEE-754 bit pattern of the double plus one."""
+    q = float(q)
+    if q != q:
+        return 0
+    return struct.unpack("<Q", struct.pack("<d", q))[0] + 1
+
+
+def ring(n, r_half):
+    """r-regular circulant graph (each node linked to the r_half nearest on
+    each side) with self-loops and GCN values fl32(1/(r+1))."""
+    rows = []
+    for i in range(n):
+        nb = sorted({(i + o) % n for o in range(-r_half, r_half + 1)})
+        rows.append(nb)
+    rowptr = np.zeros(n + 1, np.int32)
+    rowptr[1:] = np.cumsum([len(r) for r in rows])
+    col = np.array([c for r in rows for c in r], np.int32)
+    v = np.float32(1.0 / (2 * r_half + 1))
+    val = np.full(len(col), v, np.float32)
+    return synth.Csr(n, rowptr, col, val)
+
+
+@pytest.fixture(scope="module")
+def small_sym():
+    A = synth.erdos_renyi(300, 0.05, seed=3)
+    B = synth.dense_normal(300, 37, seed=4)
+    return A, B
+
+
+@pytest.fixture(scope="module")
+def small_gen():
+    """Non-symmetric, with empty rows, a hub row and negative values."""
+    A = synth.random_csr(257, 190, 12, seed=5, hub_rows=2, hub_len=150, empty_frac=0.1)
+    B = synth.dense_normal(190, 21, seed=6)
+    return A, B
+
+
+# ---------------------------------------------------------------- O0 / O1
+def test_csr_check(small_gen):
+    A, _ = small_gen
+    assert oracle.check_csr(A.rowptr, A.col, A.n, 190) == 0
+    bad = A.col.copy()
+    i = int(np.argmax(np.diff(A.rowptr) > 1))
+    bad[A.rowptr[i] + 1] = bad[A.rowptr[i]]          # duplicate column
+    assert oracle.check_csr(A.rowptr, bad, A.n, 190) == 5
+    bad = A.col.copy(); bad[0] = 190                 # out of range
+    assert oracle.check_csr(A.rowptr, bad, A.n, 190) == 4
+
+
+def test_gcn_values_closed_form_ring():
+    # every node of a circulant graph with r = 4 neighbours has degree 5
+    # (with the self-loop), so every value is fl32(1/sqrt(5*5)) = fl32(1/5)
+    A = ring(50, 2)
+    assert oracle.check_gcn_values(A.rowptr, A.col, A.val) == 0
+    v = A.val.copy(); v[7] = np.nextafter(v[7], np.float32(1))
+    assert oracle.check_gcn_values(A.rowptr, A.col, v) == 1
+    # a structure without the self-loop (A instead of A + I) is not the operand
+    keep = A.col != np.repeat(np.arange(A.n), np.diff(A.rowptr))
+    rp = np.zeros(A.n + 1, np.int32); rp[1:] = np.cumsum(np.full(A.n, 4))
+    noself = np.full(keep.sum(), np.float32(1.0 / 4.0), np.float32)
+    assert oracle.check_gcn_values(rp, A.col[keep], noself) == A.n
+
+
+def test_gcn_values_on_generated_graphs():
+    for A in (synth.erdos_renyi(500, 0.02, seed=1), synth.make_graph("tiny", 0)):
+        assert oracle.check_csr(A.rowptr, A.col, A.n, A.n) == 0
+        assert oracle.check_gcn_values(A.rowptr, A.col, A.val) == 0
+        D = dense(A)
+        assert np.array_equal(D != 0, (D != 0).T)               # symmetric structure
+        assert np.all(np.diag(D) != 0)                           # self-loops
+
+
+# ---------------------------------------------------------------- O2
+@pytest.mark.parametrize("which", ["small_sym", "small_gen"])
+def test_spmm_dense_brute_force(which, request):
+    A, B = request.getfixturevalue(which)
+    n_cols = B.shape[0]
+    Y, S = oracle.spmm(A.rowptr, A.col, A.val, B, with_mag=True)
+    D = dense(A, n_cols)
+    ref = D @ B.astype(np.float64)
+    mag = np.abs(D) @ np.abs(B.astype(np.float64))
+    # one fp32 rounding of an fp64 sum: |Y - ref| <= 2^-24 |ref| + fp64 noise
+    assert np.all(np.abs(Y - ref) <= 2.0 ** -24 * np.abs(ref) + 1e-12 * mag + 1e-300)
+    np.testing.assert_allclose(S, mag, rtol=1e-12, atol=0)
+
+
+def test_spmm_identity_is_bitwise_dense(small_gen):
+    A, _ = small_gen
+    I = np.eye(190, dtype=np.float32)
+    Y = oracle.spmm(A.rowptr, A.col, A.val, I)
+    assert np.array_equal(Y, dense(A, 190).astype(np.float32))
+
+
+def test_spmm_permutation_is_bitwise():
+    rng = np.random.default_rng(0)
+    n = 173
+    p = rng.permutation(n).astype(np.int32)
+    rowptr = np.arange(n + 1, dtype=np.int32)
+    val = np.ones(n, np.float32)
+    B = synth.dense_normal(n, 9, seed=2)
+    Y = oracle.spmm(rowptr, p, val, B)
+    assert np.array_equal(Y, B[p])
+
+
+def test_spmm_row_subset_and_ld(small_gen):
+    A, _ = small_gen
+    B = synth.dense_normal(190, 21, seed=6, ld=24)       # padded leading dimension
+    Yfull = oracle.spmm(A.rowptr, A.col, A.val, B, d=21)
+    rows = np.array([0, 5, 256, 17, 5], np.int32)
+    Ysub = oracle.spmm(A.rowptr, A.col, A.val, B, d=21, rows=rows)
+    assert np.array_equal(Ysub, Yfull[rows])
+    assert np.array_equal(Yfull, oracle.spmm(A.rowptr, A.col, A.val, B[:, :21].copy()))
+
+
+def test_spmm_linearity(small_sym):
+    A, B = small_sym
+    B2 = synth.dense_normal(300, 37, seed=9)
+    Y1, S1 = oracle.spmm(A.rowptr, A.col, A.val, B, with_mag=True)
+    Y2, S2 = oracle.spmm(A.rowptr, A.col, A.val, B2, with_mag=True)
+    Y12 = oracle.spmm(A.rowptr, A.col, A.val, (B + B2).astype(np.float32))
+    assert np.all(np.abs(Y12 - (Y1.astype(np.float64) + Y2)) <= 1e-6 * (S1 + S2) + 1e-30)
+
+
+# ---------------------------------------------------------------- O3 / O4
+def test_col_sqnorms_closed_form_regular():
+    # r-regular with self-loops, r + 1 = 7 <= 32: the sum of seven copies of
+    # x^2 (x = fl32(1/7), x^2 exact in fp64) is exact, so cn2 = 7 x^2 bitwise
+    A = ring(40, 3)
+    AT = synth.transpose(A)
+    cn2, colnnz = oracle.col_sqnorms(AT.rowptr, AT.val)
+    x = float(np.float32(1.0 / 7.0))
+    assert np.all(cn2 == 7.0 * x * x)
+    assert np.all(colnnz == 7)
+
+
+def test_col_sqnorms_dense(small_gen):
+    A, _ = small_gen
+    AT = synth.transpose(A, 190)
+    cn2, colnnz = oracle.col_sqnorms(AT.rowptr, AT.val)
+    D = dense(A, 190)
+    np.testing.assert_allclose(cn2, (D ** 2).sum(axis=0), rtol=1e-14, atol=0)
+    assert np.array_equal(colnnz, (D != 0).sum(axis=0))
+
+
+def test_pair_keys_closed_forms():
+    n, d = 6, 5
+    B = np.zeros((n, d), np.float32)
+    cs = np.float32([3.0, -0.5, 1e-20, 7.25, 0.0, 2.0 ** 60])
+    for i in range(n):
+        B[i, i % d] = cs[i]                                  # B[i,:] = c e_j
+    cn2 = np.array([1.0, 2.0, 4.0, 0.5, 9.0, 1.0])
+    out = oracle.pair_keys(cn2, B)
+    assert np.array_equal(out["rn2"], cs.astype(np.float64) ** 2)   # exact
+    assert np.array_equal(out["q"], cn2 * cs.astype(np.float64) ** 2)
+    assert [int(k) for k in out["key"]] == [key_of(q) for q in out["q"]]
+    assert out["key"][4] == 1                                # q = +0 -> key 1
+
+
+def test_pair_keys_nan_inf_and_order():
+    cn2 = np.array([1.0, 1.0, 0.0, 1.0, 2.0])
+    B = np.ones((5, 3), np.float32)
+    B[0, 1] = np.nan                                         # q NaN -> key 0
+    B[1, 2] = np.inf                                         # q +Inf
+    B[2, 0] = np.inf                                         # 0 * Inf = NaN
+    out = oracle.pair_keys(cn2, B)
+    assert out["key"][0] == 0 and out["key"][2] == 0
+    assert out["key"][1] == key_of(np.inf)
+    assert out["key"][1] > out["key"][4] > out["key"][3] > 0
+
+
+def test_pair_keys_dense_and_cauchy_schwarz(small_sym):
+    A, B = small_sym
+    cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)             # symmetric: A^T = A
+    out = oracle.pair_keys(cn2, B)
+    B64 = B.astype(np.float64)
+    np.testing.assert_allclose(out["rn2"], (B64 ** 2).sum(axis=1), rtol=1e-14)
+    # Eq. 3 written independently from dense norms
+    D = dense(A)
+    colnorm = np.linalg.norm(D, axis=0)
+    rownorm = np.linalg.norm(B64, axis=1)
+    p = colnorm * rownorm / np.sum(colnorm * rownorm)
+    assert abs(p.sum() - 1.0) < 1e-12
+    np.testing.assert_allclose(np.sqrt(out["q"]), colnorm * rownorm, rtol=1e-13)
+    # ranking by p equals ranking by the key (continuous data: no ties)
+    assert np.array_equal(np.argsort(-p, kind="stable"), oracle.rank_order(out["key"]))
+    # normalised mass is at most 1 (Cauchy-Schwarz)
+    assert np.sqrt(out["q"]).sum() <= np.sqrt(cn2.sum()) * np.sqrt(out["rn2"].sum()) * (1 + 1e-12)
+
+
+# ---------------------------------------------------------------- O5
+def topk_lexsort(key, k):
+    """Independent selection: numpy lexsort on (~key, index); ~ reverses
+    the order of unsigned integers."""
+    order = np.lexsort((np.arange(len(key)), ~key.astype(np.uint64)))
+    return np.sort(order[:k]).astype(np.int32)
+
+
+def topk_partition(key, k):
+    """Second independent route: threshold by partition, then a tie pass."""
+    n = len(key)
+    if k == 0:
+        return np.zeros(0, np.int32)
+    T = np.partition(key, n - k)[n - k]
+    gt = np.nonzero(key > T)[0]
+    eq = np.nonzero(key == T)[0][: k - len(gt)]
+    return np.sort(np.concatenate([gt, eq])).astype(np.int32)
+
+
+def mask_of(idx, n):
+    m = np.zeros((n + 31) // 32, np.uint32)
+    for i in idx:
+        m[i >> 5] |= np.uint32(1 << (int(i) & 31))
+    return m
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_topk_two_independent_methods(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 3000))
+    # few distinct values -> many ties
+    key = rng.integers(0, 40, size=n).astype(np.uint64) * np.uint64(1 << 40)
+    for k in sorted({0, 1, n // 3, n // 2, n - 1, n}):
+        if k < 0:
+            continue
+        idx, mask = oracle.topk(key, k)
+        ref = topk_lexsort(key, k)
+        assert np.array_equal(idx, ref)
+        assert np.array_equal(idx, topk_partition(key, k))
+        assert np.array_equal(mask, mask_of(ref, n))
+
+
+def test_topk_special_cases():
+    n = 100
+    eq = np.full(n, 12345, np.uint64)
+    assert np.array_equal(oracle.topk(eq, 37)[0], np.arange(37))
+    dec = np.arange(n, 0, -1).astype(np.uint64)
+    assert np.array_equal(oracle.topk(dec, 10)[0], np.arange(10))
+    inc = np.arange(1, n + 1).astype(np.uint64)
+    assert np.array_equal(oracle.topk(inc, 10)[0], np.arange(90, 100))
+    assert len(oracle.topk(inc, 0)[0]) == 0 and not oracle.topk(inc, 0)[1].any()
+    assert np.array_equal(oracle.topk(inc, n)[0], np.arange(n))
+    # NaN (key 0) last, +Inf first
+    q = np.array([1.0, np.nan, np.inf, 3.0, np.nan, np.inf])
+    keys = np.array([key_of(x) for x in q], np.uint64)
+    assert list(oracle.topk(keys, 2)[0]) == [2, 5]
+    assert list(oracle.topk(keys, 5)[0]) == [0, 1, 2, 3, 5]
+
+
+# ---------------------------------------------------------------- O6 / O7
+def test_slice_identities(small_gen):
+    A, B = small_gen
+    n_cols = 190
+    AT = synth.transpose(A, n_cols)
+    _, colnnz = oracle.col_sqnorms(AT.rowptr, AT.val)
+    rng = np.random.default_rng(1)
+    D = dense(A, n_cols)
+    for k in (0, 1, 50, 189, 190):
+        idx = np.sort(rng.choice(n_cols, size=k, replace=False)).astype(np.int32)
+        mask = mask_of(idx, n_cols)
+        ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+        S = synth.Csr(A.n, ro, co, vo)
+        keep = np.zeros(n_cols); keep[idx] = 1
+        assert np.array_equal(dense(S, n_cols), D * keep[None, :])
+        assert len(co) == int(colnnz[idx].sum())
+        assert oracle.check_csr(ro, co, A.n, n_cols) == 0
+        if k == 0:
+            assert len(co) == 0 and not ro.any()
+        if k == n_cols:
+            assert np.array_equal(ro, A.rowptr) and np.array_equal(co, A.col)
+            assert np.array_equal(vo.view(np.uint32), A.val.view(np.uint32))
+        # O7: sampled product
+        Ys = oracle.spmm(ro, co, vo, B)
+        ref = D @ np.diag(keep) @ B.astype(np.float64)
+        assert np.all(np.abs(Ys - ref) <= 2.0 ** -24 * np.abs(ref) + 1e-12 * (np.abs(D) @ np.abs(B)))
+        # textbook column-row form: sum over kept i of A[:, i] B[i, :]
+        cr = np.zeros((A.n, B.shape[1]))
+        for i in idx:
+            cr += np.outer(D[:, i], B[i].astype(np.float64))
+        np.testing.assert_allclose(Ys, cr, rtol=1e-5, atol=1e-6)
+        # complement: Y_S + Y_{S^c} = Y within rounding
+        comp = mask_of(np.setdiff1d(np.arange(n_cols), idx), n_cols)
+        rc, cc, vc = oracle.slice_csr(A.rowptr, A.col, A.val, comp)
+        Yc = oracle.spmm(rc, cc, vc, B)
+        Y, Smag = oracle.spmm(A.rowptr, A.col, A.val, B, with_mag=True)
+        assert np.all(np.abs(Ys.astype(np.float64) + Yc - Y) <= 1e-6 * Smag + 1e-30)
+        if k == n_cols:
+            assert np.array_equal(Ys, Y)
+
+
+# ---------------------------------------------------------------- O8
+def test_k_from_fraction():
+    assert oracle.k_from_fraction(4096, 50, 100) == 2048
+    assert [oracle.k_from_fraction(232_965, p, 100) for p in (10, 30, 50)] == [23_296, 69_889, 116_482]
+    assert oracle.k_from_fraction(2_449_029, 30, 100) == 734_708
+    assert oracle.k_from_fraction(132_534, 30, 100) == 39_760
+    assert oracle.k_from_fraction(7, 0, 1) == 0 and oracle.k_from_fraction(7, 1, 1) == 7
+
+
+def _keys_from_scores(scores):
+    return np.array([key_of(float(s) ** 2) for s in scores], np.uint64)
+
+
+def test_greedy_hand_worked_example():
+    g = json.load(open(os.path.join(GOLDEN, "greedy_hand_example.json")))
+    keys = [_keys_from_scores(s) for s in g["scores"]]
+    k, bud = oracle.greedy(keys, g["colnnz"], g["nnz"], g["d"], g["fro_a2"], g["fro_b2"],
+                           tuple(g["C"]), tuple(g["alpha"]))
+    assert k == g["expected_k"] and bud == g["expected_budget"]
+
+
+def test_greedy_tie_goes_to_lower_layer_and_limits():
+    scores = [5, 4, 3, 2, 1, 0]
+    keys = [_keys_from_scores(scores)] * 2
+    colnnz = [1] * 6
+    # two identical layers: first shrink goes to layer 0, second to layer 1
+    k, bud = oracle.greedy(keys, colnnz, 6, [1, 1], 1.0, [1.0, 1.0], (5, 6), (1, 6))
+    assert k == [5, 5] and bud == 10
+    # C = 1: already within budget, nothing shrinks
+    k, bud = oracle.greedy(keys, colnnz, 6, [1, 1], 1.0, [1.0, 1.0], (1, 1), (1, 6))
+    assert k == [6, 6] and bud == 12
+    # C = 0: everything goes to zero, then the loop stops (no eligible layer)
+    k, bud = oracle.greedy(keys, colnnz, 6, [1, 1], 1.0, [1.0, 1.0], (0, 1), (1, 3))
+    assert k == [0, 0] and bud == 0
+
+
+@pytest.mark.parametrize("C", [(1, 10), (3, 10), (1, 2)])
+def test_greedy_invariants(C):
+    A = synth.make_graph("tiny", 0)
+    n = A.n
+    cn2, colnnz = oracle.col_sqnorms(A.rowptr, A.val)
+    keys, fro_b2, ds = [], [], [64, 16]
+    for l, dl in enumerate(ds):
+        out = oracle.pair_keys(cn2, synth.dense_normal(n, dl, seed=10 + l))
+        keys.append(out["key"]); fro_b2.append(out["rn2"].sum())
+    k, bud = oracle.greedy(keys, colnnz, A.nnz, ds, cn2.sum(), fro_b2, C, (2, 100))
+    step = max(1, n * 2 // 100)
+    total = A.nnz * sum(ds)
+    assert bud * C[1] <= C[0] * total
+    recomputed = 0
+    for l in range(2):
+        assert k[l] == 0 or (n - k[l]) % step == 0
+        top = np.lexsort((np.arange(n), ~keys[l]))[: k[l]]
+        recomputed += ds[l] * int(colnnz[top].sum())
+    assert recomputed == bud
+    assert C[0] == C[1] or any(k[l] < n for l in range(2))
+
+
+def test_cache_policy():
+    p = oracle.CachePolicy(10)
+    seq = []
+    for s in range(25):
+        r = p.needs_refresh(s)
+        seq.append(r)
+        if r:
+            p.refreshed(s)
+    assert [i for i, r in enumerate(seq) if r] == [0, 10, 20]
