@@ -1,0 +1,209 @@
+/*
+ * rsc.h - C ABI of the MI355X (gfx950) implementation of the RSC
+ * aggregation hot path: the GCN aggregation SpMM Y = A_hat * H and its
+ * top-k column-row approximation (score pairs, keep the top k, slice the
+ * kept columns out of the CSR matrix, cache the slice, run SpMM on it).
+ *
+ * Paper: Liu et al., "RSC: Accelerate Graph Neural Networks Training via
+ * Randomized Sparse Computations", ICML 2023 (arXiv 2210.10737).
+ *
+ * Conventions
+ *   - Pointers are DEVICE pointers unless the name ends in _host.
+ *   - Every call that takes a stream enqueues its work on that stream and
+ *     returns without synchronising, unless it is marked [sync].
+ *   - Arguments are validated on the host before anything is enqueued; a
+ *     call that returns an error has enqueued nothing and changed no output
+ *     or cache state, except where stated.
+ *   - The caller owns every buffer it passes. Buffers returned by
+ *     rsc_cache_get are borrowed from the cache.
+ *   - Dense matrices are row-major fp32 with a leading dimension (in floats)
+ *     ld >= d, ld % 4 == 0, and a 16-byte-aligned base pointer. Columns
+ *     d .. ld-1 of an output are never written.
+ *   - CSR matrices: int32 row pointers and column indices, fp32 values,
+ *     nnz < 2^31, columns strictly increasing within each row.
+ *   - No C++ exception crosses this interface. Asynchronous device faults
+ *     surface at the caller's next synchronisation.
+ *   - Stateless calls are reentrant; a cache handle must not be used from
+ *     two host threads at once, and two calls that share a workspace must
+ *     not overlap on the device.
+ */
+#ifndef RSC_H
+#define RSC_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RSC_ABI_VERSION 1
+
+typedef enum {
+    RSC_OK = 0,
+    RSC_ERR_INVALID_ARGUMENT = 1, /* null pointer, d < 1, k < 0, k > n, ld < d ... */
+    RSC_ERR_UNSUPPORTED = 2,      /* nnz >= 2^31, ld % 4 != 0, misaligned base pointer */
+    RSC_ERR_OUT_OF_MEMORY = 3,    /* a device allocation by the cache failed */
+    RSC_ERR_CAPACITY = 4,         /* caller-provided buffer or workspace too small */
+    RSC_ERR_NO_DEVICE = 5,        /* no HIP device visible */
+    RSC_ERR_HIP = 6,              /* a HIP runtime call failed; see rsc_last_error() */
+    RSC_ERR_INTERNAL = 7
+} rsc_status_t;
+
+/* A CSR matrix in device memory (section 3.3.1: the entries of row i are
+ * Col/Val[Rowptr[i] .. Rowptr[i+1]-1]). rowptr has n_rows + 1 entries with
+ * rowptr[0] = 0 and rowptr[n_rows] = nnz. */
+typedef struct {
+    int32_t n_rows;
+    int32_t n_cols;
+    int64_t nnz;
+    const int32_t *rowptr;
+    const int32_t *col;
+    const float *val;
+} rsc_csr_t;
+
+/* Human-readable name of a status code (static storage). */
+const char *rsc_status_string(rsc_status_t status);
+/* Detail of the last error raised on the calling host thread (thread-local;
+ * empty string if none). */
+const char *rsc_last_error(void);
+/* RSC_ABI_VERSION of the loaded library. */
+int32_t rsc_abi_version(void);
+
+/* ---------------------------------------------------------------- A1 --- */
+/* Exact sparse-dense product Y = A * B (the SpMM of Eq. 1's implementation
+ * form, section 2.1; the forward aggregation of section 3.1).
+ *   A: n_rows x n_cols CSR.  B: n_cols x d, leading dimension ldb.
+ *   Y: n_rows x d, leading dimension ldy; every row is written (empty rows
+ *      get zeros).
+ * Accumulation: fp32 over runs of at most 64 consecutive entries, folded
+ * into fp64; one rounding to fp32 per output. Deterministic: the same
+ * inputs give bitwise the same Y, and the result of an entry depends only on
+ * its row's entries (so slicing with every column kept reproduces Y).
+ * ws / ws_bytes: scratch of at least rsc_spmm_workspace_bytes(A) bytes,
+ * 256-byte aligned, private to this call until it completes on `stream`. */
+size_t rsc_spmm_workspace_bytes(const rsc_csr_t *A);
+rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb, float *Y,
+                      int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------- A2 --- */
+/* Column square-norms of a sparse operand X (Eq. 3's ||X[:, i]||^2; the
+ * ||A_hat^T[:, i]||^2 of Eq. 4a). Pass the CSR of X^T: column i of X is
+ * row i of X^T. cn2[i] = sum of val^2 over row i of XT, fp64, in stored
+ * order. colnnz (nullable) receives the entry count of each column of X
+ * (Eq. 4b's #nnz_i). Both have XT->n_rows entries. */
+rsc_status_t rsc_col_sqnorms(const rsc_csr_t *XT, double *cn2, int32_t *colnnz,
+                             hipStream_t stream);
+
+/* ---------------------------------------------------------------- A3 --- */
+/* Pair keys (Eq. 3 and the top-k rule of section 2.2.1). For i < n:
+ *   rn2[i] = sum_{j<d} B[i, j]^2 (fp64, ascending j)
+ *   q[i]   = cn2[i] * rn2[i]       (fp64)
+ *   key[i] = isnan(q) ? 0 : bits(q) + 1   (unsigned order == order of q,
+ *            NaN last)
+ *   score[i] = fl32(sqrt(q[i]))    (nullable output)
+ * q is the squared pair score ||X[:, i]||^2 ||B[i, :]||^2 without the
+ * common normaliser, which changes no ranking. B is n x d with leading
+ * dimension ldb. */
+rsc_status_t rsc_pair_scores(const double *cn2, const float *B, int32_t n, int32_t d,
+                             int64_t ldb, uint64_t *key, float *score, hipStream_t stream);
+
+/* ---------------------------------------------------------------- A4 --- */
+/* Top-k selection (section 2.2.1): the k indices with the largest keys,
+ * ties broken by the lower index. idx receives them in ascending order
+ * (k entries); mask receives ceil(n/32) words, bit (i & 31) of word i >> 5
+ * set iff i is selected. 0 <= k <= n. Any uint64 keys are accepted.
+ * ws: at least rsc_topk_workspace_bytes(n) bytes, 256-byte aligned. */
+size_t rsc_topk_workspace_bytes(int32_t n);
+rsc_status_t rsc_topk_select(const uint64_t *key, int32_t n, int32_t k, int32_t *idx,
+                             uint32_t *mask, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------- A5 --- */
+/* Column slice A' = A[:, S] (section 3.3.1, Fig. 5's rebuild of Rowptr and
+ * Col; appendix C: whole columns dropped, every row kept). Entries whose
+ * column has its mask bit set are kept in their original order; column ids
+ * stay global; rowptr_out (n_rows + 1 entries) is the running count of kept
+ * entries; rows may become empty.
+ * nnz_out: device int64 receiving nnz'.
+ * capacity: entries available in col_out / val_out. If capacity >= A->nnz
+ * the call is asynchronous. Otherwise it is [sync]: entries beyond capacity
+ * are not written, and RSC_ERR_CAPACITY is returned when nnz' > capacity
+ * (rowptr_out and *nnz_out are still complete).
+ * ws: at least rsc_slice_workspace_bytes(A) bytes, 256-byte aligned. */
+size_t rsc_slice_workspace_bytes(const rsc_csr_t *A);
+rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, int32_t *rowptr_out,
+                           int32_t *col_out, float *val_out, int64_t capacity, int64_t *nnz_out,
+                           void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------ A6 / A7 --- */
+/* Sampled-matrix cache (section 3.3.1): keeps the sliced operand and reuses
+ * it across nearby steps; refreshed every `refresh_interval` steps (10 in
+ * section 5.1). The cache owns its device buffers (sized for the full
+ * operand, so refreshes never reallocate) until rsc_cache_destroy.
+ *   rsc_cache_create [sync]: X is the sparse operand to be sliced, XT the
+ *     CSR of its transpose (for the column norms; pass X again for a
+ *     symmetric operand). Computes cn2 and colnnz once (the operand is
+ *     fixed across steps). X and XT must stay valid for the cache's life.
+ *   rsc_cache_refresh: scores the pairs against B (n_cols x d, ldb), keeps
+ *     the top k columns and slices X; records `step` as the refresh step.
+ *   rsc_cache_get (host only): returns the current slice (its nnz is read
+ *     from the device once per refresh, waiting for the refresh if needed),
+ *     the ascending kept indices, k, the slice version (0 = never
+ *     refreshed, +1 per refresh) and needs_refresh = (never refreshed) or
+ *     (step - last_refresh_step >= refresh_interval). The returned pointers
+ *     stay valid until the next refresh or destroy.
+ *   rsc_spmm_sampled: Y' = X[:, S] * B on the cached slice (Eq. 2 with the
+ *     top-k rule: kept pairs summed with scale 1), the same kernels as
+ *     rsc_spmm; every row of Y' is written. Needs a refreshed cache. */
+typedef struct rsc_cache rsc_cache_t;
+rsc_status_t rsc_cache_create(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t refresh_interval,
+                              hipStream_t stream, rsc_cache_t **out);
+rsc_status_t rsc_cache_refresh(rsc_cache_t *cache, const float *B, int32_t d, int64_t ldb,
+                               int32_t k, int64_t step, hipStream_t stream);
+rsc_status_t rsc_cache_get(rsc_cache_t *cache, int64_t step, rsc_csr_t *slice_out,
+                           const int32_t **idx_out, int32_t *k_out, int32_t *needs_refresh_out,
+                           uint64_t *version_out);
+rsc_status_t rsc_spmm_sampled(rsc_cache_t *cache, const float *B, int32_t d, int64_t ldb,
+                              float *Y, int64_t ldy, hipStream_t stream);
+/* Device arrays owned by the cache: cn2 (fp64) and colnnz (int32), n_cols
+ * entries each; keys (uint64) and mask (ceil(n_cols/32) words) of the last
+ * refresh. Any output pointer may be NULL. */
+rsc_status_t rsc_cache_buffers(rsc_cache_t *cache, const double **cn2, const int32_t **colnnz,
+                               const uint64_t **key, const uint32_t **mask);
+/* Waits for outstanding cache work, then frees its buffers. NULL is a no-op. */
+rsc_status_t rsc_cache_destroy(rsc_cache_t *cache);
+
+/* ---------------------------------------------------------------- A8 --- */
+/* Column budget (uniform allocation of section 5.2.2, k = C |V|) with C as
+ * the rational num/den: floor(n * num / den). Returns -1 if n < 0, num < 0,
+ * den <= 0 or num > den. Host only. */
+int32_t rsc_k_from_fraction(int32_t n, int32_t num, int32_t den);
+
+/* Layer-wise allocation of k_l under a FLOPs budget (Eq. 4a/4b, solved by
+ * the greedy of section 3.2.1 / Algorithm 1). Host compute.
+ *   key_host[l]: the n pair keys of layer l (rsc_pair_scores encoding).
+ *   colnnz_host: the n column entry counts of the operand; nnz = |E|.
+ *   d_host[l]: width of layer l's dense operand; fro_a2 = ||A||_F^2;
+ *   fro_b2_host[l] = ||grad H^(l+1)||_F^2.
+ *   Budget C = C_num / C_den; step = max(1, floor(n * alpha_num / alpha_den)).
+ * Pairs rank by (key desc, index asc). Starting from k_l = n, while
+ * Bud * C_den > C_num * sum_l nnz d_l, the eligible layer (k_l > 0) whose
+ * shrink to max(0, k_l - step) loses the least normalised score mass
+ * (sum of sqrt(q) over the dropped ranks in rank order, fp64, divided by
+ * sqrt(fro_a2) * sqrt(fro_b2[l]); NaN keys count 0; lowest layer on ties)
+ * is shrunk, and Bud drops by d_l times the dropped columns' entry counts.
+ * Writes k_out_host[0..L) and, if budget_out_host is not NULL, the final
+ * Bud. */
+rsc_status_t rsc_greedy_allocate(int32_t L, int32_t n, int64_t nnz,
+                                 const uint64_t *const *key_host, const int32_t *colnnz_host,
+                                 const int32_t *d_host, double fro_a2, const double *fro_b2_host,
+                                 int32_t C_num, int32_t C_den, int32_t alpha_num,
+                                 int32_t alpha_den, int32_t *k_out_host,
+                                 int64_t *budget_out_host);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RSC_H */

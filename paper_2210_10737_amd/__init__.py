@@ -1,0 +1,332 @@
+"""Python binding of librsc.so (the MI355X RSC hot-path library).
+
+Argument marshalling only: each function takes torch tensors that live on the
+GPU, passes their data pointers and the current HIP stream to the C ABI of
+include/rsc.h, and returns torch tensors. Every step of the computation runs
+in the library's HIP kernels; there is no fallback. If librsc.so has not been
+built, every call raises.
+
+Paper: Liu et al., "RSC: Accelerate Graph Neural Networks Training via
+Randomized Sparse Computations", ICML 2023 (arXiv 2210.10737).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librsc.so")
+
+RSC_OK = 0
+STATUS = {0: "RSC_OK", 1: "RSC_ERR_INVALID_ARGUMENT", 2: "RSC_ERR_UNSUPPORTED",
+          3: "RSC_ERR_OUT_OF_MEMORY", 4: "RSC_ERR_CAPACITY", 5: "RSC_ERR_NO_DEVICE",
+          6: "RSC_ERR_HIP", 7: "RSC_ERR_INTERNAL"}
+
+EXPORTED = [
+    "rsc_status_string", "rsc_last_error", "rsc_abi_version",
+    "rsc_spmm_workspace_bytes", "rsc_spmm",
+    "rsc_col_sqnorms", "rsc_pair_scores",
+    "rsc_topk_workspace_bytes", "rsc_topk_select",
+    "rsc_slice_workspace_bytes", "rsc_slice_csr",
+    "rsc_cache_create", "rsc_cache_refresh", "rsc_cache_get", "rsc_spmm_sampled",
+    "rsc_cache_buffers", "rsc_cache_destroy",
+    "rsc_k_from_fraction", "rsc_greedy_allocate",
+]
+
+
+class RscError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{STATUS.get(status, status)}: {detail}")
+        self.status = status
+
+
+class CsrStruct(ctypes.Structure):
+    _fields_ = [("n_rows", ctypes.c_int32), ("n_cols", ctypes.c_int32), ("nnz", ctypes.c_int64),
+                ("rowptr", ctypes.c_void_p), ("col", ctypes.c_void_p), ("val", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2210_10737_amd.build` (or __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        csrp = ctypes.POINTER(CsrStruct)
+        sig = {
+            "rsc_status_string": ([ctypes.c_int], ctypes.c_char_p),
+            "rsc_last_error": ([], ctypes.c_char_p),
+            "rsc_abi_version": ([], i32),
+            "rsc_spmm_workspace_bytes": ([csrp], sz),
+            "rsc_spmm": ([csrp, vp, i32, i64, vp, i64, vp, sz, vp], ctypes.c_int),
+            "rsc_col_sqnorms": ([csrp, vp, vp, vp], ctypes.c_int),
+            "rsc_pair_scores": ([vp, vp, i32, i32, i64, vp, vp, vp], ctypes.c_int),
+            "rsc_topk_workspace_bytes": ([i32], sz),
+            "rsc_topk_select": ([vp, i32, i32, vp, vp, vp, sz, vp], ctypes.c_int),
+            "rsc_slice_workspace_bytes": ([csrp], sz),
+            "rsc_slice_csr": ([csrp, vp, vp, vp, vp, i64, vp, vp, sz, vp], ctypes.c_int),
+            "rsc_cache_create": ([csrp, csrp, i32, vp, ctypes.POINTER(vp)], ctypes.c_int),
+            "rsc_cache_refresh": ([vp, vp, i32, i64, i32, i64, vp], ctypes.c_int),
+            "rsc_cache_get": ([vp, i64, csrp, ctypes.POINTER(vp), ctypes.POINTER(i32),
+                               ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_uint64)], ctypes.c_int),
+            "rsc_spmm_sampled": ([vp, vp, i32, i64, vp, i64, vp], ctypes.c_int),
+            "rsc_cache_buffers": ([vp, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                   ctypes.POINTER(vp)], ctypes.c_int),
+            "rsc_cache_destroy": ([vp], ctypes.c_int),
+            "rsc_k_from_fraction": ([i32, i32, i32], i32),
+            "rsc_greedy_allocate": ([i32, i32, i64, vp, vp, vp, ctypes.c_double, vp, i32, i32, i32,
+                                     i32, vp, vp], ctypes.c_int),
+        }
+        for name, (args, res) in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != RSC_OK:
+        raise RscError(status, lib().rsc_last_error().decode())
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _ld(t: torch.Tensor) -> int:
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("dense operands must be 2-D with unit column stride")
+    return t.stride(0)
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    # torch's caching allocator returns 256-byte (or larger) aligned blocks
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+@dataclass
+class DeviceCsr:
+    """CSR on the GPU: rowptr int32[n_rows+1], col int32[nnz], val float32[nnz]."""
+    n_rows: int
+    n_cols: int
+    rowptr: torch.Tensor
+    col: torch.Tensor
+    val: torch.Tensor
+    nnz: int | None = None
+
+    def __post_init__(self):
+        if self.nnz is None:
+            self.nnz = int(self.col.numel())
+
+    @classmethod
+    def from_host(cls, rowptr, col, val, n_cols, device="cuda"):
+        rp = torch.as_tensor(rowptr, dtype=torch.int32).to(device)
+        c = torch.as_tensor(col, dtype=torch.int32).to(device)
+        v = torch.as_tensor(val, dtype=torch.float32).to(device)
+        return cls(len(rowptr) - 1, int(n_cols), rp, c, v)
+
+    def struct(self) -> CsrStruct:
+        return CsrStruct(self.n_rows, self.n_cols, self.nnz, self.rowptr.data_ptr(),
+                         self.col.data_ptr() if self.nnz else None,
+                         self.val.data_ptr() if self.nnz else None)
+
+
+# ---------------------------------------------------------------- A1
+def spmm_workspace_bytes(A: DeviceCsr) -> int:
+    return lib().rsc_spmm_workspace_bytes(ctypes.byref(A.struct()))
+
+
+def spmm(A: DeviceCsr, B: torch.Tensor, d: int | None = None, out: torch.Tensor | None = None,
+         ws: torch.Tensor | None = None) -> torch.Tensor:
+    """Y = A @ B[:, :d] (exact SpMM)."""
+    d = B.shape[1] if d is None else d
+    Y = torch.empty((A.n_rows, d), dtype=torch.float32, device=B.device) if out is None else out
+    s = A.struct()
+    need = lib().rsc_spmm_workspace_bytes(ctypes.byref(s))
+    ws = _workspace(need, B.device) if ws is None else ws
+    _check(lib().rsc_spmm(ctypes.byref(s), B.data_ptr(), d, _ld(B), Y.data_ptr(), _ld(Y),
+                          ws.data_ptr(), ws.numel(), _stream()))
+    return Y
+
+
+# ---------------------------------------------------------------- A2 / A3
+def col_sqnorms(XT: DeviceCsr):
+    """(cn2 float64[n], colnnz int32[n]) from the CSR of X^T."""
+    cn2 = torch.empty(XT.n_rows, dtype=torch.float64, device=XT.rowptr.device)
+    colnnz = torch.empty(XT.n_rows, dtype=torch.int32, device=XT.rowptr.device)
+    _check(lib().rsc_col_sqnorms(ctypes.byref(XT.struct()), cn2.data_ptr(), colnnz.data_ptr(), _stream()))
+    return cn2, colnnz
+
+
+def pair_scores(cn2: torch.Tensor, B: torch.Tensor, d: int | None = None, with_score: bool = False):
+    """Keys (uint64 bit patterns stored in an int64 tensor) and optionally
+    fp32 scores for the n = B.shape[0] column-row pairs."""
+    n = B.shape[0]
+    d = B.shape[1] if d is None else d
+    key = torch.empty(n, dtype=torch.int64, device=B.device)
+    score = torch.empty(n, dtype=torch.float32, device=B.device) if with_score else None
+    _check(lib().rsc_pair_scores(cn2.data_ptr(), B.data_ptr(), n, d, _ld(B), key.data_ptr(),
+                                 _ptr(score), _stream()))
+    return (key, score) if with_score else key
+
+
+# ---------------------------------------------------------------- A4
+def topk_select(key: torch.Tensor, k: int, ws: torch.Tensor | None = None):
+    """(idx int32[k] ascending, mask int32[ceil(n/32)] holding uint32 words)."""
+    n = key.numel()
+    idx = torch.empty(max(k, 1), dtype=torch.int32, device=key.device)
+    mask = torch.empty(max((n + 31) // 32, 1), dtype=torch.int32, device=key.device)
+    need = lib().rsc_topk_workspace_bytes(n)
+    ws = _workspace(need, key.device) if ws is None else ws
+    _check(lib().rsc_topk_select(key.data_ptr(), n, k, idx.data_ptr(), mask.data_ptr(), ws.data_ptr(),
+                                 ws.numel(), _stream()))
+    return idx[:k], mask[: (n + 31) // 32]
+
+
+# ---------------------------------------------------------------- A5
+def slice_csr(A: DeviceCsr, mask: torch.Tensor, capacity: int | None = None,
+              ws: torch.Tensor | None = None):
+    """(DeviceCsr slice with capacity-sized col/val, nnz' as a device int64
+    tensor). The slice's nnz field is left as None-equivalent (capacity)
+    until the caller reads nnz'."""
+    cap = A.nnz if capacity is None else capacity
+    dev = A.rowptr.device
+    rp = torch.empty(A.n_rows + 1, dtype=torch.int32, device=dev)
+    co = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    vo = torch.empty(max(cap, 1), dtype=torch.float32, device=dev)
+    nnz_out = torch.empty(1, dtype=torch.int64, device=dev)
+    s = A.struct()
+    need = lib().rsc_slice_workspace_bytes(ctypes.byref(s))
+    ws = _workspace(need, dev) if ws is None else ws
+    _check(lib().rsc_slice_csr(ctypes.byref(s), _ptr(mask), rp.data_ptr(), co.data_ptr(), vo.data_ptr(),
+                               cap, nnz_out.data_ptr(), ws.data_ptr(), ws.numel(), _stream()))
+    return DeviceCsr(A.n_rows, A.n_cols, rp, co, vo, nnz=cap), nnz_out
+
+
+# ---------------------------------------------------------------- A6 / A7
+class Cache:
+    """Sampled-matrix cache (section 3.3.1): rsc_cache_create / refresh /
+    get / spmm_sampled / destroy."""
+
+    def __init__(self, X: DeviceCsr, XT: DeviceCsr | None = None, refresh_interval: int = 10):
+        self.X = X
+        self.XT = X if XT is None else XT
+        h = ctypes.c_void_p()
+        _check(lib().rsc_cache_create(ctypes.byref(X.struct()), ctypes.byref(self.XT.struct()),
+                                      refresh_interval, _stream(), ctypes.byref(h)))
+        self._h = h
+
+    def refresh(self, B: torch.Tensor, k: int, step: int, d: int | None = None) -> None:
+        d = B.shape[1] if d is None else d
+        _check(lib().rsc_cache_refresh(self._h, B.data_ptr(), d, _ld(B), k, step, _stream()))
+
+    def get(self, step: int):
+        """dict(slice=CsrStruct, idx_ptr, k, needs_refresh, version)."""
+        s = CsrStruct()
+        idx = ctypes.c_void_p()
+        k = ctypes.c_int32()
+        nr = ctypes.c_int32()
+        ver = ctypes.c_uint64()
+        _check(lib().rsc_cache_get(self._h, step, ctypes.byref(s), ctypes.byref(idx), ctypes.byref(k),
+                                   ctypes.byref(nr), ctypes.byref(ver)))
+        return {"slice": s, "idx_ptr": idx.value, "k": k.value, "needs_refresh": bool(nr.value),
+                "version": ver.value}
+
+    def spmm_sampled(self, B: torch.Tensor, d: int | None = None, out: torch.Tensor | None = None):
+        d = B.shape[1] if d is None else d
+        Y = torch.empty((self.X.n_rows, d), dtype=torch.float32, device=B.device) if out is None else out
+        _check(lib().rsc_spmm_sampled(self._h, B.data_ptr(), d, _ld(B), Y.data_ptr(), _ld(Y), _stream()))
+        return Y
+
+    def buffers(self):
+        p = [ctypes.c_void_p() for _ in range(4)]
+        _check(lib().rsc_cache_buffers(self._h, *[ctypes.byref(x) for x in p]))
+        return [x.value for x in p]
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            _check(lib().rsc_cache_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def copy_to_host(ptr: int, count: int, np_dtype):
+    """Copies `count` elements at device address `ptr` into a new numpy
+    array (synchronises the current stream first)."""
+    import numpy as np
+    out = np.empty(count, dtype=np_dtype)
+    if count:
+        torch.cuda.current_stream().synchronize()
+        r = _hip().hipMemcpy(ctypes.c_void_p(out.ctypes.data), ctypes.c_void_p(ptr),
+                             ctypes.c_size_t(out.nbytes), 2)  # hipMemcpyDeviceToHost
+        if r != 0:
+            raise RuntimeError(f"hipMemcpy failed with code {r}")
+    return out
+
+
+def cache_snapshot(cache: Cache, step: int = 0) -> dict:
+    """Host copies of the cached slice and kept indices (for tests)."""
+    import numpy as np
+    g = cache.get(step)
+    s = g["slice"]
+    out = dict(g)
+    out["nnz"] = s.nnz
+    out["rowptr"] = copy_to_host(s.rowptr, s.n_rows + 1, np.int32) if s.rowptr else None
+    out["col"] = copy_to_host(s.col, s.nnz, np.int32) if s.col else np.zeros(0, np.int32)
+    out["val"] = copy_to_host(s.val, s.nnz, np.float32) if s.val else np.zeros(0, np.float32)
+    out["idx"] = copy_to_host(g["idx_ptr"], g["k"], np.int32) if g["idx_ptr"] else np.zeros(0, np.int32)
+    return out
+
+
+_hip_lib = None
+
+
+def _hip():
+    """The HIP runtime already loaded in this process (matched by soname, so
+    it is the one torch and librsc.so use)."""
+    global _hip_lib
+    if _hip_lib is None:
+        _hip_lib = ctypes.CDLL("libamdhip64.so.7")
+        _hip_lib.hipMemcpy.restype = ctypes.c_int
+    return _hip_lib
+
+
+# ---------------------------------------------------------------- A8
+def k_from_fraction(n: int, num: int, den: int) -> int:
+    return lib().rsc_k_from_fraction(n, num, den)
+
+
+def greedy_allocate(keys, colnnz, nnz: int, d, fro_a2: float, fro_b2, C, alpha):
+    """Layer-wise k_l (host compute). keys: list of numpy uint64 arrays."""
+    import numpy as np
+    L = len(keys)
+    keys = [np.ascontiguousarray(k, dtype=np.uint64) for k in keys]
+    n = len(keys[0])
+    ptrs = (ctypes.c_void_p * L)(*[k.ctypes.data for k in keys])
+    colnnz = np.ascontiguousarray(colnnz, dtype=np.int32)
+    d_arr = np.ascontiguousarray(d, dtype=np.int32)
+    fb = np.ascontiguousarray(fro_b2, dtype=np.float64)
+    k_out = np.zeros(L, dtype=np.int32)
+    bud = ctypes.c_int64()
+    _check(lib().rsc_greedy_allocate(L, n, nnz, ctypes.cast(ptrs, ctypes.c_void_p), colnnz.ctypes.data,
+                                     d_arr.ctypes.data, float(fro_a2), fb.ctypes.data, C[0], C[1],
+                                     alpha[0], alpha[1], k_out.ctypes.data, ctypes.byref(bud)))
+    return [int(x) for x in k_out], int(bud.value)

@@ -1,0 +1,446 @@
+// C ABI of the library (declared in include/rsc.h): argument validation,
+// status codes, the sampled-matrix cache and the host-side budget helpers.
+// Every device step is one of the kernels in spmm.hip / scores.hip /
+// topk.hip / slice.hip.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "rsc.h"
+#include "rsc_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+rsc_status_t fail(rsc_status_t s, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+rsc_status_t hip_fail(hipError_t e, const char *what) {
+    return fail(RSC_ERR_HIP, "%s: %s (%s)", what, hipGetErrorName(e), hipGetErrorString(e));
+}
+
+#define RSC_TRY(expr)                     \
+    do {                                  \
+        rsc_status_t _s = (expr);         \
+        if (_s != RSC_OK) return _s;      \
+    } while (0)
+
+#define RSC_HIP(expr, what)                         \
+    do {                                            \
+        hipError_t _e = (expr);                     \
+        if (_e != hipSuccess) return hip_fail(_e, what); \
+    } while (0)
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+rsc_status_t check_device() {
+    static int count = -1;
+    if (count < 0) {
+        int c = 0;
+        if (hipGetDeviceCount(&c) != hipSuccess) c = 0;
+        count = c;
+    }
+    if (count <= 0) return fail(RSC_ERR_NO_DEVICE, "no HIP device visible");
+    return RSC_OK;
+}
+
+rsc_status_t check_csr(const rsc_csr_t *A, const char *name) {
+    if (!A) return fail(RSC_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+    if (A->n_rows < 0 || A->n_cols < 0 || A->nnz < 0)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "%s has negative dimensions", name);
+    if (A->nnz >= (int64_t(1) << 31)) return fail(RSC_ERR_UNSUPPORTED, "%s: nnz >= 2^31", name);
+    if (!A->rowptr) return fail(RSC_ERR_INVALID_ARGUMENT, "%s->rowptr is NULL", name);
+    if (A->nnz > 0 && (!A->col || !A->val))
+        return fail(RSC_ERR_INVALID_ARGUMENT, "%s->col/val is NULL", name);
+    if (!aligned(A->rowptr, 4) || !aligned(A->col, 4) || !aligned(A->val, 4))
+        return fail(RSC_ERR_UNSUPPORTED, "%s arrays must be 4-byte aligned", name);
+    return RSC_OK;
+}
+
+rsc_status_t check_dense(const void *p, int64_t rows, int32_t d, int64_t ld, const char *name) {
+    if (d < 1) return fail(RSC_ERR_INVALID_ARGUMENT, "d = %d < 1", d);
+    if (ld < d) return fail(RSC_ERR_INVALID_ARGUMENT, "%s: ld %lld < d %d", name, (long long)ld, d);
+    if (ld % 4 != 0) return fail(RSC_ERR_UNSUPPORTED, "%s: ld %lld is not a multiple of 4", name, (long long)ld);
+    if (rows > 0 && !p) return fail(RSC_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+    if (!aligned(p, 16)) return fail(RSC_ERR_UNSUPPORTED, "%s is not 16-byte aligned", name);
+    return RSC_OK;
+}
+
+rsc_status_t check_ws(const void *ws, size_t ws_bytes, size_t need, const char *what) {
+    if (ws_bytes < need)
+        return fail(RSC_ERR_CAPACITY, "%s workspace: %zu bytes given, %zu needed", what, ws_bytes, need);
+    if (need > 0 && !ws) return fail(RSC_ERR_INVALID_ARGUMENT, "%s workspace is NULL", what);
+    if (!aligned(ws, 256)) return fail(RSC_ERR_UNSUPPORTED, "%s workspace is not 256-byte aligned", what);
+    return RSC_OK;
+}
+
+}  // namespace
+
+struct rsc_cache {
+    rsc_csr_t X{}, XT{};
+    int32_t interval = 10;
+    int32_t n = 0;  // pairs = columns of X
+    int device = 0;
+    double *cn2 = nullptr;
+    int32_t *colnnz = nullptr;
+    uint64_t *key = nullptr;
+    int32_t *idx = nullptr;
+    uint32_t *mask = nullptr;
+    int32_t *s_rowptr = nullptr;
+    int32_t *s_col = nullptr;
+    float *s_val = nullptr;
+    int64_t *d_nnz = nullptr;
+    int64_t *h_nnz = nullptr;  // pinned
+    void *ws_topk = nullptr, *ws_slice = nullptr, *ws_spmm = nullptr;
+    size_t ws_topk_bytes = 0, ws_slice_bytes = 0, ws_spmm_bytes = 0;
+    hipEvent_t ev = nullptr;
+    int32_t k = 0;
+    int64_t last_step = 0;
+    uint64_t version = 0;
+    bool nnz_known = false;
+    int64_t nnz_slice = 0;
+};
+
+extern "C" {
+
+const char *rsc_status_string(rsc_status_t s) {
+    switch (s) {
+        case RSC_OK: return "RSC_OK";
+        case RSC_ERR_INVALID_ARGUMENT: return "RSC_ERR_INVALID_ARGUMENT";
+        case RSC_ERR_UNSUPPORTED: return "RSC_ERR_UNSUPPORTED";
+        case RSC_ERR_OUT_OF_MEMORY: return "RSC_ERR_OUT_OF_MEMORY";
+        case RSC_ERR_CAPACITY: return "RSC_ERR_CAPACITY";
+        case RSC_ERR_NO_DEVICE: return "RSC_ERR_NO_DEVICE";
+        case RSC_ERR_HIP: return "RSC_ERR_HIP";
+        case RSC_ERR_INTERNAL: return "RSC_ERR_INTERNAL";
+    }
+    return "RSC_ERR_UNKNOWN";
+}
+
+const char *rsc_last_error(void) { return g_err.c_str(); }
+
+int32_t rsc_abi_version(void) { return RSC_ABI_VERSION; }
+
+// ------------------------------------------------------------------- A1
+size_t rsc_spmm_workspace_bytes(const rsc_csr_t *A) {
+    if (!A || A->n_rows < 0 || A->nnz < 0) return 0;
+    return rsc::spmm_ws_bytes(A->n_rows, A->nnz);
+}
+
+rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb, float *Y,
+                      int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream) {
+    RSC_TRY(check_csr(A, "A"));
+    RSC_TRY(check_dense(B, A->n_cols, d, ldb, "B"));
+    RSC_TRY(check_dense(Y, A->n_rows, d, ldy, "Y"));
+    RSC_TRY(check_ws(ws, ws_bytes, rsc::spmm_ws_bytes(A->n_rows, A->nnz), "spmm"));
+    RSC_TRY(check_device());
+    RSC_HIP(rsc::spmm_launch(A->n_rows, A->nnz, A->rowptr, A->col, A->val, B, d, ldb, Y, ldy, ws, stream),
+            "spmm launch");
+    return RSC_OK;
+}
+
+// ------------------------------------------------------------------- A2
+rsc_status_t rsc_col_sqnorms(const rsc_csr_t *XT, double *cn2, int32_t *colnnz, hipStream_t stream) {
+    RSC_TRY(check_csr(XT, "XT"));
+    if (XT->n_rows > 0 && !cn2) return fail(RSC_ERR_INVALID_ARGUMENT, "cn2 is NULL");
+    if (!aligned(cn2, 8)) return fail(RSC_ERR_UNSUPPORTED, "cn2 is not 8-byte aligned");
+    RSC_TRY(check_device());
+    RSC_HIP(rsc::col_sqnorms_launch(XT->n_rows, XT->rowptr, XT->val, cn2, colnnz, stream),
+            "col_sqnorms launch");
+    return RSC_OK;
+}
+
+// ------------------------------------------------------------------- A3
+rsc_status_t rsc_pair_scores(const double *cn2, const float *B, int32_t n, int32_t d, int64_t ldb,
+                             uint64_t *key, float *score, hipStream_t stream) {
+    if (n < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "n = %d < 0", n);
+    RSC_TRY(check_dense(B, n, d, ldb, "B"));
+    if (n > 0 && (!cn2 || !key)) return fail(RSC_ERR_INVALID_ARGUMENT, "cn2/key is NULL");
+    if (!aligned(cn2, 8) || !aligned(key, 8)) return fail(RSC_ERR_UNSUPPORTED, "cn2/key not 8-byte aligned");
+    RSC_TRY(check_device());
+    RSC_HIP(rsc::pair_scores_launch(cn2, B, n, d, ldb, key, score, stream), "pair_scores launch");
+    return RSC_OK;
+}
+
+// ------------------------------------------------------------------- A4
+size_t rsc_topk_workspace_bytes(int32_t n) { return n < 0 ? 0 : rsc::topk_ws_bytes(n); }
+
+rsc_status_t rsc_topk_select(const uint64_t *key, int32_t n, int32_t k, int32_t *idx, uint32_t *mask,
+                             void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (n < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "n = %d < 0", n);
+    if (k < 0 || k > n) return fail(RSC_ERR_INVALID_ARGUMENT, "k = %d outside [0, n = %d]", k, n);
+    if (n > 0 && (!key || !mask)) return fail(RSC_ERR_INVALID_ARGUMENT, "key/mask is NULL");
+    if (k > 0 && !idx) return fail(RSC_ERR_INVALID_ARGUMENT, "idx is NULL");
+    if (!aligned(key, 8) || !aligned(idx, 4) || !aligned(mask, 4))
+        return fail(RSC_ERR_UNSUPPORTED, "key/idx/mask misaligned");
+    RSC_TRY(check_ws(ws, ws_bytes, rsc::topk_ws_bytes(n), "topk"));
+    RSC_TRY(check_device());
+    RSC_HIP(rsc::topk_launch(key, n, k, idx, mask, ws, stream), "topk launch");
+    return RSC_OK;
+}
+
+// ------------------------------------------------------------------- A5
+size_t rsc_slice_workspace_bytes(const rsc_csr_t *A) {
+    if (!A || A->nnz < 0) return 0;
+    return rsc::slice_ws_bytes(A->nnz);
+}
+
+rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, int32_t *rowptr_out, int32_t *col_out,
+                           float *val_out, int64_t capacity, int64_t *nnz_out, void *ws, size_t ws_bytes,
+                           hipStream_t stream) {
+    RSC_TRY(check_csr(A, "A"));
+    if (capacity < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "capacity < 0");
+    if (!rowptr_out || !nnz_out) return fail(RSC_ERR_INVALID_ARGUMENT, "rowptr_out/nnz_out is NULL");
+    if (A->nnz > 0 && !mask) return fail(RSC_ERR_INVALID_ARGUMENT, "mask is NULL");
+    if (capacity > 0 && (!col_out || !val_out)) return fail(RSC_ERR_INVALID_ARGUMENT, "col_out/val_out is NULL");
+    if (!aligned(nnz_out, 8)) return fail(RSC_ERR_UNSUPPORTED, "nnz_out is not 8-byte aligned");
+    RSC_TRY(check_ws(ws, ws_bytes, rsc::slice_ws_bytes(A->nnz), "slice"));
+    RSC_TRY(check_device());
+    RSC_HIP(rsc::slice_launch(A->n_rows, A->nnz, A->rowptr, A->col, A->val, mask, rowptr_out, col_out, val_out,
+                              capacity, nnz_out, ws, stream),
+            "slice launch");
+    if (capacity < A->nnz) {
+        int64_t got = 0;
+        RSC_HIP(hipMemcpyAsync(&got, nnz_out, sizeof got, hipMemcpyDeviceToHost, stream), "slice nnz read");
+        RSC_HIP(hipStreamSynchronize(stream), "slice sync");
+        if (got > capacity)
+            return fail(RSC_ERR_CAPACITY, "slice has %lld entries, capacity %lld", (long long)got,
+                        (long long)capacity);
+    }
+    return RSC_OK;
+}
+
+// ------------------------------------------------------------------- A6 / A7
+static void cache_free(rsc_cache_t *c) {
+    if (!c) return;
+    void *dev[] = {c->cn2, c->colnnz, c->key, c->idx, c->mask, c->s_rowptr, c->s_col, c->s_val,
+                   c->d_nnz, c->ws_topk, c->ws_slice, c->ws_spmm};
+    for (void *p : dev)
+        if (p) (void)hipFree(p);
+    if (c->h_nnz) (void)hipHostFree(c->h_nnz);
+    if (c->ev) (void)hipEventDestroy(c->ev);
+    delete c;
+}
+
+rsc_status_t rsc_cache_create(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t refresh_interval,
+                              hipStream_t stream, rsc_cache_t **out) {
+    if (!out) return fail(RSC_ERR_INVALID_ARGUMENT, "out is NULL");
+    RSC_TRY(check_csr(X, "X"));
+    RSC_TRY(check_csr(XT, "XT"));
+    if (XT->n_rows != X->n_cols || XT->n_cols != X->n_rows || XT->nnz != X->nnz)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "XT is not shaped like the transpose of X");
+    if (refresh_interval < 1) return fail(RSC_ERR_INVALID_ARGUMENT, "refresh_interval < 1");
+    RSC_TRY(check_device());
+    rsc_cache_t *c = new rsc_cache_t();
+    c->X = *X;
+    c->XT = *XT;
+    c->interval = refresh_interval;
+    c->n = X->n_cols;
+    (void)hipGetDevice(&c->device);
+    const int64_t n = std::max<int32_t>(c->n, 1), m = std::max<int64_t>(X->nnz, 1);
+    c->ws_topk_bytes = rsc::topk_ws_bytes(c->n);
+    c->ws_slice_bytes = rsc::slice_ws_bytes(X->nnz);
+    c->ws_spmm_bytes = rsc::spmm_ws_bytes(X->n_rows, X->nnz);
+    struct {
+        void **p;
+        size_t bytes;
+    } allocs[] = {
+        {(void **)&c->cn2, sizeof(double) * n},
+        {(void **)&c->colnnz, sizeof(int32_t) * n},
+        {(void **)&c->key, sizeof(uint64_t) * n},
+        {(void **)&c->idx, sizeof(int32_t) * n},
+        {(void **)&c->mask, sizeof(uint32_t) * (size_t)rsc::ceil_div(n, 32)},
+        {(void **)&c->s_rowptr, sizeof(int32_t) * ((size_t)X->n_rows + 1)},
+        {(void **)&c->s_col, sizeof(int32_t) * m},
+        {(void **)&c->s_val, sizeof(float) * m},
+        {(void **)&c->d_nnz, sizeof(int64_t)},
+        {&c->ws_topk, c->ws_topk_bytes},
+        {&c->ws_slice, c->ws_slice_bytes},
+        {&c->ws_spmm, c->ws_spmm_bytes},
+    };
+    for (auto &a : allocs) {
+        if (hipMalloc(a.p, std::max<size_t>(a.bytes, 256)) != hipSuccess) {
+            (void)hipGetLastError();
+            cache_free(c);
+            return fail(RSC_ERR_OUT_OF_MEMORY, "cache allocation of %zu bytes failed", a.bytes);
+        }
+    }
+    hipError_t e = hipHostMalloc((void **)&c->h_nnz, sizeof(int64_t), hipHostMallocDefault);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev, hipEventDisableTiming);
+    if (e == hipSuccess) e = rsc::col_sqnorms_launch(XT->n_rows, XT->rowptr, XT->val, c->cn2, c->colnnz, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) {
+        cache_free(c);
+        return hip_fail(e, "cache create");
+    }
+    *out = c;
+    return RSC_OK;
+}
+
+rsc_status_t rsc_cache_refresh(rsc_cache_t *c, const float *B, int32_t d, int64_t ldb, int32_t k, int64_t step,
+                               hipStream_t stream) {
+    if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
+    RSC_TRY(check_dense(B, c->n, d, ldb, "B"));
+    if (k < 0 || k > c->n) return fail(RSC_ERR_INVALID_ARGUMENT, "k = %d outside [0, %d]", k, c->n);
+    RSC_HIP(rsc::pair_scores_launch(c->cn2, B, c->n, d, ldb, c->key, nullptr, stream), "refresh scores");
+    RSC_HIP(rsc::topk_launch(c->key, c->n, k, c->idx, c->mask, c->ws_topk, stream), "refresh topk");
+    RSC_HIP(rsc::slice_launch(c->X.n_rows, c->X.nnz, c->X.rowptr, c->X.col, c->X.val, c->mask, c->s_rowptr,
+                              c->s_col, c->s_val, c->X.nnz, c->d_nnz, c->ws_slice, stream),
+            "refresh slice");
+    RSC_HIP(hipMemcpyAsync(c->h_nnz, c->d_nnz, sizeof(int64_t), hipMemcpyDeviceToHost, stream), "refresh nnz");
+    RSC_HIP(hipEventRecord(c->ev, stream), "refresh event");
+    c->k = k;
+    c->last_step = step;
+    c->version += 1;
+    c->nnz_known = false;
+    return RSC_OK;
+}
+
+rsc_status_t rsc_cache_get(rsc_cache_t *c, int64_t step, rsc_csr_t *slice_out, const int32_t **idx_out,
+                           int32_t *k_out, int32_t *needs_refresh_out, uint64_t *version_out) {
+    if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
+    if (needs_refresh_out) *needs_refresh_out = (c->version == 0 || step - c->last_step >= c->interval) ? 1 : 0;
+    if (version_out) *version_out = c->version;
+    if (k_out) *k_out = c->version ? c->k : 0;
+    if (idx_out) *idx_out = c->version ? c->idx : nullptr;
+    if (slice_out) {
+        rsc_csr_t s{};
+        s.n_rows = c->X.n_rows;
+        s.n_cols = c->X.n_cols;
+        if (c->version) {
+            if (!c->nnz_known) {
+                RSC_HIP(hipEventSynchronize(c->ev), "cache get wait");
+                c->nnz_slice = *c->h_nnz;
+                c->nnz_known = true;
+            }
+            s.nnz = c->nnz_slice;
+            s.rowptr = c->s_rowptr;
+            s.col = c->s_col;
+            s.val = c->s_val;
+        }
+        *slice_out = s;
+    }
+    return RSC_OK;
+}
+
+rsc_status_t rsc_spmm_sampled(rsc_cache_t *c, const float *B, int32_t d, int64_t ldb, float *Y, int64_t ldy,
+                              hipStream_t stream) {
+    if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
+    if (c->version == 0) return fail(RSC_ERR_INVALID_ARGUMENT, "cache was never refreshed");
+    RSC_TRY(check_dense(B, c->X.n_cols, d, ldb, "B"));
+    RSC_TRY(check_dense(Y, c->X.n_rows, d, ldy, "Y"));
+    // nnz of the full operand bounds the slice's, which sizes the long-row list
+    RSC_HIP(rsc::spmm_launch(c->X.n_rows, c->X.nnz, c->s_rowptr, c->s_col, c->s_val, B, d, ldb, Y, ldy,
+                             c->ws_spmm, stream),
+            "spmm_sampled launch");
+    return RSC_OK;
+}
+
+rsc_status_t rsc_cache_buffers(rsc_cache_t *c, const double **cn2, const int32_t **colnnz, const uint64_t **key,
+                               const uint32_t **mask) {
+    if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
+    if (cn2) *cn2 = c->cn2;
+    if (colnnz) *colnnz = c->colnnz;
+    if (key) *key = c->key;
+    if (mask) *mask = c->mask;
+    return RSC_OK;
+}
+
+rsc_status_t rsc_cache_destroy(rsc_cache_t *c) {
+    if (!c) return RSC_OK;
+    hipError_t e = hipDeviceSynchronize();
+    cache_free(c);
+    if (e != hipSuccess) return hip_fail(e, "cache destroy");
+    return RSC_OK;
+}
+
+// ------------------------------------------------------------------- A8
+int32_t rsc_k_from_fraction(int32_t n, int32_t num, int32_t den) {
+    if (n < 0 || num < 0 || den <= 0 || num > den) return -1;
+    return (int32_t)(((int64_t)n * (int64_t)num) / (int64_t)den);
+}
+
+rsc_status_t rsc_greedy_allocate(int32_t L, int32_t n, int64_t nnz, const uint64_t *const *key_host,
+                                 const int32_t *colnnz_host, const int32_t *d_host, double fro_a2,
+                                 const double *fro_b2_host, int32_t C_num, int32_t C_den, int32_t alpha_num,
+                                 int32_t alpha_den, int32_t *k_out_host, int64_t *budget_out_host) {
+    if (L < 1 || n < 0 || nnz < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "L < 1, n < 0 or nnz < 0");
+    if (!key_host || !colnnz_host || !d_host || !fro_b2_host || !k_out_host)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "NULL host array");
+    if (C_num < 0 || C_den <= 0 || alpha_num < 0 || alpha_den <= 0)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "bad budget or step fraction");
+    for (int32_t l = 0; l < L; ++l) {
+        if (!key_host[l]) return fail(RSC_ERR_INVALID_ARGUMENT, "key_host[%d] is NULL", l);
+        if (d_host[l] < 1) return fail(RSC_ERR_INVALID_ARGUMENT, "d[%d] < 1", l);
+    }
+    // rank order per layer: (key desc, index asc); contribution sqrt(q) with
+    // NaN keys (0) counting 0
+    std::vector<std::vector<int32_t>> order(L);
+    std::vector<std::vector<double>> contrib(L);
+    int64_t total = 0;
+    for (int32_t l = 0; l < L; ++l) {
+        const uint64_t *key = key_host[l];
+        auto &o = order[l];
+        o.resize(n);
+        for (int32_t i = 0; i < n; ++i) o[i] = i;
+        std::sort(o.begin(), o.end(), [key](int32_t a, int32_t b) {
+            return key[a] != key[b] ? key[a] > key[b] : a < b;
+        });
+        auto &c = contrib[l];
+        c.resize(n);
+        for (int32_t p = 0; p < n; ++p) {
+            const uint64_t u = key[o[p]];
+            if (u == 0) {
+                c[p] = 0.0;
+            } else {
+                const uint64_t bits = u - 1;
+                double q;
+                std::memcpy(&q, &bits, sizeof q);
+                c[p] = std::sqrt(q);
+            }
+        }
+        k_out_host[l] = n;
+        total += nnz * (int64_t)d_host[l];
+    }
+    int32_t step = (int32_t)(((int64_t)n * alpha_num) / alpha_den);
+    if (step < 1) step = 1;
+    int64_t bud = total;
+    while (bud * (int64_t)C_den > (int64_t)C_num * total) {
+        int32_t best = -1;
+        double best_inc = 0.0;
+        for (int32_t l = 0; l < L; ++l) {
+            const int32_t k = k_out_host[l];
+            if (k <= 0) continue;
+            const int32_t k2 = std::max(0, k - step);
+            double s = 0.0;
+            for (int32_t p = k2; p < k; ++p) s += contrib[l][p];
+            const double inc = s / (std::sqrt(fro_a2) * std::sqrt(fro_b2_host[l]));
+            if (best < 0 || inc < best_inc) {
+                best = l;
+                best_inc = inc;
+            }
+        }
+        if (best < 0) break;
+        const int32_t k = k_out_host[best], k2 = std::max(0, k - step);
+        int64_t drop = 0;
+        for (int32_t p = k2; p < k; ++p) drop += colnnz_host[order[best][p]];
+        bud -= (int64_t)d_host[best] * drop;
+        k_out_host[best] = k2;
+    }
+    if (budget_out_host) *budget_out_host = bud;
+    return RSC_OK;
+}
+
+}  // extern "C"

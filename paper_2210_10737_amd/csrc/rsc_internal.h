@@ -1,0 +1,49 @@
+// Internal declarations shared by the library's HIP translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+namespace rsc {
+
+constexpr int kWave = 64;
+
+// ---- SpMM --------------------------------------------------------------
+// Rows with more than kLongRow entries are processed by a whole 4-wave
+// block (waves take interleaved runs of 64 entries, then a fixed-order LDS
+// reduction); shorter rows by one wave.
+constexpr int kLongRow = 1024;
+constexpr int kSpmmBlockWaves = 4;
+constexpr int kSpmmLongBlocks = 512;  // persistent blocks that walk the long-row list
+
+size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz);
+hipError_t spmm_launch(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr, const int32_t *col,
+                       const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
+                       int64_t ldy, void *ws, hipStream_t stream);
+
+// ---- scores ------------------------------------------------------------
+hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,
+                              int32_t *colnnz, hipStream_t stream);
+hipError_t pair_scores_launch(const double *cn2, const float *B, int32_t n, int32_t d, int64_t ldb,
+                              uint64_t *key, float *score, hipStream_t stream);
+
+// ---- top-k -------------------------------------------------------------
+size_t topk_ws_bytes(int32_t n);
+hipError_t topk_launch(const uint64_t *key, int32_t n, int32_t k, int32_t *idx, uint32_t *mask,
+                       void *ws, hipStream_t stream);
+
+// ---- slice -------------------------------------------------------------
+size_t slice_ws_bytes(int64_t nnz);
+hipError_t slice_launch(int32_t n_rows, int64_t nnz, const int32_t *rowptr, const int32_t *col,
+                        const float *val, const uint32_t *mask, int32_t *rowptr_out,
+                        int32_t *col_out, float *val_out, int64_t capacity, int64_t *nnz_out,
+                        void *ws, hipStream_t stream);
+
+// ---- helpers -----------------------------------------------------------
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace rsc

@@ -1,0 +1,95 @@
+// Pair scores of the column-row pairs (Eq. 3; the top-k rule of section
+// 2.2.1; the ||A^T[:, i]|| ||grad H[i, :]|| terms of Eq. 4a).
+//
+// Both reductions follow one canonical order so that the keys, and hence the
+// selection, are bitwise reproducible: an fp64 sum of exact fp32 squares in
+// plain index order, one lane per sum.
+#include "rsc_internal.h"
+
+namespace rsc {
+namespace {
+
+// cn2[i] = sum of val^2 over row i of X^T, in stored order (one lane per
+// row). Products of fp32 values are exact in fp64, so fma(v, v, acc) equals
+// acc + v * v.
+__global__ __launch_bounds__(256) void col_sqnorms_kernel(int32_t n, const int32_t *__restrict__ rowptr,
+                                                          const float *__restrict__ val,
+                                                          double *__restrict__ cn2,
+                                                          int32_t *__restrict__ colnnz) {
+    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const int32_t s = rowptr[i], e = rowptr[i + 1];
+    double acc = 0.0;
+    for (int32_t t = s; t < e; ++t) {
+        const double v = (double)val[t];
+        acc = fma(v, v, acc);
+    }
+    cn2[i] = acc;
+    if (colnnz) colnnz[i] = e - s;
+}
+
+// 256 rows per block, one row per thread. B is streamed through LDS in tiles
+// of 256 rows x 32 features (each row segment is one 128-byte line, read by
+// 8 lanes with 128-bit loads); each thread then sums its own row of the tile
+// in ascending feature order.
+constexpr int kRows = 256;
+constexpr int kTileF = 32;
+
+__global__ __launch_bounds__(256) void pair_scores_kernel(const double *__restrict__ cn2,
+                                                          const float *__restrict__ B, int32_t n,
+                                                          int32_t d, int64_t ldb,
+                                                          uint64_t *__restrict__ key,
+                                                          float *__restrict__ score) {
+    __shared__ float tile[kRows][kTileF + 1];
+    const int t = threadIdx.x;
+    const int64_t row0 = (int64_t)blockIdx.x * kRows;
+    double acc = 0.0;
+    for (int32_t f0 = 0; f0 < d; f0 += kTileF) {
+#pragma unroll
+        for (int it = 0; it < kRows * kTileF / 4 / 256; ++it) {
+            const int idx = t + 256 * it;
+            const int rl = idx >> 3, fq = idx & 7;
+            const int64_t row = row0 + rl;
+            const int32_t f = f0 + 4 * fq;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            // ld % 4 == 0 and ld >= d, so a float4 starting below d stays in the row
+            if (row < n && f < d) v = *reinterpret_cast<const float4 *>(B + row * ldb + f);
+            tile[rl][4 * fq + 0] = v.x;
+            tile[rl][4 * fq + 1] = v.y;
+            tile[rl][4 * fq + 2] = v.z;
+            tile[rl][4 * fq + 3] = v.w;
+        }
+        __syncthreads();
+        const int lim = min(kTileF, d - f0);
+        for (int j = 0; j < lim; ++j) {
+            const double b = (double)tile[t][j];
+            acc = fma(b, b, acc);
+        }
+        __syncthreads();
+    }
+    const int64_t row = row0 + t;
+    if (row < n) {
+        const double q = cn2[row] * acc;
+        const uint64_t bits = (uint64_t)__double_as_longlong(q);
+        key[row] = isnan(q) ? 0ull : bits + 1ull;
+        if (score) score[row] = (float)sqrt(q);
+    }
+}
+
+}  // namespace
+
+hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,
+                              int32_t *colnnz, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    col_sqnorms_kernel<<<(unsigned)ceil_div(n, 256), 256, 0, stream>>>(n, rowptr_t, val_t, cn2, colnnz);
+    return hipGetLastError();
+}
+
+hipError_t pair_scores_launch(const double *cn2, const float *B, int32_t n, int32_t d, int64_t ldb,
+                              uint64_t *key, float *score, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    pair_scores_kernel<<<(unsigned)ceil_div(n, kRows), 256, 0, stream>>>(cn2, B, n, d, ldb, key, score);
+    return hipGetLastError();
+}
+
+}  // namespace rsc

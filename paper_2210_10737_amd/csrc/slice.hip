@@ -1,0 +1,187 @@
+// Column slice of a CSR matrix, A' = A[:, S] (section 3.3.1 and Fig. 5's
+// rebuild of Rowptr and Col; appendix C: whole columns are dropped, every row
+// is kept, so rows may become empty).
+//
+// Entry t is kept iff bit col[t] of the mask is set. Because kept entries
+// stay in their original order, the output position of a kept entry is the
+// number of kept entries before it, and Rowptr'[i] is that count at position
+// Rowptr[i]. So the slice is one stream compaction over the nnz entries:
+//   1. count kept entries per tile of 4096 (reads col; the mask is an n-bit
+//      set that stays in L2);
+//   2. one block scans the tile counts (and stores nnz');
+//   3. per tile: stage col/val through LDS, scan the kept flags inside the
+//      tile, write the kept entries at their global positions, and write
+//      Rowptr'[i] for every row whose Rowptr[i] falls in the tile.
+// Integer-only and deterministic.
+#include "rsc_internal.h"
+
+namespace rsc {
+namespace {
+
+constexpr int kTile = 4096;          // entries per tile
+constexpr int kPer = kTile / 256;    // consecutive entries per thread in the emit kernel
+
+__device__ __forceinline__ bool kept(const uint32_t *__restrict__ mask, int32_t c) {
+    return (mask[c >> 5] >> (c & 31)) & 1u;
+}
+
+__global__ __launch_bounds__(256) void slice_count_kernel(const int32_t *__restrict__ col, int64_t nnz,
+                                                          const uint32_t *__restrict__ mask,
+                                                          uint32_t *__restrict__ tile_cnt) {
+    __shared__ uint32_t s[4];
+    const int64_t ts = (int64_t)blockIdx.x * kTile;
+    uint32_t c = 0;
+    for (int j = 0; j < kPer; ++j) {
+        const int64_t t = ts + threadIdx.x + 256 * j;
+        if (t < nnz) c += kept(mask, __builtin_nontemporal_load(col + t));
+    }
+    for (int off = 32; off > 0; off >>= 1) c += __shfl_down(c, off);
+    if ((threadIdx.x & 63) == 0) s[threadIdx.x >> 6] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) tile_cnt[blockIdx.x] = s[0] + s[1] + s[2] + s[3];
+}
+
+__global__ __launch_bounds__(1024) void slice_scan_kernel(int32_t nt, const uint32_t *__restrict__ tile_cnt,
+                                                          uint32_t *__restrict__ tile_off,
+                                                          int64_t *__restrict__ nnz_out) {
+    __shared__ int64_t sh[1024];
+    const int t = threadIdx.x;
+    const int32_t per = (nt + 1023) / 1024;
+    const int32_t lo = min(nt, t * per), hi = min(nt, lo + per);
+    int64_t s = 0;
+    for (int32_t i = lo; i < hi; ++i) s += tile_cnt[i];
+    sh[t] = s;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+        const int64_t x = t >= off ? sh[t - off] : 0;
+        __syncthreads();
+        sh[t] += x;
+        __syncthreads();
+    }
+    int64_t run = sh[t] - s;
+    for (int32_t i = lo; i < hi; ++i) {
+        tile_off[i] = (uint32_t)run;
+        run += tile_cnt[i];
+    }
+    if (t == 1023) *nnz_out = sh[1023];
+}
+
+// First index i in [0, n] with rowptr[i] >= x (rowptr has n + 1 entries).
+__device__ int32_t lower_bound_rowptr(const int32_t *__restrict__ rowptr, int32_t n, int64_t x) {
+    int32_t lo = 0, hi = n + 1;
+    while (lo < hi) {
+        const int32_t mid = lo + (hi - lo) / 2;
+        if (rowptr[mid] < x) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restrict__ rowptr, int32_t n_rows,
+                                                         const int32_t *__restrict__ col,
+                                                         const float *__restrict__ val, int64_t nnz,
+                                                         const uint32_t *__restrict__ mask,
+                                                         const uint32_t *__restrict__ tile_off,
+                                                         int32_t *__restrict__ rowptr_out,
+                                                         int32_t *__restrict__ col_out,
+                                                         float *__restrict__ val_out, int64_t capacity) {
+    __shared__ int32_t s_col[kTile];
+    __shared__ float s_val[kTile];
+    __shared__ uint32_t s_pre[256];   // kept entries before each thread's run
+    __shared__ uint32_t s_bits[256];  // kept flags of each thread's run
+    __shared__ int32_t s_rows[2];
+    const int t = threadIdx.x;
+    const int64_t ts = (int64_t)blockIdx.x * kTile;
+    const int64_t te = min<int64_t>(ts + kTile, nnz);
+    const bool last = blockIdx.x == gridDim.x - 1;
+    if (t == 0) s_rows[0] = lower_bound_rowptr(rowptr, n_rows, ts);
+    if (t == 1) s_rows[1] = last ? n_rows + 1 : lower_bound_rowptr(rowptr, n_rows, te);
+    for (int j = 0; j < kPer; ++j) {  // coalesced staging
+        const int64_t p = ts + t + 256 * j;
+        if (p < te) {
+            s_col[t + 256 * j] = __builtin_nontemporal_load(col + p);
+            s_val[t + 256 * j] = __builtin_nontemporal_load(val + p);
+        }
+    }
+    __syncthreads();
+    uint32_t bits = 0;
+    for (int j = 0; j < kPer; ++j) {
+        const int64_t p = ts + kPer * t + j;
+        if (p < te && kept(mask, s_col[kPer * t + j])) bits |= 1u << j;
+    }
+    const uint32_t cnt = __popc(bits);
+    s_bits[t] = bits;
+    s_pre[t] = cnt;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {  // inclusive scan of the run counts
+        const uint32_t x = t >= off ? s_pre[t - off] : 0;
+        __syncthreads();
+        s_pre[t] += x;
+        __syncthreads();
+    }
+    const uint32_t excl = s_pre[t] - cnt;
+    __syncthreads();
+    s_pre[t] = excl;
+    __syncthreads();
+    const int64_t base = (int64_t)tile_off[blockIdx.x];
+    int64_t pos = base + excl;
+    for (int j = 0; j < kPer; ++j) {
+        if ((bits >> j) & 1u) {
+            if (pos < capacity) {
+                col_out[pos] = s_col[kPer * t + j];
+                val_out[pos] = s_val[kPer * t + j];
+            }
+            ++pos;
+        }
+    }
+    // Rowptr'[i] for the rows whose Rowptr[i] lies in [ts, te) (and, in the
+    // last tile, also those equal to nnz).
+    const int32_t r0 = s_rows[0], r1 = s_rows[1];
+    for (int32_t i = r0 + t; i < r1; i += 256) {
+        const int64_t off = (int64_t)rowptr[i] - ts;
+        uint32_t c;
+        if (off >= kTile || ts + off >= te) {
+            c = s_pre[255] + __popc(s_bits[255]);
+        } else {
+            const int th = (int)(off / kPer), o = (int)(off % kPer);
+            c = s_pre[th] + __popc(s_bits[th] & ((1u << o) - 1u));
+        }
+        rowptr_out[i] = (int32_t)(base + c);
+    }
+}
+
+__global__ __launch_bounds__(256) void zero_rows_kernel(int32_t *__restrict__ p, int64_t count,
+                                                        int64_t *__restrict__ nnz_out) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *nnz_out = 0;
+}
+
+}  // namespace
+
+size_t slice_ws_bytes(int64_t nnz) {
+    const size_t nt = (size_t)ceil_div(std::max<int64_t>(nnz, 1), kTile);
+    return 2 * align_up(nt * sizeof(uint32_t), 256);
+}
+
+hipError_t slice_launch(int32_t n_rows, int64_t nnz, const int32_t *rowptr, const int32_t *col,
+                        const float *val, const uint32_t *mask, int32_t *rowptr_out,
+                        int32_t *col_out, float *val_out, int64_t capacity, int64_t *nnz_out,
+                        void *ws, hipStream_t stream) {
+    if (nnz == 0) {
+        zero_rows_kernel<<<(unsigned)std::min<int64_t>(ceil_div((int64_t)n_rows + 1, 256), 1024), 256, 0,
+                           stream>>>(rowptr_out, (int64_t)n_rows + 1, nnz_out);
+        return hipGetLastError();
+    }
+    const int32_t nt = (int32_t)ceil_div(nnz, kTile);
+    const size_t tb = align_up((size_t)nt * sizeof(uint32_t), 256);
+    uint32_t *tile_cnt = static_cast<uint32_t *>(ws);
+    uint32_t *tile_off = reinterpret_cast<uint32_t *>(static_cast<char *>(ws) + tb);
+    slice_count_kernel<<<nt, 256, 0, stream>>>(col, nnz, mask, tile_cnt);
+    slice_scan_kernel<<<1, 1024, 0, stream>>>(nt, tile_cnt, tile_off, nnz_out);
+    slice_emit_kernel<<<nt, 256, 0, stream>>>(rowptr, n_rows, col, val, nnz, mask, tile_off, rowptr_out,
+                                              col_out, val_out, capacity);
+    return hipGetLastError();
+}
+
+}  // namespace rsc

@@ -1,0 +1,272 @@
+// Top-k selection (section 2.2.1): the k largest uint64 keys, ties broken by
+// the lower index, returned as ascending indices and an n-bit mask.
+//
+// 1. Radix select of the threshold T = the k-th largest key, most significant
+//    digit first: 6 passes of 11/11/11/11/10/10 bits. Each pass builds a
+//    grid-wide histogram of the digit over the keys that match the prefix
+//    chosen so far (LDS histograms, then integer atomics into global bins),
+//    and a one-block kernel picks the digit that holds the k-th key. After
+//    the last pass T is known, and r = the number of keys equal to T that
+//    must be kept (G = k - r keys are strictly above T).
+// 2. Tiles of 4096 keys count (== T) and (> T); one block scans the tile
+//    counts; a third kernel keeps key i iff key > T, or key == T and fewer
+//    than r equal keys precede it, writing mask words from wave ballots and
+//    idx at the running count of kept keys. Everything is integer, so the
+//    result is exact and deterministic.
+#include "rsc_internal.h"
+
+namespace rsc {
+namespace {
+
+constexpr int kBins = 2048;
+constexpr int kTile = 4096;     // keys per tile: 4 waves x 16 groups of 64
+constexpr int kPasses = 6;
+__constant__ const int kShift[kPasses] = {53, 42, 31, 20, 10, 0};
+__constant__ const int kWidth[kPasses] = {11, 11, 11, 11, 10, 10};
+
+struct TopkState {
+    uint64_t prefix;  // digits of T fixed so far
+    uint64_t pmask;   // which bits of prefix are fixed
+    int64_t k_rem;    // how many keys among those matching prefix remain to be taken
+    int64_t pad[29];
+};
+
+struct TopkWs {
+    TopkState st;
+    uint32_t hist[2][kBins];
+};
+
+__global__ __launch_bounds__(256) void topk_init_kernel(TopkState *st, uint32_t *hist0, int64_t k) {
+    for (int b = threadIdx.x; b < kBins; b += blockDim.x) hist0[b] = 0;
+    if (threadIdx.x == 0) {
+        st->prefix = 0;
+        st->pmask = 0;
+        st->k_rem = k;
+    }
+}
+
+__global__ __launch_bounds__(256) void topk_hist_kernel(const uint64_t *__restrict__ key, int32_t n,
+                                                        const TopkState *__restrict__ st,
+                                                        uint32_t *__restrict__ hist, int pass) {
+    __shared__ uint32_t lh[kBins];
+    const int shift = kShift[pass];
+    const uint64_t dmask = (1ull << kWidth[pass]) - 1ull;
+    for (int b = threadIdx.x; b < kBins; b += blockDim.x) lh[b] = 0;
+    __syncthreads();
+    const uint64_t prefix = st->prefix, pmask = st->pmask;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const uint64_t k = key[i];
+        if ((k & pmask) == prefix) atomicAdd(&lh[(k >> shift) & dmask], 1u);
+    }
+    __syncthreads();
+    for (int b = threadIdx.x; b < (1 << kWidth[pass]); b += blockDim.x)
+        if (lh[b]) atomicAdd(&hist[b], lh[b]);
+}
+
+// One block of 256 threads. Thread t owns the bins nb-1-t*per .. nb-per-t*per
+// (descending); an exclusive scan over threads gives the count of keys in
+// higher bins.
+__global__ __launch_bounds__(256) void topk_pick_kernel(TopkState *st, const uint32_t *__restrict__ hist,
+                                                        uint32_t *__restrict__ hist_next, int pass) {
+    __shared__ int64_t part[256];
+    const int t = threadIdx.x;
+    // read before any thread updates the state (the scan's barriers order it)
+    const int64_t k_rem = st->k_rem;
+    const int shift = kShift[pass];
+    const int nb = 1 << kWidth[pass];
+    const int per = nb / 256;
+    int64_t s = 0;
+    for (int j = 0; j < per; ++j) s += hist[nb - 1 - (t * per + j)];
+    part[t] = s;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {  // inclusive Hillis-Steele scan
+        const int64_t v = t >= off ? part[t - off] : 0;
+        __syncthreads();
+        part[t] += v;
+        __syncthreads();
+    }
+    int64_t run = part[t] - s;  // keys in bins above this thread's range
+    for (int j = 0; j < per; ++j) {
+        const int b = nb - 1 - (t * per + j);
+        const int64_t c = hist[b];
+        if (run < k_rem && run + c >= k_rem) {  // exactly one (thread, bin) satisfies this
+            st->prefix |= (uint64_t)b << shift;
+            st->pmask |= (uint64_t)(nb - 1) << shift;
+            st->k_rem = k_rem - run;
+        }
+        run += c;
+    }
+    for (int b = t; b < kBins; b += 256) hist_next[b] = 0;
+}
+
+__global__ __launch_bounds__(256) void topk_tile_count_kernel(const uint64_t *__restrict__ key,
+                                                              int32_t n,
+                                                              const TopkState *__restrict__ st,
+                                                              uint32_t *__restrict__ tile_eq,
+                                                              uint32_t *__restrict__ tile_gt) {
+    __shared__ uint32_t s_eq[4], s_gt[4];
+    const uint64_t T = st->prefix;
+    const int64_t ts = (int64_t)blockIdx.x * kTile;
+    uint32_t eq = 0, gt = 0;
+    for (int j = 0; j < kTile / 256; ++j) {
+        const int64_t i = ts + threadIdx.x + 256 * j;
+        if (i < n) {
+            const uint64_t k = key[i];
+            eq += k == T;
+            gt += k > T;
+        }
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        eq += __shfl_down(eq, off);
+        gt += __shfl_down(gt, off);
+    }
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    if (lane == 0) { s_eq[w] = eq; s_gt[w] = gt; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        tile_eq[blockIdx.x] = s_eq[0] + s_eq[1] + s_eq[2] + s_eq[3];
+        tile_gt[blockIdx.x] = s_gt[0] + s_gt[1] + s_gt[2] + s_gt[3];
+    }
+}
+
+// Block-wide exclusive scan helper (1024 threads, values int64).
+__device__ int64_t block_exclusive_scan_1024(int64_t v, int64_t *sh, int64_t *total) {
+    const int t = threadIdx.x;
+    sh[t] = v;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+        const int64_t x = t >= off ? sh[t - off] : 0;
+        __syncthreads();
+        sh[t] += x;
+        __syncthreads();
+    }
+    const int64_t incl = sh[t];
+    *total = sh[1023];
+    __syncthreads();
+    return incl - v;
+}
+
+// One block of 1024 threads; thread t owns a contiguous range of tiles.
+__global__ __launch_bounds__(1024) void topk_tile_scan_kernel(int32_t nt, const TopkState *__restrict__ st,
+                                                              const uint32_t *__restrict__ tile_eq,
+                                                              const uint32_t *__restrict__ tile_gt,
+                                                              uint32_t *__restrict__ eq_before,
+                                                              uint32_t *__restrict__ sel_before) {
+    __shared__ int64_t sh[1024];
+    const int t = threadIdx.x;
+    const int32_t per = (nt + 1023) / 1024;
+    const int32_t lo = min(nt, t * per), hi = min(nt, lo + per);
+    const int64_t r = st->k_rem;
+    int64_t tot;
+    int64_t s = 0;
+    for (int32_t i = lo; i < hi; ++i) s += tile_eq[i];
+    int64_t run = block_exclusive_scan_1024(s, sh, &tot);
+    int64_t sel_local = 0;
+    for (int32_t i = lo; i < hi; ++i) {
+        eq_before[i] = (uint32_t)run;
+        const int64_t take = min<int64_t>(max<int64_t>(r - run, 0), tile_eq[i]);
+        sel_local += tile_gt[i] + take;
+        run += tile_eq[i];
+    }
+    int64_t srun = block_exclusive_scan_1024(sel_local, sh, &tot);
+    for (int32_t i = lo; i < hi; ++i) {
+        sel_before[i] = (uint32_t)srun;
+        const int64_t eb = eq_before[i];
+        const int64_t take = min<int64_t>(max<int64_t>(r - eb, 0), tile_eq[i]);
+        srun += tile_gt[i] + take;
+    }
+}
+
+__global__ __launch_bounds__(256) void topk_emit_kernel(const uint64_t *__restrict__ key, int32_t n,
+                                                        const TopkState *__restrict__ st,
+                                                        const uint32_t *__restrict__ eq_before,
+                                                        const uint32_t *__restrict__ sel_before,
+                                                        int32_t *__restrict__ idx,
+                                                        uint32_t *__restrict__ mask, int32_t k) {
+    __shared__ uint32_t s_eq[4], s_gt[4];
+    const uint64_t T = st->prefix;
+    const int64_t r = st->k_rem;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const uint64_t lt_mask = (1ull << lane) - 1ull;
+    const int64_t wbase = (int64_t)blockIdx.x * kTile + (int64_t)w * (kTile / 4);
+    const int64_t nwords = ((int64_t)n + 31) / 32;
+    uint32_t eq = 0, gt = 0;
+    for (int g = 0; g < kTile / 4 / 64; ++g) {
+        const int64_t i = wbase + 64 * g + lane;
+        const bool in = i < n;
+        const uint64_t kv = in ? key[i] : 0ull;
+        eq += __popcll(__ballot(in && kv == T));
+        gt += __popcll(__ballot(in && kv > T));
+    }
+    if (lane == 0) { s_eq[w] = eq; s_gt[w] = gt; }
+    __syncthreads();
+    int64_t eq_base = eq_before[blockIdx.x], sel_base = sel_before[blockIdx.x];
+    for (int v = 0; v < w; ++v) {
+        const int64_t take = min<int64_t>(max<int64_t>(r - eq_base, 0), s_eq[v]);
+        sel_base += s_gt[v] + take;
+        eq_base += s_eq[v];
+    }
+    for (int g = 0; g < kTile / 4 / 64; ++g) {
+        const int64_t base = wbase + 64 * g;
+        const int64_t i = base + lane;
+        const bool in = i < n;
+        const uint64_t kv = in ? key[i] : 0ull;
+        const bool is_eq = in && kv == T;
+        const uint64_t eqbal = __ballot(is_eq);
+        const bool sel = (in && kv > T) || (is_eq && eq_base + __popcll(eqbal & lt_mask) < r);
+        const uint64_t selbal = __ballot(sel);
+        const int64_t pos = sel_base + __popcll(selbal & lt_mask);
+        if (sel && pos < k) idx[pos] = (int32_t)i;
+        const int64_t word = base / 32;
+        if (lane == 0 && word < nwords) mask[word] = (uint32_t)selbal;
+        if (lane == 32 && word + 1 < nwords) mask[word + 1] = (uint32_t)(selbal >> 32);
+        eq_base += __popcll(eqbal);
+        sel_base += __popcll(selbal);
+    }
+}
+
+__global__ __launch_bounds__(256) void fill_u32_kernel(uint32_t *p, int64_t count, uint32_t v) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+}  // namespace
+
+size_t topk_ws_bytes(int32_t n) {
+    const size_t nt = (size_t)ceil_div(std::max<int32_t>(n, 1), kTile);
+    return align_up(sizeof(TopkWs), 256) + 4 * align_up(nt * sizeof(uint32_t), 256);
+}
+
+hipError_t topk_launch(const uint64_t *key, int32_t n, int32_t k, int32_t *idx, uint32_t *mask,
+                       void *ws, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const int64_t nwords = ceil_div(n, 32);
+    if (k == 0) {
+        fill_u32_kernel<<<(unsigned)std::min<int64_t>(ceil_div(nwords, 256), 1024), 256, 0, stream>>>(
+            mask, nwords, 0u);
+        return hipGetLastError();
+    }
+    TopkWs *h = static_cast<TopkWs *>(ws);
+    const int32_t nt = (int32_t)ceil_div(n, kTile);
+    char *p = static_cast<char *>(ws) + align_up(sizeof(TopkWs), 256);
+    const size_t tb = align_up((size_t)nt * sizeof(uint32_t), 256);
+    uint32_t *tile_eq = reinterpret_cast<uint32_t *>(p);
+    uint32_t *tile_gt = reinterpret_cast<uint32_t *>(p + tb);
+    uint32_t *eq_before = reinterpret_cast<uint32_t *>(p + 2 * tb);
+    uint32_t *sel_before = reinterpret_cast<uint32_t *>(p + 3 * tb);
+
+    topk_init_kernel<<<1, 256, 0, stream>>>(&h->st, h->hist[0], k);
+    const unsigned hgrid = (unsigned)std::min<int64_t>(ceil_div(n, 256 * 8), 2048);
+    for (int pass = 0; pass < kPasses; ++pass) {
+        topk_hist_kernel<<<hgrid, 256, 0, stream>>>(key, n, &h->st, h->hist[pass & 1], pass);
+        topk_pick_kernel<<<1, 256, 0, stream>>>(&h->st, h->hist[pass & 1], h->hist[(pass + 1) & 1], pass);
+    }
+    topk_tile_count_kernel<<<nt, 256, 0, stream>>>(key, n, &h->st, tile_eq, tile_gt);
+    topk_tile_scan_kernel<<<1, 1024, 0, stream>>>(nt, &h->st, tile_eq, tile_gt, eq_before, sel_before);
+    topk_emit_kernel<<<nt, 256, 0, stream>>>(key, n, &h->st, eq_before, sel_before, idx, mask, k);
+    return hipGetLastError();
+}
+
+}  // namespace rsc

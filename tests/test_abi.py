@@ -1,0 +1,165 @@
+"""C-ABI checks that need no GPU: the library loads, exports exactly what
+include/rsc.h declares, rejects bad arguments with the documented status
+before touching the device, and its host-side budget helpers (the column
+budget and the greedy allocation) agree with the oracle."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2210_10737_amd as rsc
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rsc.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rsc_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_matches_exports():
+    declared = declared_functions()
+    assert declared == sorted(rsc.EXPORTED)
+    out = subprocess.run(["nm", "-D", "--defined-only", rsc.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = sorted(set(re.findall(r"\bT (rsc_[a-z0-9_]+)$", out, flags=re.M)))
+    assert exported == declared
+    L = rsc.lib()
+    for name in declared:
+        assert getattr(L, name) is not None
+    assert L.rsc_abi_version() == 1
+
+
+def test_status_strings():
+    L = rsc.lib()
+    for code, name in rsc.STATUS.items():
+        assert L.rsc_status_string(code).decode() == name
+
+
+def _csr(n_rows=4, n_cols=4, nnz=4, rowptr=0x1000, col=0x2000, val=0x3000):
+    return rsc.CsrStruct(n_rows, n_cols, nnz, rowptr, col, val)
+
+
+def _err(status):
+    return rsc.STATUS[status]
+
+
+def test_spmm_argument_validation():
+    L = rsc.lib()
+    A = _csr()
+    ws_need = L.rsc_spmm_workspace_bytes(ctypes.byref(A))
+    ws = 0x10000
+    good = dict(B=0x4000, d=8, ldb=8, Y=0x8000, ldy=8)
+
+    def call(A=A, B=good["B"], d=good["d"], ldb=good["ldb"], Y=good["Y"], ldy=good["ldy"], ws=ws,
+             wsb=ws_need):
+        return L.rsc_spmm(ctypes.byref(A) if A is not None else None, B, d, ldb, Y, ldy, ws, wsb, None)
+
+    assert _err(call(A=None)) == "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(call(d=0)) == "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(call(ldb=4)) == "RSC_ERR_INVALID_ARGUMENT"          # ld < d
+    assert _err(call(ldb=10)) == "RSC_ERR_UNSUPPORTED"              # ld % 4
+    assert _err(call(B=0x4004)) == "RSC_ERR_UNSUPPORTED"            # misaligned
+    assert _err(call(B=None)) == "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(call(A=_csr(nnz=1 << 31))) == "RSC_ERR_UNSUPPORTED"
+    assert _err(call(A=_csr(n_rows=-1))) == "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(call(A=_csr(col=None))) == "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(call(wsb=ws_need - 1)) == "RSC_ERR_CAPACITY"
+    assert _err(call(ws=0x10010)) == "RSC_ERR_UNSUPPORTED"           # ws alignment
+    assert "ld" in L.rsc_last_error().decode() or "aligned" in L.rsc_last_error().decode()
+
+
+def test_topk_and_slice_argument_validation():
+    L = rsc.lib()
+    n = 100
+    need = L.rsc_topk_workspace_bytes(n)
+    assert _err(L.rsc_topk_select(0x1000, n, -1, 0x2000, 0x3000, 0x4000, need, None)) == \
+        "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(L.rsc_topk_select(0x1000, n, n + 1, 0x2000, 0x3000, 0x4000, need, None)) == \
+        "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(L.rsc_topk_select(0x1000, n, 5, None, 0x3000, 0x4000, need, None)) == \
+        "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(L.rsc_topk_select(0x1000, n, 5, 0x2000, 0x3000, 0x4000, need - 1, None)) == \
+        "RSC_ERR_CAPACITY"
+    A = _csr()
+    sneed = L.rsc_slice_workspace_bytes(ctypes.byref(A))
+    assert _err(L.rsc_slice_csr(ctypes.byref(A), 0x1000, 0x2000, 0x3000, 0x4000, -1, 0x5000, 0x10000,
+                                sneed, None)) == "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(L.rsc_slice_csr(ctypes.byref(A), None, 0x2000, 0x3000, 0x4000, 4, 0x5000, 0x10000,
+                                sneed, None)) == "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(L.rsc_slice_csr(ctypes.byref(A), 0x1000, 0x2000, 0x3000, 0x4000, 4, 0x5004, 0x10000,
+                                sneed, None)) == "RSC_ERR_UNSUPPORTED"
+
+
+def test_cache_argument_validation():
+    L = rsc.lib()
+    out = ctypes.c_void_p()
+    A = _csr()
+    bad_t = _csr(n_rows=5)
+    assert _err(L.rsc_cache_create(ctypes.byref(A), ctypes.byref(bad_t), 10, None, ctypes.byref(out))) == \
+        "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(L.rsc_cache_create(ctypes.byref(A), ctypes.byref(A), 0, None, ctypes.byref(out))) == \
+        "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(L.rsc_cache_refresh(None, 0x1000, 4, 4, 1, 0, None)) == "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(L.rsc_spmm_sampled(None, 0x1000, 4, 4, 0x2000, 4, None)) == "RSC_ERR_INVALID_ARGUMENT"
+    assert L.rsc_cache_destroy(None) == 0
+
+
+@pytest.mark.skipif(os.environ.get("HIP_VISIBLE_DEVICES", None) is None and
+                    __import__("torch").cuda.is_available(), reason="a GPU is visible")
+def test_no_device_status():
+    L = rsc.lib()
+    A = _csr()
+    need = L.rsc_spmm_workspace_bytes(ctypes.byref(A))
+    st = L.rsc_spmm(ctypes.byref(A), 0x4000, 8, 8, 0x8000, 8, 0x10000, need, None)
+    assert _err(st) == "RSC_ERR_NO_DEVICE"
+
+
+def test_k_from_fraction_matches_oracle():
+    L = rsc.lib()
+    for n in (0, 1, 7, 4096, 232_965, 2_449_029, 132_534):
+        for num, den in ((0, 100), (10, 100), (30, 100), (50, 100), (1, 3), (100, 100)):
+            assert L.rsc_k_from_fraction(n, num, den) == oracle.k_from_fraction(n, num, den)
+    assert L.rsc_k_from_fraction(10, 1, 0) == -1
+    assert L.rsc_k_from_fraction(10, 3, 2) == -1
+
+
+def _keys_and_norms(A, ds, seed):
+    cn2, colnnz = oracle.col_sqnorms(A.rowptr, A.val)
+    keys, fb = [], []
+    for l, dl in enumerate(ds):
+        o = oracle.pair_keys(cn2, synth.dense_normal(A.n, dl, seed=seed + l))
+        keys.append(o["key"]); fb.append(float(o["rn2"].sum()))
+    return cn2, colnnz, keys, fb
+
+
+@pytest.mark.parametrize("C", [(1, 10), (3, 10), (1, 2), (0, 1), (1, 1)])
+def test_greedy_matches_oracle(C):
+    A = synth.make_graph("tiny", 0)
+    ds = [64, 16, 8]
+    cn2, colnnz, keys, fb = _keys_and_norms(A, ds, seed=20)
+    # ties and NaN keys in the third layer
+    keys[2] = keys[2].copy()
+    keys[2][::7] = keys[2][3]
+    keys[2][5::11] = 0
+    k_lib, b_lib = rsc.greedy_allocate(keys, colnnz, A.nnz, ds, cn2.sum(), fb, C, (2, 100))
+    k_orc, b_orc = oracle.greedy(keys, colnnz, A.nnz, ds, cn2.sum(), fb, C, (2, 100))
+    assert k_lib == k_orc and b_lib == b_orc
+
+
+def test_greedy_hand_example_through_abi():
+    import json
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "greedy_hand_example.json")))
+    import struct
+    keys = [np.array([struct.unpack("<Q", struct.pack("<d", float(s) ** 2))[0] + 1 for s in row],
+                     np.uint64) for row in g["scores"]]
+    k, bud = rsc.greedy_allocate(keys, g["colnnz"], g["nnz"], g["d"], g["fro_a2"], g["fro_b2"],
+                                 tuple(g["C"]), tuple(g["alpha"]))
+    assert k == g["expected_k"] and bud == g["expected_budget"]
