@@ -1,0 +1,282 @@
+"""Benchmark of the RSC aggregation hot path on one MI355X.
+
+One step = one pass of the whole hot path over the workload, in the order a
+GCN training step uses it (sections 3.1 and 3.3): the exact forward SpMM
+Y = A_hat H; the cache lookup, and every `refresh_interval` steps a cache
+refresh (pair scores of A_hat^T and the backward operand G, top-k at the
+column budget, CSR column slice); then the sampled backward SpMM
+G' = A_hat^T[:, S] G on the cached slice. H and G are resident in HBM before
+timing starts. The column budget k = floor(n * pct / 100) is computed once.
+
+Prints ONE JSON line. `value` is the step's algorithmic HBM bytes (exact +
+sampled SpMM compulsory traffic, plus one tenth of a refresh) divided by the
+measured step time, in GB/s. `roofline` describes the dominant kernel (the
+exact SpMM): algorithmic bytes per launch over its average duration measured
+with HIP events on the stream the kernels run on, against the 8 TB/s HBM
+peak. `cpu_baseline` times the oracle (all its OpenMP threads) on a bounded
+sample of the same step.
+
+usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload copurchase]
+                       [--budget-pct 30] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+COUNTERS = os.path.join(ROOT, "profiles", "spmm_copurchase_counters.json")
+
+
+def spmm_bytes(n: int, nnz: int, n_src: int, d: int) -> int:
+    """Compulsory HBM bytes of one SpMM launch: rowptr (4(n+1)), col + val
+    (8 per entry), each referenced B row once (4 d per source row), and Y
+    written once (4 n d)."""
+    return 4 * (n + 1) + 8 * nnz + 4 * n_src * d + 4 * n * d
+
+
+def refresh_bytes(n: int, nnz: int, nnz_kept: int, k: int, d: int) -> int:
+    """Algorithmic bytes of one cache refresh: B row norms (4nd) with cn2 in
+    (8n) and keys out (8n); six histogram passes and two tile passes over the
+    keys (8 * 8n); the slice's count pass over col (4 nnz) and compaction
+    pass over col + val (8 nnz), rowptr in/out (8(n+1)), kept entries out
+    (8 nnz'); idx and mask out (4k + n/8)."""
+    return (4 * n * d + 16 * n + 64 * n + 12 * nnz + 8 * (n + 1) + 8 * nnz_kept
+            + 4 * k + n // 8)
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    for f in ("spmm.hip", "rsc_internal.h"):
+        with open(os.path.join(ROOT, "paper_2210_10737_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(digest: str, launch_bytes: int):
+    """HBM traffic of the exact SpMM from the committed rocprofv3 counter
+    record, if it was taken on the current kernel source; else None."""
+    try:
+        rec = json.load(open(COUNTERS))
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_src_digest") != digest:
+        return None
+    return {"fetch_bytes": rec["fetch_bytes_per_launch"], "write_bytes": rec["write_bytes_per_launch"],
+            "total_bytes": rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"],
+            "over_algorithmic": (rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]) / launch_bytes,
+            "source": os.path.relpath(COUNTERS, ROOT)}
+
+
+def cpu_baseline(A, Hh, Gh, k, pct, refresh_interval, step_bytes_full, n_rows_sample):
+    """Oracle timing on a bounded sample: the refresh steps (pair keys, top-k,
+    slice) on the whole graph, and both SpMMs on the first n_rows_sample rows;
+    the step time is extrapolated linearly in rows."""
+    import numpy as np
+    import oracle
+    n = A.n
+    rows = np.arange(n_rows_sample, dtype=np.int32)
+    t0 = time.perf_counter()
+    oracle.spmm(A.rowptr, A.col, A.val, Hh, rows=rows)
+    t_exact = time.perf_counter() - t0
+    cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)
+    t0 = time.perf_counter()
+    key = oracle.pair_keys(cn2, Gh)["key"]
+    idx, mask = oracle.topk(key, k)
+    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+    t_refresh = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.spmm(ro, co, vo, Gh, rows=rows)
+    t_sampled = time.perf_counter() - t0
+    scale = n / n_rows_sample
+    step_s = (t_exact + t_sampled) * scale + t_refresh / refresh_interval
+    return {
+        "value": round(step_bytes_full / step_s / 1e9, 3),
+        "unit": "GB/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": (f"exact and sampled SpMM on rows [0, {n_rows_sample}) of {n} "
+                   f"(x{scale:.1f} to the full graph), one refresh (keys, top-k at {pct}%, slice) "
+                   f"on the whole graph amortised over {refresh_interval} steps"),
+        "ms_per_step": round(step_s * 1e3, 1),
+        "measured_s": round(t_exact + t_sampled + t_refresh, 2),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="copurchase")
+    ap.add_argument("--budget-pct", type=int, default=None)
+    ap.add_argument("--refresh", type=int, default=10)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=None,
+                    help="rows of the CPU-baseline SpMM sample (default: all rows)")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="after timing, copy a buffer of this many MiB once (a plain copy of known "
+                         "size, so hardware byte counters can be scaled)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2210_10737_amd as rsc
+    import synth
+
+    torch.cuda.set_device(0)
+    w = synth.WORKLOADS[args.workload]
+    pct = args.budget_pct if args.budget_pct is not None else w.budgets_pct[-1 if args.workload != "social" else 1]
+    d = w.d
+    t_gen = time.perf_counter()
+    A = synth.make_graph(args.workload, args.seed)
+    Hh = synth.dense_normal(A.n, d, seed=args.seed + 1)
+    Gh = synth.dense_normal(A.n, d, seed=args.seed + 3)
+    t_gen = time.perf_counter() - t_gen
+    n, nnz = A.n, A.nnz
+    print(f"[bench] {args.workload}: n={n} nnz={nnz} d={d} budget={pct}% (inputs {t_gen:.1f}s)",
+          file=sys.stderr, flush=True)
+
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n)     # A_hat is symmetric: A_hat^T = A_hat
+    H = torch.from_numpy(Hh).cuda()
+    G = torch.from_numpy(Gh).cuda()
+    Y = torch.empty((n, d), dtype=torch.float32, device="cuda")
+    Yb = torch.empty((n, d), dtype=torch.float32, device="cuda")
+    ws = torch.empty(rsc.spmm_workspace_bytes(X), dtype=torch.uint8, device="cuda")
+    k = rsc.k_from_fraction(n, pct, 100)
+    cache = rsc.Cache(X, X, refresh_interval=args.refresh)
+    torch.cuda.synchronize()
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    records = []   # (kind, start_event, end_event)
+
+    def step(s: int, timed: bool):
+        e0, e1 = ev(), ev()
+        e0.record()
+        rsc.spmm(X, H, out=Y, ws=ws)                     # forward, exact
+        e1.record()
+        if timed:
+            records.append(("exact", e0, e1))
+        if cache.get(s, with_slice=False)["needs_refresh"]:
+            r0, r1 = ev(), ev()
+            r0.record()
+            cache.refresh(G, k, step=s)
+            r1.record()
+            if timed:
+                records.append(("refresh", r0, r1))
+        s0, s1 = ev(), ev()
+        s0.record()
+        cache.spmm_sampled(G, out=Yb)                    # backward, sampled on the cached slice
+        s1.record()
+        if timed:
+            records.append(("sampled", s0, s1))
+
+    for s in range(args.warmup):
+        step(s, False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    g0, g1 = ev(), ev()
+    g0.record()
+    for s in range(args.warmup, args.warmup + args.steps):
+        step(s, True)
+    g1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = g0.elapsed_time(g1)
+
+    per = {"exact": [], "refresh": [], "sampled": []}
+    for kind, a, b in records:
+        per[kind].append(a.elapsed_time(b))
+    snap = cache.get(args.warmup + args.steps)
+    nnz_kept = int(snap["slice"].nnz)
+    idx = rsc.copy_to_host(snap["idx_ptr"], snap["k"], np.int32)
+    deg = np.diff(A.rowptr)
+    exact_ms = float(np.mean(per["exact"]))
+    sampled_ms = float(np.mean(per["sampled"]))
+    refresh_ms = float(np.mean(per["refresh"])) if per["refresh"] else None
+    ms_per_step = max(wall * 1e3, gpu_ms) / args.steps
+
+    b_exact = spmm_bytes(n, nnz, n, d)
+    b_sampled = spmm_bytes(n, nnz_kept, k, d)
+    b_refresh = refresh_bytes(n, nnz, nnz_kept, k, d)
+    step_bytes = b_exact + b_sampled + b_refresh / args.refresh
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
+    achieved = b_exact / (exact_ms * 1e-3) / 1e9
+    digest = kernel_source_digest()
+
+    out = {
+        "metric": "SpMM ms + achieved HBM GB/s (exact vs top-k sampled) on 1 MI355X; % of roofline",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "graph": w.description, "n": n, "nnz": nnz, "d": d,
+                   "budget_pct": pct, "k": k, "refresh_interval": args.refresh, "seed": args.seed},
+        "exact_spmm_ms": round(exact_ms, 4),
+        "sampled_spmm_ms": round(sampled_ms, 4),
+        "refresh_ms": None if refresh_ms is None else round(refresh_ms, 4),
+        "sampled_speedup": round(exact_ms / sampled_ms, 3),
+        "backward_amortised_ms": round(sampled_ms + (refresh_ms or 0.0) / args.refresh, 4),
+        "amortised_speedup": round(exact_ms / (sampled_ms + (refresh_ms or 0.0) / args.refresh), 3),
+        "nnz_kept": nnz_kept,
+        "kept_nnz_frac": round(nnz_kept / nnz, 4),
+        "mean_degree_selected": round(float(deg[idx].mean()), 2) if len(idx) else None,
+        "mean_degree_all": round(float(deg.mean()), 2),
+        "exact_logical_gather_GBs": round(4.0 * nnz * d / (exact_ms * 1e-3) / 1e9, 1),
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "spmm_kernel (exact SpMM)",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "algorithmic_bytes_per_launch": b_exact,
+            "avg_launch_ms": round(exact_ms, 4),
+            "traffic": load_traffic(digest, b_exact),
+            "kernel_src_digest": digest,
+        },
+    }
+    cache.close()
+    del X, H, G, Y, Yb, ws
+    torch.cuda.empty_cache()
+    if args.copy_probe_mib > 0:
+        src = torch.ones(args.copy_probe_mib << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_probe_bytes"] = src.numel() * 4
+        del src, dst
+    if not args.no_cpu_baseline:
+        rows = args.cpu_rows or n
+        print(f"[bench] gpu done ({ms_per_step:.3f} ms/step); timing the oracle on {rows} rows",
+              file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(A, Hh, Gh, k, pct, args.refresh, step_bytes, rows)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -53,6 +53,7 @@ def _load():
         lib.orc_k_from_fraction.restype = i32
         lib.orc_greedy.argtypes = [i32, i32, i64, vp, vp, vp, f64, vp, i32, i32, i32, i32, vp]
         lib.orc_greedy.restype = i64
+        lib.orc_num_threads.restype = i32
         _lib = lib
     return _lib
 
@@ -163,6 +164,10 @@ def greedy(keys, colnnz, nnz, d, fro_a2, fro_b2, C, alpha):
     bud = _load().orc_greedy(L, n, nnz, ctypes.cast(ptrs, ctypes.c_void_p), _p(colnnz), _p(d_arr),
                              float(fro_a2), _p(fb), C[0], C[1], alpha[0], alpha[1], _p(k_out))
     return [int(x) for x in k_out], int(bud)
+
+
+def num_threads() -> int:
+    return int(_load().orc_num_threads())
 
 
 class CachePolicy:

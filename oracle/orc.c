@@ -287,3 +287,7 @@ int64_t orc_greedy(int32_t L, int32_t n, int64_t nnz, const uint64_t *const *key
     free(order);
     return bud;
 }
+
+/* Threads the oracle's row loops use (OpenMP's current maximum). */
+#include <omp.h>
+int32_t orc_num_threads(void) { return (int32_t)omp_get_max_threads(); }

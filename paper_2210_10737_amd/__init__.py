@@ -233,17 +233,19 @@ class Cache:
         d = B.shape[1] if d is None else d
         _check(lib().rsc_cache_refresh(self._h, B.data_ptr(), d, _ld(B), k, step, _stream()))
 
-    def get(self, step: int):
-        """dict(slice=CsrStruct, idx_ptr, k, needs_refresh, version)."""
+    def get(self, step: int, with_slice: bool = True):
+        """dict(slice=CsrStruct or None, idx_ptr, k, needs_refresh, version).
+        Asking for the slice waits (once per refresh) for its nnz."""
         s = CsrStruct()
         idx = ctypes.c_void_p()
         k = ctypes.c_int32()
         nr = ctypes.c_int32()
         ver = ctypes.c_uint64()
-        _check(lib().rsc_cache_get(self._h, step, ctypes.byref(s), ctypes.byref(idx), ctypes.byref(k),
-                                   ctypes.byref(nr), ctypes.byref(ver)))
-        return {"slice": s, "idx_ptr": idx.value, "k": k.value, "needs_refresh": bool(nr.value),
-                "version": ver.value}
+        _check(lib().rsc_cache_get(self._h, step, ctypes.byref(s) if with_slice else None,
+                                   ctypes.byref(idx), ctypes.byref(k), ctypes.byref(nr),
+                                   ctypes.byref(ver)))
+        return {"slice": s if with_slice else None, "idx_ptr": idx.value, "k": k.value,
+                "needs_refresh": bool(nr.value), "version": ver.value}
 
     def spmm_sampled(self, B: torch.Tensor, d: int | None = None, out: torch.Tensor | None = None):
         d = B.shape[1] if d is None else d
