@@ -78,9 +78,12 @@ int32_t rsc_abi_version(void);
  *   Y: n_rows x d, leading dimension ldy; every row is written (empty rows
  *      get zeros).
  * Accumulation: fp32 over runs of at most 64 consecutive entries, folded
- * into fp64; one rounding to fp32 per output. Deterministic: the same
- * inputs give bitwise the same Y, and the result of an entry depends only on
- * its row's entries (so slicing with every column kept reproduces Y).
+ * into fp64; one rounding to fp32 per output. The features may be processed
+ * in several passes of 32/64 columns of B (chosen from n_rows, nnz, n_cols
+ * and d only, with the environment variable RSC_SPMM_SLICE = 16/32/64/128/256
+ * as an override); the pass layout sets the summation order. Deterministic:
+ * equal arguments give bitwise equal Y, and rsc_spmm_sampled with every
+ * column kept reproduces rsc_spmm bitwise.
  * ws / ws_bytes: scratch of at least rsc_spmm_workspace_bytes(A) bytes,
  * 256-byte aligned, private to this call until it completes on `stream`. */
 size_t rsc_spmm_workspace_bytes(const rsc_csr_t *A);

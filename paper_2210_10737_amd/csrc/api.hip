@@ -146,7 +146,8 @@ rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb
     RSC_TRY(check_dense(Y, A->n_rows, d, ldy, "Y"));
     RSC_TRY(check_ws(ws, ws_bytes, rsc::spmm_ws_bytes(A->n_rows, A->nnz), "spmm"));
     RSC_TRY(check_device());
-    RSC_HIP(rsc::spmm_launch(A->n_rows, A->nnz, A->rowptr, A->col, A->val, B, d, ldb, Y, ldy, ws, stream),
+    RSC_HIP(rsc::spmm_launch(A->n_rows, A->nnz, A->rowptr, A->col, A->val, B, d, ldb, Y, ldy, ws, stream,
+                             A->nnz, A->n_cols),
             "spmm launch");
     return RSC_OK;
 }
@@ -341,9 +342,13 @@ rsc_status_t rsc_spmm_sampled(rsc_cache_t *c, const float *B, int32_t d, int64_t
     if (c->version == 0) return fail(RSC_ERR_INVALID_ARGUMENT, "cache was never refreshed");
     RSC_TRY(check_dense(B, c->X.n_cols, d, ldb, "B"));
     RSC_TRY(check_dense(Y, c->X.n_rows, d, ldy, "Y"));
-    // nnz of the full operand bounds the slice's, which sizes the long-row list
+    // nnz of the full operand bounds the slice's and sizes the long-row list;
+    // the expected kept share k/n of the entries and the k kept source rows
+    // choose the feature slice (a function of the arguments only, so results
+    // never depend on which calls came before).
+    const int64_t nnz_hint = c->n > 0 ? c->X.nnz * (int64_t)c->k / c->n : 0;
     RSC_HIP(rsc::spmm_launch(c->X.n_rows, c->X.nnz, c->s_rowptr, c->s_col, c->s_val, B, d, ldb, Y, ldy,
-                             c->ws_spmm, stream),
+                             c->ws_spmm, stream, nnz_hint, c->k),
             "spmm_sampled launch");
     return RSC_OK;
 }

@@ -12,17 +12,23 @@ namespace rsc {
 constexpr int kWave = 64;
 
 // ---- SpMM --------------------------------------------------------------
-// Rows with more than kLongRow entries are processed by a whole 4-wave
+// Rows with more than kLongRow entries are processed by a whole 8-wave
 // block (waves take interleaved runs of 64 entries, then a fixed-order LDS
-// reduction); shorter rows by one wave.
+// reduction); shorter rows by one wave. Long rows are handed out to
+// persistent blocks through an atomic counter.
 constexpr int kLongRow = 1024;
-constexpr int kSpmmBlockWaves = 4;
-constexpr int kSpmmLongBlocks = 512;  // persistent blocks that walk the long-row list
+constexpr int kSpmmRowWaves = 4;      // rows (waves) per block of the row kernel
+constexpr int kSpmmLongWaves = 8;     // waves per block of the long-row kernel
+constexpr int kSpmmLongBlocks = 1024;  // persistent blocks that walk the long-row list
 
 size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz);
+// nnz_bound sizes the long-row list; nnz_hint (expected entries) and
+// n_src_hint (distinct B rows the entries reference) choose the feature slice.
+int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d);
 hipError_t spmm_launch(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr, const int32_t *col,
                        const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
-                       int64_t ldy, void *ws, hipStream_t stream);
+                       int64_t ldy, void *ws, hipStream_t stream, int64_t nnz_hint,
+                       int64_t n_src_hint);
 
 // ---- scores ------------------------------------------------------------
 hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,

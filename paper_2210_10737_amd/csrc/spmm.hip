@@ -17,6 +17,8 @@
 //     blocks: the waves take interleaved runs of 64 entries and their fp64
 //     sums are combined in LDS in fixed wave order. No float atomics, so the
 //     result is bitwise reproducible.
+#include <cstdlib>
+
 #include "rsc_internal.h"
 
 namespace rsc {
@@ -25,24 +27,48 @@ namespace {
 constexpr int kUnroll = 8;
 typedef float vf4 __attribute__((ext_vector_type(4)));
 
-__global__ void fill_i32_kernel(int32_t *p, int32_t v) { *p = v; }
+__global__ void zero_counters_kernel(int32_t *p) { p[0] = 0; p[1] = 0; }
+__global__ void zero_next_kernel(int32_t *p) { *p = 0; }
 
+// Appends every row longer than kLongRow to `list` (one atomic per wave).
 __global__ __launch_bounds__(256) void collect_long_rows_kernel(const int32_t *__restrict__ rowptr,
                                                                 int32_t n_rows, int32_t *count,
                                                                 int32_t *list) {
     const int32_t r = blockIdx.x * blockDim.x + threadIdx.x;
-    if (r < n_rows && rowptr[r + 1] - rowptr[r] > kLongRow) list[atomicAdd(count, 1)] = r;
+    const bool is_long = r < n_rows && rowptr[r + 1] - rowptr[r] > kLongRow;
+    const uint64_t bal = __ballot(is_long);
+    if (bal == 0) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    int32_t base = 0;
+    if (lane == __ffsll((unsigned long long)bal) - 1) base = atomicAdd(count, __popcll(bal));
+    base = __shfl(base, __ffsll((unsigned long long)bal) - 1);
+    if (is_long) list[base + __popcll(bal & ((1ull << lane) - 1ull))] = r;
 }
+
+// Lane layout: LPE lanes per gathered entry, G = 64 / LPE entries per load
+// instruction. Lane L belongs to entry-group g = L / LPE and owns features
+// 4 * (L % LPE) .. +3 of the current feature slice (plus +256 for NV = 2,
+// which is only used with LPE = 64).
+template <int LPE>
+struct Layout {
+    static constexpr int G = kWave / LPE;
+    static_assert(kWave % LPE == 0, "LPE must divide the wave");
+};
 
 // Accumulates runs of 64 entries starting at beg, beg + stride, ... (< end)
 // into acc. `act[q]` says whether this lane's q-th float4 lies inside d.
-template <int NV>
+// Within a run, entry-group g takes entries g, g + G, g + 2G, ...; the group
+// partials are combined by a butterfly over the groups (fixed order, every
+// lane ends with the same sum) before the run is folded into fp64.
+template <int LPE, int NV>
 __device__ __forceinline__ void accumulate_runs(const int32_t *__restrict__ col,
                                                 const float *__restrict__ val,
                                                 const float *__restrict__ B, int64_t ldb,
                                                 int32_t beg, int32_t end, int32_t stride,
                                                 const bool (&act)[NV], int lane,
                                                 double (&acc)[NV][4]) {
+    constexpr int G = Layout<LPE>::G;
+    const int g = lane / LPE, sl = lane % LPE;
     for (int32_t base = beg; base < end; base += stride) {
         const int32_t cnt = __builtin_amdgcn_readfirstlane(min(kWave, end - base));
         int32_t my_c = 0;
@@ -55,32 +81,67 @@ __device__ __forceinline__ void accumulate_runs(const int32_t *__restrict__ col,
 #pragma unroll
         for (int q = 0; q < NV; ++q) a[q][0] = a[q][1] = a[q][2] = a[q][3] = 0.f;
 
-        for (int32_t t = 0; t < cnt; t += kUnroll) {
-            float4 b[kUnroll][NV];
-            float v[kUnroll];
+        if constexpr (G == 1) {
+            // one entry per instruction: broadcast (col, val) into SGPRs
+            for (int32_t t = 0; t < cnt; t += kUnroll) {
+                float4 b[kUnroll][NV];
+                float v[kUnroll];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
+                for (int u = 0; u < kUnroll; ++u) {
 #pragma unroll
-                for (int q = 0; q < NV; ++q) b[u][q] = make_float4(0.f, 0.f, 0.f, 0.f);
-                v[u] = 0.f;
-                if (t + u < cnt) {  // wave-uniform
-                    const int32_t c = __builtin_amdgcn_readlane(my_c, t + u);
-                    v[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_v), t + u));
-                    const float4 *brow = reinterpret_cast<const float4 *>(B + (int64_t)c * ldb) + lane;
+                    for (int q = 0; q < NV; ++q) b[u][q] = make_float4(0.f, 0.f, 0.f, 0.f);
+                    v[u] = 0.f;
+                    if (t + u < cnt) {  // wave-uniform
+                        const int32_t c = __builtin_amdgcn_readlane(my_c, t + u);
+                        v[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_v), t + u));
+                        const float4 *brow = reinterpret_cast<const float4 *>(B + (int64_t)c * ldb) + lane;
 #pragma unroll
-                    for (int q = 0; q < NV; ++q)
-                        if (act[q]) b[u][q] = brow[q * kWave];
+                        for (int q = 0; q < NV; ++q)
+                            if (act[q]) b[u][q] = brow[q * kWave];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+                    for (int q = 0; q < NV; ++q) {
+                        a[q][0] = fmaf(v[u], b[u][q].x, a[q][0]);
+                        a[q][1] = fmaf(v[u], b[u][q].y, a[q][1]);
+                        a[q][2] = fmaf(v[u], b[u][q].z, a[q][2]);
+                        a[q][3] = fmaf(v[u], b[u][q].w, a[q][3]);
+                    }
+            }
+        } else {
+            static_assert(NV == 1, "sliced layouts hold one float4 per lane");
+            constexpr int kSteps = kWave / G;  // steps that cover the 64-entry run
+#pragma unroll
+            for (int t0 = 0; t0 < kSteps; t0 += kUnroll) {
+                if (t0 * G >= cnt) break;  // wave-uniform
+                float4 b[kUnroll];
+                float v[kUnroll];
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) {
+                    const int j = (t0 + u) * G + g;  // entry of this group within the run
+                    const int32_t c = __shfl(my_c, j & (kWave - 1));
+                    const float vv = __shfl(my_v, j & (kWave - 1));
+                    b[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+                    v[u] = 0.f;
+                    if (t0 + u < kSteps && j < cnt && act[0]) {
+                        b[u] = reinterpret_cast<const float4 *>(B + (int64_t)c * ldb)[sl];
+                        v[u] = vv;
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) {
+                    a[0][0] = fmaf(v[u], b[u].x, a[0][0]);
+                    a[0][1] = fmaf(v[u], b[u].y, a[0][1]);
+                    a[0][2] = fmaf(v[u], b[u].z, a[0][2]);
+                    a[0][3] = fmaf(v[u], b[u].w, a[0][3]);
                 }
             }
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
+            for (int m = LPE; m < kWave; m <<= 1)
 #pragma unroll
-                for (int q = 0; q < NV; ++q) {
-                    a[q][0] = fmaf(v[u], b[u][q].x, a[q][0]);
-                    a[q][1] = fmaf(v[u], b[u][q].y, a[q][1]);
-                    a[q][2] = fmaf(v[u], b[u][q].z, a[q][2]);
-                    a[q][3] = fmaf(v[u], b[u][q].w, a[q][3]);
-                }
+                for (int x = 0; x < 4; ++x) a[0][x] += __shfl_xor(a[0][x], m);
         }
 #pragma unroll
         for (int q = 0; q < NV; ++q)
@@ -89,9 +150,10 @@ __device__ __forceinline__ void accumulate_runs(const int32_t *__restrict__ col,
     }
 }
 
-template <int NV>
+template <int LPE, int NV>
 __device__ __forceinline__ void store_row(float *__restrict__ yrow, int32_t d, int lane,
                                           const double (&acc)[NV][4]) {
+    if (lane >= LPE) return;  // every entry-group holds the same sums; group 0 stores
 #pragma unroll
     for (int q = 0; q < NV; ++q) {
         const int32_t f = 4 * lane + 4 * kWave * q;
@@ -104,72 +166,87 @@ __device__ __forceinline__ void store_row(float *__restrict__ yrow, int32_t d, i
     }
 }
 
-// Blocks [0, n_long_blocks) walk the long-row list; the remaining blocks take
-// 4 consecutive rows each (one per wave) and skip long rows.
-template <int NV>
-__global__ __launch_bounds__(256) void spmm_kernel(const int32_t *__restrict__ rowptr,
-                                                   const int32_t *__restrict__ col,
-                                                   const float *__restrict__ val,
-                                                   const float *__restrict__ B, int64_t ldb,
-                                                   float *__restrict__ Y, int64_t ldy, int32_t n_rows,
-                                                   int32_t d, const int32_t *__restrict__ long_count,
-                                                   const int32_t *__restrict__ long_rows,
-                                                   int32_t n_long_blocks) {
+// Long rows: persistent blocks of kSpmmLongWaves waves take rows from the list
+// through an atomic counter; within a row the waves take interleaved runs of
+// 64 entries and their fp64 sums are added in LDS in fixed wave order.
+// B and Y point at the first feature of the current slice; d is its width.
+template <int LPE, int NV>
+__global__ __launch_bounds__(kSpmmLongWaves * 64) void spmm_long_kernel(
+    const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col, const float *__restrict__ val,
+    const float *__restrict__ B, int64_t ldb, float *__restrict__ Y, int64_t ldy, int32_t d,
+    const int32_t *__restrict__ long_count, int32_t *__restrict__ long_next,
+    const int32_t *__restrict__ long_rows) {
+    __shared__ double red[kSpmmLongWaves][NV * 4][kWave];
+    __shared__ int32_t s_job;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int sl = lane % LPE;
     bool act[NV];
 #pragma unroll
-    for (int q = 0; q < NV; ++q) act[q] = 4 * lane + 4 * kWave * q < d;
-
-    if ((int32_t)blockIdx.x < n_long_blocks) {
-        __shared__ double red[kSpmmBlockWaves][NV * 4][kWave];
-        const int32_t nl = __builtin_amdgcn_readfirstlane(*long_count);
-        for (int32_t j = blockIdx.x; j < nl; j += n_long_blocks) {
-            const int32_t r = __builtin_amdgcn_readfirstlane(long_rows[j]);
-            const int32_t s = __builtin_amdgcn_readfirstlane(rowptr[r]);
-            const int32_t e = __builtin_amdgcn_readfirstlane(rowptr[r + 1]);
-            double acc[NV][4];
+    for (int q = 0; q < NV; ++q) act[q] = 4 * sl + 4 * kWave * q < d;
+    const int32_t nl = __builtin_amdgcn_readfirstlane(*long_count);
+    for (;;) {
+        if (threadIdx.x == 0) s_job = atomicAdd(long_next, 1);
+        __syncthreads();
+        const int32_t j = __builtin_amdgcn_readfirstlane(s_job);
+        if (j >= nl) break;  // block-uniform: every wave read the same s_job
+        const int32_t r = __builtin_amdgcn_readfirstlane(long_rows[j]);
+        const int32_t s = __builtin_amdgcn_readfirstlane(rowptr[r]);
+        const int32_t e = __builtin_amdgcn_readfirstlane(rowptr[r + 1]);
+        double acc[NV][4];
 #pragma unroll
-            for (int q = 0; q < NV; ++q) acc[q][0] = acc[q][1] = acc[q][2] = acc[q][3] = 0.0;
-            accumulate_runs<NV>(col, val, B, ldb, s + kWave * wave, e, kWave * kSpmmBlockWaves, act,
-                                lane, acc);
+        for (int q = 0; q < NV; ++q) acc[q][0] = acc[q][1] = acc[q][2] = acc[q][3] = 0.0;
+        accumulate_runs<LPE, NV>(col, val, B, ldb, s + kWave * wave, e, kWave * kSpmmLongWaves, act,
+                                 lane, acc);
+#pragma unroll
+        for (int q = 0; q < NV; ++q)
+#pragma unroll
+            for (int x = 0; x < 4; ++x) red[wave][q * 4 + x][lane] = acc[q][x];
+        __syncthreads();
+        if (wave == 0) {
 #pragma unroll
             for (int q = 0; q < NV; ++q)
 #pragma unroll
-                for (int x = 0; x < 4; ++x) red[wave][q * 4 + x][lane] = acc[q][x];
-            __syncthreads();
-            if (wave == 0) {
-#pragma unroll
-                for (int q = 0; q < NV; ++q)
-#pragma unroll
-                    for (int x = 0; x < 4; ++x) {
-                        double t = red[0][q * 4 + x][lane];
-#pragma unroll
-                        for (int w = 1; w < kSpmmBlockWaves; ++w) t += red[w][q * 4 + x][lane];
-                        acc[q][x] = t;
-                    }
-                store_row<NV>(Y + (int64_t)r * ldy, d, lane, acc);
-            }
-            __syncthreads();
+                for (int x = 0; x < 4; ++x) {
+                    double t = red[0][q * 4 + x][lane];
+                    for (int w = 1; w < kSpmmLongWaves; ++w) t += red[w][q * 4 + x][lane];
+                    acc[q][x] = t;
+                }
+            store_row<LPE, NV>(Y + (int64_t)r * ldy, d, lane, acc);
         }
-        return;
+        __syncthreads();  // red and s_job are reused by the next row
     }
+}
 
-    const int32_t r = (blockIdx.x - n_long_blocks) * kSpmmBlockWaves + wave;
+// Short rows: one wave per row, kSpmmRowWaves consecutive rows per block;
+// rows longer than kLongRow are left to spmm_long_kernel when skip_long.
+template <int LPE, int NV>
+__global__ __launch_bounds__(kSpmmRowWaves * 64) void spmm_rows_kernel(
+    const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col, const float *__restrict__ val,
+    const float *__restrict__ B, int64_t ldb, float *__restrict__ Y, int64_t ldy, int32_t n_rows,
+    int32_t d, int32_t skip_long) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int sl = lane % LPE;
+    bool act[NV];
+#pragma unroll
+    for (int q = 0; q < NV; ++q) act[q] = 4 * sl + 4 * kWave * q < d;
+    const int32_t r = blockIdx.x * kSpmmRowWaves + wave;
     if (r >= n_rows) return;
     const int32_t s = __builtin_amdgcn_readfirstlane(rowptr[r]);
     const int32_t e = __builtin_amdgcn_readfirstlane(rowptr[r + 1]);
-    if (n_long_blocks > 0 && e - s > kLongRow) return;
+    if (skip_long && e - s > kLongRow) return;
     double acc[NV][4];
 #pragma unroll
     for (int q = 0; q < NV; ++q) acc[q][0] = acc[q][1] = acc[q][2] = acc[q][3] = 0.0;
-    accumulate_runs<NV>(col, val, B, ldb, s, e, kWave, act, lane, acc);
-    store_row<NV>(Y + (int64_t)r * ldy, d, lane, acc);
+    accumulate_runs<LPE, NV>(col, val, B, ldb, s, e, kWave, act, lane, acc);
+    store_row<LPE, NV>(Y + (int64_t)r * ldy, d, lane, acc);
 }
 
 struct SpmmWs {
-    int32_t long_count;
-    int32_t pad[63];
+    int32_t long_count;  // rows in the long-row list
+    int32_t long_next;   // next long row to hand out (one counter per feature pass)
+    int32_t pad[62];
 };
 
 inline int64_t long_rows_bound(int32_t n_rows, int64_t nnz) {
@@ -182,29 +259,64 @@ size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz) {
     return sizeof(SpmmWs) + align_up(sizeof(int32_t) * (size_t)std::max<int64_t>(1, long_rows_bound(n_rows, nnz)), 256);
 }
 
+int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) {
+    // Feature-slice width (floats) of one pass. Slices of 16/32/64/128 use
+    // 4/8/16/32 lanes per gathered entry; 256 (512 for d > 256) is one pass.
+    // Gathers are limited by the rate of L2-miss requests, so a narrower slice
+    // pays off when the slice of the referenced B rows comes close to L2 size
+    // and rows are long enough to amortise the extra passes over rowptr/col/val.
+    if (const char *env = getenv("RSC_SPMM_SLICE")) {
+        const int v = atoi(env);
+        if (v == 16 || v == 32 || v == 64 || v == 128) return v;
+        if (v == 256 || v == 512) return d > 256 ? 512 : 256;
+    }
+    const int32_t full = d > 256 ? 512 : 256;
+    if (d <= 32 || n_rows <= 0 || nnz < 128LL * n_rows) return full;
+    const double mib = 1024.0 * 1024.0;
+    const double ws32 = (double)n_src * 32 * 4 / mib, ws64 = 2 * ws32;
+    if (ws32 > 64.0) return full;
+    if (ws64 <= 20.0 && ws32 > 8.0) return 64;
+    return 32;
+}
+
 hipError_t spmm_launch(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr, const int32_t *col,
                        const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
-                       int64_t ldy, void *ws, hipStream_t stream) {
+                       int64_t ldy, void *ws, hipStream_t stream, int64_t nnz_hint,
+                       int64_t n_src_hint) {
     if (n_rows == 0) return hipSuccess;
     SpmmWs *h = static_cast<SpmmWs *>(ws);
     int32_t *list = reinterpret_cast<int32_t *>(h + 1);
     const int64_t lbound = long_rows_bound(n_rows, nnz_bound);
     const int32_t n_long_blocks = (int32_t)std::min<int64_t>(lbound, kSpmmLongBlocks);
     if (n_long_blocks > 0) {
-        fill_i32_kernel<<<1, 1, 0, stream>>>(&h->long_count, 0);
+        zero_counters_kernel<<<1, 1, 0, stream>>>(&h->long_count);
         collect_long_rows_kernel<<<(unsigned)ceil_div(n_rows, 256), 256, 0, stream>>>(
             rowptr, n_rows, &h->long_count, list);
     }
-    const unsigned grid = (unsigned)(n_long_blocks + ceil_div(n_rows, kSpmmBlockWaves));
-    // features are processed 512 at a time (two float4 per lane)
-    for (int32_t f0 = 0; f0 < d; f0 += 8 * kWave) {
-        const int32_t dl = std::min<int32_t>(d - f0, 8 * kWave);
-        if (dl <= 4 * kWave)
-            spmm_kernel<1><<<grid, 256, 0, stream>>>(rowptr, col, val, B + f0, ldb, Y + f0, ldy, n_rows,
-                                                     dl, &h->long_count, list, n_long_blocks);
-        else
-            spmm_kernel<2><<<grid, 256, 0, stream>>>(rowptr, col, val, B + f0, ldb, Y + f0, ldy, n_rows,
-                                                     dl, &h->long_count, list, n_long_blocks);
+    const unsigned grid = (unsigned)ceil_div(n_rows, kSpmmRowWaves);
+    const int32_t slice = spmm_slice_width(n_rows, nnz_hint, n_src_hint, d);
+    for (int32_t f0 = 0; f0 < d;) {
+        const int32_t dl = std::min<int32_t>(d - f0, slice);
+#define RSC_SPMM_LAUNCH(LPE_, NV_)                                                                     \
+    do {                                                                                               \
+        if (n_long_blocks > 0) {                                                                       \
+            if (f0 > 0) zero_next_kernel<<<1, 1, 0, stream>>>(&h->long_next);                          \
+            spmm_long_kernel<LPE_, NV_><<<n_long_blocks, kSpmmLongWaves * 64, 0, stream>>>(             \
+                rowptr, col, val, B + f0, ldb, Y + f0, ldy, dl, &h->long_count, &h->long_next, list);  \
+        }                                                                                              \
+        spmm_rows_kernel<LPE_, NV_><<<grid, kSpmmRowWaves * 64, 0, stream>>>(                          \
+            rowptr, col, val, B + f0, ldb, Y + f0, ldy, n_rows, dl, n_long_blocks > 0 ? 1 : 0);        \
+    } while (0)
+        switch (slice) {
+            case 16: RSC_SPMM_LAUNCH(4, 1); break;
+            case 32: RSC_SPMM_LAUNCH(8, 1); break;
+            case 64: RSC_SPMM_LAUNCH(16, 1); break;
+            case 128: RSC_SPMM_LAUNCH(32, 1); break;
+            default:
+                if (dl <= 4 * kWave) RSC_SPMM_LAUNCH(64, 1); else RSC_SPMM_LAUNCH(64, 2);
+        }
+#undef RSC_SPMM_LAUNCH
+        f0 += dl;
     }
     return hipGetLastError();
 }

@@ -83,6 +83,57 @@ def test_spmm_general(gen_graph, d):
     assert np.all(Yh[empty, :d] == 0.0)
 
 
+@pytest.fixture
+def slice_env(request):
+    """Forces the SpMM feature-slice width for one test (the library reads
+    RSC_SPMM_SLICE on every call)."""
+    import os
+    old = os.environ.get("RSC_SPMM_SLICE")
+    os.environ["RSC_SPMM_SLICE"] = str(request.param)
+    yield request.param
+    if old is None:
+        del os.environ["RSC_SPMM_SLICE"]
+    else:
+        os.environ["RSC_SPMM_SLICE"] = old
+
+
+@pytest.mark.parametrize("slice_env", [16, 32, 64, 128, 256], indirect=True)
+@pytest.mark.parametrize("d", [1, 5, 64, 100, 256, 300])
+def test_spmm_feature_slices(gen_graph, slice_env, d):
+    A = gen_graph
+    B, ld = padded(2500, d, seed=200 + d)
+    Yo, S = oracle.spmm(A.rowptr, A.col, A.val, B, d=d, with_mag=True)
+    Y = torch.full((A.n, ld), 7.0, device="cuda")
+    rsc.spmm(to_dev(A, 2500), dense_dev(B), d=d, out=Y)
+    Yh = Y.cpu().numpy()
+    assert rel_err(Yh[:, :d], Yo, S) <= TOL_EXACT
+    assert np.all(Yh[:, d:] == 7.0)
+
+
+@pytest.mark.parametrize("slice_env", [16, 32, 64, 128], indirect=True)
+def test_spmm_slices_identity_and_thresholds(slice_env):
+    lens = [5, 0, 1100, 64, 1, 1025, 300, 1023, 1024, 63, 65]
+    A = csr_with_lengths(lens, 1100, seed=4)
+    I = np.eye(1100, dtype=np.float32)
+    Y = rsc.spmm(to_dev(A, 1100), dense_dev(I)).cpu().numpy()
+    D = np.zeros((len(lens), 1100), np.float32)
+    for i in range(len(lens)):
+        s, e = A.rowptr[i], A.rowptr[i + 1]
+        D[i, A.col[s:e]] = A.val[s:e]
+    assert np.array_equal(Y, D)
+
+
+@pytest.mark.parametrize("slice_env", [16, 32, 64, 128], indirect=True)
+def test_sampled_full_budget_bitwise_per_slice(gen_graph, slice_env):
+    X = to_dev(gen_graph, 2500)
+    cache = rsc.Cache(X, to_dev(synth.transpose(gen_graph, 2500), gen_graph.n))
+    B = dense_dev(synth.dense_normal(2500, 256, seed=13))
+    cache.refresh(B, 2500, step=0)
+    assert np.array_equal(cache.spmm_sampled(B).cpu().numpy().view(np.uint32),
+                          rsc.spmm(X, B).cpu().numpy().view(np.uint32))
+    cache.close()
+
+
 def test_spmm_tiny_config():
     A = synth.make_graph("tiny", 0)
     B = synth.dense_normal(A.n, 64, seed=1)
