@@ -30,19 +30,48 @@ typedef float vf4 __attribute__((ext_vector_type(4)));
 __global__ void zero_counters_kernel(int32_t *p) { p[0] = 0; p[1] = 0; }
 __global__ void zero_next_kernel(int32_t *p) { *p = 0; }
 
-// Appends every row longer than kLongRow to `list` (one atomic per wave).
-__global__ __launch_bounds__(256) void collect_long_rows_kernel(const int32_t *__restrict__ rowptr,
-                                                                int32_t n_rows, int32_t *count,
-                                                                int32_t *list) {
-    const int32_t r = blockIdx.x * blockDim.x + threadIdx.x;
-    const bool is_long = r < n_rows && rowptr[r + 1] - rowptr[r] > kLongRow;
-    const uint64_t bal = __ballot(is_long);
-    if (bal == 0) return;
-    const int lane = threadIdx.x & (kWave - 1);
-    int32_t base = 0;
-    if (lane == __ffsll((unsigned long long)bal) - 1) base = atomicAdd(count, __popcll(bal));
-    base = __shfl(base, __ffsll((unsigned long long)bal) - 1);
-    if (is_long) list[base + __popcll(bal & ((1ull << lane) - 1ull))] = r;
+// Appends every row longer than kLongRow to `list`. Each thread checks
+// kCollectPerThread rows (coalesced rowptr reads); a block-wide scan gives
+// each long row its place, and one atomic per block reserves the block's
+// range, so the list costs a few hundred atomics rather than one per row.
+// The list order only decides which block takes which row.
+constexpr int kCollectThreads = 1024;
+constexpr int kCollectPerThread = 4;
+
+__global__ __launch_bounds__(kCollectThreads) void collect_long_rows_kernel(
+    const int32_t *__restrict__ rowptr, int32_t n_rows, int32_t *count, int32_t *list) {
+    __shared__ int32_t s_wave[kCollectThreads / 64];
+    __shared__ int32_t s_base;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int64_t base = (int64_t)blockIdx.x * kCollectThreads * kCollectPerThread;
+    bool is_long[kCollectPerThread];
+    int32_t mine = 0;
+#pragma unroll
+    for (int i = 0; i < kCollectPerThread; ++i) {
+        const int64_t r = base + t + (int64_t)kCollectThreads * i;
+        is_long[i] = r < n_rows && rowptr[r + 1] - rowptr[r] > kLongRow;
+        mine += is_long[i];
+    }
+    // exclusive scan of `mine` over the block: within the wave, then across waves
+    int32_t incl = mine;
+    for (int off = 1; off < 64; off <<= 1) {
+        const int32_t x = __shfl_up(incl, off);
+        if (lane >= off) incl += x;
+    }
+    if (lane == 63) s_wave[wave] = incl;
+    __syncthreads();
+    int32_t before = incl - mine, total = 0;
+    for (int w = 0; w < kCollectThreads / 64; ++w) {
+        before += w < wave ? s_wave[w] : 0;
+        total += s_wave[w];
+    }
+    if (total == 0) return;  // block-uniform
+    if (t == 0) s_base = atomicAdd(count, total);
+    __syncthreads();
+    int32_t pos = s_base + before;
+#pragma unroll
+    for (int i = 0; i < kCollectPerThread; ++i)
+        if (is_long[i]) list[pos++] = (int32_t)(base + t + (int64_t)kCollectThreads * i);
 }
 
 // Lane layout: LPE lanes per gathered entry, G = 64 / LPE entries per load
@@ -290,8 +319,8 @@ hipError_t spmm_launch(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr,
     const int32_t n_long_blocks = (int32_t)std::min<int64_t>(lbound, kSpmmLongBlocks);
     if (n_long_blocks > 0) {
         zero_counters_kernel<<<1, 1, 0, stream>>>(&h->long_count);
-        collect_long_rows_kernel<<<(unsigned)ceil_div(n_rows, 256), 256, 0, stream>>>(
-            rowptr, n_rows, &h->long_count, list);
+        collect_long_rows_kernel<<<(unsigned)ceil_div(n_rows, kCollectThreads * kCollectPerThread),
+                                   kCollectThreads, 0, stream>>>(rowptr, n_rows, &h->long_count, list);
     }
     const unsigned grid = (unsigned)ceil_div(n_rows, kSpmmRowWaves);
     const int32_t slice = spmm_slice_width(n_rows, nnz_hint, n_src_hint, d);
