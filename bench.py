@@ -18,6 +18,7 @@ sample of the same step.
 
 usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload copurchase]
                        [--budget-pct 30] [--no-cpu-baseline]
+       python bench.py --workload gcn2-train [--budget-pct 10]   (training-step comparison)
 """
 from __future__ import annotations
 
@@ -110,6 +111,73 @@ def cpu_baseline(A, Hh, Gh, k, pct, refresh_interval, step_bytes_full, n_rows_sa
     }
 
 
+def train_bench(args) -> int:
+    """Two-layer GCN training on the gcn2 workload (716,847 nodes, 300 input
+    features, hidden 512, 100 labels, multi-label BCE, Adam): exact training
+    against RSC training (exact forward, cached top-k backward, greedy
+    allocation and refresh every `refresh` steps, FLOPs budget C). Every
+    timed step includes forward, backward and the optimizer update; RSC steps
+    include the greedy and refreshes."""
+    import numpy as np
+    import torch
+
+    import paper_2210_10737_amd as rsc
+    import synth
+    from paper_2210_10737_amd.gcn import GCN, RscConfig
+
+    torch.cuda.set_device(0)
+    torch.backends.cuda.matmul.allow_tf32 = False
+    w = synth.WORKLOADS["gcn2"]
+    p = w.params
+    pct = args.budget_pct if args.budget_pct is not None else 10
+    A = synth.make_graph("gcn2", args.seed)
+    n = A.n
+    X = torch.from_numpy(synth.dense_normal(n, p["in_features"], seed=args.seed + 1)).cuda()
+    rng = np.random.Generator(np.random.PCG64(args.seed + 4))
+    Y = torch.from_numpy((rng.random((n, p["classes"]), dtype=np.float32) < 0.5).astype(np.float32)).cuda()
+    Ad = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n)
+    print(f"[bench] gcn2 training: n={n} nnz={A.nnz} hidden={p['hidden']} classes={p['classes']} "
+          f"C={pct}%", file=sys.stderr, flush=True)
+    results = {}
+    for name, enabled in (("exact", False), ("rsc", True)):
+        cfg = RscConfig(budget=(pct, 100), alpha=(2, 100), refresh_interval=args.refresh, enabled=enabled)
+        model = GCN(Ad, p["in_features"], p["hidden"], p["classes"], cfg, seed=args.seed + 2)
+        opt = torch.optim.Adam(model.parameters(), lr=0.01)
+        for s in range(args.warmup):
+            model.train_step(X, Y, opt, s)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        losses = []
+        for s in range(args.warmup, args.warmup + args.steps):
+            losses.append(model.train_step(X, Y, opt, s).detach())
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        hist = model.controller.history[args.warmup:]
+        greedy = [r.greedy_s * 1e3 for r in hist if r.mode == "score"]
+        results[name] = {"ms_per_step": round(ms, 3), "final_loss": round(float(losses[-1]), 5),
+                         "refresh_steps": sum(r.mode == "score" for r in hist),
+                         "greedy_ms_per_call": round(float(np.mean(greedy)), 2) if greedy else None,
+                         "k_per_layer": hist[-1].k}
+        model.close()
+        del model, opt
+        torch.cuda.empty_cache()
+    out = {
+        "metric": "GCN training step ms (exact vs RSC) on 1 MI355X",
+        "value": round(results["exact"]["ms_per_step"] / results["rsc"]["ms_per_step"], 3),
+        "unit": "x speedup (exact step / RSC step)",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": results["rsc"]["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "gcn2-train", "n": n, "nnz": A.nnz, "in_features": p["in_features"],
+                   "hidden": p["hidden"], "classes": p["classes"], "budget_pct": pct,
+                   "refresh_interval": args.refresh, "alpha_pct": 2, "seed": args.seed},
+        "exact": results["exact"], "rsc": results["rsc"],
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -130,6 +198,9 @@ def main() -> int:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         return 2
+
+    if args.workload == "gcn2-train":
+        return train_bench(args)
 
     import numpy as np
     import torch

@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define RSC_ABI_VERSION 1
+#define RSC_ABI_VERSION 2
 
 typedef enum {
     RSC_OK = 0,
@@ -106,11 +106,14 @@ rsc_status_t rsc_col_sqnorms(const rsc_csr_t *XT, double *cn2, int32_t *colnnz,
  *   key[i] = isnan(q) ? 0 : bits(q) + 1   (unsigned order == order of q,
  *            NaN last)
  *   score[i] = fl32(sqrt(q[i]))    (nullable output)
+ *   rn2 (nullable output, fp64[n]) receives rn2[i]; its sum is ||B||_F^2,
+ *   the normaliser of Eq. 4a.
  * q is the squared pair score ||X[:, i]||^2 ||B[i, :]||^2 without the
  * common normaliser, which changes no ranking. B is n x d with leading
  * dimension ldb. */
 rsc_status_t rsc_pair_scores(const double *cn2, const float *B, int32_t n, int32_t d,
-                             int64_t ldb, uint64_t *key, float *score, hipStream_t stream);
+                             int64_t ldb, uint64_t *key, float *score, double *rn2,
+                             hipStream_t stream);
 
 /* ---------------------------------------------------------------- A4 --- */
 /* Top-k selection (section 2.2.1): the k indices with the largest keys,
@@ -150,6 +153,13 @@ rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, int32_t *ro
  *     fixed across steps). X and XT must stay valid for the cache's life.
  *   rsc_cache_refresh: scores the pairs against B (n_cols x d, ldb), keeps
  *     the top k columns and slices X; records `step` as the refresh step.
+ *     It is rsc_cache_score followed by rsc_cache_select.
+ *   rsc_cache_score: only computes the pair keys and the rows' square-norms
+ *     against B into the cache (readable through rsc_cache_buffers), leaving
+ *     the current slice in place; used when k comes from the keys of several
+ *     operands, as in the layer-wise allocation of section 3.2.
+ *   rsc_cache_select: top k of the keys last scored, then the slice; records
+ *     `step` as the refresh step.
  *   rsc_cache_get (host only): returns the current slice (its nnz is read
  *     from the device once per refresh, waiting for the refresh if needed),
  *     the ascending kept indices, k, the slice version (0 = never
@@ -164,16 +174,20 @@ rsc_status_t rsc_cache_create(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t r
                               hipStream_t stream, rsc_cache_t **out);
 rsc_status_t rsc_cache_refresh(rsc_cache_t *cache, const float *B, int32_t d, int64_t ldb,
                                int32_t k, int64_t step, hipStream_t stream);
+rsc_status_t rsc_cache_score(rsc_cache_t *cache, const float *B, int32_t d, int64_t ldb,
+                             hipStream_t stream);
+rsc_status_t rsc_cache_select(rsc_cache_t *cache, int32_t k, int64_t step, hipStream_t stream);
 rsc_status_t rsc_cache_get(rsc_cache_t *cache, int64_t step, rsc_csr_t *slice_out,
                            const int32_t **idx_out, int32_t *k_out, int32_t *needs_refresh_out,
                            uint64_t *version_out);
 rsc_status_t rsc_spmm_sampled(rsc_cache_t *cache, const float *B, int32_t d, int64_t ldb,
                               float *Y, int64_t ldy, hipStream_t stream);
 /* Device arrays owned by the cache: cn2 (fp64) and colnnz (int32), n_cols
- * entries each; keys (uint64) and mask (ceil(n_cols/32) words) of the last
- * refresh. Any output pointer may be NULL. */
+ * entries each; keys (uint64) and row square-norms rn2 (fp64) of the last
+ * scored operand; mask (ceil(n_cols/32) words) of the last selection. Any
+ * output pointer may be NULL. */
 rsc_status_t rsc_cache_buffers(rsc_cache_t *cache, const double **cn2, const int32_t **colnnz,
-                               const uint64_t **key, const uint32_t **mask);
+                               const uint64_t **key, const double **rn2, const uint32_t **mask);
 /* Waits for outstanding cache work, then frees its buffers. NULL is a no-op. */
 rsc_status_t rsc_cache_destroy(rsc_cache_t *cache);
 
@@ -204,6 +218,35 @@ rsc_status_t rsc_greedy_allocate(int32_t L, int32_t n, int64_t nnz,
                                  int32_t C_num, int32_t C_den, int32_t alpha_num,
                                  int32_t alpha_den, int32_t *k_out_host,
                                  int64_t *budget_out_host);
+
+/* Device-assisted form of the same allocation, for large n. The greedy
+ * shrinks a layer by step = max(1, floor(n * alpha_num / alpha_den)) ranks
+ * at a time from the bottom of its ranking, so per layer it only needs the
+ * profile over blocks of `step` ranks counted from the lowest rank: block j
+ * covers ranks [max(0, n - (j+1) step), n - j step) of the ranking
+ * (key desc, index asc), and
+ *   mass[j]  = sum of sqrt(q) over the block in ascending rank order (fp64;
+ *              NaN keys count 0), q decoded from the key;
+ *   count[j] = sum of colnnz over the block.
+ * rsc_greedy_profile computes it on the device (stable radix sort of the
+ * keys); order (nullable, int32[n]) receives the ranking itself. mass and
+ * count hold rsc_greedy_blocks(n, alpha_num, alpha_den) entries. ws: at
+ * least rsc_greedy_profile_workspace_bytes(n) bytes, 256-byte aligned.
+ * rsc_greedy_allocate_profiles runs the greedy loop on the host from the
+ * layers' profiles (copied to the host); given the same keys it returns the
+ * same k_l and budget as rsc_greedy_allocate. */
+size_t rsc_greedy_profile_workspace_bytes(int32_t n);
+int32_t rsc_greedy_blocks(int32_t n, int32_t alpha_num, int32_t alpha_den);
+rsc_status_t rsc_greedy_profile(const uint64_t *key, const int32_t *colnnz, int32_t n,
+                                int32_t alpha_num, int32_t alpha_den, double *mass,
+                                int64_t *count, int32_t *order, void *ws, size_t ws_bytes,
+                                hipStream_t stream);
+rsc_status_t rsc_greedy_allocate_profiles(int32_t L, int32_t n, int64_t nnz, int32_t alpha_num,
+                                          int32_t alpha_den, const double *const *mass_host,
+                                          const int64_t *const *count_host, const int32_t *d_host,
+                                          double fro_a2, const double *fro_b2_host, int32_t C_num,
+                                          int32_t C_den, int32_t *k_out_host,
+                                          int64_t *budget_out_host);
 
 #ifdef __cplusplus
 }

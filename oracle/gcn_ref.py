@@ -1,0 +1,73 @@
+"""Reference RSC training step of a two-layer GCN, in fp64 (oracle).
+
+TEST INFRASTRUCTURE ONLY. It follows the paper's procedure directly:
+forward H1 = ReLU(A J1), J1 = X W1; logits P2 = A J2, J2 = H1 W2 (Eq. 1 and
+its SpMM/MatMul form, section 2.1); mean binary cross-entropy with logits;
+backward through each aggregation as grad J = A^T grad P exactly, or on the
+top-k column slice of A^T (section 2.2.1, section 3.1: only the backward is
+approximated); at a refresh step the backward is exact, both layers' pairs are
+scored (O4 keys of the fp32-rounded gradients), k_l comes from the greedy of
+section 3.2.1 (O8) and each layer's columns are selected (O5) and sliced (O6).
+Products are scipy sparse / numpy dense in fp64.
+"""
+from __future__ import annotations
+
+import numpy as np
+import scipy.sparse as sp
+
+from . import col_sqnorms, greedy, pair_keys, slice_csr, topk
+
+
+class RscReference:
+    def __init__(self, rowptr, col, val, n, widths, budget, alpha, refresh_interval):
+        self.n = n
+        self.A = sp.csr_matrix((val.astype(np.float64), col, rowptr), shape=(n, n))
+        self.AT = self.A.T.tocsr()
+        self.csr_t = (rowptr, col, val)  # A^T of a symmetric A is A itself
+        self.cn2, self.colnnz = col_sqnorms(rowptr, val)
+        self.fro_a2 = float(self.cn2.sum())
+        self.nnz = int(rowptr[-1])
+        self.widths = list(widths)
+        self.budget, self.alpha, self.R = budget, alpha, refresh_interval
+        self.last = None
+        self.k = [n] * len(widths)
+        self.idx = [None] * len(widths)
+        self.slices = [None] * len(widths)
+
+    def _backward_spmm(self, l, g, mode):
+        if mode == "sampled":
+            return self.slices[l] @ g
+        return self.AT @ g
+
+    def step(self, X, W1, W2, Y, step):
+        mode = "score" if (self.last is None or step - self.last >= self.R) else "sampled"
+        J1 = X @ W1
+        P1 = self.A @ J1
+        H1 = np.maximum(P1, 0.0)
+        J2 = H1 @ W2
+        P2 = self.A @ J2
+        loss = float(np.mean(np.maximum(P2, 0) - P2 * Y + np.log1p(np.exp(-np.abs(P2)))))
+        gP2 = (1.0 / (1.0 + np.exp(-P2)) - Y) / P2.size
+        gJ2 = self._backward_spmm(1, gP2, mode)
+        gW2 = H1.T @ gJ2
+        gP1 = (gJ2 @ W2.T) * (P1 > 0)
+        gJ1 = self._backward_spmm(0, gP1, mode)
+        gW1 = X.T @ gJ1
+        out = {"mode": mode, "loss": loss, "gW1": gW1, "gW2": gW2}
+        if mode == "score":
+            keys, fro_b2 = [], []
+            for g in (gP1, gP2):
+                o = pair_keys(self.cn2, g.astype(np.float32))
+                keys.append(o["key"])
+                fro_b2.append(float(o["rn2"].sum()))
+            self.k, _ = greedy(keys, self.colnnz, self.nnz, self.widths, self.fro_a2, fro_b2,
+                               self.budget, self.alpha)
+            rowptr, col, val = self.csr_t
+            for l in range(2):
+                self.idx[l], mask = topk(keys[l], self.k[l])
+                ro, co, vo = slice_csr(rowptr, col, val, mask)
+                self.slices[l] = sp.csr_matrix((vo.astype(np.float64), co, ro), shape=(self.n, self.n))
+            self.last = step
+        out["k"] = list(self.k)
+        out["idx"] = [None if i is None else i.copy() for i in self.idx]
+        return out

@@ -31,9 +31,12 @@ EXPORTED = [
     "rsc_col_sqnorms", "rsc_pair_scores",
     "rsc_topk_workspace_bytes", "rsc_topk_select",
     "rsc_slice_workspace_bytes", "rsc_slice_csr",
-    "rsc_cache_create", "rsc_cache_refresh", "rsc_cache_get", "rsc_spmm_sampled",
+    "rsc_cache_create", "rsc_cache_refresh", "rsc_cache_score", "rsc_cache_select",
+    "rsc_cache_get", "rsc_spmm_sampled",
     "rsc_cache_buffers", "rsc_cache_destroy",
     "rsc_k_from_fraction", "rsc_greedy_allocate",
+    "rsc_greedy_profile_workspace_bytes", "rsc_greedy_blocks", "rsc_greedy_profile",
+    "rsc_greedy_allocate_profiles",
 ]
 
 
@@ -68,22 +71,29 @@ def lib():
             "rsc_spmm_workspace_bytes": ([csrp], sz),
             "rsc_spmm": ([csrp, vp, i32, i64, vp, i64, vp, sz, vp], ctypes.c_int),
             "rsc_col_sqnorms": ([csrp, vp, vp, vp], ctypes.c_int),
-            "rsc_pair_scores": ([vp, vp, i32, i32, i64, vp, vp, vp], ctypes.c_int),
+            "rsc_pair_scores": ([vp, vp, i32, i32, i64, vp, vp, vp, vp], ctypes.c_int),
             "rsc_topk_workspace_bytes": ([i32], sz),
             "rsc_topk_select": ([vp, i32, i32, vp, vp, vp, sz, vp], ctypes.c_int),
             "rsc_slice_workspace_bytes": ([csrp], sz),
             "rsc_slice_csr": ([csrp, vp, vp, vp, vp, i64, vp, vp, sz, vp], ctypes.c_int),
             "rsc_cache_create": ([csrp, csrp, i32, vp, ctypes.POINTER(vp)], ctypes.c_int),
             "rsc_cache_refresh": ([vp, vp, i32, i64, i32, i64, vp], ctypes.c_int),
+            "rsc_cache_score": ([vp, vp, i32, i64, vp], ctypes.c_int),
+            "rsc_cache_select": ([vp, i32, i64, vp], ctypes.c_int),
             "rsc_cache_get": ([vp, i64, csrp, ctypes.POINTER(vp), ctypes.POINTER(i32),
                                ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_uint64)], ctypes.c_int),
             "rsc_spmm_sampled": ([vp, vp, i32, i64, vp, i64, vp], ctypes.c_int),
             "rsc_cache_buffers": ([vp, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
-                                   ctypes.POINTER(vp)], ctypes.c_int),
+                                   ctypes.POINTER(vp), ctypes.POINTER(vp)], ctypes.c_int),
             "rsc_cache_destroy": ([vp], ctypes.c_int),
             "rsc_k_from_fraction": ([i32, i32, i32], i32),
             "rsc_greedy_allocate": ([i32, i32, i64, vp, vp, vp, ctypes.c_double, vp, i32, i32, i32,
                                      i32, vp, vp], ctypes.c_int),
+            "rsc_greedy_profile_workspace_bytes": ([i32], sz),
+            "rsc_greedy_blocks": ([i32, i32, i32], i32),
+            "rsc_greedy_profile": ([vp, vp, i32, i32, i32, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+            "rsc_greedy_allocate_profiles": ([i32, i32, i64, i32, i32, vp, vp, vp, ctypes.c_double, vp,
+                                              i32, i32, vp, vp], ctypes.c_int),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
@@ -171,16 +181,20 @@ def col_sqnorms(XT: DeviceCsr):
     return cn2, colnnz
 
 
-def pair_scores(cn2: torch.Tensor, B: torch.Tensor, d: int | None = None, with_score: bool = False):
-    """Keys (uint64 bit patterns stored in an int64 tensor) and optionally
-    fp32 scores for the n = B.shape[0] column-row pairs."""
+def pair_scores(cn2: torch.Tensor, B: torch.Tensor, d: int | None = None, with_score: bool = False,
+                with_rn2: bool = False):
+    """Keys (uint64 bit patterns stored in an int64 tensor) for the
+    n = B.shape[0] column-row pairs; with_score / with_rn2 also return the
+    fp32 scores and the fp64 row square-norms."""
     n = B.shape[0]
     d = B.shape[1] if d is None else d
     key = torch.empty(n, dtype=torch.int64, device=B.device)
     score = torch.empty(n, dtype=torch.float32, device=B.device) if with_score else None
+    rn2 = torch.empty(n, dtype=torch.float64, device=B.device) if with_rn2 else None
     _check(lib().rsc_pair_scores(cn2.data_ptr(), B.data_ptr(), n, d, _ld(B), key.data_ptr(),
-                                 _ptr(score), _stream()))
-    return (key, score) if with_score else key
+                                 _ptr(score), _ptr(rn2), _stream()))
+    out = [key] + ([score] if with_score else []) + ([rn2] if with_rn2 else [])
+    return out[0] if len(out) == 1 else tuple(out)
 
 
 # ---------------------------------------------------------------- A4
@@ -233,6 +247,13 @@ class Cache:
         d = B.shape[1] if d is None else d
         _check(lib().rsc_cache_refresh(self._h, B.data_ptr(), d, _ld(B), k, step, _stream()))
 
+    def score(self, B: torch.Tensor, d: int | None = None) -> None:
+        d = B.shape[1] if d is None else d
+        _check(lib().rsc_cache_score(self._h, B.data_ptr(), d, _ld(B), _stream()))
+
+    def select(self, k: int, step: int) -> None:
+        _check(lib().rsc_cache_select(self._h, k, step, _stream()))
+
     def get(self, step: int, with_slice: bool = True):
         """dict(slice=CsrStruct or None, idx_ptr, k, needs_refresh, version).
         Asking for the slice waits (once per refresh) for its nnz."""
@@ -254,7 +275,8 @@ class Cache:
         return Y
 
     def buffers(self):
-        p = [ctypes.c_void_p() for _ in range(4)]
+        """Device pointers [cn2, colnnz, key, rn2, mask]."""
+        p = [ctypes.c_void_p() for _ in range(5)]
         _check(lib().rsc_cache_buffers(self._h, *[ctypes.byref(x) for x in p]))
         return [x.value for x in p]
 
@@ -331,4 +353,41 @@ def greedy_allocate(keys, colnnz, nnz: int, d, fro_a2: float, fro_b2, C, alpha):
     _check(lib().rsc_greedy_allocate(L, n, nnz, ctypes.cast(ptrs, ctypes.c_void_p), colnnz.ctypes.data,
                                      d_arr.ctypes.data, float(fro_a2), fb.ctypes.data, C[0], C[1],
                                      alpha[0], alpha[1], k_out.ctypes.data, ctypes.byref(bud)))
+    return [int(x) for x in k_out], int(bud.value)
+
+
+def greedy_profile(key: torch.Tensor, colnnz: torch.Tensor, alpha, with_order: bool = False,
+                   ws: torch.Tensor | None = None):
+    """Device profile of one layer's ranking for the greedy: (mass float64[nb],
+    count int64[nb]) and optionally the ranking int32[n]."""
+    n = key.numel()
+    nb = lib().rsc_greedy_blocks(n, alpha[0], alpha[1])
+    mass = torch.empty(max(nb, 1), dtype=torch.float64, device=key.device)
+    count = torch.empty(max(nb, 1), dtype=torch.int64, device=key.device)
+    order = torch.empty(max(n, 1), dtype=torch.int32, device=key.device) if with_order else None
+    need = lib().rsc_greedy_profile_workspace_bytes(n)
+    ws = _workspace(need, key.device) if ws is None else ws
+    _check(lib().rsc_greedy_profile(key.data_ptr(), colnnz.data_ptr(), n, alpha[0], alpha[1],
+                                    mass.data_ptr(), count.data_ptr(), _ptr(order), ws.data_ptr(),
+                                    ws.numel(), _stream()))
+    out = (mass[:nb], count[:nb])
+    return out + (order[:n],) if with_order else out
+
+
+def greedy_allocate_profiles(masses, counts, n: int, nnz: int, d, fro_a2: float, fro_b2, C, alpha):
+    """Greedy loop on host numpy profiles (one mass/count array per layer)."""
+    import numpy as np
+    L = len(masses)
+    masses = [np.ascontiguousarray(m, dtype=np.float64) for m in masses]
+    counts = [np.ascontiguousarray(c, dtype=np.int64) for c in counts]
+    mp = (ctypes.c_void_p * L)(*[m.ctypes.data for m in masses])
+    cp = (ctypes.c_void_p * L)(*[c.ctypes.data for c in counts])
+    d_arr = np.ascontiguousarray(d, dtype=np.int32)
+    fb = np.ascontiguousarray(fro_b2, dtype=np.float64)
+    k_out = np.zeros(L, dtype=np.int32)
+    bud = ctypes.c_int64()
+    _check(lib().rsc_greedy_allocate_profiles(L, n, nnz, alpha[0], alpha[1], ctypes.cast(mp, ctypes.c_void_p),
+                                              ctypes.cast(cp, ctypes.c_void_p), d_arr.ctypes.data,
+                                              float(fro_a2), fb.ctypes.data, C[0], C[1],
+                                              k_out.ctypes.data, ctypes.byref(bud)))
     return [int(x) for x in k_out], int(bud.value)

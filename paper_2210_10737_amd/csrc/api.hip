@@ -96,6 +96,7 @@ struct rsc_cache {
     double *cn2 = nullptr;
     int32_t *colnnz = nullptr;
     uint64_t *key = nullptr;
+    double *rn2 = nullptr;  // row square-norms of the last scored dense operand
     int32_t *idx = nullptr;
     uint32_t *mask = nullptr;
     int32_t *s_rowptr = nullptr;
@@ -165,13 +166,14 @@ rsc_status_t rsc_col_sqnorms(const rsc_csr_t *XT, double *cn2, int32_t *colnnz, 
 
 // ------------------------------------------------------------------- A3
 rsc_status_t rsc_pair_scores(const double *cn2, const float *B, int32_t n, int32_t d, int64_t ldb,
-                             uint64_t *key, float *score, hipStream_t stream) {
+                             uint64_t *key, float *score, double *rn2, hipStream_t stream) {
     if (n < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "n = %d < 0", n);
     RSC_TRY(check_dense(B, n, d, ldb, "B"));
     if (n > 0 && (!cn2 || !key)) return fail(RSC_ERR_INVALID_ARGUMENT, "cn2/key is NULL");
-    if (!aligned(cn2, 8) || !aligned(key, 8)) return fail(RSC_ERR_UNSUPPORTED, "cn2/key not 8-byte aligned");
+    if (!aligned(cn2, 8) || !aligned(key, 8) || !aligned(rn2, 8))
+        return fail(RSC_ERR_UNSUPPORTED, "cn2/key/rn2 not 8-byte aligned");
     RSC_TRY(check_device());
-    RSC_HIP(rsc::pair_scores_launch(cn2, B, n, d, ldb, key, score, stream), "pair_scores launch");
+    RSC_HIP(rsc::pair_scores_launch(cn2, B, n, d, ldb, key, score, rn2, stream), "pair_scores launch");
     return RSC_OK;
 }
 
@@ -226,7 +228,7 @@ rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, int32_t *ro
 // ------------------------------------------------------------------- A6 / A7
 static void cache_free(rsc_cache_t *c) {
     if (!c) return;
-    void *dev[] = {c->cn2, c->colnnz, c->key, c->idx, c->mask, c->s_rowptr, c->s_col, c->s_val,
+    void *dev[] = {c->cn2, c->colnnz, c->key, c->rn2, c->idx, c->mask, c->s_rowptr, c->s_col, c->s_val,
                    c->d_nnz, c->ws_topk, c->ws_slice, c->ws_spmm};
     for (void *p : dev)
         if (p) (void)hipFree(p);
@@ -261,6 +263,7 @@ rsc_status_t rsc_cache_create(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t r
         {(void **)&c->cn2, sizeof(double) * n},
         {(void **)&c->colnnz, sizeof(int32_t) * n},
         {(void **)&c->key, sizeof(uint64_t) * n},
+        {(void **)&c->rn2, sizeof(double) * n},
         {(void **)&c->idx, sizeof(int32_t) * n},
         {(void **)&c->mask, sizeof(uint32_t) * (size_t)rsc::ceil_div(n, 32)},
         {(void **)&c->s_rowptr, sizeof(int32_t) * ((size_t)X->n_rows + 1)},
@@ -290,23 +293,36 @@ rsc_status_t rsc_cache_create(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t r
     return RSC_OK;
 }
 
-rsc_status_t rsc_cache_refresh(rsc_cache_t *c, const float *B, int32_t d, int64_t ldb, int32_t k, int64_t step,
-                               hipStream_t stream) {
+rsc_status_t rsc_cache_score(rsc_cache_t *c, const float *B, int32_t d, int64_t ldb, hipStream_t stream) {
     if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
     RSC_TRY(check_dense(B, c->n, d, ldb, "B"));
+    RSC_HIP(rsc::pair_scores_launch(c->cn2, B, c->n, d, ldb, c->key, nullptr, c->rn2, stream), "cache scores");
+    return RSC_OK;
+}
+
+rsc_status_t rsc_cache_select(rsc_cache_t *c, int32_t k, int64_t step, hipStream_t stream) {
+    if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
     if (k < 0 || k > c->n) return fail(RSC_ERR_INVALID_ARGUMENT, "k = %d outside [0, %d]", k, c->n);
-    RSC_HIP(rsc::pair_scores_launch(c->cn2, B, c->n, d, ldb, c->key, nullptr, stream), "refresh scores");
-    RSC_HIP(rsc::topk_launch(c->key, c->n, k, c->idx, c->mask, c->ws_topk, stream), "refresh topk");
+    RSC_HIP(rsc::topk_launch(c->key, c->n, k, c->idx, c->mask, c->ws_topk, stream), "cache topk");
     RSC_HIP(rsc::slice_launch(c->X.n_rows, c->X.nnz, c->X.rowptr, c->X.col, c->X.val, c->mask, c->s_rowptr,
                               c->s_col, c->s_val, c->X.nnz, c->d_nnz, c->ws_slice, stream),
-            "refresh slice");
-    RSC_HIP(hipMemcpyAsync(c->h_nnz, c->d_nnz, sizeof(int64_t), hipMemcpyDeviceToHost, stream), "refresh nnz");
-    RSC_HIP(hipEventRecord(c->ev, stream), "refresh event");
+            "cache slice");
+    RSC_HIP(hipMemcpyAsync(c->h_nnz, c->d_nnz, sizeof(int64_t), hipMemcpyDeviceToHost, stream), "cache nnz");
+    RSC_HIP(hipEventRecord(c->ev, stream), "cache event");
     c->k = k;
     c->last_step = step;
     c->version += 1;
     c->nnz_known = false;
     return RSC_OK;
+}
+
+rsc_status_t rsc_cache_refresh(rsc_cache_t *c, const float *B, int32_t d, int64_t ldb, int32_t k, int64_t step,
+                               hipStream_t stream) {
+    if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
+    RSC_TRY(check_dense(B, c->n, d, ldb, "B"));
+    if (k < 0 || k > c->n) return fail(RSC_ERR_INVALID_ARGUMENT, "k = %d outside [0, %d]", k, c->n);
+    RSC_TRY(rsc_cache_score(c, B, d, ldb, stream));
+    return rsc_cache_select(c, k, step, stream);
 }
 
 rsc_status_t rsc_cache_get(rsc_cache_t *c, int64_t step, rsc_csr_t *slice_out, const int32_t **idx_out,
@@ -354,11 +370,12 @@ rsc_status_t rsc_spmm_sampled(rsc_cache_t *c, const float *B, int32_t d, int64_t
 }
 
 rsc_status_t rsc_cache_buffers(rsc_cache_t *c, const double **cn2, const int32_t **colnnz, const uint64_t **key,
-                               const uint32_t **mask) {
+                               const double **rn2, const uint32_t **mask) {
     if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
     if (cn2) *cn2 = c->cn2;
     if (colnnz) *colnnz = c->colnnz;
     if (key) *key = c->key;
+    if (rn2) *rn2 = c->rn2;
     if (mask) *mask = c->mask;
     return RSC_OK;
 }
@@ -443,6 +460,72 @@ rsc_status_t rsc_greedy_allocate(int32_t L, int32_t n, int64_t nnz, const uint64
         for (int32_t p = k2; p < k; ++p) drop += colnnz_host[order[best][p]];
         bud -= (int64_t)d_host[best] * drop;
         k_out_host[best] = k2;
+    }
+    if (budget_out_host) *budget_out_host = bud;
+    return RSC_OK;
+}
+
+size_t rsc_greedy_profile_workspace_bytes(int32_t n) { return n < 0 ? 0 : rsc::greedy_profile_ws_bytes(n); }
+
+int32_t rsc_greedy_blocks(int32_t n, int32_t alpha_num, int32_t alpha_den) {
+    if (n < 0 || alpha_num < 0 || alpha_den <= 0) return -1;
+    return rsc::greedy_blocks(n, rsc::greedy_step(n, alpha_num, alpha_den));
+}
+
+rsc_status_t rsc_greedy_profile(const uint64_t *key, const int32_t *colnnz, int32_t n, int32_t alpha_num,
+                                int32_t alpha_den, double *mass, int64_t *count, int32_t *order, void *ws,
+                                size_t ws_bytes, hipStream_t stream) {
+    if (n < 0 || alpha_num < 0 || alpha_den <= 0)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "n < 0 or bad step fraction");
+    if (n > 0 && (!key || !colnnz || !mass || !count))
+        return fail(RSC_ERR_INVALID_ARGUMENT, "key/colnnz/mass/count is NULL");
+    if (!aligned(key, 8) || !aligned(mass, 8) || !aligned(count, 8) || !aligned(colnnz, 4) || !aligned(order, 4))
+        return fail(RSC_ERR_UNSUPPORTED, "misaligned profile argument");
+    RSC_TRY(check_ws(ws, ws_bytes, rsc::greedy_profile_ws_bytes(n), "greedy profile"));
+    RSC_TRY(check_device());
+    RSC_HIP(rsc::greedy_profile_launch(key, colnnz, n, rsc::greedy_step(n, alpha_num, alpha_den), mass, count,
+                                       order, ws, stream),
+            "greedy profile launch");
+    return RSC_OK;
+}
+
+rsc_status_t rsc_greedy_allocate_profiles(int32_t L, int32_t n, int64_t nnz, int32_t alpha_num,
+                                          int32_t alpha_den, const double *const *mass_host,
+                                          const int64_t *const *count_host, const int32_t *d_host,
+                                          double fro_a2, const double *fro_b2_host, int32_t C_num,
+                                          int32_t C_den, int32_t *k_out_host, int64_t *budget_out_host) {
+    if (L < 1 || n < 0 || nnz < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "L < 1, n < 0 or nnz < 0");
+    if (!mass_host || !count_host || !d_host || !fro_b2_host || !k_out_host)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "NULL host array");
+    if (C_num < 0 || C_den <= 0 || alpha_num < 0 || alpha_den <= 0)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "bad budget or step fraction");
+    for (int32_t l = 0; l < L; ++l) {
+        if (!mass_host[l] || !count_host[l]) return fail(RSC_ERR_INVALID_ARGUMENT, "profile %d is NULL", l);
+        if (d_host[l] < 1) return fail(RSC_ERR_INVALID_ARGUMENT, "d[%d] < 1", l);
+    }
+    const int32_t step = rsc::greedy_step(n, alpha_num, alpha_den);
+    int64_t total = 0;
+    for (int32_t l = 0; l < L; ++l) {
+        k_out_host[l] = n;
+        total += nnz * (int64_t)d_host[l];
+    }
+    int64_t bud = total;
+    while (bud * (int64_t)C_den > (int64_t)C_num * total) {
+        int32_t best = -1;
+        double best_inc = 0.0;
+        for (int32_t l = 0; l < L; ++l) {
+            if (k_out_host[l] <= 0) continue;
+            const int32_t j = (n - k_out_host[l]) / step;  // next block from the bottom of the ranking
+            const double inc = mass_host[l][j] / (std::sqrt(fro_a2) * std::sqrt(fro_b2_host[l]));
+            if (best < 0 || inc < best_inc) {
+                best = l;
+                best_inc = inc;
+            }
+        }
+        if (best < 0) break;
+        const int32_t j = (n - k_out_host[best]) / step;
+        bud -= (int64_t)d_host[best] * count_host[best][j];
+        k_out_host[best] = std::max(0, k_out_host[best] - step);
     }
     if (budget_out_host) *budget_out_host = bud;
     return RSC_OK;

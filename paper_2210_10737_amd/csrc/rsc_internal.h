@@ -34,7 +34,7 @@ hipError_t spmm_launch(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr,
 hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,
                               int32_t *colnnz, hipStream_t stream);
 hipError_t pair_scores_launch(const double *cn2, const float *B, int32_t n, int32_t d, int64_t ldb,
-                              uint64_t *key, float *score, hipStream_t stream);
+                              uint64_t *key, float *score, double *rn2, hipStream_t stream);
 
 // ---- top-k -------------------------------------------------------------
 size_t topk_ws_bytes(int32_t n);
@@ -47,6 +47,14 @@ hipError_t slice_launch(int32_t n_rows, int64_t nnz, const int32_t *rowptr, cons
                         const float *val, const uint32_t *mask, int32_t *rowptr_out,
                         int32_t *col_out, float *val_out, int64_t capacity, int64_t *nnz_out,
                         void *ws, hipStream_t stream);
+
+// ---- layer-wise allocation ---------------------------------------------
+int32_t greedy_step(int32_t n, int32_t alpha_num, int32_t alpha_den);
+int32_t greedy_blocks(int32_t n, int32_t step);
+size_t greedy_profile_ws_bytes(int32_t n);
+hipError_t greedy_profile_launch(const uint64_t *key, const int32_t *colnnz, int32_t n, int32_t step,
+                                 double *mass, int64_t *count, int32_t *order_out, void *ws,
+                                 hipStream_t stream);
 
 // ---- helpers -----------------------------------------------------------
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }

@@ -39,7 +39,8 @@ __global__ __launch_bounds__(256) void pair_scores_kernel(const double *__restri
                                                           const float *__restrict__ B, int32_t n,
                                                           int32_t d, int64_t ldb,
                                                           uint64_t *__restrict__ key,
-                                                          float *__restrict__ score) {
+                                                          float *__restrict__ score,
+                                                          double *__restrict__ rn2) {
     __shared__ float tile[kRows][kTileF + 1];
     const int t = threadIdx.x;
     const int64_t row0 = (int64_t)blockIdx.x * kRows;
@@ -73,6 +74,7 @@ __global__ __launch_bounds__(256) void pair_scores_kernel(const double *__restri
         const uint64_t bits = (uint64_t)__double_as_longlong(q);
         key[row] = isnan(q) ? 0ull : bits + 1ull;
         if (score) score[row] = (float)sqrt(q);
+        if (rn2) rn2[row] = acc;
     }
 }
 
@@ -86,9 +88,9 @@ hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *v
 }
 
 hipError_t pair_scores_launch(const double *cn2, const float *B, int32_t n, int32_t d, int64_t ldb,
-                              uint64_t *key, float *score, hipStream_t stream) {
+                              uint64_t *key, float *score, double *rn2, hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    pair_scores_kernel<<<(unsigned)ceil_div(n, kRows), 256, 0, stream>>>(cn2, B, n, d, ldb, key, score);
+    pair_scores_kernel<<<(unsigned)ceil_div(n, kRows), 256, 0, stream>>>(cn2, B, n, d, ldb, key, score, rn2);
     return hipGetLastError();
 }
 

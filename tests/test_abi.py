@@ -34,7 +34,7 @@ def test_header_matches_exports():
     L = rsc.lib()
     for name in declared:
         assert getattr(L, name) is not None
-    assert L.rsc_abi_version() == 1
+    assert L.rsc_abi_version() == 2
 
 
 def test_status_strings():
@@ -163,3 +163,44 @@ def test_greedy_hand_example_through_abi():
     k, bud = rsc.greedy_allocate(keys, g["colnnz"], g["nnz"], g["d"], g["fro_a2"], g["fro_b2"],
                                  tuple(g["C"]), tuple(g["alpha"]))
     assert k == g["expected_k"] and bud == g["expected_budget"]
+
+
+def host_profile(key, colnnz, alpha):
+    """The greedy's per-block profile from the oracle's ranking: block j
+    covers ranks [max(0, n-(j+1)step), n-j*step); sqrt(q) summed in ascending
+    rank order one by one (fp64), NaN keys counting 0."""
+    import math
+    import struct
+    n = len(key)
+    step = max(1, n * alpha[0] // alpha[1])
+    order = oracle.rank_order(key)
+    nb = -(-n // step)
+    mass, count = np.zeros(nb), np.zeros(nb, np.int64)
+    for j in range(nb):
+        hi = n - j * step
+        lo = max(0, hi - step)
+        s = 0.0
+        for p in range(lo, hi):
+            u = int(key[order[p]])
+            if u:
+                s += math.sqrt(struct.unpack("<d", struct.pack("<Q", u - 1))[0])
+        mass[j] = s
+        count[j] = int(colnnz[order[lo:hi]].sum())
+    return mass, count
+
+
+@pytest.mark.parametrize("C", [(1, 10), (3, 10), (1, 2), (0, 1), (1, 1)])
+def test_greedy_profiles_match_oracle(C):
+    A = synth.make_graph("tiny", 0)
+    ds = [64, 16, 8]
+    cn2, colnnz, keys, fb = _keys_and_norms(A, ds, seed=30)
+    keys[1] = keys[1].copy()
+    keys[1][::5] = keys[1][7]
+    keys[1][3::13] = 0
+    alpha = (3, 100)
+    profs = [host_profile(k, colnnz, alpha) for k in keys]
+    k_p, b_p = rsc.greedy_allocate_profiles([m for m, _ in profs], [c for _, c in profs], A.n, A.nnz, ds,
+                                            cn2.sum(), fb, C, alpha)
+    k_o, b_o = oracle.greedy(keys, colnnz, A.nnz, ds, cn2.sum(), fb, C, alpha)
+    assert k_p == k_o and b_p == b_o
+    assert rsc.lib().rsc_greedy_blocks(A.n, 3, 100) == len(profs[0][0])

@@ -1,0 +1,133 @@
+"""RSC training step (exact forward, per-layer cached top-k backward, greedy
+layer allocation at refresh steps) against the fp64 reference step.
+
+At refresh ("score") steps the backward is exact, both layers' pairs are
+scored and the greedy sets k_l; at the steps in between the backward runs
+on the cached slices. The selections are compared exactly (keys of the
+fp32 gradients vs keys of the fp64 gradients rounded to fp32: on this
+continuous data no key lies near the k-th one), the loss and the weight
+gradients within fp32 tolerance."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2210_10737_amd as rsc
+import synth
+from oracle.gcn_ref import RscReference
+from paper_2210_10737_amd.gcn import GCN, RscConfig
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu(gpu):
+    torch.backends.cuda.matmul.allow_tf32 = False
+    yield
+
+
+def _setup(budget, refresh, hidden=64, classes=16, feats=32):
+    A = synth.make_graph("tiny", 0)
+    n = A.n
+    X = synth.dense_normal(n, feats, seed=1)
+    Y = (np.random.default_rng(3).random((n, classes)) < 0.5).astype(np.float32)
+    cfg = RscConfig(budget=budget, alpha=(2, 100), refresh_interval=refresh)
+    model = GCN(rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n), feats, hidden, classes, cfg, seed=2)
+    ref = RscReference(A.rowptr, A.col, A.val, n, [hidden, classes], budget, (2, 100), refresh)
+    return A, X, Y, model, ref
+
+
+@pytest.mark.parametrize("budget", [(1, 2), (1, 10)])
+def test_rsc_step_matches_reference(budget):
+    A, X, Y, model, ref = _setup(budget, refresh=2)
+    W1 = model.W1.detach().cpu().numpy().astype(np.float64)
+    W2 = model.W2.detach().cpu().numpy().astype(np.float64)
+    Xd, Yd = torch.from_numpy(X).cuda(), torch.from_numpy(Y).cuda()
+    modes = []
+    for step in range(4):
+        model.W1.grad = None
+        model.W2.grad = None
+        loss = float(model.train_step(Xd, Yd, None, step).detach())
+        g1 = model.W1.grad.cpu().numpy()
+        g2 = model.W2.grad.cpu().numpy()
+        r = ref.step(X.astype(np.float64), W1, W2, Y.astype(np.float64), step)
+        rec = model.controller.history[-1]
+        modes.append(rec.mode)
+        assert rec.mode == r["mode"]
+        assert abs(loss - r["loss"]) <= 1e-5 * abs(r["loss"])
+        for g, gr in ((g1, r["gW1"]), (g2, r["gW2"])):
+            assert np.max(np.abs(g - gr)) <= 1e-4 * np.max(np.abs(gr))
+        assert rec.k == r["k"]
+        if rec.mode == "score":
+            for l, layer in enumerate((model.agg1, model.agg2)):
+                snap = rsc.cache_snapshot(layer.cache, step)
+                assert np.array_equal(snap["idx"], r["idx"][l])
+    assert modes == ["score", "sampled", "score", "sampled"]
+    assert 0 < sum(rec.k[0] for rec in model.controller.history) < 4 * A.n * 2
+    model.close()
+
+
+@pytest.mark.parametrize("name,d", [("tiny", 64), ("gcn2", 100)])
+def test_device_greedy_profile_bitwise(name, d):
+    """Device ranking (stable radix sort) and block profile against the
+    oracle's ranking and sequential block sums; then the greedy on device
+    profiles equals the oracle's greedy on the keys."""
+    import oracle
+    from tests.test_abi import host_profile
+    A = synth.make_graph(name, 0)
+    cn2, colnnz = oracle.col_sqnorms(A.rowptr, A.val)
+    keys, fb = [], []
+    for l, dl in enumerate((d, d // 4)):
+        o = oracle.pair_keys(cn2, synth.dense_normal(A.n, dl, seed=40 + l))
+        k = o["key"].copy()
+        k[11::97] = k[5]           # ties
+        k[7::211] = 0              # NaN keys
+        keys.append(k)
+        fb.append(float(o["rn2"].sum()))
+    alpha = (2, 100)
+    colnnz_d = torch.from_numpy(colnnz).cuda()
+    masses, counts = [], []
+    for k in keys:
+        mass, count, order = rsc.greedy_profile(torch.from_numpy(k.view(np.int64)).cuda(), colnnz_d, alpha,
+                                                with_order=True)
+        assert np.array_equal(order.cpu().numpy(), oracle.rank_order(k))
+        if name == "tiny":
+            hm, hc = host_profile(k, colnnz, alpha)
+            assert np.array_equal(mass.cpu().numpy().view(np.uint64), hm.view(np.uint64))
+            assert np.array_equal(count.cpu().numpy(), hc)
+        masses.append(mass.cpu().numpy())
+        counts.append(count.cpu().numpy())
+    for C in ((1, 10), (3, 10), (1, 2)):
+        kp, bp = rsc.greedy_allocate_profiles(masses, counts, A.n, A.nnz, [d, d // 4], cn2.sum(), fb, C, alpha)
+        ko, bo = oracle.greedy(keys, colnnz, A.nnz, [d, d // 4], cn2.sum(), fb, C, alpha)
+        assert kp == ko and bp == bo
+
+
+def test_full_budget_is_exact_bitwise():
+    """C = 1: the greedy keeps every column, and the sampled backward equals
+    the exact backward bitwise."""
+    A, X, Y, model, _ = _setup((1, 1), refresh=10)
+    Xd, Yd = torch.from_numpy(X).cuda(), torch.from_numpy(Y).cuda()
+    grads = []
+    for step in range(2):
+        model.W1.grad = None
+        model.W2.grad = None
+        model.train_step(Xd, Yd, None, step)
+        grads.append((model.W1.grad.clone(), model.W2.grad.clone()))
+    assert [r.mode for r in model.controller.history] == ["score", "sampled"]
+    assert model.controller.k == [A.n, A.n]
+    assert torch.equal(grads[0][0], grads[1][0]) and torch.equal(grads[0][1], grads[1][1])
+    model.close()
+
+
+def test_training_reduces_loss_and_switches_back():
+    A, X, Y, model, _ = _setup((1, 10), refresh=10)
+    model.controller.cfg.total_steps = 30
+    Xd, Yd = torch.from_numpy(X).cuda(), torch.from_numpy(Y).cuda()
+    opt = torch.optim.Adam(model.parameters(), lr=0.01)
+    losses = [float(model.train_step(Xd, Yd, opt, s).detach()) for s in range(30)]
+    modes = [r.mode for r in model.controller.history]
+    assert modes[0] == "score" and modes[10] == "score" and modes[20] == "score"
+    assert modes[1:10] == ["sampled"] * 9
+    assert modes[24:] == ["exact"] * 6          # last 20 % of the steps run exactly
+    assert losses[-1] < losses[0]
+    model.close()

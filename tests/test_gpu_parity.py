@@ -211,8 +211,10 @@ def test_pair_scores_bitwise(d):
     cn2[5] = 0.0
     B[5, 0] = np.inf                 # 0 * inf -> NaN key
     o = oracle.pair_keys(cn2, B, d=d)
-    key, score = rsc.pair_scores(torch.from_numpy(cn2).cuda(), dense_dev(B), d=d, with_score=True)
+    key, score, rn2 = rsc.pair_scores(torch.from_numpy(cn2).cuda(), dense_dev(B), d=d, with_score=True,
+                                      with_rn2=True)
     assert np.array_equal(key.cpu().numpy().view(np.uint64), o["key"])
+    assert np.array_equal(rn2.cpu().numpy().view(np.uint64), o["rn2"].view(np.uint64))
     sc = score.cpu().numpy()
     fin = np.isfinite(o["score"])
     assert np.array_equal(np.isnan(sc), np.isnan(o["score"]))
