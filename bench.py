@@ -190,6 +190,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=None,
                     help="rows of the CPU-baseline SpMM sample (default: all rows)")
+    ap.add_argument("--aggregator", choices=("gcn", "mean"), default="gcn",
+                    help="gcn: A_hat = D^-1/2 (A+I) D^-1/2 (symmetric); mean: the MEAN aggregator "
+                         "D^-1 (A+I) forward, its transpose (A+I) D^-1 in the backward")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB once (a plain copy of known "
                          "size, so hardware byte counters can be scaled)")
@@ -221,14 +224,24 @@ def main() -> int:
     print(f"[bench] {args.workload}: n={n} nnz={nnz} d={d} budget={pct}% (inputs {t_gen:.1f}s)",
           file=sys.stderr, flush=True)
 
-    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n)     # A_hat is symmetric: A_hat^T = A_hat
+    if args.aggregator == "gcn":
+        X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n)  # A_hat is symmetric: A_hat^T = A_hat
+        XB = XT = X
+    else:
+        # MEAN aggregator on the same (symmetric) structure with unit values:
+        # forward D^-1 A, backward operand A^T D^-1 (whose column norms come
+        # from its transpose, D^-1 A)
+        ones = rsc.DeviceCsr.from_host(A.rowptr, A.col, np.ones_like(A.val), n)
+        X = rsc.degree_scale(ones)
+        XB = rsc.degree_scale(ones, by_column=True, deg_rowptr=ones.rowptr)
+        XT = X
     H = torch.from_numpy(Hh).cuda()
     G = torch.from_numpy(Gh).cuda()
     Y = torch.empty((n, d), dtype=torch.float32, device="cuda")
     Yb = torch.empty((n, d), dtype=torch.float32, device="cuda")
     ws = torch.empty(rsc.spmm_workspace_bytes(X), dtype=torch.uint8, device="cuda")
     k = rsc.k_from_fraction(n, pct, 100)
-    cache = rsc.Cache(X, X, refresh_interval=args.refresh)
+    cache = rsc.Cache(XB, XT, refresh_interval=args.refresh)
     torch.cuda.synchronize()
 
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
@@ -301,7 +314,8 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": args.workload, "graph": w.description, "n": n, "nnz": nnz, "d": d,
+        "config": {"workload": args.workload, "aggregator": args.aggregator, "graph": w.description,
+                   "n": n, "nnz": nnz, "d": d,
                    "budget_pct": pct, "k": k, "refresh_interval": args.refresh, "seed": args.seed},
         "exact_spmm_ms": round(exact_ms, 4),
         "sampled_spmm_ms": round(sampled_ms, 4),
@@ -328,7 +342,7 @@ def main() -> int:
         },
     }
     cache.close()
-    del X, H, G, Y, Yb, ws
+    del X, XB, XT, H, G, Y, Yb, ws
     torch.cuda.empty_cache()
     if args.copy_probe_mib > 0:
         src = torch.ones(args.copy_probe_mib << 18, dtype=torch.float32, device="cuda")
@@ -338,7 +352,7 @@ def main() -> int:
         torch.cuda.synchronize()
         out["copy_probe_bytes"] = src.numel() * 4
         del src, dst
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.aggregator == "gcn":
         rows = args.cpu_rows or n
         print(f"[bench] gpu done ({ms_per_step:.3f} ms/step); timing the oracle on {rows} rows",
               file=sys.stderr, flush=True)

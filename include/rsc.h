@@ -90,6 +90,20 @@ size_t rsc_spmm_workspace_bytes(const rsc_csr_t *A);
 rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb, float *Y,
                       int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* MEAN aggregator operand (appendix A.3: SpMM_MEAN(A, H) = D^-1 A H, D the
+ * degree matrix of A, D_ii = stored entries of row i). Writes A's values
+ * divided by a degree into val_out (nnz entries, same structure as A), each
+ * fp32(val / deg) computed in fp64 and rounded once; a zero degree gives 0.
+ *   by_column = 0: deg = the length of the entry's own row -> D^-1 A, the
+ *     forward operand (deg_rowptr unused, may be NULL);
+ *   by_column = 1: deg = deg_rowptr[c+1] - deg_rowptr[c] for the entry's
+ *     column c -> pass the CSR of A^T as A and A's rowptr as deg_rowptr to
+ *     get A^T D^-1 = (D^-1 A)^T, the backward operand.
+ * rsc_spmm on the result is SpMM_MEAN; the cache and sampled SpMM apply to it
+ * unchanged (its column norms come from the CSR of its transpose). */
+rsc_status_t rsc_degree_scale(const rsc_csr_t *A, const int32_t *deg_rowptr, int32_t by_column,
+                              float *val_out, hipStream_t stream);
+
 /* ---------------------------------------------------------------- A2 --- */
 /* Column square-norms of a sparse operand X (Eq. 3's ||X[:, i]||^2; the
  * ||A_hat^T[:, i]||^2 of Eq. 4a). Pass the CSR of X^T: column i of X is

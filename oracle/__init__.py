@@ -54,6 +54,7 @@ def _load():
         lib.orc_greedy.argtypes = [i32, i32, i64, vp, vp, vp, f64, vp, i32, i32, i32, i32, vp]
         lib.orc_greedy.restype = i64
         lib.orc_num_threads.restype = i32
+        lib.orc_spmm_mean.argtypes = [i32, vp, vp, vp, vp, i32, i64, vp, i64]
         _lib = lib
     return _lib
 
@@ -92,6 +93,18 @@ def spmm(rowptr, col, val, B, d=None, rows=None, with_mag=False):
     _load().orc_spmm(n_rows, _p(rowptr), _p(col), _p(val), _p(B), d, B.shape[1], _p(Y), d,
                      _p(S), d, _p(sel), 0 if sel is None else len(sel))
     return (Y, S) if with_mag else Y
+
+
+def spmm_mean(rowptr, col, val, B, d=None):
+    """SpMM_MEAN: D^-1 A B with D_ii = stored entries of row i (fp64 sum,
+    one division, one fp32 rounding)."""
+    rowptr, col, val = _c(rowptr, np.int32), _c(col, np.int32), _c(val, np.float32)
+    B = _c(B, np.float32)
+    d = B.shape[1] if d is None else d
+    n_rows = len(rowptr) - 1
+    Y = np.zeros((n_rows, d), dtype=np.float32)
+    _load().orc_spmm_mean(n_rows, _p(rowptr), _p(col), _p(val), _p(B), d, B.shape[1], _p(Y), d)
+    return Y
 
 
 def col_sqnorms(rowptr_t, val_t):

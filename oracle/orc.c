@@ -291,3 +291,24 @@ int64_t orc_greedy(int32_t L, int32_t n, int64_t nnz, const uint64_t *const *key
 /* Threads the oracle's row loops use (OpenMP's current maximum). */
 #include <omp.h>
 int32_t orc_num_threads(void) { return (int32_t)omp_get_max_threads(); }
+
+/* ------------------------------------------------------------------------ */
+/* SpMM_MEAN (appendix A.3): the MEAN aggregator D^-1 A H, D the degree
+ * matrix of A, read as D_ii = number of stored entries of row i (the paper's
+ * worked example divides every row by 2, the column count, which disagrees
+ * with D^-1 A for its rows 0 and 1; the definition D^-1 A is followed here).
+ * Y[i, j] = fl32( (sum_t val[t] * B[col[t], j]) / len_i ), the sum in fp64
+ * in stored order; empty rows give 0. */
+void orc_spmm_mean(int32_t n_rows, const int32_t *rowptr, const int32_t *col, const float *val,
+                   const float *B, int32_t d, int64_t ldb, float *Y, int64_t ldy) {
+#pragma omp parallel for schedule(dynamic, 64)
+    for (int32_t i = 0; i < n_rows; ++i) {
+        int32_t len = rowptr[i + 1] - rowptr[i];
+        for (int32_t j = 0; j < d; ++j) {
+            double acc = 0.0;
+            for (int32_t t = rowptr[i]; t < rowptr[i + 1]; ++t)
+                acc += (double)val[t] * (double)B[(int64_t)col[t] * ldb + j];
+            Y[(int64_t)i * ldy + j] = len ? (float)(acc / (double)len) : 0.0f;
+        }
+    }
+}

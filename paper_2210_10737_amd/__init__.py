@@ -27,7 +27,7 @@ STATUS = {0: "RSC_OK", 1: "RSC_ERR_INVALID_ARGUMENT", 2: "RSC_ERR_UNSUPPORTED",
 
 EXPORTED = [
     "rsc_status_string", "rsc_last_error", "rsc_abi_version",
-    "rsc_spmm_workspace_bytes", "rsc_spmm",
+    "rsc_spmm_workspace_bytes", "rsc_spmm", "rsc_degree_scale",
     "rsc_col_sqnorms", "rsc_pair_scores",
     "rsc_topk_workspace_bytes", "rsc_topk_select",
     "rsc_slice_workspace_bytes", "rsc_slice_csr",
@@ -71,6 +71,7 @@ def lib():
             "rsc_spmm_workspace_bytes": ([csrp], sz),
             "rsc_spmm": ([csrp, vp, i32, i64, vp, i64, vp, sz, vp], ctypes.c_int),
             "rsc_col_sqnorms": ([csrp, vp, vp, vp], ctypes.c_int),
+            "rsc_degree_scale": ([csrp, vp, i32, vp, vp], ctypes.c_int),
             "rsc_pair_scores": ([vp, vp, i32, i32, i64, vp, vp, vp, vp], ctypes.c_int),
             "rsc_topk_workspace_bytes": ([i32], sz),
             "rsc_topk_select": ([vp, i32, i32, vp, vp, vp, sz, vp], ctypes.c_int),
@@ -122,6 +123,12 @@ def _ld(t: torch.Tensor) -> int:
     return t.stride(0)
 
 
+def _new_out(rows: int, d: int, device) -> torch.Tensor:
+    """rows x d output view with a leading dimension rounded up to 4 floats."""
+    ld = (d + 3) // 4 * 4
+    return torch.empty((rows, ld), dtype=torch.float32, device=device)[:, :d]
+
+
 def _workspace(nbytes: int, device) -> torch.Tensor:
     # torch's caching allocator returns 256-byte (or larger) aligned blocks
     return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
@@ -163,13 +170,22 @@ def spmm(A: DeviceCsr, B: torch.Tensor, d: int | None = None, out: torch.Tensor 
          ws: torch.Tensor | None = None) -> torch.Tensor:
     """Y = A @ B[:, :d] (exact SpMM)."""
     d = B.shape[1] if d is None else d
-    Y = torch.empty((A.n_rows, d), dtype=torch.float32, device=B.device) if out is None else out
+    Y = _new_out(A.n_rows, d, B.device) if out is None else out
     s = A.struct()
     need = lib().rsc_spmm_workspace_bytes(ctypes.byref(s))
     ws = _workspace(need, B.device) if ws is None else ws
     _check(lib().rsc_spmm(ctypes.byref(s), B.data_ptr(), d, _ld(B), Y.data_ptr(), _ld(Y),
                           ws.data_ptr(), ws.numel(), _stream()))
     return Y
+
+
+def degree_scale(A: DeviceCsr, by_column: bool = False, deg_rowptr: torch.Tensor | None = None) -> DeviceCsr:
+    """MEAN-aggregator operand: D^-1 A (by_column=False) or, for A = CSR of
+    M^T and deg_rowptr = M's rowptr, M^T D^-1 (by_column=True)."""
+    out = torch.empty_like(A.val)
+    _check(lib().rsc_degree_scale(ctypes.byref(A.struct()), _ptr(deg_rowptr), 1 if by_column else 0,
+                                  out.data_ptr() if A.nnz else None, _stream()))
+    return DeviceCsr(A.n_rows, A.n_cols, A.rowptr, A.col, out, nnz=A.nnz)
 
 
 # ---------------------------------------------------------------- A2 / A3
@@ -270,7 +286,7 @@ class Cache:
 
     def spmm_sampled(self, B: torch.Tensor, d: int | None = None, out: torch.Tensor | None = None):
         d = B.shape[1] if d is None else d
-        Y = torch.empty((self.X.n_rows, d), dtype=torch.float32, device=B.device) if out is None else out
+        Y = _new_out(self.X.n_rows, d, B.device) if out is None else out
         _check(lib().rsc_spmm_sampled(self._h, B.data_ptr(), d, _ld(B), Y.data_ptr(), _ld(Y), _stream()))
         return Y
 

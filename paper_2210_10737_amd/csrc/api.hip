@@ -153,6 +153,19 @@ rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb
     return RSC_OK;
 }
 
+rsc_status_t rsc_degree_scale(const rsc_csr_t *A, const int32_t *deg_rowptr, int32_t by_column, float *val_out,
+                              hipStream_t stream) {
+    RSC_TRY(check_csr(A, "A"));
+    if (A->nnz > 0 && !val_out) return fail(RSC_ERR_INVALID_ARGUMENT, "val_out is NULL");
+    if (by_column && !deg_rowptr) return fail(RSC_ERR_INVALID_ARGUMENT, "deg_rowptr is NULL");
+    if (!aligned(val_out, 4) || !aligned(deg_rowptr, 4)) return fail(RSC_ERR_UNSUPPORTED, "misaligned argument");
+    RSC_TRY(check_device());
+    RSC_HIP(rsc::degree_scale_launch(A->n_rows, A->rowptr, A->col, A->val, deg_rowptr, by_column ? 1 : 0, val_out,
+                                     stream),
+            "degree scale launch");
+    return RSC_OK;
+}
+
 // ------------------------------------------------------------------- A2
 rsc_status_t rsc_col_sqnorms(const rsc_csr_t *XT, double *cn2, int32_t *colnnz, hipStream_t stream) {
     RSC_TRY(check_csr(XT, "XT"));

@@ -48,6 +48,10 @@ hipError_t slice_launch(int32_t n_rows, int64_t nnz, const int32_t *rowptr, cons
                         int32_t *col_out, float *val_out, int64_t capacity, int64_t *nnz_out,
                         void *ws, hipStream_t stream);
 
+// ---- MEAN aggregator operand -------------------------------------------
+hipError_t degree_scale_launch(int32_t n_rows, const int32_t *rowptr, const int32_t *col, const float *val,
+                               const int32_t *deg_rowptr, int32_t by_column, float *out, hipStream_t stream);
+
 // ---- layer-wise allocation ---------------------------------------------
 int32_t greedy_step(int32_t n, int32_t alpha_num, int32_t alpha_den);
 int32_t greedy_blocks(int32_t n, int32_t step);

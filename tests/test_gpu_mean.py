@@ -1,0 +1,91 @@
+"""SpMM_MEAN (appendix A.3: D^-1 A H) on the GPU: the operand built by
+rsc_degree_scale, the exact product against the oracle's definition, and the
+sampled backward on (D^-1 A)^T through the cache."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2210_10737_amd as rsc
+import synth
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+FLT_MIN = np.float32(np.finfo(np.float32).tiny)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu(gpu):
+    yield
+
+
+def to_dev(A, n_cols):
+    return rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
+
+
+def mean_mag(A, B, n_cols):
+    """|D^-1 A| |B| in fp64 (the magnitude the error is relative to)."""
+    Ab = synth.Csr(A.n, A.rowptr, A.col, np.abs(A.val))
+    deg = np.maximum(np.diff(A.rowptr), 1)
+    _, S = oracle.spmm(Ab.rowptr, Ab.col, Ab.val, np.abs(B), with_mag=True)
+    return S / deg[:, None]
+
+
+def test_appendix_example_bitwise():
+    g = json.load(open(os.path.join(GOLDEN, "spmm_mean_appendix_example.json")))
+    Ad = np.array(g["A"], np.float32)
+    rowptr = np.concatenate([[0], np.cumsum((Ad != 0).sum(axis=1))]).astype(np.int32)
+    col = np.concatenate([np.nonzero(r)[0] for r in Ad]).astype(np.int32)
+    A = synth.Csr(3, rowptr, col, Ad[Ad != 0].astype(np.float32))
+    M = rsc.degree_scale(to_dev(A, 2))
+    H = np.zeros((2, 4), np.float32)
+    H[:, :2] = np.array(g["H"], np.float32)
+    Y = rsc.spmm(M, torch.from_numpy(H).cuda(), d=2).cpu().numpy()
+    assert np.array_equal(Y, np.array(g["expected_reading"], np.float32))
+
+
+@pytest.mark.parametrize("d", [16, 100, 256])
+def test_spmm_mean_matches_oracle(d):
+    A = synth.random_csr(2000, 1500, 30, seed=21, hub_rows=2, hub_len=1400, empty_frac=0.1)
+    B = synth.dense_normal(1500, d, seed=22)
+    M = rsc.degree_scale(to_dev(A, 1500))
+    # the scaled values are the definition, bit for bit
+    deg = np.repeat(np.diff(A.rowptr), np.diff(A.rowptr))
+    want = (A.val.astype(np.float64) / deg).astype(np.float32)
+    assert np.array_equal(M.val.cpu().numpy().view(np.uint32), want.view(np.uint32))
+    Y = rsc.spmm(M, torch.from_numpy(B).cuda()).cpu().numpy()
+    Yo = oracle.spmm_mean(A.rowptr, A.col, A.val, B)
+    S = mean_mag(A, B, 1500)
+    assert np.max(np.abs(Y.astype(np.float64) - Yo) / np.maximum(S, FLT_MIN)) <= 1e-5
+
+
+def test_sampled_mean_backward():
+    """Backward operand (D^-1 A)^T = A^T D^-1 built from A^T's CSR scaled by
+    A's row lengths; cache + top-k + slice + sampled SpMM against the oracle
+    on the same operand."""
+    A = synth.random_csr(1800, 1800, 40, seed=31, hub_rows=2, hub_len=1500, empty_frac=0.05)
+    AT = synth.transpose(A, 1800)
+    dA, dAT = to_dev(A, 1800), to_dev(AT, 1800)
+    fwd = rsc.degree_scale(dA)                                        # D^-1 A
+    bwd = rsc.degree_scale(dAT, by_column=True, deg_rowptr=dA.rowptr)  # A^T D^-1
+    deg_of_col = np.diff(A.rowptr)[AT.col]
+    want = np.where(deg_of_col > 0, AT.val.astype(np.float64) / np.maximum(deg_of_col, 1), 0).astype(np.float32)
+    assert np.array_equal(bwd.val.cpu().numpy().view(np.uint32), want.view(np.uint32))
+    fwd_vals = (A.val.astype(np.float64) / np.repeat(np.diff(A.rowptr), np.diff(A.rowptr))).astype(np.float32)
+    G = synth.dense_normal(1800, 64, seed=33)
+    cache = rsc.Cache(bwd, fwd, refresh_interval=10)
+    k = 540
+    cache.refresh(torch.from_numpy(G).cuda(), k, step=0)
+    snap = rsc.cache_snapshot(cache)
+    cn2, _ = oracle.col_sqnorms(A.rowptr, fwd_vals)        # columns of A^T D^-1 = rows of D^-1 A
+    idx, mask = oracle.topk(oracle.pair_keys(cn2, G)["key"], k)
+    assert np.array_equal(snap["idx"], idx)
+    ro, co, vo = oracle.slice_csr(AT.rowptr, AT.col, want, mask)
+    assert np.array_equal(snap["rowptr"], ro) and np.array_equal(snap["col"], co)
+    Ys = cache.spmm_sampled(torch.from_numpy(G).cuda()).cpu().numpy()
+    Yo, S = oracle.spmm(ro, co, vo, G, with_mag=True)
+    assert np.max(np.abs(Ys.astype(np.float64) - Yo) / np.maximum(S, FLT_MIN)) <= 1e-4
+    cache.close()

@@ -383,3 +383,28 @@ def test_cache_policy():
         if r:
             p.refreshed(s)
     assert [i for i, r in enumerate(seq) if r] == [0, 10, 20]
+
+
+# ---------------------------------------------------------------- SpMM_MEAN
+def test_spmm_mean_appendix_example():
+    g = json.load(open(os.path.join(GOLDEN, "spmm_mean_appendix_example.json")))
+    Ad = np.array(g["A"], np.float32)
+    rowptr = np.concatenate([[0], np.cumsum((Ad != 0).sum(axis=1))]).astype(np.int32)
+    col = np.concatenate([np.nonzero(r)[0] for r in Ad]).astype(np.int32)
+    val = Ad[Ad != 0].astype(np.float32)
+    Y = oracle.spmm_mean(rowptr, col, val, np.array(g["H"], np.float32))
+    assert np.array_equal(Y, np.array(g["expected_reading"], np.float32))
+    # the printed example agrees with D^-1 A H on the row that has two entries
+    assert np.array_equal(Y[2], np.array(g["printed"][2], np.float32))
+    assert not np.array_equal(Y[:2], np.array(g["printed"][:2], np.float32))
+
+
+def test_spmm_mean_dense_and_empty_rows(small_gen):
+    A, B = small_gen
+    Y = oracle.spmm_mean(A.rowptr, A.col, A.val, B)
+    D = dense(A, 190)
+    deg = (D != 0).sum(axis=1)
+    ref = np.where(deg[:, None] > 0, (D @ B.astype(np.float64)) / np.maximum(deg, 1)[:, None], 0.0)
+    mag = (np.abs(D) @ np.abs(B.astype(np.float64))) / np.maximum(deg, 1)[:, None]
+    assert np.all(np.abs(Y - ref) <= 2.0 ** -24 * np.abs(ref) + 1e-12 * mag + 1e-300)
+    assert np.all(Y[deg == 0] == 0)
