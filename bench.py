@@ -161,6 +161,24 @@ def train_bench(args) -> int:
         model.close()
         del model, opt
         torch.cuda.empty_cache()
+    staleness = None
+    if args.staleness_steps > 0:
+        # untimed diagnostic run: AUC / overlap of each layer's selection
+        # between consecutive refreshes, and the k_l trace (Figs. 4 and 7)
+        cfg = RscConfig(budget=(pct, 100), alpha=(2, 100), refresh_interval=args.refresh,
+                        track_staleness=True)
+        model = GCN(Ad, p["in_features"], p["hidden"], p["classes"], cfg, seed=args.seed + 2)
+        opt = torch.optim.Adam(model.parameters(), lr=0.01)
+        for s_ in range(args.staleness_steps):
+            model.train_step(X, Y, opt, s_)
+        recs = [r for r in model.controller.history if r.mode == "score"]
+        staleness = {"steps": args.staleness_steps,
+                     "refresh_steps": [r.step for r in recs],
+                     "k_trace": [r.k for r in recs],
+                     "auc": [[round(a, 5) for a in r.auc] for r in recs[1:]],
+                     "overlap": [[round(o, 5) for o in r.overlap] for r in recs[1:]]}
+        model.close()
+        del model, opt
     out = {
         "metric": "GCN training step ms (exact vs RSC) on 1 MI355X",
         "value": round(results["exact"]["ms_per_step"] / results["rsc"]["ms_per_step"], 3),
@@ -173,6 +191,7 @@ def train_bench(args) -> int:
                    "hidden": p["hidden"], "classes": p["classes"], "budget_pct": pct,
                    "refresh_interval": args.refresh, "alpha_pct": 2, "seed": args.seed},
         "exact": results["exact"], "rsc": results["rsc"],
+        "staleness": staleness,
     }
     print(json.dumps(out), flush=True)
     return 0
@@ -193,6 +212,8 @@ def main() -> int:
     ap.add_argument("--aggregator", choices=("gcn", "mean"), default="gcn",
                     help="gcn: A_hat = D^-1/2 (A+I) D^-1/2 (symmetric); mean: the MEAN aggregator "
                          "D^-1 (A+I) forward, its transpose (A+I) D^-1 in the backward")
+    ap.add_argument("--staleness-steps", type=int, default=60,
+                    help="gcn2-train only: steps of the untimed selection-staleness run (0 = skip)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB once (a plain copy of known "
                          "size, so hardware byte counters can be scaled)")

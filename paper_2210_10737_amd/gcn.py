@@ -78,6 +78,7 @@ class RscConfig:
     switch_fraction: tuple = (8, 10)  # approximate for this share of the steps (section 5.1)
     total_steps: int | None = None
     enabled: bool = True
+    track_staleness: bool = False    # record AUC / overlap of successive selections
 
 
 @dataclass
@@ -86,6 +87,22 @@ class StepRecord:
     mode: str
     k: list = field(default_factory=list)
     greedy_s: float = 0.0
+    auc: list = field(default_factory=list)      # previous selection under the new ranking
+    overlap: list = field(default_factory=list)  # |S_prev & S_new| / |S_prev|
+
+
+def selection_auc(order: np.ndarray, selected: np.ndarray) -> float:
+    """AUC of a previous top-k selection under a new ranking (the matching
+    score of section 3.3.1 / Fig. 4): the probability that a previously
+    selected pair is ranked above a previously unselected one. `order` lists
+    the pairs from best to worst. NaN if the selection is empty or full."""
+    n, k = len(order), len(selected)
+    if k == 0 or k == n:
+        return float("nan")
+    pos = np.empty(n, dtype=np.int64)
+    pos[order] = np.arange(n)
+    above = float(np.sum(n - 1 - pos[selected])) - k * (k - 1) / 2.0
+    return above / (float(k) * (n - k))
 
 
 class RscController:
@@ -109,6 +126,8 @@ class RscController:
         self.nb = nb
         self.ws = torch.empty(max(lib().rsc_greedy_profile_workspace_bytes(self.n), 1), dtype=torch.uint8,
                               device=dev)
+        self.order = torch.empty(max(self.n, 1), dtype=torch.int32, device=dev) if cfg.track_staleness else None
+        self.prev_idx = [None] * len(layers)
         self.last_refresh = None
         self.k = [self.n] * len(layers)
         self.history: list[StepRecord] = []
@@ -143,9 +162,12 @@ class RscController:
             ptrs = layer.cache.buffers()
             _check(lib().rsc_greedy_profile(ptrs[2], self.colnnz_ptr, self.n, self.cfg.alpha[0],
                                             self.cfg.alpha[1], self.mass[l].data_ptr(),
-                                            self.count[l].data_ptr(), None, self.ws.data_ptr(),
-                                            self.ws.numel(), _stream()))
+                                            self.count[l].data_ptr(),
+                                            None if self.order is None else self.order.data_ptr(),
+                                            self.ws.data_ptr(), self.ws.numel(), _stream()))
             fro_b2.append(float(copy_to_host(ptrs[3], self.n, np.float64).sum()))
+            if self.order is not None and self.prev_idx[l] is not None:
+                rec.auc.append(selection_auc(self.order.cpu().numpy(), self.prev_idx[l]))
         masses = self.mass[:, :self.nb].cpu().numpy()
         counts = self.count[:, :self.nb].cpu().numpy()
         widths = [layer.width for layer in self.layers]
@@ -155,6 +177,14 @@ class RscController:
         for layer, k in zip(self.layers, self.k):
             layer.cache.select(k, step)
         rec.greedy_s = time.perf_counter() - t0
+        if self.order is not None:
+            for l, layer in enumerate(self.layers):
+                g = layer.cache.get(step, with_slice=False)
+                new_idx = copy_to_host(g["idx_ptr"], g["k"], np.int32) if g["k"] else np.zeros(0, np.int32)
+                if self.prev_idx[l] is not None and len(self.prev_idx[l]):
+                    rec.overlap.append(len(np.intersect1d(self.prev_idx[l], new_idx, assume_unique=True))
+                                       / len(self.prev_idx[l]))
+                self.prev_idx[l] = new_idx
         rec.k = list(self.k)
         self.last_refresh = step
 

@@ -204,3 +204,19 @@ def test_greedy_profiles_match_oracle(C):
     k_o, b_o = oracle.greedy(keys, colnnz, A.nnz, ds, cn2.sum(), fb, C, alpha)
     assert k_p == k_o and b_p == b_o
     assert rsc.lib().rsc_greedy_blocks(A.n, 3, 100) == len(profs[0][0])
+
+
+def test_selection_auc_brute_force():
+    from paper_2210_10737_amd.gcn import selection_auc
+    rng = np.random.default_rng(5)
+    for n, k in ((10, 3), (50, 1), (64, 63), (200, 77)):
+        order = rng.permutation(n)
+        sel = rng.choice(n, size=k, replace=False)
+        pos = np.empty(n, int)
+        pos[order] = np.arange(n)
+        pairs = [(i, j) for i in sel for j in range(n) if j not in set(sel)]
+        want = sum(pos[i] < pos[j] for i, j in pairs) / len(pairs)
+        assert abs(selection_auc(order, sel) - want) < 1e-12
+    # identical ranking: the previous top-k is ranked first -> AUC 1
+    assert selection_auc(np.arange(20), np.arange(5)) == 1.0
+    assert selection_auc(np.arange(20)[::-1].copy(), np.arange(5)) == 0.0

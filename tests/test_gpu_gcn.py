@@ -131,3 +131,20 @@ def test_training_reduces_loss_and_switches_back():
     assert modes[24:] == ["exact"] * 6          # last 20 % of the steps run exactly
     assert losses[-1] < losses[0]
     model.close()
+
+
+def test_staleness_tracking():
+    """With tracking on, every refresh after the first records an AUC and an
+    overlap per layer; with frozen weights the ranking does not move, so the
+    previous selection is ranked first again (AUC 1, overlap 1)."""
+    A, X, Y, model, _ = _setup((1, 4), refresh=2)
+    model.controller.cfg.track_staleness = True
+    model.controller.order = torch.empty(A.n, dtype=torch.int32, device="cuda")
+    Xd, Yd = torch.from_numpy(X).cuda(), torch.from_numpy(Y).cuda()
+    for step in range(6):
+        model.train_step(Xd, Yd, None, step)
+    recs = [r for r in model.controller.history if r.mode == "score"]
+    assert len(recs) == 3 and recs[0].auc == [] and recs[0].overlap == []
+    for r in recs[1:]:
+        assert r.auc == [1.0, 1.0] and r.overlap == [1.0, 1.0]
+    model.close()
