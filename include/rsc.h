@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define RSC_ABI_VERSION 2
+#define RSC_ABI_VERSION 3
 
 typedef enum {
     RSC_OK = 0,
@@ -145,6 +145,9 @@ rsc_status_t rsc_topk_select(const uint64_t *key, int32_t n, int32_t k, int32_t 
  * column has its mask bit set are kept in their original order; column ids
  * stay global; rowptr_out (n_rows + 1 entries) is the running count of kept
  * entries; rows may become empty.
+ * colw (nullable, fp64[n_cols]): per-column scale; when given, each kept
+ * value becomes fl32(val * colw[col]) (fp64 product, one rounding), as the
+ * randomized sampler's 1/(k p) weighting needs.
  * nnz_out: device int64 receiving nnz'.
  * capacity: entries available in col_out / val_out. If capacity >= A->nnz
  * the call is asynchronous. Otherwise it is [sync]: entries beyond capacity
@@ -152,9 +155,31 @@ rsc_status_t rsc_topk_select(const uint64_t *key, int32_t n, int32_t k, int32_t 
  * (rowptr_out and *nnz_out are still complete).
  * ws: at least rsc_slice_workspace_bytes(A) bytes, 256-byte aligned. */
 size_t rsc_slice_workspace_bytes(const rsc_csr_t *A);
-rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, int32_t *rowptr_out,
-                           int32_t *col_out, float *val_out, int64_t capacity, int64_t *nnz_out,
-                           void *ws, size_t ws_bytes, hipStream_t stream);
+rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, const double *colw,
+                           int32_t *rowptr_out, int32_t *col_out, float *val_out, int64_t capacity,
+                           int64_t *nnz_out, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* -------------------------------------------- randomized sampling --- */
+/* Unbiased column-row sampling (section 2.2, Eq. 2 with the probabilities
+ * of Eq. 3), the alternative to top-k: k i.i.d. draws i_t ~ p over the n
+ * pairs, p_i proportional to ||X[:, i]|| ||B[i, :]|| = sqrt(q_i) (q decoded
+ * from the rsc_pair_scores key; NaN -> 0), each drawn pair scaled by
+ * 1/(k p_{i_t}), so E[approx] = X B. Exactly:
+ *   w_i = floor(sqrt(q_i) * 2^38 / max_j sqrt(q_j)) (int64; if some score is
+ *         +Inf the infinite ones get 2^38 and the rest 0), W = inclusive
+ *         prefix sum of w, total = W[n-1];
+ *   draw t (0 <= t < k): z = t-th output of SplitMix64 seeded with `seed`
+ *         (Steele, Lea & Flood 2014), u = floor(z * total / 2^64),
+ *         i_t = smallest i with W[i] > u;
+ *   count[i] = draws of i; colw[i] = count[i] * total / (k * w_i) (fp64,
+ *         0 if not drawn); mask bit i set iff count[i] > 0.
+ * All decisions are integer, so results are bitwise reproducible. If every
+ * weight is 0 nothing is drawn. ws: rsc_sample_workspace_bytes(n) bytes,
+ * 256-byte aligned. */
+size_t rsc_sample_workspace_bytes(int32_t n);
+rsc_status_t rsc_sample_columns(const uint64_t *key, int32_t n, int32_t k, uint64_t seed,
+                                int32_t *count, double *colw, uint32_t *mask, void *ws,
+                                size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------ A6 / A7 --- */
 /* Sampled-matrix cache (section 3.3.1): keeps the sliced operand and reuses
@@ -174,6 +199,10 @@ rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, int32_t *ro
  *     operands, as in the layer-wise allocation of section 3.2.
  *   rsc_cache_select: top k of the keys last scored, then the slice; records
  *     `step` as the refresh step.
+ *   rsc_cache_refresh_random: scores against B, then the randomized sampler
+ *     (rsc_sample_columns: k_draws draws with `seed`) instead of top-k, and
+ *     the slice with each kept column scaled by its colw; rsc_cache_get then
+ *     reports k = k_draws and no index list (idx_out = NULL).
  *   rsc_cache_get (host only): returns the current slice (its nnz is read
  *     from the device once per refresh, waiting for the refresh if needed),
  *     the ascending kept indices, k, the slice version (0 = never
@@ -191,6 +220,9 @@ rsc_status_t rsc_cache_refresh(rsc_cache_t *cache, const float *B, int32_t d, in
 rsc_status_t rsc_cache_score(rsc_cache_t *cache, const float *B, int32_t d, int64_t ldb,
                              hipStream_t stream);
 rsc_status_t rsc_cache_select(rsc_cache_t *cache, int32_t k, int64_t step, hipStream_t stream);
+rsc_status_t rsc_cache_refresh_random(rsc_cache_t *cache, const float *B, int32_t d, int64_t ldb,
+                                      int32_t k_draws, uint64_t seed, int64_t step,
+                                      hipStream_t stream);
 rsc_status_t rsc_cache_get(rsc_cache_t *cache, int64_t step, rsc_csr_t *slice_out,
                            const int32_t **idx_out, int32_t *k_out, int32_t *needs_refresh_out,
                            uint64_t *version_out);

@@ -55,6 +55,11 @@ def _load():
         lib.orc_greedy.restype = i64
         lib.orc_num_threads.restype = i32
         lib.orc_spmm_mean.argtypes = [i32, vp, vp, vp, vp, i32, i64, vp, i64]
+        lib.orc_splitmix64.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        lib.orc_splitmix64.restype = ctypes.c_uint64
+        lib.orc_sample_columns.argtypes = [i32, vp, i32, ctypes.c_uint64, vp, vp, vp, vp]
+        lib.orc_slice_scaled.argtypes = [i32, vp, vp, vp, vp, vp, vp, vp, vp]
+        lib.orc_slice_scaled.restype = i64
         _lib = lib
     return _lib
 
@@ -177,6 +182,32 @@ def greedy(keys, colnnz, nnz, d, fro_a2, fro_b2, C, alpha):
     bud = _load().orc_greedy(L, n, nnz, ctypes.cast(ptrs, ctypes.c_void_p), _p(colnnz), _p(d_arr),
                              float(fro_a2), _p(fb), C[0], C[1], alpha[0], alpha[1], _p(k_out))
     return [int(x) for x in k_out], int(bud)
+
+
+def splitmix64(seed: int, t: int) -> int:
+    return int(_load().orc_splitmix64(seed, t))
+
+
+def sample_columns(key, k, seed):
+    """Randomized column-row sampling: dict(count, colw, mask, w)."""
+    key = _c(key, np.uint64)
+    n = len(key)
+    out = {"count": np.zeros(n, np.int32), "colw": np.zeros(n, np.float64),
+           "mask": np.zeros((n + 31) // 32, np.uint32), "w": np.zeros(n, np.int64)}
+    _load().orc_sample_columns(n, _p(key), k, seed, _p(out["count"]), _p(out["colw"]), _p(out["mask"]),
+                               _p(out["w"]))
+    return out
+
+
+def slice_scaled(rowptr, col, val, mask, colw):
+    rowptr, col, val = _c(rowptr, np.int32), _c(col, np.int32), _c(val, np.float32)
+    mask, colw = _c(mask, np.uint32), _c(colw, np.float64)
+    n = len(rowptr) - 1
+    ro = np.zeros(n + 1, dtype=np.int32)
+    co = np.zeros(max(len(col), 1), dtype=np.int32)
+    vo = np.zeros(max(len(col), 1), dtype=np.float32)
+    m = _load().orc_slice_scaled(n, _p(rowptr), _p(col), _p(val), _p(mask), _p(colw), _p(ro), _p(co), _p(vo))
+    return ro, co[:m].copy(), vo[:m].copy()
 
 
 def num_threads() -> int:

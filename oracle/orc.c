@@ -312,3 +312,96 @@ void orc_spmm_mean(int32_t n_rows, const int32_t *rowptr, const int32_t *col, co
         }
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Randomized column-row sampling (section 2.2, Eq. 2 with the probabilities
+ * of Eq. 3): k i.i.d. draws i_t ~ p, p_i = ||X[:, i]|| ||Y[i, :]|| / sum_j
+ * (the same product), and the t-th sampled pair scaled by 1/(k p_{i_t}), the
+ * unbiased estimator the section builds on. Readings fixed here:
+ *   - p is held as integer weights w_i = floor(sqrt(q_i) * (2^38 / m)),
+ *     m = max_j sqrt(q_j), q decoded from the key (NaN -> 0), so the CDF is an
+ *     exact int64 prefix sum W_i = w_0 + ... + w_i, total = W_{n-1};
+ *   - draw t uses the t-th output (t = 0, 1, ...) of the SplitMix64
+ *     generator seeded with `seed` (Steele, Lea & Flood 2014),
+ *     u_t = floor(z_t * total / 2^64), and i_t = the smallest i with W_i > u_t;
+ *   - the pairs drawn c_i times enter once, scaled by
+ *     colw_i = c_i * total / (k * w_i) (fp64), i.e. c_i / (k p_i);
+ *   - if some score is +Inf, the infinite ones share the mass uniformly
+ *     (weight 2^38 each, every other weight 0).
+ * Outputs count[i] = c_i, colw[i] (0 where c_i = 0) and the mask of columns
+ * with c_i > 0. If every weight is 0 nothing is drawn. */
+uint64_t orc_splitmix64(uint64_t seed, uint64_t t) {
+    uint64_t z = seed + (t + 1) * 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+static double key_sqrt(uint64_t u) {
+    if (u == 0) return 0.0;
+    uint64_t bits = u - 1;
+    double q;
+    memcpy(&q, &bits, sizeof q);
+    return sqrt(q);
+}
+
+void orc_sample_columns(int32_t n, const uint64_t *key, int32_t k, uint64_t seed, int32_t *count,
+                        double *colw, uint32_t *mask, int64_t *w_out) {
+    int64_t *W = (int64_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(int64_t));
+    int64_t *w = (int64_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(int64_t));
+    double m = 0.0;
+    for (int32_t i = 0; i < n; ++i) {
+        double r = key_sqrt(key[i]);
+        if (r > m) m = r;
+    }
+    double scale = m > 0.0 ? ldexp(1.0, 38) / m : 0.0;
+    int64_t acc = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        double r = key_sqrt(key[i]);
+        /* infinite scores share the mass uniformly */
+        w[i] = isinf(m) ? (isinf(r) ? ((int64_t)1 << 38) : 0) : (int64_t)(r * scale);
+        acc += w[i];
+        W[i] = acc;
+        count[i] = 0;
+        if (w_out) w_out[i] = w[i];
+    }
+    int64_t total = acc;
+    for (int32_t t = 0; total > 0 && t < k; ++t) {
+        uint64_t z = orc_splitmix64(seed, (uint64_t)t);
+        uint64_t u = (uint64_t)(((unsigned __int128)z * (uint64_t)total) >> 64);
+        int32_t lo = 0, hi = n - 1; /* smallest i with W[i] > u */
+        while (lo < hi) {
+            int32_t mid = lo + (hi - lo) / 2;
+            if ((uint64_t)W[mid] > u) hi = mid; else lo = mid + 1;
+        }
+        count[lo] += 1;
+    }
+    memset(mask, 0, (size_t)((n + 31) / 32) * sizeof(uint32_t));
+    for (int32_t i = 0; i < n; ++i) {
+        colw[i] = count[i] ? (double)count[i] * (double)total / ((double)k * (double)w[i]) : 0.0;
+        if (count[i]) mask[i >> 5] |= 1u << (i & 31);
+    }
+    free(W);
+    free(w);
+}
+
+/* Slice with per-column scale: as orc_slice, each kept value becomes
+ * fl32(val * colw[col]) (fp64 product, one rounding). */
+int64_t orc_slice_scaled(int32_t n_rows, const int32_t *rowptr, const int32_t *col, const float *val,
+                         const uint32_t *mask, const double *colw, int32_t *rowptr_out,
+                         int32_t *col_out, float *val_out) {
+    int64_t w = 0;
+    rowptr_out[0] = 0;
+    for (int32_t i = 0; i < n_rows; ++i) {
+        for (int32_t t = rowptr[i]; t < rowptr[i + 1]; ++t) {
+            int32_t c = col[t];
+            if ((mask[c >> 5] >> (c & 31)) & 1u) {
+                col_out[w] = c;
+                val_out[w] = (float)((double)val[t] * colw[c]);
+                ++w;
+            }
+        }
+        rowptr_out[i + 1] = (int32_t)w;
+    }
+    return w;
+}

@@ -31,7 +31,9 @@ EXPORTED = [
     "rsc_col_sqnorms", "rsc_pair_scores",
     "rsc_topk_workspace_bytes", "rsc_topk_select",
     "rsc_slice_workspace_bytes", "rsc_slice_csr",
+    "rsc_sample_workspace_bytes", "rsc_sample_columns",
     "rsc_cache_create", "rsc_cache_refresh", "rsc_cache_score", "rsc_cache_select",
+    "rsc_cache_refresh_random",
     "rsc_cache_get", "rsc_spmm_sampled",
     "rsc_cache_buffers", "rsc_cache_destroy",
     "rsc_k_from_fraction", "rsc_greedy_allocate",
@@ -76,7 +78,10 @@ def lib():
             "rsc_topk_workspace_bytes": ([i32], sz),
             "rsc_topk_select": ([vp, i32, i32, vp, vp, vp, sz, vp], ctypes.c_int),
             "rsc_slice_workspace_bytes": ([csrp], sz),
-            "rsc_slice_csr": ([csrp, vp, vp, vp, vp, i64, vp, vp, sz, vp], ctypes.c_int),
+            "rsc_slice_csr": ([csrp, vp, vp, vp, vp, vp, i64, vp, vp, sz, vp], ctypes.c_int),
+            "rsc_sample_workspace_bytes": ([i32], sz),
+            "rsc_sample_columns": ([vp, i32, i32, ctypes.c_uint64, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+            "rsc_cache_refresh_random": ([vp, vp, i32, i64, i32, ctypes.c_uint64, i64, vp], ctypes.c_int),
             "rsc_cache_create": ([csrp, csrp, i32, vp, ctypes.POINTER(vp)], ctypes.c_int),
             "rsc_cache_refresh": ([vp, vp, i32, i64, i32, i64, vp], ctypes.c_int),
             "rsc_cache_score": ([vp, vp, i32, i64, vp], ctypes.c_int),
@@ -228,7 +233,7 @@ def topk_select(key: torch.Tensor, k: int, ws: torch.Tensor | None = None):
 
 # ---------------------------------------------------------------- A5
 def slice_csr(A: DeviceCsr, mask: torch.Tensor, capacity: int | None = None,
-              ws: torch.Tensor | None = None):
+              ws: torch.Tensor | None = None, colw: torch.Tensor | None = None):
     """(DeviceCsr slice with capacity-sized col/val, nnz' as a device int64
     tensor). The slice's nnz field is left as None-equivalent (capacity)
     until the caller reads nnz'."""
@@ -241,9 +246,23 @@ def slice_csr(A: DeviceCsr, mask: torch.Tensor, capacity: int | None = None,
     s = A.struct()
     need = lib().rsc_slice_workspace_bytes(ctypes.byref(s))
     ws = _workspace(need, dev) if ws is None else ws
-    _check(lib().rsc_slice_csr(ctypes.byref(s), _ptr(mask), rp.data_ptr(), co.data_ptr(), vo.data_ptr(),
-                               cap, nnz_out.data_ptr(), ws.data_ptr(), ws.numel(), _stream()))
+    _check(lib().rsc_slice_csr(ctypes.byref(s), _ptr(mask), _ptr(colw), rp.data_ptr(), co.data_ptr(),
+                               vo.data_ptr(), cap, nnz_out.data_ptr(), ws.data_ptr(), ws.numel(), _stream()))
     return DeviceCsr(A.n_rows, A.n_cols, rp, co, vo, nnz=cap), nnz_out
+
+
+def sample_columns(key: torch.Tensor, k: int, seed: int, ws: torch.Tensor | None = None):
+    """Randomized column-row sampling: (count int32[n], colw float64[n],
+    mask int32[ceil(n/32)] holding uint32 words)."""
+    n = key.numel()
+    count = torch.empty(max(n, 1), dtype=torch.int32, device=key.device)
+    colw = torch.empty(max(n, 1), dtype=torch.float64, device=key.device)
+    mask = torch.empty(max((n + 31) // 32, 1), dtype=torch.int32, device=key.device)
+    need = lib().rsc_sample_workspace_bytes(n)
+    ws = _workspace(need, key.device) if ws is None else ws
+    _check(lib().rsc_sample_columns(key.data_ptr(), n, k, seed, count.data_ptr(), colw.data_ptr(),
+                                    mask.data_ptr(), ws.data_ptr(), ws.numel(), _stream()))
+    return count[:n], colw[:n], mask[: (n + 31) // 32]
 
 
 # ---------------------------------------------------------------- A6 / A7
@@ -269,6 +288,10 @@ class Cache:
 
     def select(self, k: int, step: int) -> None:
         _check(lib().rsc_cache_select(self._h, k, step, _stream()))
+
+    def refresh_random(self, B: torch.Tensor, k_draws: int, seed: int, step: int, d: int | None = None) -> None:
+        d = B.shape[1] if d is None else d
+        _check(lib().rsc_cache_refresh_random(self._h, B.data_ptr(), d, _ld(B), k_draws, seed, step, _stream()))
 
     def get(self, step: int, with_slice: bool = True):
         """dict(slice=CsrStruct or None, idx_ptr, k, needs_refresh, version).

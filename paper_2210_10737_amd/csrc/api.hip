@@ -97,6 +97,11 @@ struct rsc_cache {
     int32_t *colnnz = nullptr;
     uint64_t *key = nullptr;
     double *rn2 = nullptr;  // row square-norms of the last scored dense operand
+    int32_t *count = nullptr;  // randomized refresh: draws per column
+    double *colw = nullptr;    // randomized refresh: per-column scale
+    void *ws_sample = nullptr;
+    size_t ws_sample_bytes = 0;
+    bool random = false;       // the current slice comes from rsc_cache_refresh_random
     int32_t *idx = nullptr;
     uint32_t *mask = nullptr;
     int32_t *s_rowptr = nullptr;
@@ -207,25 +212,42 @@ rsc_status_t rsc_topk_select(const uint64_t *key, int32_t n, int32_t k, int32_t 
     return RSC_OK;
 }
 
+// ------------------------------------------------------------------- randomized sampling
+size_t rsc_sample_workspace_bytes(int32_t n) { return n < 0 ? 0 : rsc::sample_ws_bytes(n); }
+
+rsc_status_t rsc_sample_columns(const uint64_t *key, int32_t n, int32_t k, uint64_t seed, int32_t *count,
+                                double *colw, uint32_t *mask, void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (n < 0 || k < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "n < 0 or k < 0");
+    if (n > 0 && (!key || !count || !colw || !mask))
+        return fail(RSC_ERR_INVALID_ARGUMENT, "key/count/colw/mask is NULL");
+    if (!aligned(key, 8) || !aligned(colw, 8) || !aligned(count, 4) || !aligned(mask, 4))
+        return fail(RSC_ERR_UNSUPPORTED, "misaligned sampler argument");
+    RSC_TRY(check_ws(ws, ws_bytes, rsc::sample_ws_bytes(n), "sample"));
+    RSC_TRY(check_device());
+    RSC_HIP(rsc::sample_launch(key, n, k, seed, count, colw, mask, ws, stream), "sample launch");
+    return RSC_OK;
+}
+
 // ------------------------------------------------------------------- A5
 size_t rsc_slice_workspace_bytes(const rsc_csr_t *A) {
     if (!A || A->nnz < 0) return 0;
     return rsc::slice_ws_bytes(A->nnz);
 }
 
-rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, int32_t *rowptr_out, int32_t *col_out,
-                           float *val_out, int64_t capacity, int64_t *nnz_out, void *ws, size_t ws_bytes,
-                           hipStream_t stream) {
+rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, const double *colw, int32_t *rowptr_out,
+                           int32_t *col_out, float *val_out, int64_t capacity, int64_t *nnz_out, void *ws,
+                           size_t ws_bytes, hipStream_t stream) {
     RSC_TRY(check_csr(A, "A"));
     if (capacity < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "capacity < 0");
     if (!rowptr_out || !nnz_out) return fail(RSC_ERR_INVALID_ARGUMENT, "rowptr_out/nnz_out is NULL");
     if (A->nnz > 0 && !mask) return fail(RSC_ERR_INVALID_ARGUMENT, "mask is NULL");
     if (capacity > 0 && (!col_out || !val_out)) return fail(RSC_ERR_INVALID_ARGUMENT, "col_out/val_out is NULL");
     if (!aligned(nnz_out, 8)) return fail(RSC_ERR_UNSUPPORTED, "nnz_out is not 8-byte aligned");
+    if (!aligned(colw, 8)) return fail(RSC_ERR_UNSUPPORTED, "colw is not 8-byte aligned");
     RSC_TRY(check_ws(ws, ws_bytes, rsc::slice_ws_bytes(A->nnz), "slice"));
     RSC_TRY(check_device());
     RSC_HIP(rsc::slice_launch(A->n_rows, A->nnz, A->rowptr, A->col, A->val, mask, rowptr_out, col_out, val_out,
-                              capacity, nnz_out, ws, stream),
+                              capacity, nnz_out, ws, stream, colw),
             "slice launch");
     if (capacity < A->nnz) {
         int64_t got = 0;
@@ -241,8 +263,8 @@ rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, int32_t *ro
 // ------------------------------------------------------------------- A6 / A7
 static void cache_free(rsc_cache_t *c) {
     if (!c) return;
-    void *dev[] = {c->cn2, c->colnnz, c->key, c->rn2, c->idx, c->mask, c->s_rowptr, c->s_col, c->s_val,
-                   c->d_nnz, c->ws_topk, c->ws_slice, c->ws_spmm};
+    void *dev[] = {c->cn2, c->colnnz, c->key, c->rn2, c->count, c->colw, c->idx, c->mask, c->s_rowptr,
+                   c->s_col, c->s_val, c->d_nnz, c->ws_topk, c->ws_slice, c->ws_spmm, c->ws_sample};
     for (void *p : dev)
         if (p) (void)hipFree(p);
     if (c->h_nnz) (void)hipHostFree(c->h_nnz);
@@ -269,6 +291,7 @@ rsc_status_t rsc_cache_create(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t r
     c->ws_topk_bytes = rsc::topk_ws_bytes(c->n);
     c->ws_slice_bytes = rsc::slice_ws_bytes(X->nnz);
     c->ws_spmm_bytes = rsc::spmm_ws_bytes(X->n_rows, X->nnz);
+    c->ws_sample_bytes = rsc::sample_ws_bytes(c->n);
     struct {
         void **p;
         size_t bytes;
@@ -277,6 +300,8 @@ rsc_status_t rsc_cache_create(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t r
         {(void **)&c->colnnz, sizeof(int32_t) * n},
         {(void **)&c->key, sizeof(uint64_t) * n},
         {(void **)&c->rn2, sizeof(double) * n},
+        {(void **)&c->count, sizeof(int32_t) * n},
+        {(void **)&c->colw, sizeof(double) * n},
         {(void **)&c->idx, sizeof(int32_t) * n},
         {(void **)&c->mask, sizeof(uint32_t) * (size_t)rsc::ceil_div(n, 32)},
         {(void **)&c->s_rowptr, sizeof(int32_t) * ((size_t)X->n_rows + 1)},
@@ -286,6 +311,7 @@ rsc_status_t rsc_cache_create(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t r
         {&c->ws_topk, c->ws_topk_bytes},
         {&c->ws_slice, c->ws_slice_bytes},
         {&c->ws_spmm, c->ws_spmm_bytes},
+        {&c->ws_sample, c->ws_sample_bytes},
     };
     for (auto &a : allocs) {
         if (hipMalloc(a.p, std::max<size_t>(a.bytes, 256)) != hipSuccess) {
@@ -329,6 +355,27 @@ rsc_status_t rsc_cache_select(rsc_cache_t *c, int32_t k, int64_t step, hipStream
     return RSC_OK;
 }
 
+rsc_status_t rsc_cache_refresh_random(rsc_cache_t *c, const float *B, int32_t d, int64_t ldb, int32_t k_draws,
+                                      uint64_t seed, int64_t step, hipStream_t stream) {
+    if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
+    RSC_TRY(check_dense(B, c->n, d, ldb, "B"));
+    if (k_draws < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "k_draws < 0");
+    RSC_TRY(rsc_cache_score(c, B, d, ldb, stream));
+    RSC_HIP(rsc::sample_launch(c->key, c->n, k_draws, seed, c->count, c->colw, c->mask, c->ws_sample, stream),
+            "cache sample");
+    RSC_HIP(rsc::slice_launch(c->X.n_rows, c->X.nnz, c->X.rowptr, c->X.col, c->X.val, c->mask, c->s_rowptr,
+                              c->s_col, c->s_val, c->X.nnz, c->d_nnz, c->ws_slice, stream, c->colw),
+            "cache weighted slice");
+    RSC_HIP(hipMemcpyAsync(c->h_nnz, c->d_nnz, sizeof(int64_t), hipMemcpyDeviceToHost, stream), "cache nnz");
+    RSC_HIP(hipEventRecord(c->ev, stream), "cache event");
+    c->k = k_draws;
+    c->last_step = step;
+    c->version += 1;
+    c->nnz_known = false;
+    c->random = true;
+    return RSC_OK;
+}
+
 rsc_status_t rsc_cache_refresh(rsc_cache_t *c, const float *B, int32_t d, int64_t ldb, int32_t k, int64_t step,
                                hipStream_t stream) {
     if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
@@ -344,7 +391,7 @@ rsc_status_t rsc_cache_get(rsc_cache_t *c, int64_t step, rsc_csr_t *slice_out, c
     if (needs_refresh_out) *needs_refresh_out = (c->version == 0 || step - c->last_step >= c->interval) ? 1 : 0;
     if (version_out) *version_out = c->version;
     if (k_out) *k_out = c->version ? c->k : 0;
-    if (idx_out) *idx_out = c->version ? c->idx : nullptr;
+    if (idx_out) *idx_out = (c->version && !c->random) ? c->idx : nullptr;
     if (slice_out) {
         rsc_csr_t s{};
         s.n_rows = c->X.n_rows;
@@ -375,9 +422,10 @@ rsc_status_t rsc_spmm_sampled(rsc_cache_t *c, const float *B, int32_t d, int64_t
     // the expected kept share k/n of the entries and the k kept source rows
     // choose the feature slice (a function of the arguments only, so results
     // never depend on which calls came before).
-    const int64_t nnz_hint = c->n > 0 ? c->X.nnz * (int64_t)c->k / c->n : 0;
+    const int64_t kk = std::min<int64_t>(c->k, c->n);
+    const int64_t nnz_hint = c->n > 0 ? c->X.nnz * kk / c->n : 0;
     RSC_HIP(rsc::spmm_launch(c->X.n_rows, c->X.nnz, c->s_rowptr, c->s_col, c->s_val, B, d, ldb, Y, ldy,
-                             c->ws_spmm, stream, nnz_hint, c->k),
+                             c->ws_spmm, stream, nnz_hint, kk),
             "spmm_sampled launch");
     return RSC_OK;
 }

@@ -46,7 +46,12 @@ size_t slice_ws_bytes(int64_t nnz);
 hipError_t slice_launch(int32_t n_rows, int64_t nnz, const int32_t *rowptr, const int32_t *col,
                         const float *val, const uint32_t *mask, int32_t *rowptr_out,
                         int32_t *col_out, float *val_out, int64_t capacity, int64_t *nnz_out,
-                        void *ws, hipStream_t stream);
+                        void *ws, hipStream_t stream, const double *colw = nullptr);
+
+// ---- randomized column-row sampling ------------------------------------
+size_t sample_ws_bytes(int32_t n);
+hipError_t sample_launch(const uint64_t *key, int32_t n, int32_t k, uint64_t seed, int32_t *count,
+                         double *colw, uint32_t *mask, void *ws, hipStream_t stream);
 
 // ---- MEAN aggregator operand -------------------------------------------
 hipError_t degree_scale_launch(int32_t n_rows, const int32_t *rowptr, const int32_t *col, const float *val,

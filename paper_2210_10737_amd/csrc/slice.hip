@@ -12,7 +12,8 @@
 //   3. per tile: stage col/val through LDS, scan the kept flags inside the
 //      tile, write the kept entries at their global positions, and write
 //      Rowptr'[i] for every row whose Rowptr[i] falls in the tile.
-// Integer-only and deterministic.
+// Integer-only and deterministic. With a per-column scale (the randomized
+// sampler's 1/(k p)), each kept value becomes fl32(val * colw[col]).
 #include "rsc_internal.h"
 
 namespace rsc {
@@ -83,7 +84,8 @@ __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restri
                                                          const uint32_t *__restrict__ tile_off,
                                                          int32_t *__restrict__ rowptr_out,
                                                          int32_t *__restrict__ col_out,
-                                                         float *__restrict__ val_out, int64_t capacity) {
+                                                         float *__restrict__ val_out, int64_t capacity,
+                                                         const double *__restrict__ colw) {
     __shared__ int32_t s_col[kTile];
     __shared__ float s_val[kTile];
     __shared__ uint32_t s_pre[256];   // kept entries before each thread's run
@@ -127,8 +129,10 @@ __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restri
     for (int j = 0; j < kPer; ++j) {
         if ((bits >> j) & 1u) {
             if (pos < capacity) {
-                col_out[pos] = s_col[kPer * t + j];
-                val_out[pos] = s_val[kPer * t + j];
+                const int32_t c = s_col[kPer * t + j];
+                const float v = s_val[kPer * t + j];
+                col_out[pos] = c;
+                val_out[pos] = colw ? (float)((double)v * colw[c]) : v;
             }
             ++pos;
         }
@@ -167,7 +171,7 @@ size_t slice_ws_bytes(int64_t nnz) {
 hipError_t slice_launch(int32_t n_rows, int64_t nnz, const int32_t *rowptr, const int32_t *col,
                         const float *val, const uint32_t *mask, int32_t *rowptr_out,
                         int32_t *col_out, float *val_out, int64_t capacity, int64_t *nnz_out,
-                        void *ws, hipStream_t stream) {
+                        void *ws, hipStream_t stream, const double *colw) {
     if (nnz == 0) {
         zero_rows_kernel<<<(unsigned)std::min<int64_t>(ceil_div((int64_t)n_rows + 1, 256), 1024), 256, 0,
                            stream>>>(rowptr_out, (int64_t)n_rows + 1, nnz_out);
@@ -180,7 +184,7 @@ hipError_t slice_launch(int32_t n_rows, int64_t nnz, const int32_t *rowptr, cons
     slice_count_kernel<<<nt, 256, 0, stream>>>(col, nnz, mask, tile_cnt);
     slice_scan_kernel<<<1, 1024, 0, stream>>>(nt, tile_cnt, tile_off, nnz_out);
     slice_emit_kernel<<<nt, 256, 0, stream>>>(rowptr, n_rows, col, val, nnz, mask, tile_off, rowptr_out,
-                                              col_out, val_out, capacity);
+                                              col_out, val_out, capacity, colw);
     return hipGetLastError();
 }
 

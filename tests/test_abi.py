@@ -34,7 +34,7 @@ def test_header_matches_exports():
     L = rsc.lib()
     for name in declared:
         assert getattr(L, name) is not None
-    assert L.rsc_abi_version() == 2
+    assert L.rsc_abi_version() == 3
 
 
 def test_status_strings():
@@ -90,12 +90,19 @@ def test_topk_and_slice_argument_validation():
         "RSC_ERR_CAPACITY"
     A = _csr()
     sneed = L.rsc_slice_workspace_bytes(ctypes.byref(A))
-    assert _err(L.rsc_slice_csr(ctypes.byref(A), 0x1000, 0x2000, 0x3000, 0x4000, -1, 0x5000, 0x10000,
+    assert _err(L.rsc_slice_csr(ctypes.byref(A), 0x1000, None, 0x2000, 0x3000, 0x4000, -1, 0x5000, 0x10000,
                                 sneed, None)) == "RSC_ERR_INVALID_ARGUMENT"
-    assert _err(L.rsc_slice_csr(ctypes.byref(A), None, 0x2000, 0x3000, 0x4000, 4, 0x5000, 0x10000,
+    assert _err(L.rsc_slice_csr(ctypes.byref(A), None, None, 0x2000, 0x3000, 0x4000, 4, 0x5000, 0x10000,
                                 sneed, None)) == "RSC_ERR_INVALID_ARGUMENT"
-    assert _err(L.rsc_slice_csr(ctypes.byref(A), 0x1000, 0x2000, 0x3000, 0x4000, 4, 0x5004, 0x10000,
+    assert _err(L.rsc_slice_csr(ctypes.byref(A), 0x1000, None, 0x2000, 0x3000, 0x4000, 4, 0x5004, 0x10000,
                                 sneed, None)) == "RSC_ERR_UNSUPPORTED"
+    assert _err(L.rsc_slice_csr(ctypes.byref(A), 0x1000, 0x1004, 0x2000, 0x3000, 0x4000, 4, 0x5000, 0x10000,
+                                sneed, None)) == "RSC_ERR_UNSUPPORTED"
+    swn = L.rsc_sample_workspace_bytes(100)
+    assert _err(L.rsc_sample_columns(0x1000, 100, -1, 0, 0x2000, 0x3000, 0x4000, 0x10000, swn, None)) == \
+        "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(L.rsc_sample_columns(0x1000, 100, 5, 0, 0x2000, 0x3000, 0x4000, 0x10000, swn - 1, None)) == \
+        "RSC_ERR_CAPACITY"
 
 
 def test_cache_argument_validation():

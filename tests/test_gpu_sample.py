@@ -1,0 +1,99 @@
+"""Randomized column-row sampling on the GPU (Eq. 2 with Eq. 3's
+probabilities, scale 1/(k p)) against the oracle: draw counts, per-column
+scales and masks bit for bit, the scaled slice bit for bit, the sampled
+product within fp32 tolerance, and unbiasedness over seeds."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2210_10737_amd as rsc
+import synth
+
+pytestmark = pytest.mark.gpu
+FLT_MIN = np.float32(np.finfo(np.float32).tiny)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu(gpu):
+    yield
+
+
+def keys_for(name, d, seed):
+    A = synth.make_graph(name, 0)
+    cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)
+    return A, oracle.pair_keys(cn2, synth.dense_normal(A.n, d, seed=seed))["key"]
+
+
+def _check(key, k, seed):
+    o = oracle.sample_columns(key, k, seed)
+    cnt, colw, mask = rsc.sample_columns(torch.from_numpy(key.view(np.int64)).cuda(), k, seed)
+    assert np.array_equal(cnt.cpu().numpy(), o["count"])
+    assert np.array_equal(colw.cpu().numpy().view(np.uint64), o["colw"].view(np.uint64))
+    assert np.array_equal(mask.cpu().numpy().view(np.uint32), o["mask"])
+    return o
+
+
+@pytest.mark.parametrize("k,seed", [(0, 1), (1, 2), (2048, 3), (20_000, 4)])
+def test_sample_columns_bitwise_tiny(k, seed):
+    _, key = keys_for("tiny", 64, 1)
+    key = key.copy()
+    key[::37] = 0
+    _check(key, k, seed)
+
+
+def test_sample_columns_bitwise_full_size():
+    _, key = keys_for("gcn2", 100, 5)
+    o = _check(key, 215_054, 11)
+    assert o["count"].sum() == 215_054
+
+
+def test_sample_columns_degenerate():
+    n = 5000
+    _check(np.zeros(n, np.uint64), 100, 1)                      # nothing to draw
+    key = np.arange(1, n + 1, dtype=np.uint64) << np.uint64(40)
+    inf_key = np.uint64(0x7FF0000000000000 + 1)
+    key[[10, 4000]] = inf_key                                   # infinite scores share the mass
+    o = _check(key, 999, 7)
+    assert o["count"][[10, 4000]].sum() == 999
+
+
+def test_cache_random_refresh_and_sampled_product():
+    A = synth.random_csr(3000, 2500, 40, seed=51, hub_rows=2, hub_len=2200, empty_frac=0.1)
+    AT = synth.transpose(A, 2500)
+    cache = rsc.Cache(rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, 2500),
+                      rsc.DeviceCsr.from_host(AT.rowptr, AT.col, AT.val, 3000), refresh_interval=10)
+    B = synth.dense_normal(2500, 96, seed=52)
+    Bd = torch.from_numpy(B).cuda()
+    cache.refresh_random(Bd, 1500, seed=9, step=0)
+    snap = rsc.cache_snapshot(cache)
+    assert snap["k"] == 1500 and snap["idx_ptr"] is None
+    cn2, _ = oracle.col_sqnorms(AT.rowptr, AT.val)
+    o = oracle.sample_columns(oracle.pair_keys(cn2, B)["key"], 1500, 9)
+    ro, co, vo = oracle.slice_scaled(A.rowptr, A.col, A.val, o["mask"], o["colw"])
+    assert np.array_equal(snap["rowptr"], ro) and np.array_equal(snap["col"], co)
+    assert np.array_equal(snap["val"].view(np.uint32), vo.view(np.uint32))
+    Ys = cache.spmm_sampled(Bd).cpu().numpy()
+    Yo, S = oracle.spmm(ro, co, vo, B, with_mag=True)
+    assert np.max(np.abs(Ys.astype(np.float64) - Yo) / np.maximum(S, FLT_MIN)) <= 1e-4
+    cache.close()
+
+
+def test_sampled_product_unbiased_on_gpu():
+    A = synth.random_csr(400, 300, 20, seed=61)
+    AT = synth.transpose(A, 300)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, 300)
+    cache = rsc.Cache(X, rsc.DeviceCsr.from_host(AT.rowptr, AT.col, AT.val, 400))
+    B = synth.dense_normal(300, 32, seed=62)
+    Bd = torch.from_numpy(B).cuda()
+    exact = rsc.spmm(X, Bd).double()
+    acc = torch.zeros_like(exact)
+    first = None
+    seeds = 300
+    for s in range(seeds):
+        cache.refresh_random(Bd, 60, seed=1000 + s, step=s)
+        Y = cache.spmm_sampled(Bd).double()
+        acc += Y
+        first = Y.clone() if first is None else first
+    assert float(torch.linalg.norm(acc / seeds - exact)) < 0.2 * float(torch.linalg.norm(first - exact))
+    cache.close()

@@ -408,3 +408,79 @@ def test_spmm_mean_dense_and_empty_rows(small_gen):
     mag = (np.abs(D) @ np.abs(B.astype(np.float64))) / np.maximum(deg, 1)[:, None]
     assert np.all(np.abs(Y - ref) <= 2.0 ** -24 * np.abs(ref) + 1e-12 * mag + 1e-300)
     assert np.all(Y[deg == 0] == 0)
+
+
+# ---------------------------------------------------------------- randomized sampling
+def test_splitmix64_reference_outputs():
+    g = json.load(open(os.path.join(GOLDEN, "splitmix64_seed1234567.json")))
+    assert [oracle.splitmix64(g["seed"], t) for t in range(len(g["outputs"]))] == [int(x) for x in g["outputs"]]
+
+
+def _weights_by_definition(key):
+    """w_i = floor(sqrt(q_i) * 2^38 / max_j sqrt(q_j)), written independently."""
+    import math
+    r = []
+    for u in key:
+        u = int(u)
+        r.append(0.0 if u == 0 else math.sqrt(struct.unpack("<d", struct.pack("<Q", u - 1))[0]))
+    m = max(r)
+    scale = math.ldexp(1.0, 38) / m
+    return np.array([int(x * scale) for x in r], np.int64)
+
+
+def test_sample_columns_counts_weights_and_scale():
+    A = synth.make_graph("tiny", 0)
+    cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)
+    key = oracle.pair_keys(cn2, synth.dense_normal(A.n, 16, seed=3))["key"]
+    key[::50] = 0                                            # NaN pairs never drawn
+    o = oracle.sample_columns(key, 1000, seed=7)
+    assert o["count"].sum() == 1000
+    assert np.array_equal(o["w"], _weights_by_definition(key))
+    assert np.all(o["count"][::50] == 0)
+    drawn = np.nonzero(o["count"])[0]
+    assert np.array_equal(mask_of(drawn, A.n), o["mask"])
+    total = float(o["w"].sum())
+    want = o["count"][drawn] * total / (1000.0 * o["w"][drawn])
+    assert np.array_equal(o["colw"][drawn], want) and not o["colw"][o["count"] == 0].any()
+
+
+def test_sample_columns_single_weight_is_exact_slice():
+    key = np.zeros(40, np.uint64)
+    key[17] = key_of(2.5)
+    o = oracle.sample_columns(key, 33, seed=1)
+    assert o["count"][17] == 33 and o["count"].sum() == 33 and o["colw"][17] == 1.0
+
+
+def test_sample_columns_frequencies():
+    # 12 pairs with sqrt(q) = 1..12: p_i = i / 78
+    key = np.array([key_of(float(i) ** 2) for i in range(1, 13)], np.uint64)
+    k = 200_000
+    o = oracle.sample_columns(key, k, seed=99)
+    p = o["w"] / o["w"].sum()
+    sd = np.sqrt(k * p * (1 - p))
+    assert np.all(np.abs(o["count"] - k * p) <= 5 * sd)
+    np.testing.assert_allclose(p, np.arange(1, 13) / 78.0, rtol=1e-9)
+
+
+def test_sampled_product_is_unbiased():
+    """E[sum_i colw_i A[:, i] B[i, :]] = A B (Eq. 2 with s = 1/(k p)): the
+    mean over many seeds converges to the exact product while one draw does
+    not."""
+    A = synth.random_csr(60, 50, 12, seed=8)
+    B = synth.dense_normal(50, 6, seed=9)
+    AT = synth.transpose(A, 50)
+    cn2, _ = oracle.col_sqnorms(AT.rowptr, AT.val)
+    key = oracle.pair_keys(cn2, B)["key"]
+    exact = dense(A, 50) @ B.astype(np.float64)
+    acc = np.zeros_like(exact)
+    one = None
+    seeds = 400
+    for s in range(seeds):
+        o = oracle.sample_columns(key, 10, seed=s)
+        ro, co, vo = oracle.slice_scaled(A.rowptr, A.col, A.val, o["mask"], o["colw"])
+        Y = oracle.spmm(ro, co, vo, B).astype(np.float64)
+        acc += Y
+        one = Y if one is None else one
+    err_mean = np.linalg.norm(acc / seeds - exact)
+    err_one = np.linalg.norm(one - exact)
+    assert err_mean < 0.2 * err_one
