@@ -17,7 +17,8 @@ peak. `cpu_baseline` times the oracle (all its OpenMP threads) on a bounded
 sample of the same step.
 
 usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload copurchase]
-                       [--budget-pct 30] [--no-cpu-baseline]
+                       [--budget-pct 30] [--aggregator gcn|mean] [--selector topk|random]
+                       [--no-cpu-baseline]
        python bench.py --workload gcn2-train [--budget-pct 10]   (training-step comparison)
 """
 from __future__ import annotations
@@ -53,11 +54,21 @@ def refresh_bytes(n: int, nnz: int, nnz_kept: int, k: int, d: int) -> int:
             + 4 * k + n // 8)
 
 
+def refresh_random_bytes(n: int, nnz: int, nnz_kept: int, k: int, d: int) -> int:
+    """Algorithmic bytes of one randomized refresh: B row norms with cn2 in and
+    keys out (4nd + 16n); key max and weight passes (16n), w out and back in
+    (16n), the prefix W out (8n); k draws (one 8-byte CDF read and one 4-byte
+    count update each); count zeroing, the per-column pass over count, w and W
+    writing colw (4n + 20n + 8n) and the mask (n/8); the slice as for top-k
+    (12 nnz + 8(n+1) + 8 nnz') plus one 8-byte scale per kept entry."""
+    return (4 * n * d + 16 * n + 16 * n + 16 * n + 8 * n + 12 * k + 32 * n + n // 8
+            + 12 * nnz + 8 * (n + 1) + 16 * nnz_kept)
+
+
 def kernel_source_digest() -> str:
     h = hashlib.sha256()
-    for f in ("spmm.hip", "rsc_internal.h"):
-        with open(os.path.join(ROOT, "paper_2210_10737_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    with open(os.path.join(ROOT, "paper_2210_10737_amd", "csrc", "spmm.hip"), "rb") as fh:
+        h.update(fh.read())
     return h.hexdigest()[:16]
 
 
@@ -146,18 +157,28 @@ def train_bench(args) -> int:
         for s in range(args.warmup):
             model.train_step(X, Y, opt, s)
         torch.cuda.synchronize()
+        for layer in (model.agg1, model.agg2):
+            layer.timings = []   # events around each SpMM: its share of the step (Fig. 1)
         t0 = time.perf_counter()
         losses = []
         for s in range(args.warmup, args.warmup + args.steps):
             losses.append(model.train_step(X, Y, opt, s).detach())
         torch.cuda.synchronize()
         ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        spmm_ms = {"forward": 0.0, "backward": 0.0}
+        for layer in (model.agg1, model.agg2):
+            for kind, a, b in layer.timings:
+                spmm_ms[kind] += a.elapsed_time(b) / args.steps
+            layer.timings = None
         hist = model.controller.history[args.warmup:]
         greedy = [r.greedy_s * 1e3 for r in hist if r.mode == "score"]
         results[name] = {"ms_per_step": round(ms, 3), "final_loss": round(float(losses[-1]), 5),
                          "refresh_steps": sum(r.mode == "score" for r in hist),
                          "greedy_ms_per_call": round(float(np.mean(greedy)), 2) if greedy else None,
-                         "k_per_layer": hist[-1].k}
+                         "k_per_layer": hist[-1].k,
+                         "spmm_fwd_ms_per_step": round(spmm_ms["forward"], 3),
+                         "spmm_bwd_ms_per_step": round(spmm_ms["backward"], 3),
+                         "spmm_share": round((spmm_ms["forward"] + spmm_ms["backward"]) / ms, 4)}
         model.close()
         del model, opt
         torch.cuda.empty_cache()
@@ -212,6 +233,10 @@ def main() -> int:
     ap.add_argument("--aggregator", choices=("gcn", "mean"), default="gcn",
                     help="gcn: A_hat = D^-1/2 (A+I) D^-1/2 (symmetric); mean: the MEAN aggregator "
                          "D^-1 (A+I) forward, its transpose (A+I) D^-1 in the backward")
+    ap.add_argument("--selector", choices=("topk", "random"), default="topk",
+                    help="topk: the k pairs with the largest scores, unscaled (section 2.2.1); random: k "
+                         "i.i.d. draws with p_i proportional to the pair score, scaled by 1/(k p_i) "
+                         "(Eq. 2 with Eq. 3)")
     ap.add_argument("--staleness-steps", type=int, default=60,
                     help="gcn2-train only: steps of the untimed selection-staleness run (0 = skip)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -278,7 +303,10 @@ def main() -> int:
         if cache.get(s, with_slice=False)["needs_refresh"]:
             r0, r1 = ev(), ev()
             r0.record()
-            cache.refresh(G, k, step=s)
+            if args.selector == "topk":
+                cache.refresh(G, k, step=s)
+            else:
+                cache.refresh_random(G, k, seed=args.seed * 1_000_003 + s, step=s)
             r1.record()
             if timed:
                 records.append(("refresh", r0, r1))
@@ -307,7 +335,13 @@ def main() -> int:
         per[kind].append(a.elapsed_time(b))
     snap = cache.get(args.warmup + args.steps)
     nnz_kept = int(snap["slice"].nnz)
-    idx = rsc.copy_to_host(snap["idx_ptr"], snap["k"], np.int32)
+    mask_words = rsc.copy_to_host(cache.buffers()[4], (n + 31) // 32, np.uint32)
+    idx = np.flatnonzero(np.unpackbits(mask_words.view(np.uint8), bitorder="little")[:n])
+    # approximation quality of the last backward (a diagnostic outside the
+    # timed region): relative Frobenius error of the sampled product
+    Yx = rsc.spmm(XB, G)
+    approx_err = float(torch.linalg.norm((Yb - Yx).double()) / torch.linalg.norm(Yx.double()))
+    del Yx
     deg = np.diff(A.rowptr)
     exact_ms = float(np.mean(per["exact"]))
     sampled_ms = float(np.mean(per["sampled"]))
@@ -315,8 +349,9 @@ def main() -> int:
     ms_per_step = max(wall * 1e3, gpu_ms) / args.steps
 
     b_exact = spmm_bytes(n, nnz, n, d)
-    b_sampled = spmm_bytes(n, nnz_kept, k, d)
-    b_refresh = refresh_bytes(n, nnz, nnz_kept, k, d)
+    b_sampled = spmm_bytes(n, nnz_kept, len(idx), d)
+    b_refresh = (refresh_bytes(n, nnz, nnz_kept, k, d) if args.selector == "topk"
+                 else refresh_random_bytes(n, nnz, nnz_kept, k, d))
     step_bytes = b_exact + b_sampled + b_refresh / args.refresh
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     achieved = b_exact / (exact_ms * 1e-3) / 1e9
@@ -337,14 +372,17 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": args.workload, "aggregator": args.aggregator, "graph": w.description,
                    "n": n, "nnz": nnz, "d": d,
-                   "budget_pct": pct, "k": k, "refresh_interval": args.refresh, "seed": args.seed},
+                   "budget_pct": pct, "k": k, "selector": args.selector, "refresh_interval": args.refresh,
+                   "seed": args.seed},
         "exact_spmm_ms": round(exact_ms, 4),
         "sampled_spmm_ms": round(sampled_ms, 4),
         "refresh_ms": None if refresh_ms is None else round(refresh_ms, 4),
         "sampled_speedup": round(exact_ms / sampled_ms, 3),
         "backward_amortised_ms": round(sampled_ms + (refresh_ms or 0.0) / args.refresh, 4),
         "amortised_speedup": round(exact_ms / (sampled_ms + (refresh_ms or 0.0) / args.refresh), 3),
+        "columns_kept": int(len(idx)),
         "nnz_kept": nnz_kept,
+        "approx_rel_fro_error": round(approx_err, 5),
         "kept_nnz_frac": round(nnz_kept / nnz, 4),
         "mean_degree_selected": round(float(deg[idx].mean()), 2) if len(idx) else None,
         "mean_degree_all": round(float(deg.mean()), 2),
@@ -358,10 +396,14 @@ def main() -> int:
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "algorithmic_bytes_per_launch": b_exact,
             "avg_launch_ms": round(exact_ms, 4),
-            "traffic": load_traffic(digest, b_exact),
+            "traffic": None,
             "kernel_src_digest": digest,
         },
     }
+    traffic = load_traffic(digest, b_exact) if args.workload == "copurchase" and args.aggregator == "gcn" else None
+    if traffic is not None:
+        out["roofline"]["traffic"] = round(traffic["total_bytes"])
+        out["roofline"]["traffic_detail"] = traffic
     cache.close()
     del X, XB, XT, H, G, Y, Yb, ws
     torch.cuda.empty_cache()
@@ -373,7 +415,7 @@ def main() -> int:
         torch.cuda.synchronize()
         out["copy_probe_bytes"] = src.numel() * 4
         del src, dst
-    if not args.no_cpu_baseline and args.aggregator == "gcn":
+    if not args.no_cpu_baseline and args.aggregator == "gcn" and args.selector == "topk":
         rows = args.cpu_rows or n
         print(f"[bench] gpu done ({ms_per_step:.3f} ms/step); timing the oracle on {rows} rows",
               file=sys.stderr, flush=True)

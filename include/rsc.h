@@ -165,8 +165,9 @@ rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, const doubl
  * pairs, p_i proportional to ||X[:, i]|| ||B[i, :]|| = sqrt(q_i) (q decoded
  * from the rsc_pair_scores key; NaN -> 0), each drawn pair scaled by
  * 1/(k p_{i_t}), so E[approx] = X B. Exactly:
- *   w_i = floor(sqrt(q_i) * 2^38 / max_j sqrt(q_j)) (int64; if some score is
- *         +Inf the infinite ones get 2^38 and the rest 0), W = inclusive
+ *   w_i = floor(sqrt(q_i) * 2^S / max_j sqrt(q_j)) (int64; S = 38 for
+ *         n <= 2^24, else 62 - ceil(log2 n), so total <= 2^62; if some score
+ *         is +Inf the infinite ones get 2^S and the rest 0), W = inclusive
  *         prefix sum of w, total = W[n-1];
  *   draw t (0 <= t < k): z = t-th output of SplitMix64 seeded with `seed`
  *         (Steele, Lea & Flood 2014), u = floor(z * total / 2^64),

@@ -318,16 +318,17 @@ void orc_spmm_mean(int32_t n_rows, const int32_t *rowptr, const int32_t *col, co
  * of Eq. 3): k i.i.d. draws i_t ~ p, p_i = ||X[:, i]|| ||Y[i, :]|| / sum_j
  * (the same product), and the t-th sampled pair scaled by 1/(k p_{i_t}), the
  * unbiased estimator the section builds on. Readings fixed here:
- *   - p is held as integer weights w_i = floor(sqrt(q_i) * (2^38 / m)),
+ *   - p is held as integer weights w_i = floor(sqrt(q_i) * (2^S / m)),
  *     m = max_j sqrt(q_j), q decoded from the key (NaN -> 0), so the CDF is an
- *     exact int64 prefix sum W_i = w_0 + ... + w_i, total = W_{n-1};
+ *     exact int64 prefix sum W_i = w_0 + ... + w_i, total = W_{n-1}; S = 38
+ *     for n <= 2^24, else 62 - ceil(log2 n), so that total <= 2^62;
  *   - draw t uses the t-th output (t = 0, 1, ...) of the SplitMix64
  *     generator seeded with `seed` (Steele, Lea & Flood 2014),
  *     u_t = floor(z_t * total / 2^64), and i_t = the smallest i with W_i > u_t;
  *   - the pairs drawn c_i times enter once, scaled by
  *     colw_i = c_i * total / (k * w_i) (fp64), i.e. c_i / (k p_i);
  *   - if some score is +Inf, the infinite ones share the mass uniformly
- *     (weight 2^38 each, every other weight 0).
+ *     (weight 2^S each, every other weight 0).
  * Outputs count[i] = c_i, colw[i] (0 where c_i = 0) and the mask of columns
  * with c_i > 0. If every weight is 0 nothing is drawn. */
 uint64_t orc_splitmix64(uint64_t seed, uint64_t t) {
@@ -354,12 +355,18 @@ void orc_sample_columns(int32_t n, const uint64_t *key, int32_t k, uint64_t seed
         double r = key_sqrt(key[i]);
         if (r > m) m = r;
     }
-    double scale = m > 0.0 ? ldexp(1.0, 38) / m : 0.0;
+    int bits = 38; /* weight resolution S */
+    if (n > (1 << 24)) {
+        int lg = 0;
+        while (((int64_t)1 << lg) < (int64_t)n) ++lg;
+        bits = 62 - lg;
+    }
+    double scale = m > 0.0 ? ldexp(1.0, bits) / m : 0.0;
     int64_t acc = 0;
     for (int32_t i = 0; i < n; ++i) {
         double r = key_sqrt(key[i]);
         /* infinite scores share the mass uniformly */
-        w[i] = isinf(m) ? (isinf(r) ? ((int64_t)1 << 38) : 0) : (int64_t)(r * scale);
+        w[i] = isinf(m) ? (isinf(r) ? ((int64_t)1 << bits) : 0) : (int64_t)(r * scale);
         acc += w[i];
         W[i] = acc;
         count[i] = 0;

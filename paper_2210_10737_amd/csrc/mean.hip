@@ -19,7 +19,7 @@ __global__ __launch_bounds__(256) void degree_scale_kernel(int32_t n_rows, const
     if (r >= n_rows) return;
     const int32_t s = rowptr[r], e = rowptr[r + 1];
     const int32_t row_len = e - s;
-    for (int32_t t = s + lane; t < e; t += 64) {
+    for (int64_t t = (int64_t)s + lane; t < e; t += 64) {  // int64: t + 64 may pass 2^31 - 1
         int32_t deg = row_len;
         if (by_column) {
             const int32_t c = col[t];

@@ -12,15 +12,6 @@ namespace rsc {
 constexpr int kWave = 64;
 
 // ---- SpMM --------------------------------------------------------------
-// Rows with more than kLongRow entries are processed by a whole 8-wave
-// block (waves take interleaved runs of 64 entries, then a fixed-order LDS
-// reduction); shorter rows by one wave. Long rows are handed out to
-// persistent blocks through an atomic counter.
-constexpr int kLongRow = 1024;
-constexpr int kSpmmRowWaves = 4;      // rows (waves) per block of the row kernel
-constexpr int kSpmmLongWaves = 8;     // waves per block of the long-row kernel
-constexpr int kSpmmLongBlocks = 1024;  // persistent blocks that walk the long-row list
-
 size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz);
 // nnz_bound sizes the long-row list; nnz_hint (expected entries) and
 // n_src_hint (distinct B rows the entries reference) choose the feature slice.

@@ -3,8 +3,9 @@
 // drawn pair scaled by 1/(k p_{i_t}).
 //
 // Every decision is integer, so the draws are reproducible bit for bit:
-//   * p is held as integer weights w_i = floor(sqrt(q_i) * 2^38 / m),
-//     m = max_j sqrt(q_j) (a max over the keys, order-free);
+//   * p is held as integer weights w_i = floor(sqrt(q_i) * 2^S / m),
+//     m = max_j sqrt(q_j) (a max over the keys, order-free), with S = 38 up
+//     to 2^24 pairs and 62 - ceil(log2 n) above, so the total stays <= 2^62;
 //   * the CDF W_i = w_0 + ... + w_i is an exact int64 inclusive scan;
 //   * draw t takes the t-th output z_t of the SplitMix64 generator seeded
 //     with `seed`, u_t = floor(z_t * total / 2^64), and i_t = the smallest i
@@ -46,12 +47,12 @@ __global__ __launch_bounds__(256) void max_key_kernel(const uint64_t *__restrict
 }
 
 // w_i and the per-tile sums of w
-__global__ __launch_bounds__(256) void weights_kernel(const uint64_t *__restrict__ key, int32_t n,
+__global__ __launch_bounds__(256) void weights_kernel(const uint64_t *__restrict__ key, int32_t n, int bits,
                                                       const SampleWs *__restrict__ h, int64_t *__restrict__ w,
                                                       int64_t *__restrict__ tile_sum) {
     __shared__ int64_t s[4];
     const double m = key_sqrt(h->max_key);
-    const double scale = m > 0.0 ? 274877906944.0 / m : 0.0;  // 2^38 / m
+    const double scale = m > 0.0 ? ldexp(1.0, bits) / m : 0.0;  // 2^S / m
     const int64_t ts = (int64_t)blockIdx.x * kScanTile;
     int64_t acc = 0;
     for (int j = 0; j < kScanTile / 256; ++j) {
@@ -59,7 +60,7 @@ __global__ __launch_bounds__(256) void weights_kernel(const uint64_t *__restrict
         if (i < n) {
             const double r = key_sqrt(key[i]);
             // infinite scores share the mass uniformly
-            const int64_t wi = isinf(m) ? (isinf(r) ? (int64_t)274877906944 : 0) : (int64_t)(r * scale);
+            const int64_t wi = isinf(m) ? (isinf(r) ? ((int64_t)1 << bits) : 0) : (int64_t)(r * scale);
             w[i] = wi;
             acc += wi;
         }
@@ -187,7 +188,13 @@ hipError_t sample_launch(const uint64_t *key, int32_t n, int32_t k, uint64_t see
     sample_init_kernel<<<1, 1, 0, stream>>>(h);
     zero_i32_kernel<<<g, 256, 0, stream>>>(count, n);
     max_key_kernel<<<std::min<unsigned>(g, 1024), 256, 0, stream>>>(key, n, h);
-    weights_kernel<<<nt, 256, 0, stream>>>(key, n, h, w, tile);
+    int bits = 38;  // weight resolution S
+    if (n > (1 << 24)) {
+        int lg = 0;
+        while ((int64_t{1} << lg) < (int64_t)n) ++lg;
+        bits = 62 - lg;
+    }
+    weights_kernel<<<nt, 256, 0, stream>>>(key, n, bits, h, w, tile);
     tile_scan_kernel<<<1, 1024, 0, stream>>>(tile, nt);
     prefix_kernel<<<nt, 256, 0, stream>>>(w, n, tile, W);
     if (k > 0) draw_kernel<<<(unsigned)ceil_div(k, 256), 256, 0, stream>>>(W, n, k, seed, count);

@@ -140,7 +140,7 @@ __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restri
     // Rowptr'[i] for the rows whose Rowptr[i] lies in [ts, te) (and, in the
     // last tile, also those equal to nnz).
     const int32_t r0 = s_rows[0], r1 = s_rows[1];
-    for (int32_t i = r0 + t; i < r1; i += 256) {
+    for (int64_t i = (int64_t)r0 + t; i < r1; i += 256) {
         const int64_t off = (int64_t)rowptr[i] - ts;
         uint32_t c;
         if (off >= kTile || ts + off >= te) {

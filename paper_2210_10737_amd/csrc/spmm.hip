@@ -22,6 +22,16 @@
 #include "rsc_internal.h"
 
 namespace rsc {
+
+// Rows with more than kLongRow entries are processed by a whole 8-wave
+// block (waves take interleaved runs of 64 entries, then a fixed-order LDS
+// reduction); shorter rows by one wave. Long rows are handed out to
+// persistent blocks through an atomic counter.
+constexpr int kLongRow = 1024;
+constexpr int kSpmmRowWaves = 4;      // rows (waves) per block of the row kernel
+constexpr int kSpmmLongWaves = 8;     // waves per block of the long-row kernel
+constexpr int kSpmmLongBlocks = 1024;  // persistent blocks that walk the long-row list
+
 namespace {
 
 constexpr int kUnroll = 8;
@@ -93,13 +103,13 @@ template <int LPE, int NV>
 __device__ __forceinline__ void accumulate_runs(const int32_t *__restrict__ col,
                                                 const float *__restrict__ val,
                                                 const float *__restrict__ B, int64_t ldb,
-                                                int32_t beg, int32_t end, int32_t stride,
+                                                int64_t beg, int64_t end, int32_t stride,
                                                 const bool (&act)[NV], int lane,
                                                 double (&acc)[NV][4]) {
     constexpr int G = Layout<LPE>::G;
     const int g = lane / LPE, sl = lane % LPE;
-    for (int32_t base = beg; base < end; base += stride) {
-        const int32_t cnt = __builtin_amdgcn_readfirstlane(min(kWave, end - base));
+    for (int64_t base = beg; base < end; base += stride) {  // int64: base + stride may pass 2^31 - 1
+        const int32_t cnt = __builtin_amdgcn_readfirstlane((int32_t)min<int64_t>(kWave, end - base));
         int32_t my_c = 0;
         float my_v = 0.f;
         if (lane < cnt) {
@@ -225,7 +235,7 @@ __global__ __launch_bounds__(kSpmmLongWaves * 64) void spmm_long_kernel(
         double acc[NV][4];
 #pragma unroll
         for (int q = 0; q < NV; ++q) acc[q][0] = acc[q][1] = acc[q][2] = acc[q][3] = 0.0;
-        accumulate_runs<LPE, NV>(col, val, B, ldb, s + kWave * wave, e, kWave * kSpmmLongWaves, act,
+        accumulate_runs<LPE, NV>(col, val, B, ldb, (int64_t)s + kWave * wave, e, kWave * kSpmmLongWaves, act,
                                  lane, acc);
 #pragma unroll
         for (int q = 0; q < NV; ++q)

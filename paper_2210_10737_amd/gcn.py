@@ -36,18 +36,23 @@ class _Aggregate(torch.autograd.Function):
     @staticmethod
     def forward(ctx, J: torch.Tensor, layer: "AggregationLayer") -> torch.Tensor:
         ctx.layer = layer
-        return spmm(layer.A, J.contiguous(), ws=layer.ws)
+        t = layer._tick()
+        P = spmm(layer.A, J.contiguous(), ws=layer.ws)
+        layer._tock(t, "forward")
+        return P
 
     @staticmethod
     def backward(ctx, grad_P: torch.Tensor):
         layer = ctx.layer
         g = grad_P.contiguous()
+        t = layer._tick()
         if layer.mode == "sampled":
             grad_J = layer.cache.spmm_sampled(g)
         else:
             grad_J = spmm(layer.AT, g, ws=layer.ws)
-            if layer.mode == "score":
-                layer.cache.score(g)
+        layer._tock(t, "backward")
+        if layer.mode == "score":
+            layer.cache.score(g)
         return grad_J, None
 
 
@@ -65,6 +70,20 @@ class AggregationLayer:
         self.ws = torch.empty(max(spmm_workspace_bytes(A), spmm_workspace_bytes(self.AT)),
                               dtype=torch.uint8, device=A.rowptr.device)
         self.mode = "exact"
+        self.timings = None  # set to a list to record (kind, start, end) events of each SpMM
+
+    def _tick(self):
+        if self.timings is None:
+            return None
+        e = torch.cuda.Event(enable_timing=True)
+        e.record()
+        return e
+
+    def _tock(self, start, kind: str) -> None:
+        if start is not None:
+            e = torch.cuda.Event(enable_timing=True)
+            e.record()
+            self.timings.append((kind, start, e))
 
     def __call__(self, J: torch.Tensor) -> torch.Tensor:
         return _Aggregate.apply(J, self)

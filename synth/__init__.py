@@ -53,6 +53,8 @@ def _load():
         i32p = ctypes.POINTER(ctypes.c_int32)
         lib.syn_dense_normal.argtypes = [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64,
                                          ctypes.c_int64, ctypes.c_void_p]
+        lib.syn_bucket_csr.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_void_p]
         lib.syn_gcn_values.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
         lib.syn_er.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_double, ctypes.c_void_p,
                                ctypes.POINTER(i32p)]
@@ -154,6 +156,25 @@ def random_csr(n: int, n_cols: int, row_len_max: int, seed: int, hub_rows: int =
     col = (np.concatenate(cols) if cols else np.zeros(0, dtype=np.int64)).astype(np.int32)
     val = rng.standard_normal(int(rowptr[-1]), dtype=np.float32)
     return Csr(n, rowptr.astype(np.int32), col, val)
+
+
+def bucket_csr(lens, n_cols: int, seed: int) -> Csr:
+    """CSR with the given row lengths (each <= n_cols, total < 2^31): row r
+    takes one uniform random column from each of len_r near-equal buckets of
+    [0, n_cols) (strictly increasing columns), values uniform in [-1, 1).
+    Generated in C in O(nnz), for inputs up to the int32 index limit."""
+    lens = np.asarray(lens, dtype=np.int64)
+    if lens.size and (lens.min() < 0 or lens.max() > n_cols):
+        raise ValueError("row lengths must lie in [0, n_cols]")
+    rowptr = np.zeros(len(lens) + 1, dtype=np.int64)
+    np.cumsum(lens, out=rowptr[1:])
+    nnz = int(rowptr[-1])
+    if nnz > np.iinfo(np.int32).max:
+        raise ValueError("nnz exceeds the int32 index range")
+    col = np.empty(max(nnz, 1), dtype=np.int32)
+    val = np.empty(max(nnz, 1), dtype=np.float32)
+    _load().syn_bucket_csr(seed, len(lens), n_cols, rowptr.ctypes.data, col.ctypes.data, val.ctypes.data)
+    return Csr(len(lens), rowptr.astype(np.int32), col[:nnz], val[:nnz])
 
 
 def transpose(A: Csr, n_cols: int | None = None) -> Csr:

@@ -31,7 +31,8 @@ static inline uint64_t draw(uint64_t seed, uint64_t stream, uint64_t i) {
 /* uniform double in [0, 1) with 53 random bits */
 static inline double unif(uint64_t r) { return (double)(r >> 11) * 0x1.0p-53; }
 
-enum { ST_PERM = 1, ST_WEIGHT = 2, ST_EDGE_U = 3, ST_EDGE_V = 4, ST_EDGE_P = 5, ST_ER = 6, ST_DENSE = 7 };
+enum { ST_PERM = 1, ST_WEIGHT = 2, ST_EDGE_U = 3, ST_EDGE_V = 4, ST_EDGE_P = 5, ST_ER = 6, ST_DENSE = 7,
+       ST_BUCKET_C = 8, ST_BUCKET_V = 9 };
 
 /* ---- dense N(0,1) fp32 matrix, Box-Muller on counter pairs ---------------- */
 void syn_dense_normal(uint64_t seed, int64_t rows, int64_t cols, int64_t ld, float *out) {
@@ -253,4 +254,23 @@ int64_t syn_chung_lu_uniform(uint64_t seed, int32_t n, double wlo, double whi, i
 void syn_copy_free(int32_t *src, int64_t count, int32_t *dst) {
     memcpy(dst, src, (size_t)count * sizeof(int32_t));
     free(src);
+}
+
+/* ---- bucketed CSR of given row lengths (large-size edge cases) ------------
+ * Row r with L_r <= n_cols entries splits [0, n_cols) into L_r buckets of
+ * near-equal width and takes one uniformly random column from each, so the
+ * columns of a row are strictly increasing without sorting; values are
+ * uniform in [-1, 1). O(1) work per entry and parallel over rows. */
+void syn_bucket_csr(uint64_t seed, int32_t n_rows, int32_t n_cols, const int64_t *rowptr, int32_t *col,
+                    float *val) {
+#pragma omp parallel for schedule(dynamic, 1024)
+    for (int32_t r = 0; r < n_rows; ++r) {
+        const int64_t s = rowptr[r], len = rowptr[r + 1] - s;
+        for (int64_t j = 0; j < len; ++j) {
+            const int64_t lo = j * (int64_t)n_cols / len, hi = (j + 1) * (int64_t)n_cols / len;
+            const uint64_t t = (uint64_t)(s + j);
+            col[s + j] = (int32_t)(lo + (int64_t)(draw(seed, ST_BUCKET_C, t) % (uint64_t)(hi - lo)));
+            val[s + j] = (float)(2.0 * unif(draw(seed, ST_BUCKET_V, t)) - 1.0);
+        }
+    }
 }

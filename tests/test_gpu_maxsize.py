@@ -1,0 +1,97 @@
+"""Largest inputs the int32 CSR format admits: nnz = 2^31 - 2 on a square
+2^21-node operand, with long rows and a short row ending at the last entry
+(so 64-entry runs and the long-row waves' strides step past 2^31 - 1).
+Exact SpMM, the cache at k = n (must equal the exact path bitwise) and at
+k = n/2 (selection and slice bit for bit, sampled product within 1e-4) are
+checked against the oracle on sampled rows and on the full row pointers."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2210_10737_amd as rsc
+import synth
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+FLT_MIN = np.float32(np.finfo(np.float32).tiny)
+N = 1 << 21
+NNZ = (1 << 31) - 2
+D = 4
+
+
+def max_lens():
+    lens = np.full(N, 1023, np.int64)
+    lens[-1] = 70                      # two runs, the second ends at entry 2^31 - 3
+    lens[-3] = 0                       # an empty row
+    long_rows = np.concatenate([[N - 2], np.arange(5, N - 10, N // 39)])[:40]
+    deficit = NNZ - int(lens.sum())
+    lens[long_rows] += deficit // len(long_rows)
+    lens[long_rows[0]] += deficit - (deficit // len(long_rows)) * len(long_rows)
+    assert int(lens.sum()) == NNZ and lens.max() <= N
+    return lens, long_rows
+
+
+@pytest.fixture(scope="module")
+def big(gpu):
+    lens, long_rows = max_lens()
+    print(f"[maxsize] generating nnz={NNZ} n={N}", flush=True)
+    A = synth.bucket_csr(lens, N, seed=71)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, N)
+    B = synth.dense_normal(N, D, seed=72)
+    rng = np.random.Generator(np.random.PCG64(73))
+    rows = np.unique(np.concatenate([[0, 1, 2, N - 3, N - 2, N - 1], long_rows,
+                                     rng.integers(0, N, 300)])).astype(np.int32)
+    yield A, X, B, torch.from_numpy(B).cuda(), rows
+    del X
+    torch.cuda.empty_cache()
+
+
+def dev_range(ptr, start, count, dtype):
+    return rsc.copy_to_host(ptr + start * np.dtype(dtype).itemsize, count, dtype)
+
+
+def check_rows(Y, rowptr, col, val, B, rows, tol):
+    Yo, S = oracle.spmm(rowptr, col, val, B, rows=rows, with_mag=True)
+    err = np.abs(Y[rows].astype(np.float64) - Yo) / np.maximum(S, FLT_MIN)
+    assert np.max(err) <= tol
+
+
+def test_exact_spmm_at_int32_limit(big):
+    A, X, B, Bd, rows = big
+    Y = rsc.spmm(X, Bd).cpu().numpy()
+    check_rows(Y, A.rowptr, A.col, A.val, B, rows, 1e-5)
+    assert not np.any(Y[N - 3])
+
+
+def test_cache_at_int32_limit(big):
+    A, X, B, Bd, rows = big
+    cache = rsc.Cache(X, X, refresh_interval=10)    # X passed as its own transpose: norms of its rows
+    Y = rsc.spmm(X, Bd)
+    # k = n keeps every column: the slice is X and the sampled product is the exact one, bitwise
+    cache.refresh(Bd, N, step=0)
+    g = cache.get(0)
+    s = g["slice"]
+    assert s.nnz == NNZ
+    assert np.array_equal(rsc.copy_to_host(s.rowptr, N + 1, np.int32), A.rowptr)
+    for r in rows:
+        a, b = int(A.rowptr[r]), int(A.rowptr[r + 1])
+        assert np.array_equal(dev_range(s.col, a, b - a, np.int32), A.col[a:b])
+    assert torch.equal(cache.spmm_sampled(Bd), Y)
+    # k = n/2: selection and slice against the oracle
+    k = N // 2
+    cache.refresh(Bd, k, step=1)
+    g = cache.get(1)
+    s = g["slice"]
+    cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)
+    idx, mask = oracle.topk(oracle.pair_keys(cn2, B)["key"], k)
+    assert np.array_equal(rsc.copy_to_host(g["idx_ptr"], k, np.int32), idx)
+    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+    assert s.nnz == int(ro[-1])
+    assert np.array_equal(rsc.copy_to_host(s.rowptr, N + 1, np.int32), ro)
+    for r in rows:
+        a, b = int(ro[r]), int(ro[r + 1])
+        assert np.array_equal(dev_range(s.col, a, b - a, np.int32), co[a:b])
+        assert np.array_equal(dev_range(s.val, a, b - a, np.float32).view(np.uint32), vo[a:b].view(np.uint32))
+    Ys = cache.spmm_sampled(Bd).cpu().numpy()
+    check_rows(Ys, ro, co, vo, B, rows, 1e-4)
+    cache.close()

@@ -58,6 +58,17 @@ def test_sample_columns_degenerate():
     assert o["count"][[10, 4000]].sum() == 999
 
 
+def test_sample_columns_reduced_weight_resolution():
+    """Above 2^24 pairs the weights keep fewer bits (the CDF stays below
+    2^63); draws still match the oracle bit for bit."""
+    n = (1 << 24) + 1000
+    key = np.full(n, np.uint64(0x3FF0000000000001), np.uint64)      # q = 1
+    key[::7] = np.uint64(0x4010000000000001)                        # q = 4
+    key[5::11] = 0
+    o = _check(key, 300_000, 21)
+    assert np.all(o["w"][::7][o["w"][::7] > 0] == 1 << 37)
+
+
 def test_cache_random_refresh_and_sampled_product():
     A = synth.random_csr(3000, 2500, 40, seed=51, hub_rows=2, hub_len=2200, empty_frac=0.1)
     AT = synth.transpose(A, 2500)

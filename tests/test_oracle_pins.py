@@ -416,15 +416,21 @@ def test_splitmix64_reference_outputs():
     assert [oracle.splitmix64(g["seed"], t) for t in range(len(g["outputs"]))] == [int(x) for x in g["outputs"]]
 
 
+def _weight_bits(n):
+    """Weight resolution S: 38 bits up to 2^24 pairs, then fewer, so that
+    n * 2^S <= 2^62 and the int64 CDF cannot overflow."""
+    return 38 if n <= 1 << 24 else 62 - (n - 1).bit_length()
+
+
 def _weights_by_definition(key):
-    """w_i = floor(sqrt(q_i) * 2^38 / max_j sqrt(q_j)), written independently."""
+    """w_i = floor(sqrt(q_i) * 2^S / max_j sqrt(q_j)), written independently."""
     import math
     r = []
     for u in key:
         u = int(u)
         r.append(0.0 if u == 0 else math.sqrt(struct.unpack("<d", struct.pack("<Q", u - 1))[0]))
     m = max(r)
-    scale = math.ldexp(1.0, 38) / m
+    scale = math.ldexp(1.0, _weight_bits(len(key))) / m
     return np.array([int(x * scale) for x in r], np.int64)
 
 
@@ -460,6 +466,20 @@ def test_sample_columns_frequencies():
     sd = np.sqrt(k * p * (1 - p))
     assert np.all(np.abs(o["count"] - k * p) <= 5 * sd)
     np.testing.assert_allclose(p, np.arange(1, 13) / 78.0, rtol=1e-9)
+
+
+def test_sample_weight_resolution_keeps_cdf_in_range():
+    """Above 2^24 pairs the weights lose bits so the CDF total stays below
+    2^63: with equal scores every weight is exactly 2^S, and the scale of a
+    column drawn c times is c n / k."""
+    for n, bits in ((1 << 24, 38), ((1 << 24) + 1, 37)):
+        assert _weight_bits(n) == bits
+        key = np.full(n, key_of(3.0), np.uint64)
+        o = oracle.sample_columns(key, 5000, seed=n)
+        assert np.all(o["w"] == 1 << bits) and int(o["w"].sum()) == n << bits < 1 << 63
+        drawn = np.nonzero(o["count"])[0]
+        assert o["count"].sum() == 5000
+        assert np.array_equal(o["colw"][drawn], o["count"][drawn] * float(n) / 5000.0)
 
 
 def test_sampled_product_is_unbiased():
