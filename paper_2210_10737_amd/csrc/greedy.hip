@@ -8,10 +8,13 @@
 // (ascending rank order) and the sum of the blocks' column entry counts.
 // 1. The ranking (key descending, index ascending) is a stable LSD radix sort
 //    of (~key, index) pairs: 8 passes of 8 bits; per pass a per-tile digit
-//    histogram, one scan over (digit, tile), and a stable scatter that ranks
-//    each element among equal digits with wave ballots.
-// 2. One lane per block sums its ranks in order (the order the reference
-//    sums them in), so the profile is bit-identical to the sequential one.
+//    histogram, a scan of each digit's tile counts (one wave per digit), and
+//    a stable scatter that places each digit after the smaller digits' totals
+//    and ranks each element among equal digits with wave ballots.
+// 2. sqrt(q) and the column entry count are gathered per rank in parallel;
+//    then one wave per block adds its ranks' sqrt(q) one after another in
+//    rank order (the order that defines the sum), so the profile is
+//    bit-identical to the sequential one.
 #include "rsc_internal.h"
 
 namespace rsc {
@@ -46,29 +49,27 @@ __global__ __launch_bounds__(256) void sort_hist_kernel(const uint64_t *__restri
     counts[(int64_t)threadIdx.x * n_tiles + blockIdx.x] = h[threadIdx.x];
 }
 
-// Exclusive scan of counts (length m) in place; one block of 1024 threads,
-// each owning a contiguous range.
-__global__ __launch_bounds__(1024) void sort_scan_kernel(uint32_t *__restrict__ counts, int64_t m) {
-    __shared__ uint32_t sh[1024];
-    const int t = threadIdx.x;
-    const int64_t per = (m + 1023) / 1024;
-    const int64_t lo = std::min<int64_t>(m, t * per), hi = std::min<int64_t>(m, lo + per);
-    uint32_t s = 0;
-    for (int64_t i = lo; i < hi; ++i) s += counts[i];
-    sh[t] = s;
-    __syncthreads();
-    for (int off = 1; off < 1024; off <<= 1) {
-        const uint32_t x = t >= off ? sh[t - off] : 0;
-        __syncthreads();
-        sh[t] += x;
-        __syncthreads();
+// Per digit: exclusive scan of its tile counts in place (counts are stored
+// digit-major, counts[digit * n_tiles + tile]) and the digit's total. One
+// wave per digit, 64 tiles per step.
+__global__ __launch_bounds__(256) void sort_digit_scan_kernel(uint32_t *__restrict__ counts, int32_t n_tiles,
+                                                              uint32_t *__restrict__ dtot) {
+    const int lane = threadIdx.x & 63;
+    const int dg = blockIdx.x * 4 + (threadIdx.x >> 6);
+    uint32_t *row = counts + (int64_t)dg * n_tiles;
+    uint32_t carry = 0;
+    for (int32_t t0 = 0; t0 < n_tiles; t0 += 64) {
+        const int32_t t = t0 + lane;
+        const uint32_t v = t < n_tiles ? row[t] : 0u;
+        uint32_t incl = v;
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t x = __shfl_up(incl, off);
+            if (lane >= off) incl += x;
+        }
+        if (t < n_tiles) row[t] = carry + incl - v;
+        carry += __shfl(incl, 63);
     }
-    uint32_t run = sh[t] - s;
-    for (int64_t i = lo; i < hi; ++i) {
-        const uint32_t c = counts[i];
-        counts[i] = run;
-        run += c;
-    }
+    if (lane == 0) dtot[dg] = carry;
 }
 
 // Stable scatter: elements are taken in index order, 256 per chunk; an
@@ -77,13 +78,26 @@ __global__ __launch_bounds__(1024) void sort_scan_kernel(uint32_t *__restrict__ 
 __global__ __launch_bounds__(256) void sort_scatter_kernel(const uint64_t *__restrict__ k_in,
                                                            const int32_t *__restrict__ v_in, int32_t n,
                                                            int shift, const uint32_t *__restrict__ offsets,
-                                                           int32_t n_tiles, uint64_t *__restrict__ k_out,
+                                                           const uint32_t *__restrict__ dtot, int32_t n_tiles,
+                                                           uint64_t *__restrict__ k_out,
                                                            int32_t *__restrict__ v_out) {
     __shared__ uint32_t base[kDigits];            // running position per digit in this tile
     __shared__ uint32_t wcnt[4][kDigits];         // per-wave digit counts of the current chunk
+    __shared__ uint32_t wsum[4];
     const int t = threadIdx.x, lane = t & 63, w = t >> 6;
     const uint64_t lt = (1ull << lane) - 1ull;
-    base[t] = offsets[(int64_t)t * n_tiles + blockIdx.x];
+    // start of digit t in the output: exclusive scan of the digit totals
+    const uint32_t tot = dtot[t];
+    uint32_t incl = tot;
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t x = __shfl_up(incl, off);
+        if (lane >= off) incl += x;
+    }
+    if (lane == 63) wsum[w] = incl;
+    __syncthreads();
+    uint32_t before = incl - tot;
+    for (int v = 0; v < w; ++v) before += wsum[v];
+    base[t] = before + offsets[(int64_t)t * n_tiles + blockIdx.x];
     const int64_t ts = (int64_t)blockIdx.x * kSortTile;
     for (int c = 0; c < kSortChunks; ++c) {
         const int64_t i = ts + c * 256 + t;
@@ -105,10 +119,10 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const uint64_t *__res
         if (in && (peers & lt) == 0) wcnt[w][dg] = __popcll(peers);
         __syncthreads();
         if (in) {
-            uint32_t before = base[dg] + rank_w;
-            for (int v = 0; v < w; ++v) before += wcnt[v][dg];
-            k_out[before] = kv;
-            v_out[before] = vv;
+            uint32_t pos = base[dg] + rank_w;
+            for (int v = 0; v < w; ++v) pos += wcnt[v][dg];
+            k_out[pos] = kv;
+            v_out[pos] = vv;
         }
         __syncthreads();
         base[t] += wcnt[0][t] + wcnt[1][t] + wcnt[2][t] + wcnt[3][t];
@@ -116,27 +130,58 @@ __global__ __launch_bounds__(256) void sort_scatter_kernel(const uint64_t *__res
     }
 }
 
+// Per rank p (ascending = best first): sqrt(q) of the pair at that rank in
+// fp64 and the entry count of its column, gathered in parallel so the
+// in-order sums below read contiguous arrays.
+__global__ __launch_bounds__(256) void rank_values_kernel(const uint64_t *__restrict__ sorted_notkey,
+                                                          const int32_t *__restrict__ order,
+                                                          const int32_t *__restrict__ colnnz, int32_t n,
+                                                          double *__restrict__ rv, int32_t *__restrict__ rc) {
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n;
+         p += (int64_t)gridDim.x * blockDim.x) {
+        const uint64_t u = ~sorted_notkey[p];
+        rv[p] = u != 0 ? sqrt(__longlong_as_double((long long)(u - 1))) : 0.0;
+        rc[p] = colnnz[order[p]];
+    }
+}
+
 // Block j (counted from the lowest rank) covers ranks
-// [max(0, n - (j+1) step), n - j step). One lane per block.
-__global__ __launch_bounds__(256) void greedy_profile_kernel(const uint64_t *__restrict__ sorted_notkey,
-                                                             const int32_t *__restrict__ order,
-                                                             const int32_t *__restrict__ colnnz, int32_t n,
-                                                             int32_t step, int32_t n_blocks,
-                                                             double *__restrict__ mass,
-                                                             int64_t *__restrict__ count) {
-    const int32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+// [max(0, n - (j+1) step), n - j step); one wave per block. The wave loads 64
+// ranks at a time; the fp64 mass is added one rank after another in
+// ascending rank order (the order that defines it), the integer count by a
+// wave reduction (exact in any order).
+__global__ __launch_bounds__(64) void greedy_profile_kernel(const double *__restrict__ rv,
+                                                            const int32_t *__restrict__ rc, int32_t n,
+                                                            int32_t step, int32_t n_blocks,
+                                                            double *__restrict__ mass,
+                                                            int64_t *__restrict__ count) {
+    const int32_t j = blockIdx.x;
     if (j >= n_blocks) return;
+    const int lane = threadIdx.x;
     const int64_t hi = (int64_t)n - (int64_t)j * step;
     const int64_t lo = std::max<int64_t>(0, hi - step);
     double s = 0.0;
     int64_t c = 0;
-    for (int64_t p = lo; p < hi; ++p) {
-        const uint64_t u = ~sorted_notkey[p];
-        if (u != 0) s += sqrt(__longlong_as_double((long long)(u - 1)));
-        c += colnnz[order[p]];
+    for (int64_t base = lo; base < hi; base += 64) {
+        const int32_t cnt = (int32_t)std::min<int64_t>(64, hi - base);
+        const double x = lane < cnt ? rv[base + lane] : 0.0;
+        int64_t y = lane < cnt ? rc[base + lane] : 0;
+        for (int off = 32; off > 0; off >>= 1) y += __shfl_xor(y, off);
+        c += y;
+        const int lo_bits = __double2loint(x), hi_bits = __double2hiint(x);
+        if (cnt == 64) {
+#pragma unroll
+            for (int t = 0; t < 64; ++t)
+                s += __hiloint2double(__builtin_amdgcn_readlane(hi_bits, t), __builtin_amdgcn_readlane(lo_bits, t));
+        } else {
+            for (int t = 0; t < cnt; ++t)
+                s += __hiloint2double(__builtin_amdgcn_readlane(hi_bits, t), __builtin_amdgcn_readlane(lo_bits, t));
+        }
     }
-    mass[j] = s;
-    count[j] = c;
+    if (lane == 0) {
+        mass[j] = s;
+        count[j] = c;
+    }
 }
 
 }  // namespace
@@ -151,7 +196,8 @@ int32_t greedy_blocks(int32_t n, int32_t step) { return n <= 0 ? 0 : (int32_t)ce
 size_t greedy_profile_ws_bytes(int32_t n) {
     const size_t nn = (size_t)std::max<int32_t>(n, 1);
     const size_t tiles = (size_t)ceil_div((int64_t)nn, kSortTile);
-    return 2 * align_up(nn * 8, 256) + 2 * align_up(nn * 4, 256) + align_up(tiles * kDigits * 4, 256);
+    return 2 * align_up(nn * 8, 256) + 2 * align_up(nn * 4, 256) + align_up(tiles * kDigits * 4, 256) +
+           align_up(kDigits * 4, 256);
 }
 
 hipError_t greedy_profile_launch(const uint64_t *key, const int32_t *colnnz, int32_t n, int32_t step,
@@ -170,19 +216,24 @@ hipError_t greedy_profile_launch(const uint64_t *key, const int32_t *colnnz, int
     int32_t *vb = reinterpret_cast<int32_t *>(p);
     p += align_up(nn * 4, 256);
     uint32_t *counts = reinterpret_cast<uint32_t *>(p);
+    p += align_up((size_t)n_tiles * kDigits * 4, 256);
+    uint32_t *dtot = reinterpret_cast<uint32_t *>(p);
     const unsigned g = (unsigned)std::min<int64_t>(ceil_div(n, 256), 4096);
     sort_init_kernel<<<g, 256, 0, stream>>>(key, n, ka, va);
     for (int pass = 0; pass < 8; ++pass) {
         const int shift = 8 * pass;
         sort_hist_kernel<<<n_tiles, 256, 0, stream>>>(ka, n, shift, counts, n_tiles);
-        sort_scan_kernel<<<1, 1024, 0, stream>>>(counts, (int64_t)kDigits * n_tiles);
-        sort_scatter_kernel<<<n_tiles, 256, 0, stream>>>(ka, va, n, shift, counts, n_tiles, kb, vb);
+        sort_digit_scan_kernel<<<kDigits / 4, 256, 0, stream>>>(counts, n_tiles, dtot);
+        sort_scatter_kernel<<<n_tiles, 256, 0, stream>>>(ka, va, n, shift, counts, dtot, n_tiles, kb, vb);
         std::swap(ka, kb);
         std::swap(va, vb);
     }
+    // after an even number of passes the ranking is back in (ka, va); kb and vb are free
+    double *rv = reinterpret_cast<double *>(kb);
+    int32_t *rc = vb;
+    rank_values_kernel<<<g, 256, 0, stream>>>(ka, va, colnnz, n, rv, rc);
     const int32_t nb = greedy_blocks(n, step);
-    greedy_profile_kernel<<<(unsigned)ceil_div(nb, 256), 256, 0, stream>>>(ka, va, colnnz, n, step, nb,
-                                                                          mass, count);
+    greedy_profile_kernel<<<(unsigned)nb, 64, 0, stream>>>(rv, rc, n, step, nb, mass, count);
     if (order_out) {
         const hipError_t e = hipMemcpyAsync(order_out, va, nn * 4, hipMemcpyDeviceToDevice, stream);
         if (e != hipSuccess) return e;
