@@ -84,30 +84,49 @@ def load_traffic(digest: str, launch_bytes: int):
     return {"fetch_bytes": rec["fetch_bytes_per_launch"], "write_bytes": rec["write_bytes_per_launch"],
             "total_bytes": rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"],
             "over_algorithmic": (rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]) / launch_bytes,
+            "l2_hit_rate": rec.get("l2_hit_rate"),
             "source": os.path.relpath(COUNTERS, ROOT)}
 
 
-def cpu_baseline(A, Hh, Gh, k, pct, refresh_interval, step_bytes_full, n_rows_sample):
-    """Oracle timing on a bounded sample: the refresh steps (pair keys, top-k,
-    slice) on the whole graph, and both SpMMs on the first n_rows_sample rows;
-    the step time is extrapolated linearly in rows."""
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(A, Hh, Gh, k, pct, refresh_interval, step_bytes_full, n_rows_sample,
+                 min_s: float = 10.0, max_reps: int = 8):
+    """Oracle timing on a bounded sample: the refresh (pair keys, top-k,
+    slice) on the whole graph, and both SpMMs on the first n_rows_sample rows
+    (the step time is extrapolated linearly in rows); repeated until about
+    min_s seconds of CPU work, each op's median taken."""
     import numpy as np
     import oracle
     n = A.n
     rows = np.arange(n_rows_sample, dtype=np.int32)
-    t0 = time.perf_counter()
-    oracle.spmm(A.rowptr, A.col, A.val, Hh, rows=rows)
-    t_exact = time.perf_counter() - t0
     cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)
-    t0 = time.perf_counter()
-    key = oracle.pair_keys(cn2, Gh)["key"]
-    idx, mask = oracle.topk(key, k)
-    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
-    t_refresh = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    oracle.spmm(ro, co, vo, Gh, rows=rows)
-    t_sampled = time.perf_counter() - t0
+    te, tr, ts = [], [], []
+    t_all = time.perf_counter()
+    while len(te) < max_reps and (time.perf_counter() - t_all < min_s or not te):
+        t0 = time.perf_counter()
+        oracle.spmm(A.rowptr, A.col, A.val, Hh, rows=rows)
+        te.append(time.perf_counter() - t0)
+        t0 = time.perf_counter()
+        key = oracle.pair_keys(cn2, Gh)["key"]
+        idx, mask = oracle.topk(key, k)
+        ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+        tr.append(time.perf_counter() - t0)
+        t0 = time.perf_counter()
+        oracle.spmm(ro, co, vo, Gh, rows=rows)
+        ts.append(time.perf_counter() - t0)
+    measured = time.perf_counter() - t_all
     scale = n / n_rows_sample
+    t_exact, t_refresh, t_sampled = (float(np.median(x)) for x in (te, tr, ts))
     step_s = (t_exact + t_sampled) * scale + t_refresh / refresh_interval
     return {
         "value": round(step_bytes_full / step_s / 1e9, 3),
@@ -116,9 +135,14 @@ def cpu_baseline(A, Hh, Gh, k, pct, refresh_interval, step_bytes_full, n_rows_sa
         "kind": "oracle",
         "sample": (f"exact and sampled SpMM on rows [0, {n_rows_sample}) of {n} "
                    f"(x{scale:.1f} to the full graph), one refresh (keys, top-k at {pct}%, slice) "
-                   f"on the whole graph amortised over {refresh_interval} steps"),
+                   f"on the whole graph amortised over {refresh_interval} steps; {len(te)} repetitions, "
+                   f"median per op"),
         "ms_per_step": round(step_s * 1e3, 1),
-        "measured_s": round(t_exact + t_sampled + t_refresh, 2),
+        "exact_spmm_ms": round(t_exact * scale * 1e3, 1),
+        "sampled_spmm_ms": round(t_sampled * scale * 1e3, 1),
+        "refresh_ms": round(t_refresh * 1e3, 1),
+        "cpu_model": _cpu_model(),
+        "measured_s": round(measured, 2),
     }
 
 
@@ -239,6 +263,8 @@ def main() -> int:
                          "(Eq. 2 with Eq. 3)")
     ap.add_argument("--staleness-steps", type=int, default=60,
                     help="gcn2-train only: steps of the untimed selection-staleness run (0 = skip)")
+    ap.add_argument("--cold-reps", type=int, default=5,
+                    help="after the timed steps, repetitions of each op that follow a 1 GiB cache flush")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB once (a plain copy of known "
                          "size, so hardware byte counters can be scaled)")
@@ -346,6 +372,49 @@ def main() -> int:
     exact_ms = float(np.mean(per["exact"]))
     sampled_ms = float(np.mean(per["sampled"]))
     refresh_ms = float(np.mean(per["refresh"])) if per["refresh"] else None
+
+    def stats(v):
+        if not v:
+            return None
+        q = np.percentile(v, [10, 50, 90])
+        return {"mean": round(float(np.mean(v)), 4), "p10": round(float(q[0]), 4),
+                "p50": round(float(q[1]), 4), "p90": round(float(q[2]), 4), "n": len(v)}
+
+    # cold-cache repetitions, outside the timed steps: before each, write a
+    # 1 GiB scratch buffer (more than the 4 MB L2s and the 256 MB MALL)
+    scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    cold = {"exact": [], "sampled": [], "refresh": []}
+    for r in range(args.cold_reps):
+        for kind in ("exact", "refresh", "sampled"):
+            scratch.fill_(float(r))
+            e0, e1 = ev(), ev()
+            e0.record()
+            if kind == "exact":
+                rsc.spmm(X, H, out=Y, ws=ws)
+            elif kind == "refresh":
+                if args.selector == "topk":
+                    cache.refresh(G, k, step=args.warmup + args.steps)
+                else:
+                    cache.refresh_random(G, k, seed=args.seed * 1_000_003 + args.warmup + args.steps,
+                                         step=args.warmup + args.steps)
+            else:
+                cache.spmm_sampled(G, out=Yb)
+            e1.record()
+            cold[kind].append((e0, e1))
+    # the measured copy ceiling: device-to-device copy of the 1 GiB buffer
+    dst = torch.empty_like(scratch)
+    copies = []
+    for _ in range(5):
+        e0, e1 = ev(), ev()
+        e0.record()
+        dst.copy_(scratch)
+        e1.record()
+        copies.append((e0, e1))
+    torch.cuda.synchronize()
+    cold = {kk: [a.elapsed_time(b) for a, b in v] for kk, v in cold.items()}
+    copy_ms = float(np.median([a.elapsed_time(b) for a, b in copies]))
+    copy_gbs = 2.0 * scratch.numel() * 4 / (copy_ms * 1e-3) / 1e9
+    del scratch, dst
     ms_per_step = max(wall * 1e3, gpu_ms) / args.steps
 
     b_exact = spmm_bytes(n, nnz, n, d)
@@ -387,6 +456,9 @@ def main() -> int:
         "mean_degree_selected": round(float(deg[idx].mean()), 2) if len(idx) else None,
         "mean_degree_all": round(float(deg.mean()), 2),
         "exact_logical_gather_GBs": round(4.0 * nnz * d / (exact_ms * 1e-3) / 1e9, 1),
+        "ops_ms": {"warm": {kk: stats(v) for kk, v in per.items()},
+                   "cold": {kk: stats(v) for kk, v in cold.items()}},
+        "copy_ceiling_GBs": round(copy_gbs, 1),
         "roofline": {
             "bound": "hbm",
             "kernel": "spmm_kernel (exact SpMM)",
@@ -394,6 +466,7 @@ def main() -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "frac_of_copy_ceiling": round(achieved / copy_gbs, 4),
             "algorithmic_bytes_per_launch": b_exact,
             "avg_launch_ms": round(exact_ms, 4),
             "traffic": None,
