@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define RSC_ABI_VERSION 3
+#define RSC_ABI_VERSION 4
 
 typedef enum {
     RSC_OK = 0,
@@ -70,6 +70,19 @@ const char *rsc_status_string(rsc_status_t status);
 const char *rsc_last_error(void);
 /* RSC_ABI_VERSION of the loaded library. */
 int32_t rsc_abi_version(void);
+
+/* CSR well-formedness (the form section 3.3.1's Rowptr/Col/Val describe,
+ * with sorted unique columns so that column norms are well defined):
+ * rowptr[0] = 0, rowptr[n_rows] = nnz, rowptr non-decreasing, every col in
+ * [0, n_cols), columns strictly increasing within each row. [sync] Checked
+ * on the device in O(nnz); a row's entries are read only once its bounds are
+ * in range. Returns RSC_OK (and *bad_row_host = -1 if given) or
+ * RSC_ERR_INVALID_ARGUMENT with *bad_row_host = the first offending row.
+ * With the environment variable RSC_VALIDATE=1, every entry point that takes
+ * a caller's CSR (rsc_spmm, rsc_col_sqnorms, rsc_degree_scale,
+ * rsc_slice_csr, rsc_cache_create) runs this check first and returns its
+ * error without launching anything else. */
+rsc_status_t rsc_csr_validate(const rsc_csr_t *A, int64_t *bad_row_host, hipStream_t stream);
 
 /* ---------------------------------------------------------------- A1 --- */
 /* Exact sparse-dense product Y = A * B (the SpMM of Eq. 1's implementation
@@ -216,6 +229,23 @@ rsc_status_t rsc_sample_columns(const uint64_t *key, int32_t n, int32_t k, uint6
 typedef struct rsc_cache rsc_cache_t;
 rsc_status_t rsc_cache_create(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t refresh_interval,
                               hipStream_t stream, rsc_cache_t **out);
+/* Device memory provider for a cache (for example a framework's caching
+ * allocator): alloc returns device memory of at least `bytes` bytes,
+ * 256-byte aligned, usable on `stream`, or NULL; free releases it. Both are
+ * called on the calling host thread, only inside rsc_cache_create_ex (and its
+ * failure path) and rsc_cache_destroy, with the create call's stream. */
+typedef struct {
+    void *(*alloc)(size_t bytes, hipStream_t stream, void *ctx);
+    void (*free)(void *ptr, hipStream_t stream, void *ctx);
+    void *ctx;
+} rsc_allocator_t;
+/* rsc_cache_create with the cache's device buffers taken from `allocator`
+ * (NULL: hipMalloc/hipFree). A pointer from alloc that is NULL gives
+ * RSC_ERR_OUT_OF_MEMORY; one that is not 256-byte aligned gives
+ * RSC_ERR_UNSUPPORTED (both after freeing what was taken). The allocator
+ * struct is copied; ctx must stay valid until rsc_cache_destroy. */
+rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t refresh_interval,
+                                 const rsc_allocator_t *allocator, hipStream_t stream, rsc_cache_t **out);
 rsc_status_t rsc_cache_refresh(rsc_cache_t *cache, const float *B, int32_t d, int64_t ldb,
                                int32_t k, int64_t step, hipStream_t stream);
 rsc_status_t rsc_cache_score(rsc_cache_t *cache, const float *B, int32_t d, int64_t ldb,

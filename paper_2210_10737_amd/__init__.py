@@ -26,13 +26,13 @@ STATUS = {0: "RSC_OK", 1: "RSC_ERR_INVALID_ARGUMENT", 2: "RSC_ERR_UNSUPPORTED",
           6: "RSC_ERR_HIP", 7: "RSC_ERR_INTERNAL"}
 
 EXPORTED = [
-    "rsc_status_string", "rsc_last_error", "rsc_abi_version",
+    "rsc_status_string", "rsc_last_error", "rsc_abi_version", "rsc_csr_validate",
     "rsc_spmm_workspace_bytes", "rsc_spmm", "rsc_degree_scale",
     "rsc_col_sqnorms", "rsc_pair_scores",
     "rsc_topk_workspace_bytes", "rsc_topk_select",
     "rsc_slice_workspace_bytes", "rsc_slice_csr",
     "rsc_sample_workspace_bytes", "rsc_sample_columns",
-    "rsc_cache_create", "rsc_cache_refresh", "rsc_cache_score", "rsc_cache_select",
+    "rsc_cache_create", "rsc_cache_create_ex", "rsc_cache_refresh", "rsc_cache_score", "rsc_cache_select",
     "rsc_cache_refresh_random",
     "rsc_cache_get", "rsc_spmm_sampled",
     "rsc_cache_buffers", "rsc_cache_destroy",
@@ -46,6 +46,31 @@ class RscError(RuntimeError):
     def __init__(self, status: int, detail: str):
         super().__init__(f"{STATUS.get(status, status)}: {detail}")
         self.status = status
+
+
+_ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p)
+_FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p)
+
+
+class Allocator(ctypes.Structure):
+    _fields_ = [("alloc", _ALLOC_FN), ("free", _FREE_FN), ("ctx", ctypes.c_void_p)]
+
+
+def _torch_allocator() -> Allocator:
+    """rsc_allocator_t backed by torch's caching allocator on the current
+    device (its blocks are 512-byte aligned)."""
+    dev = torch.cuda.current_device()
+
+    def alloc(nbytes, stream, ctx):
+        try:
+            return torch.cuda.caching_allocator_alloc(int(nbytes), device=dev, stream=stream)
+        except Exception:  # out of memory: the library reports RSC_ERR_OUT_OF_MEMORY
+            return None
+
+    def free(ptr, stream, ctx):
+        torch.cuda.caching_allocator_delete(ptr)
+
+    return Allocator(_ALLOC_FN(alloc), _FREE_FN(free), None)
 
 
 class CsrStruct(ctypes.Structure):
@@ -83,6 +108,9 @@ def lib():
             "rsc_sample_columns": ([vp, i32, i32, ctypes.c_uint64, vp, vp, vp, vp, sz, vp], ctypes.c_int),
             "rsc_cache_refresh_random": ([vp, vp, i32, i64, i32, ctypes.c_uint64, i64, vp], ctypes.c_int),
             "rsc_cache_create": ([csrp, csrp, i32, vp, ctypes.POINTER(vp)], ctypes.c_int),
+            "rsc_cache_create_ex": ([csrp, csrp, i32, ctypes.POINTER(Allocator), vp, ctypes.POINTER(vp)],
+                                    ctypes.c_int),
+            "rsc_csr_validate": ([csrp, ctypes.POINTER(i64), vp], ctypes.c_int),
             "rsc_cache_refresh": ([vp, vp, i32, i64, i32, i64, vp], ctypes.c_int),
             "rsc_cache_score": ([vp, vp, i32, i64, vp], ctypes.c_int),
             "rsc_cache_select": ([vp, i32, i64, vp], ctypes.c_int),
@@ -107,6 +135,13 @@ def lib():
             fn.restype = res
         _lib = L
     return _lib
+
+
+def csr_validate(A: "DeviceCsr") -> None:
+    """Device check that A is a well-formed CSR with sorted unique columns
+    (rsc_csr_validate); raises RscError naming the first bad row."""
+    bad = ctypes.c_int64(-1)
+    _check(lib().rsc_csr_validate(ctypes.byref(A.struct()), ctypes.byref(bad), _stream()))
 
 
 def _check(status: int) -> None:
@@ -270,12 +305,24 @@ class Cache:
     """Sampled-matrix cache (section 3.3.1): rsc_cache_create / refresh /
     get / spmm_sampled / destroy."""
 
-    def __init__(self, X: DeviceCsr, XT: DeviceCsr | None = None, refresh_interval: int = 10):
+    def __init__(self, X: DeviceCsr, XT: DeviceCsr | None = None, refresh_interval: int = 10,
+                 allocator: str | None = None):
+        """allocator: None (the library's hipMalloc) or "torch" (torch's
+        caching allocator, through rsc_cache_create_ex)."""
         self.X = X
         self.XT = X if XT is None else XT
         h = ctypes.c_void_p()
-        _check(lib().rsc_cache_create(ctypes.byref(X.struct()), ctypes.byref(self.XT.struct()),
-                                      refresh_interval, _stream(), ctypes.byref(h)))
+        self._alloc = None
+        if allocator is None:
+            _check(lib().rsc_cache_create(ctypes.byref(X.struct()), ctypes.byref(self.XT.struct()),
+                                          refresh_interval, _stream(), ctypes.byref(h)))
+        elif allocator == "torch":
+            self._alloc = _torch_allocator()  # kept alive until destroy
+            _check(lib().rsc_cache_create_ex(ctypes.byref(X.struct()), ctypes.byref(self.XT.struct()),
+                                             refresh_interval, ctypes.byref(self._alloc), _stream(),
+                                             ctypes.byref(h)))
+        else:
+            raise ValueError(f"unknown allocator {allocator!r}")
         self._h = h
 
     def refresh(self, B: torch.Tensor, k: int, step: int, d: int | None = None) -> None:

@@ -86,9 +86,44 @@ rsc_status_t check_ws(const void *ws, size_t ws_bytes, size_t need, const char *
     return RSC_OK;
 }
 
+bool validate_env() {
+    const char *v = getenv("RSC_VALIDATE");
+    return v && v[0] == '1';
+}
+
+rsc_status_t validate(const rsc_csr_t *A, const char *name, int64_t *bad_row, hipStream_t stream) {
+    if (bad_row) *bad_row = -1;
+    if (A->n_rows == 0) {
+        if (A->nnz != 0) {
+            if (bad_row) *bad_row = 0;
+            return fail(RSC_ERR_INVALID_ARGUMENT, "%s: no rows but nnz = %lld", name, (long long)A->nnz);
+        }
+        return RSC_OK;
+    }
+    unsigned long long *d_bad = nullptr, h_bad = 0;
+    RSC_HIP(hipMalloc((void **)&d_bad, sizeof(unsigned long long)), "validate alloc");
+    hipError_t e = rsc::csr_validate_launch(A->n_rows, A->n_cols, A->nnz, A->rowptr, A->col, d_bad, stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(&h_bad, d_bad, sizeof h_bad, hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    (void)hipFree(d_bad);
+    if (e != hipSuccess) return hip_fail(e, "validate");
+    if (h_bad != ~0ull) {
+        if (bad_row) *bad_row = (int64_t)h_bad;
+        return fail(RSC_ERR_INVALID_ARGUMENT, "%s: malformed CSR at row %llu", name, h_bad);
+    }
+    return RSC_OK;
+}
+
+// with RSC_VALIDATE=1, the device check of a caller's CSR before any launch
+rsc_status_t maybe_validate(const rsc_csr_t *A, const char *name, hipStream_t stream) {
+    return validate_env() ? validate(A, name, nullptr, stream) : RSC_OK;
+}
+
 }  // namespace
 
 struct rsc_cache {
+    rsc_allocator_t alloc{};   // alloc.alloc == NULL: hipMalloc / hipFree
+    hipStream_t alloc_stream = nullptr;
     rsc_csr_t X{}, XT{};
     int32_t interval = 10;
     int32_t n = 0;  // pairs = columns of X
@@ -139,6 +174,13 @@ const char *rsc_last_error(void) { return g_err.c_str(); }
 
 int32_t rsc_abi_version(void) { return RSC_ABI_VERSION; }
 
+rsc_status_t rsc_csr_validate(const rsc_csr_t *A, int64_t *bad_row_host, hipStream_t stream) {
+    if (bad_row_host) *bad_row_host = -1;
+    RSC_TRY(check_csr(A, "A"));
+    RSC_TRY(check_device());
+    return validate(A, "A", bad_row_host, stream);
+}
+
 // ------------------------------------------------------------------- A1
 size_t rsc_spmm_workspace_bytes(const rsc_csr_t *A) {
     if (!A || A->n_rows < 0 || A->nnz < 0) return 0;
@@ -152,6 +194,7 @@ rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb
     RSC_TRY(check_dense(Y, A->n_rows, d, ldy, "Y"));
     RSC_TRY(check_ws(ws, ws_bytes, rsc::spmm_ws_bytes(A->n_rows, A->nnz), "spmm"));
     RSC_TRY(check_device());
+    RSC_TRY(maybe_validate(A, "A", stream));
     RSC_HIP(rsc::spmm_launch(A->n_rows, A->nnz, A->rowptr, A->col, A->val, B, d, ldb, Y, ldy, ws, stream,
                              A->nnz, A->n_cols),
             "spmm launch");
@@ -165,6 +208,7 @@ rsc_status_t rsc_degree_scale(const rsc_csr_t *A, const int32_t *deg_rowptr, int
     if (by_column && !deg_rowptr) return fail(RSC_ERR_INVALID_ARGUMENT, "deg_rowptr is NULL");
     if (!aligned(val_out, 4) || !aligned(deg_rowptr, 4)) return fail(RSC_ERR_UNSUPPORTED, "misaligned argument");
     RSC_TRY(check_device());
+    RSC_TRY(maybe_validate(A, "A", stream));
     RSC_HIP(rsc::degree_scale_launch(A->n_rows, A->rowptr, A->col, A->val, deg_rowptr, by_column ? 1 : 0, val_out,
                                      stream),
             "degree scale launch");
@@ -177,6 +221,7 @@ rsc_status_t rsc_col_sqnorms(const rsc_csr_t *XT, double *cn2, int32_t *colnnz, 
     if (XT->n_rows > 0 && !cn2) return fail(RSC_ERR_INVALID_ARGUMENT, "cn2 is NULL");
     if (!aligned(cn2, 8)) return fail(RSC_ERR_UNSUPPORTED, "cn2 is not 8-byte aligned");
     RSC_TRY(check_device());
+    RSC_TRY(maybe_validate(XT, "XT", stream));
     RSC_HIP(rsc::col_sqnorms_launch(XT->n_rows, XT->rowptr, XT->val, cn2, colnnz, stream),
             "col_sqnorms launch");
     return RSC_OK;
@@ -246,6 +291,7 @@ rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, const doubl
     if (!aligned(colw, 8)) return fail(RSC_ERR_UNSUPPORTED, "colw is not 8-byte aligned");
     RSC_TRY(check_ws(ws, ws_bytes, rsc::slice_ws_bytes(A->nnz), "slice"));
     RSC_TRY(check_device());
+    RSC_TRY(maybe_validate(A, "A", stream));
     RSC_HIP(rsc::slice_launch(A->n_rows, A->nnz, A->rowptr, A->col, A->val, mask, rowptr_out, col_out, val_out,
                               capacity, nnz_out, ws, stream, colw),
             "slice launch");
@@ -265,8 +311,13 @@ static void cache_free(rsc_cache_t *c) {
     if (!c) return;
     void *dev[] = {c->cn2, c->colnnz, c->key, c->rn2, c->count, c->colw, c->idx, c->mask, c->s_rowptr,
                    c->s_col, c->s_val, c->d_nnz, c->ws_topk, c->ws_slice, c->ws_spmm, c->ws_sample};
-    for (void *p : dev)
-        if (p) (void)hipFree(p);
+    for (void *p : dev) {
+        if (!p) continue;
+        if (c->alloc.alloc)
+            c->alloc.free(p, c->alloc_stream, c->alloc.ctx);
+        else
+            (void)hipFree(p);
+    }
     if (c->h_nnz) (void)hipHostFree(c->h_nnz);
     if (c->ev) (void)hipEventDestroy(c->ev);
     delete c;
@@ -274,14 +325,25 @@ static void cache_free(rsc_cache_t *c) {
 
 rsc_status_t rsc_cache_create(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t refresh_interval,
                               hipStream_t stream, rsc_cache_t **out) {
+    return rsc_cache_create_ex(X, XT, refresh_interval, nullptr, stream, out);
+}
+
+rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t refresh_interval,
+                                 const rsc_allocator_t *allocator, hipStream_t stream, rsc_cache_t **out) {
     if (!out) return fail(RSC_ERR_INVALID_ARGUMENT, "out is NULL");
     RSC_TRY(check_csr(X, "X"));
     RSC_TRY(check_csr(XT, "XT"));
     if (XT->n_rows != X->n_cols || XT->n_cols != X->n_rows || XT->nnz != X->nnz)
         return fail(RSC_ERR_INVALID_ARGUMENT, "XT is not shaped like the transpose of X");
     if (refresh_interval < 1) return fail(RSC_ERR_INVALID_ARGUMENT, "refresh_interval < 1");
+    if (allocator && (!allocator->alloc || !allocator->free))
+        return fail(RSC_ERR_INVALID_ARGUMENT, "allocator without alloc or free");
     RSC_TRY(check_device());
+    RSC_TRY(maybe_validate(X, "X", stream));
+    if (XT != X) RSC_TRY(maybe_validate(XT, "XT", stream));
     rsc_cache_t *c = new rsc_cache_t();
+    if (allocator) c->alloc = *allocator;
+    c->alloc_stream = stream;
     c->X = *X;
     c->XT = *XT;
     c->interval = refresh_interval;
@@ -314,7 +376,18 @@ rsc_status_t rsc_cache_create(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t r
         {&c->ws_sample, c->ws_sample_bytes},
     };
     for (auto &a : allocs) {
-        if (hipMalloc(a.p, std::max<size_t>(a.bytes, 256)) != hipSuccess) {
+        const size_t bytes = std::max<size_t>(a.bytes, 256);
+        if (c->alloc.alloc) {
+            *a.p = c->alloc.alloc(bytes, stream, c->alloc.ctx);
+            if (!*a.p) {
+                cache_free(c);
+                return fail(RSC_ERR_OUT_OF_MEMORY, "allocator returned NULL for %zu bytes", bytes);
+            }
+            if (!aligned(*a.p, 256)) {
+                cache_free(c);
+                return fail(RSC_ERR_UNSUPPORTED, "allocator returned memory that is not 256-byte aligned");
+            }
+        } else if (hipMalloc(a.p, bytes) != hipSuccess) {
             (void)hipGetLastError();
             cache_free(c);
             return fail(RSC_ERR_OUT_OF_MEMORY, "cache allocation of %zu bytes failed", a.bytes);

@@ -44,6 +44,10 @@ size_t sample_ws_bytes(int32_t n);
 hipError_t sample_launch(const uint64_t *key, int32_t n, int32_t k, uint64_t seed, int32_t *count,
                          double *colw, uint32_t *mask, void *ws, hipStream_t stream);
 
+// ---- CSR validation ----------------------------------------------------
+hipError_t csr_validate_launch(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr,
+                               const int32_t *col, unsigned long long *first_bad, hipStream_t stream);
+
 // ---- MEAN aggregator operand -------------------------------------------
 hipError_t degree_scale_launch(int32_t n_rows, const int32_t *rowptr, const int32_t *col, const float *val,
                                const int32_t *deg_rowptr, int32_t by_column, float *out, hipStream_t stream);

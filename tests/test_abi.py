@@ -34,7 +34,7 @@ def test_header_matches_exports():
     L = rsc.lib()
     for name in declared:
         assert getattr(L, name) is not None
-    assert L.rsc_abi_version() == 3
+    assert L.rsc_abi_version() == 4
 
 
 def test_status_strings():
@@ -117,6 +117,18 @@ def test_cache_argument_validation():
     assert _err(L.rsc_cache_refresh(None, 0x1000, 4, 4, 1, 0, None)) == "RSC_ERR_INVALID_ARGUMENT"
     assert _err(L.rsc_spmm_sampled(None, 0x1000, 4, 4, 0x2000, 4, None)) == "RSC_ERR_INVALID_ARGUMENT"
     assert L.rsc_cache_destroy(None) == 0
+    half = rsc.Allocator(rsc._ALLOC_FN(lambda n, s, c: None), rsc._FREE_FN(), None)  # no free
+    assert _err(L.rsc_cache_create_ex(ctypes.byref(A), ctypes.byref(A), 10, ctypes.byref(half), None,
+                                      ctypes.byref(out))) == "RSC_ERR_INVALID_ARGUMENT"
+
+
+def test_csr_validate_argument_checks():
+    L = rsc.lib()
+    bad = ctypes.c_int64(7)
+    assert _err(L.rsc_csr_validate(None, ctypes.byref(bad), None)) == "RSC_ERR_INVALID_ARGUMENT"
+    assert bad.value == -1
+    big = _csr(nnz=1 << 31)
+    assert _err(L.rsc_csr_validate(ctypes.byref(big), None, None)) == "RSC_ERR_UNSUPPORTED"
 
 
 @pytest.mark.skipif(os.environ.get("HIP_VISIBLE_DEVICES", None) is None and
