@@ -263,6 +263,9 @@ def main() -> int:
                          "(Eq. 2 with Eq. 3)")
     ap.add_argument("--staleness-steps", type=int, default=60,
                     help="gcn2-train only: steps of the untimed selection-staleness run (0 = skip)")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the exact + sampled SpMM of each step from one captured HIP graph "
+                         "(refreshes stay eager)")
     ap.add_argument("--cold-reps", type=int, default=5,
                     help="after the timed steps, repetitions of each op that follow a 1 GiB cache flush")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -346,6 +349,45 @@ def main() -> int:
     for s in range(args.warmup):
         step(s, False)
     torch.cuda.synchronize()
+    if args.graph:
+        # in graph mode, per-op times come from eager steps run before capture
+        for s in range(args.warmup, args.warmup + args.steps):
+            step(s, True)
+        torch.cuda.synchronize()
+    eager_records = records[:]
+    records.clear()
+    graph = None
+    if args.graph:
+        # one HIP graph holds the exact and the sampled SpMM of a step (kernel
+        # launches only); refreshes stay eager, every `refresh` steps
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            rsc.spmm(X, H, out=Y, ws=ws)
+            cache.spmm_sampled(G, out=Yb)
+        torch.cuda.current_stream().wait_stream(side)
+        with torch.cuda.graph(graph):
+            rsc.spmm(X, H, out=Y, ws=ws)
+            cache.spmm_sampled(G, out=Yb)
+        torch.cuda.synchronize()
+
+        def step(s: int, timed: bool):  # noqa: F811
+            if cache.get(s, with_slice=False)["needs_refresh"]:
+                r0, r1 = ev(), ev()
+                r0.record()
+                if args.selector == "topk":
+                    cache.refresh(G, k, step=s)
+                else:
+                    cache.refresh_random(G, k, seed=args.seed * 1_000_003 + s, step=s)
+                r1.record()
+                if timed:
+                    records.append(("refresh", r0, r1))
+            graph.replay()
+
+        for s in range(args.warmup):
+            step(s, False)
+        torch.cuda.synchronize()
     t0 = time.perf_counter()
     g0, g1 = ev(), ev()
     g0.record()
@@ -355,6 +397,9 @@ def main() -> int:
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gpu_ms = g0.elapsed_time(g1)
+    if graph is not None:
+        # per-op times of the eager steps that preceded capture stand for the ops
+        records.extend(eager_records)
 
     per = {"exact": [], "refresh": [], "sampled": []}
     for kind, a, b in records:
@@ -441,7 +486,8 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": args.workload, "aggregator": args.aggregator, "graph": w.description,
                    "n": n, "nnz": nnz, "d": d,
-                   "budget_pct": pct, "k": k, "selector": args.selector, "refresh_interval": args.refresh,
+                   "budget_pct": pct, "k": k, "selector": args.selector, "graph": bool(args.graph),
+                   "refresh_interval": args.refresh,
                    "seed": args.seed},
         "exact_spmm_ms": round(exact_ms, 4),
         "sampled_spmm_ms": round(sampled_ms, 4),
