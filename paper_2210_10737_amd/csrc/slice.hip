@@ -10,8 +10,9 @@
 //      set that stays in L2);
 //   2. one block scans the tile counts (and stores nnz');
 //   3. per tile: stage col/val through LDS, scan the kept flags inside the
-//      tile, write the kept entries at their global positions, and write
-//      Rowptr'[i] for every row whose Rowptr[i] falls in the tile.
+//      tile, compact the kept entries in LDS and write them out coalesced at
+//      their global positions, and write Rowptr'[i] for every row whose
+//      Rowptr[i] falls in the tile.
 // Integer-only and deterministic. With a per-column scale (the randomized
 // sampler's 1/(k p)), each kept value becomes fl32(val * colw[col]).
 #include "rsc_internal.h"
@@ -20,7 +21,8 @@ namespace rsc {
 namespace {
 
 constexpr int kTile = 4096;          // entries per tile
-constexpr int kPer = kTile / 256;    // consecutive entries per thread in the emit kernel
+constexpr int kPer = kTile / 256;    // 256-entry chunks per tile
+static_assert(kPer * 4 == 64, "one wave scans the (chunk, wave) ballots of a tile");
 
 __device__ __forceinline__ bool kept(const uint32_t *__restrict__ mask, int32_t c) {
     return (mask[c >> 5] >> (c & 31)) & 1u;
@@ -31,11 +33,16 @@ __global__ __launch_bounds__(256) void slice_count_kernel(const int32_t *__restr
                                                           uint32_t *__restrict__ tile_cnt) {
     __shared__ uint32_t s[4];
     const int64_t ts = (int64_t)blockIdx.x * kTile;
-    uint32_t c = 0;
+    // all column loads first (independent, coalesced), then the mask bits
+    int32_t cv[kPer];
+#pragma unroll
     for (int j = 0; j < kPer; ++j) {
         const int64_t t = ts + threadIdx.x + 256 * j;
-        if (t < nnz) c += kept(mask, __builtin_nontemporal_load(col + t));
+        cv[j] = t < nnz ? __builtin_nontemporal_load(col + t) : -1;
     }
+    uint32_t c = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) c += cv[j] >= 0 && kept(mask, cv[j]);
     for (int off = 32; off > 0; off >>= 1) c += __shfl_down(c, off);
     if ((threadIdx.x & 63) == 0) s[threadIdx.x >> 6] = c;
     __syncthreads();
@@ -77,6 +84,10 @@ __device__ int32_t lower_bound_rowptr(const int32_t *__restrict__ rowptr, int32_
     return lo;
 }
 
+// Entry o of a tile (0 <= o < kTile) is position o & 255 of chunk o >> 8;
+// within a chunk, wave (o >> 6) & 3, lane o & 63. Each wave's kept flags of
+// a chunk are one ballot, so the kept entries before o are the counts of the
+// earlier (chunk, wave) ballots plus the ballot's bits below the lane.
 __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restrict__ rowptr, int32_t n_rows,
                                                          const int32_t *__restrict__ col,
                                                          const float *__restrict__ val, int64_t nnz,
@@ -86,55 +97,62 @@ __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restri
                                                          int32_t *__restrict__ col_out,
                                                          float *__restrict__ val_out, int64_t capacity,
                                                          const double *__restrict__ colw) {
-    __shared__ int32_t s_col[kTile];
+    constexpr int kGroups = kPer * 4;  // (chunk, wave) ballots per tile
+    __shared__ int32_t s_col[kTile];   // kept entries of the tile, compacted
     __shared__ float s_val[kTile];
-    __shared__ uint32_t s_pre[256];   // kept entries before each thread's run
-    __shared__ uint32_t s_bits[256];  // kept flags of each thread's run
+    __shared__ uint64_t s_ball[kGroups];
+    __shared__ uint32_t s_pre[kGroups + 1];  // kept entries before each ballot; [kGroups] = tile total
     __shared__ int32_t s_rows[2];
-    const int t = threadIdx.x;
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
     const int64_t ts = (int64_t)blockIdx.x * kTile;
     const int64_t te = min<int64_t>(ts + kTile, nnz);
     const bool last = blockIdx.x == gridDim.x - 1;
     if (t == 0) s_rows[0] = lower_bound_rowptr(rowptr, n_rows, ts);
     if (t == 1) s_rows[1] = last ? n_rows + 1 : lower_bound_rowptr(rowptr, n_rows, te);
-    for (int j = 0; j < kPer; ++j) {  // coalesced staging
-        const int64_t p = ts + t + 256 * j;
-        if (p < te) {
-            s_col[t + 256 * j] = __builtin_nontemporal_load(col + p);
-            s_val[t + 256 * j] = __builtin_nontemporal_load(val + p);
+    int32_t rc[kPer];
+    float rv[kPer];
+    uint64_t ball[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {  // coalesced loads
+        const int64_t p = ts + 256 * j + t;
+        rc[j] = p < te ? __builtin_nontemporal_load(col + p) : -1;
+        rv[j] = p < te ? __builtin_nontemporal_load(val + p) : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        ball[j] = __ballot(rc[j] >= 0 && kept(mask, rc[j]));
+        if (lane == 0) s_ball[j * 4 + w] = ball[j];
+    }
+    __syncthreads();
+    if (w == 0) {  // exclusive scan of the kGroups ballot counts (kGroups == 64)
+        const uint32_t cnt = __popcll(s_ball[lane]);
+        uint32_t incl = cnt;
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t x = __shfl_up(incl, off);
+            if (lane >= off) incl += x;
+        }
+        s_pre[lane] = incl - cnt;
+        if (lane == 63) s_pre[kGroups] = incl;
+    }
+    __syncthreads();
+    const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        if ((ball[j] >> lane) & 1ull) {
+            const uint32_t q = s_pre[j * 4 + w] + __popcll(ball[j] & below);
+            s_col[q] = rc[j];
+            s_val[q] = rv[j];
         }
     }
     __syncthreads();
-    uint32_t bits = 0;
-    for (int j = 0; j < kPer; ++j) {
-        const int64_t p = ts + kPer * t + j;
-        if (p < te && kept(mask, s_col[kPer * t + j])) bits |= 1u << j;
-    }
-    const uint32_t cnt = __popc(bits);
-    s_bits[t] = bits;
-    s_pre[t] = cnt;
-    __syncthreads();
-    for (int off = 1; off < 256; off <<= 1) {  // inclusive scan of the run counts
-        const uint32_t x = t >= off ? s_pre[t - off] : 0;
-        __syncthreads();
-        s_pre[t] += x;
-        __syncthreads();
-    }
-    const uint32_t excl = s_pre[t] - cnt;
-    __syncthreads();
-    s_pre[t] = excl;
-    __syncthreads();
     const int64_t base = (int64_t)tile_off[blockIdx.x];
-    int64_t pos = base + excl;
-    for (int j = 0; j < kPer; ++j) {
-        if ((bits >> j) & 1u) {
-            if (pos < capacity) {
-                const int32_t c = s_col[kPer * t + j];
-                const float v = s_val[kPer * t + j];
-                col_out[pos] = c;
-                val_out[pos] = colw ? (float)((double)v * colw[c]) : v;
-            }
-            ++pos;
+    const uint32_t total = s_pre[kGroups];
+    for (uint32_t i = t; i < total; i += 256) {
+        const int64_t pos = base + i;
+        if (pos < capacity) {
+            const int32_t c = s_col[i];
+            col_out[pos] = c;
+            val_out[pos] = colw ? (float)((double)s_val[i] * colw[c]) : s_val[i];
         }
     }
     // Rowptr'[i] for the rows whose Rowptr[i] lies in [ts, te) (and, in the
@@ -144,10 +162,10 @@ __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restri
         const int64_t off = (int64_t)rowptr[i] - ts;
         uint32_t c;
         if (off >= kTile || ts + off >= te) {
-            c = s_pre[255] + __popc(s_bits[255]);
+            c = total;
         } else {
-            const int th = (int)(off / kPer), o = (int)(off % kPer);
-            c = s_pre[th] + __popc(s_bits[th] & ((1u << o) - 1u));
+            const int g = (int)(off >> 6), l = (int)(off & 63);  // g = chunk * 4 + wave
+            c = s_pre[g] + __popcll(s_ball[g] & ((1ull << l) - 1ull));
         }
         rowptr_out[i] = (int32_t)(base + c);
     }
