@@ -3,29 +3,47 @@
 //
 // Both reductions follow one canonical order so that the keys, and hence the
 // selection, are bitwise reproducible: an fp64 sum of exact fp32 squares in
-// plain index order, one lane per sum.
+// plain index order.
 #include "rsc_internal.h"
 
 namespace rsc {
 namespace {
 
-// cn2[i] = sum of val^2 over row i of X^T, in stored order (one lane per
-// row). Products of fp32 values are exact in fp64, so fma(v, v, acc) equals
-// acc + v * v.
+// cn2[i] = sum of val^2 over row i of X^T, in stored order. One wave per
+// row: the wave loads 64 values at a time (coalesced) and adds their squares
+// one after another in stored order, each value broadcast with readlane, so
+// the sum is the sequential one while the loads stay wide. Products of fp32
+// values are exact in fp64, so fma(v, v, acc) equals acc + v * v.
 __global__ __launch_bounds__(256) void col_sqnorms_kernel(int32_t n, const int32_t *__restrict__ rowptr,
                                                           const float *__restrict__ val,
                                                           double *__restrict__ cn2,
                                                           int32_t *__restrict__ colnnz) {
-    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (i >= n) return;
-    const int32_t s = rowptr[i], e = rowptr[i + 1];
+    const int32_t s = __builtin_amdgcn_readfirstlane(rowptr[i]);
+    const int32_t e = __builtin_amdgcn_readfirstlane(rowptr[i + 1]);
     double acc = 0.0;
-    for (int32_t t = s; t < e; ++t) {
-        const double v = (double)val[t];
-        acc = fma(v, v, acc);
+    for (int64_t base = s; base < e; base += 64) {
+        const int32_t cnt = (int32_t)min<int64_t>(64, e - base);
+        const int vb = lane < cnt ? __float_as_int(__builtin_nontemporal_load(val + base + lane)) : 0;
+        if (cnt == 64) {
+#pragma unroll
+            for (int t = 0; t < 64; ++t) {
+                const double v = (double)__int_as_float(__builtin_amdgcn_readlane(vb, t));
+                acc = fma(v, v, acc);
+            }
+        } else {
+            for (int t = 0; t < cnt; ++t) {
+                const double v = (double)__int_as_float(__builtin_amdgcn_readlane(vb, t));
+                acc = fma(v, v, acc);
+            }
+        }
     }
-    cn2[i] = acc;
-    if (colnnz) colnnz[i] = e - s;
+    if (lane == 0) {
+        cn2[i] = acc;
+        if (colnnz) colnnz[i] = e - s;
+    }
 }
 
 // 256 rows per block, one row per thread. B is streamed through LDS in tiles
@@ -83,7 +101,7 @@ __global__ __launch_bounds__(256) void pair_scores_kernel(const double *__restri
 hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,
                               int32_t *colnnz, hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    col_sqnorms_kernel<<<(unsigned)ceil_div(n, 256), 256, 0, stream>>>(n, rowptr_t, val_t, cn2, colnnz);
+    col_sqnorms_kernel<<<(unsigned)ceil_div(n, 4), 256, 0, stream>>>(n, rowptr_t, val_t, cn2, colnnz);
     return hipGetLastError();
 }
 
