@@ -2,7 +2,9 @@
  * rsc.h - C ABI of the MI355X (gfx950) implementation of the RSC
  * aggregation hot path: the GCN aggregation SpMM Y = A_hat * H and its
  * top-k column-row approximation (score pairs, keep the top k, slice the
- * kept columns out of the CSR matrix, cache the slice, run SpMM on it).
+ * kept columns out of the CSR matrix, cache the slice, run SpMM on it);
+ * also the unbiased randomized column-row sampler, the MEAN-aggregator
+ * operand, the layer-wise budget allocation and a CSR validity check.
  *
  * Paper: Liu et al., "RSC: Accelerate Graph Neural Networks Training via
  * Randomized Sparse Computations", ICML 2023 (arXiv 2210.10737).

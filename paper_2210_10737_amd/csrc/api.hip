@@ -1,7 +1,7 @@
 // C ABI of the library (declared in include/rsc.h): argument validation,
 // status codes, the sampled-matrix cache and the host-side budget helpers.
-// Every device step is one of the kernels in spmm.hip / scores.hip /
-// topk.hip / slice.hip.
+// Every device step is a kernel of spmm.hip, scores.hip, topk.hip,
+// slice.hip, sample.hip, mean.hip, greedy.hip or validate.hip.
 #include <algorithm>
 #include <cmath>
 #include <cstdarg>
