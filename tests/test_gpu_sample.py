@@ -108,3 +108,18 @@ def test_sampled_product_unbiased_on_gpu():
         first = Y.clone() if first is None else first
     assert float(torch.linalg.norm(acc / seeds - exact)) < 0.2 * float(torch.linalg.norm(first - exact))
     cache.close()
+
+
+def test_cache_random_zero_draws_and_unrefreshed_cache():
+    A = synth.random_csr(500, 400, 20, seed=71)
+    AT = synth.transpose(A, 400)
+    cache = rsc.Cache(rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, 400),
+                      rsc.DeviceCsr.from_host(AT.rowptr, AT.col, AT.val, 500))
+    B = torch.from_numpy(synth.dense_normal(400, 16, seed=72)).cuda()
+    with pytest.raises(rsc.RscError):          # never refreshed
+        cache.spmm_sampled(B)
+    cache.refresh_random(B, 0, seed=1, step=0)  # no draws: empty slice, zero product
+    snap = rsc.cache_snapshot(cache)
+    assert snap["nnz"] == 0 and not snap["rowptr"].any()
+    assert not cache.spmm_sampled(B).any()
+    cache.close()
