@@ -6,13 +6,14 @@
 // stay in their original order, the output position of a kept entry is the
 // number of kept entries before it, and Rowptr'[i] is that count at position
 // Rowptr[i]. So the slice is one stream compaction over the nnz entries:
-//   1. count kept entries per tile of 4096 (reads col; the mask is an n-bit
-//      set that stays in L2);
+//   1. per tile of 4096 entries: the kept flags as 64 wave ballots (reads
+//      col; the mask is an n-bit set that stays in L2), stored for step 3,
+//      and their count;
 //   2. one block scans the tile counts (and stores nnz');
-//   3. per tile: stage col/val through LDS, scan the kept flags inside the
-//      tile, compact the kept entries in LDS and write them out coalesced at
-//      their global positions, and write Rowptr'[i] for every row whose
-//      Rowptr[i] falls in the tile.
+//   3. per tile: load col/val into registers, scan the tile's ballot counts,
+//      compact the kept entries in LDS and write them out coalesced at their
+//      global positions, and write Rowptr'[i] for every row whose Rowptr[i]
+//      falls in the tile.
 // Integer-only and deterministic. With a per-column scale (the randomized
 // sampler's 1/(k p)), each kept value becomes fl32(val * colw[col]).
 #include "rsc_internal.h"
@@ -22,29 +23,40 @@ namespace {
 
 constexpr int kTile = 4096;          // entries per tile
 constexpr int kPer = kTile / 256;    // 256-entry chunks per tile
-static_assert(kPer * 4 == 64, "one wave scans the (chunk, wave) ballots of a tile");
 
 __device__ __forceinline__ bool kept(const uint32_t *__restrict__ mask, int32_t c) {
     return (mask[c >> 5] >> (c & 31)) & 1u;
 }
 
+// Entry o of a tile (0 <= o < kTile) is position o & 255 of chunk o >> 8;
+// within a chunk, wave (o >> 6) & 3, lane o & 63. The kept flags of one
+// (chunk, wave) are one 64-bit ballot, stored per tile in that order
+// (tile_bits[tile * kGroups + chunk * 4 + wave]) for the emit kernel.
+constexpr int kGroups = kPer * 4;
+static_assert(kGroups == 64, "one wave scans the (chunk, wave) ballots of a tile");
+
 __global__ __launch_bounds__(256) void slice_count_kernel(const int32_t *__restrict__ col, int64_t nnz,
                                                           const uint32_t *__restrict__ mask,
-                                                          uint32_t *__restrict__ tile_cnt) {
+                                                          uint32_t *__restrict__ tile_cnt,
+                                                          uint64_t *__restrict__ tile_bits) {
     __shared__ uint32_t s[4];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int64_t ts = (int64_t)blockIdx.x * kTile;
     // all column loads first (independent, coalesced), then the mask bits
     int32_t cv[kPer];
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
-        const int64_t t = ts + threadIdx.x + 256 * j;
+        const int64_t t = ts + 256 * j + threadIdx.x;
         cv[j] = t < nnz ? __builtin_nontemporal_load(col + t) : -1;
     }
     uint32_t c = 0;
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) c += cv[j] >= 0 && kept(mask, cv[j]);
-    for (int off = 32; off > 0; off >>= 1) c += __shfl_down(c, off);
-    if ((threadIdx.x & 63) == 0) s[threadIdx.x >> 6] = c;
+    for (int j = 0; j < kPer; ++j) {
+        const uint64_t b = __ballot(cv[j] >= 0 && kept(mask, cv[j]));
+        if (lane == 0) tile_bits[(int64_t)blockIdx.x * kGroups + j * 4 + w] = b;
+        c += __popcll(b);
+    }
+    if (lane == 0) s[w] = c;
     __syncthreads();
     if (threadIdx.x == 0) tile_cnt[blockIdx.x] = s[0] + s[1] + s[2] + s[3];
 }
@@ -84,20 +96,17 @@ __device__ int32_t lower_bound_rowptr(const int32_t *__restrict__ rowptr, int32_
     return lo;
 }
 
-// Entry o of a tile (0 <= o < kTile) is position o & 255 of chunk o >> 8;
-// within a chunk, wave (o >> 6) & 3, lane o & 63. Each wave's kept flags of
-// a chunk are one ballot, so the kept entries before o are the counts of the
-// earlier (chunk, wave) ballots plus the ballot's bits below the lane.
+// The kept entries before entry o of a tile are the counts of the earlier
+// (chunk, wave) ballots plus the ballot's bits below o's lane.
 __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restrict__ rowptr, int32_t n_rows,
                                                          const int32_t *__restrict__ col,
                                                          const float *__restrict__ val, int64_t nnz,
-                                                         const uint32_t *__restrict__ mask,
+                                                         const uint64_t *__restrict__ tile_bits,
                                                          const uint32_t *__restrict__ tile_off,
                                                          int32_t *__restrict__ rowptr_out,
                                                          int32_t *__restrict__ col_out,
                                                          float *__restrict__ val_out, int64_t capacity,
                                                          const double *__restrict__ colw) {
-    constexpr int kGroups = kPer * 4;  // (chunk, wave) ballots per tile
     __shared__ int32_t s_col[kTile];   // kept entries of the tile, compacted
     __shared__ float s_val[kTile];
     __shared__ uint64_t s_ball[kGroups];
@@ -118,12 +127,10 @@ __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restri
         rc[j] = p < te ? __builtin_nontemporal_load(col + p) : -1;
         rv[j] = p < te ? __builtin_nontemporal_load(val + p) : 0.f;
     }
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-        ball[j] = __ballot(rc[j] >= 0 && kept(mask, rc[j]));
-        if (lane == 0) s_ball[j * 4 + w] = ball[j];
-    }
+    if (t < kGroups) s_ball[t] = tile_bits[(int64_t)blockIdx.x * kGroups + t];
     __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) ball[j] = s_ball[j * 4 + w];
     if (w == 0) {  // exclusive scan of the kGroups ballot counts (kGroups == 64)
         const uint32_t cnt = __popcll(s_ball[lane]);
         uint32_t incl = cnt;
@@ -183,7 +190,7 @@ __global__ __launch_bounds__(256) void zero_rows_kernel(int32_t *__restrict__ p,
 
 size_t slice_ws_bytes(int64_t nnz) {
     const size_t nt = (size_t)ceil_div(std::max<int64_t>(nnz, 1), kTile);
-    return 2 * align_up(nt * sizeof(uint32_t), 256);
+    return 2 * align_up(nt * sizeof(uint32_t), 256) + align_up(nt * kGroups * sizeof(uint64_t), 256);
 }
 
 hipError_t slice_launch(int32_t n_rows, int64_t nnz, const int32_t *rowptr, const int32_t *col,
@@ -199,9 +206,10 @@ hipError_t slice_launch(int32_t n_rows, int64_t nnz, const int32_t *rowptr, cons
     const size_t tb = align_up((size_t)nt * sizeof(uint32_t), 256);
     uint32_t *tile_cnt = static_cast<uint32_t *>(ws);
     uint32_t *tile_off = reinterpret_cast<uint32_t *>(static_cast<char *>(ws) + tb);
-    slice_count_kernel<<<nt, 256, 0, stream>>>(col, nnz, mask, tile_cnt);
+    uint64_t *tile_bits = reinterpret_cast<uint64_t *>(static_cast<char *>(ws) + 2 * tb);
+    slice_count_kernel<<<nt, 256, 0, stream>>>(col, nnz, mask, tile_cnt, tile_bits);
     slice_scan_kernel<<<1, 1024, 0, stream>>>(nt, tile_cnt, tile_off, nnz_out);
-    slice_emit_kernel<<<nt, 256, 0, stream>>>(rowptr, n_rows, col, val, nnz, mask, tile_off, rowptr_out,
+    slice_emit_kernel<<<nt, 256, 0, stream>>>(rowptr, n_rows, col, val, nnz, tile_bits, tile_off, rowptr_out,
                                               col_out, val_out, capacity, colw);
     return hipGetLastError();
 }
