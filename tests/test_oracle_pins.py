@@ -468,6 +468,29 @@ def test_sample_columns_frequencies():
     np.testing.assert_allclose(p, np.arange(1, 13) / 78.0, rtol=1e-9)
 
 
+def test_slice_scaled_against_dense_definition(small_gen):
+    """Scaled slice = dense(A) diag(mask * colw), each value rounded once to
+    fp32; unit scales give the plain slice bit for bit, power-of-two scales
+    are exact."""
+    A, _ = small_gen
+    n_cols = 190
+    rng = np.random.default_rng(4)
+    idx = np.sort(rng.choice(n_cols, size=70, replace=False)).astype(np.int32)
+    mask = mask_of(idx, n_cols)
+    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+    r1, c1, v1 = oracle.slice_scaled(A.rowptr, A.col, A.val, mask, np.ones(n_cols))
+    assert np.array_equal(r1, ro) and np.array_equal(c1, co) and np.array_equal(v1.view(np.uint32), vo.view(np.uint32))
+    colw = rng.uniform(0.1, 9.0, n_cols)
+    colw[::3] = 2.0 ** rng.integers(-4, 5, size=len(colw[::3]))
+    rs, cs, vs = oracle.slice_scaled(A.rowptr, A.col, A.val, mask, colw)
+    assert np.array_equal(rs, ro) and np.array_equal(cs, co)
+    pow2 = (np.arange(n_cols) % 3 == 0)[cs]
+    assert np.array_equal(vs[pow2].astype(np.float64), vo[pow2].astype(np.float64) * colw[cs[pow2]])
+    keep = np.zeros(n_cols); keep[idx] = colw[idx]
+    np.testing.assert_allclose(dense(synth.Csr(A.n, rs, cs, vs), n_cols), dense(A, n_cols) * keep[None, :],
+                               rtol=2.0 ** -23, atol=0)
+
+
 def test_sample_weight_resolution_keeps_cdf_in_range():
     """Above 2^24 pairs the weights lose bits so the CDF total stays below
     2^63: with equal scores every weight is exactly 2^S, and the scale of a
