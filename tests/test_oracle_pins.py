@@ -457,6 +457,19 @@ def test_sample_columns_single_weight_is_exact_slice():
     assert o["count"][17] == 33 and o["count"].sum() == 33 and o["colw"][17] == 1.0
 
 
+def test_sample_columns_infinite_scores_share_the_mass():
+    """With +Inf scores present only those pairs can be drawn, uniformly
+    (p = 1/2 each here), so colw = c / (k / 2)."""
+    key = np.array([key_of(float(i)) for i in range(1, 41)], np.uint64)
+    key[[7, 30]] = key_of(float("inf"))
+    key[3] = 0
+    k = 4000
+    o = oracle.sample_columns(key, k, seed=5)
+    assert o["count"][[7, 30]].sum() == k and o["count"].sum() == k
+    assert abs(int(o["count"][7]) - k // 2) <= 5 * np.sqrt(k / 4)
+    assert np.array_equal(o["colw"][[7, 30]], o["count"][[7, 30]] / (k / 2.0))
+
+
 def test_sample_columns_frequencies():
     # 12 pairs with sqrt(q) = 1..12: p_i = i / 78
     key = np.array([key_of(float(i) ** 2) for i in range(1, 13)], np.uint64)
