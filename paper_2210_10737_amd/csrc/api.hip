@@ -292,7 +292,7 @@ rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, const doubl
     RSC_TRY(check_ws(ws, ws_bytes, rsc::slice_ws_bytes(A->nnz), "slice"));
     RSC_TRY(check_device());
     RSC_TRY(maybe_validate(A, "A", stream));
-    RSC_HIP(rsc::slice_launch(A->n_rows, A->nnz, A->rowptr, A->col, A->val, mask, rowptr_out, col_out, val_out,
+    RSC_HIP(rsc::slice_launch(A->n_rows, A->n_cols, A->nnz, A->rowptr, A->col, A->val, mask, rowptr_out, col_out, val_out,
                               capacity, nnz_out, ws, stream, colw),
             "slice launch");
     if (capacity < A->nnz) {
@@ -416,7 +416,7 @@ rsc_status_t rsc_cache_select(rsc_cache_t *c, int32_t k, int64_t step, hipStream
     if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
     if (k < 0 || k > c->n) return fail(RSC_ERR_INVALID_ARGUMENT, "k = %d outside [0, %d]", k, c->n);
     RSC_HIP(rsc::topk_launch(c->key, c->n, k, c->idx, c->mask, c->ws_topk, stream), "cache topk");
-    RSC_HIP(rsc::slice_launch(c->X.n_rows, c->X.nnz, c->X.rowptr, c->X.col, c->X.val, c->mask, c->s_rowptr,
+    RSC_HIP(rsc::slice_launch(c->X.n_rows, c->X.n_cols, c->X.nnz, c->X.rowptr, c->X.col, c->X.val, c->mask, c->s_rowptr,
                               c->s_col, c->s_val, c->X.nnz, c->d_nnz, c->ws_slice, stream),
             "cache slice");
     RSC_HIP(hipMemcpyAsync(c->h_nnz, c->d_nnz, sizeof(int64_t), hipMemcpyDeviceToHost, stream), "cache nnz");
@@ -436,7 +436,7 @@ rsc_status_t rsc_cache_refresh_random(rsc_cache_t *c, const float *B, int32_t d,
     RSC_TRY(rsc_cache_score(c, B, d, ldb, stream));
     RSC_HIP(rsc::sample_launch(c->key, c->n, k_draws, seed, c->count, c->colw, c->mask, c->ws_sample, stream),
             "cache sample");
-    RSC_HIP(rsc::slice_launch(c->X.n_rows, c->X.nnz, c->X.rowptr, c->X.col, c->X.val, c->mask, c->s_rowptr,
+    RSC_HIP(rsc::slice_launch(c->X.n_rows, c->X.n_cols, c->X.nnz, c->X.rowptr, c->X.col, c->X.val, c->mask, c->s_rowptr,
                               c->s_col, c->s_val, c->X.nnz, c->d_nnz, c->ws_slice, stream, c->colw),
             "cache weighted slice");
     RSC_HIP(hipMemcpyAsync(c->h_nnz, c->d_nnz, sizeof(int64_t), hipMemcpyDeviceToHost, stream), "cache nnz");

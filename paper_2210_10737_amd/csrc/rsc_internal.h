@@ -34,7 +34,7 @@ hipError_t topk_launch(const uint64_t *key, int32_t n, int32_t k, int32_t *idx, 
 
 // ---- slice -------------------------------------------------------------
 size_t slice_ws_bytes(int64_t nnz);
-hipError_t slice_launch(int32_t n_rows, int64_t nnz, const int32_t *rowptr, const int32_t *col,
+hipError_t slice_launch(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr, const int32_t *col,
                         const float *val, const uint32_t *mask, int32_t *rowptr_out,
                         int32_t *col_out, float *val_out, int64_t capacity, int64_t *nnz_out,
                         void *ws, hipStream_t stream, const double *colw = nullptr);

@@ -35,30 +35,80 @@ __device__ __forceinline__ bool kept(const uint32_t *__restrict__ mask, int32_t 
 constexpr int kGroups = kPer * 4;
 static_assert(kGroups == 64, "one wave scans the (chunk, wave) ballots of a tile");
 
-__global__ __launch_bounds__(256) void slice_count_kernel(const int32_t *__restrict__ col, int64_t nnz,
-                                                          const uint32_t *__restrict__ mask,
-                                                          uint32_t *__restrict__ tile_cnt,
-                                                          uint64_t *__restrict__ tile_bits) {
-    __shared__ uint32_t s[4];
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int64_t ts = (int64_t)blockIdx.x * kTile;
-    // all column loads first (independent, coalesced), then the mask bits
-    int32_t cv[kPer];
+// Count pass with the mask in LDS: random 4-byte lookups into a bit set of
+// up to 306 KB would each touch an L2 line (larger than L1); in LDS they
+// cost a few cycles. Persistent blocks of 1024 threads (one per CU, 128 KB
+// of LDS each) walk the column range in pieces of 2^20 columns: load that
+// piece of the mask, then test every tile's entries against it, taking
+// kTilesPerIter tiles per step so each thread has 16 column loads in flight.
+// A tile's ballots and count from later pieces are OR-ed / added by the same
+// threads that wrote them (the tile-to-block assignment is the same in every
+// piece).
+constexpr int kMaskLdsWords = 32768;  // 128 KB: 2^20 columns per piece
+constexpr int kCountThreads = 1024;
+constexpr int kTilesPerIter = 4;
+constexpr int kCountWaves = kCountThreads / 64;
+static_assert(kTile == kCountThreads * 4, "four entries per thread per tile");
+
+__global__ __launch_bounds__(kCountThreads) void slice_count_kernel(const int32_t *__restrict__ col, int64_t nnz,
+                                                                    const uint32_t *__restrict__ mask,
+                                                                    int32_t n_words, int32_t nt,
+                                                                    uint32_t *__restrict__ tile_cnt,
+                                                                    uint64_t *__restrict__ tile_bits) {
+    __shared__ uint32_t s_mask[kMaskLdsWords];
+    __shared__ uint32_t s_cnt[kTilesPerIter][kCountWaves];
+    const int T = threadIdx.x, lane = T & 63, wv = T >> 6;
+    for (int32_t w0 = 0; w0 == 0 || w0 < n_words; w0 += kMaskLdsWords) {
+        const int32_t words = max(0, min(kMaskLdsWords, n_words - w0));
+        __syncthreads();  // the previous piece's lookups are done
+        for (int i = T; i < words; i += kCountThreads) s_mask[i] = mask[w0 + i];
+        __syncthreads();
+        const int64_t lo = (int64_t)w0 * 32, hi = lo + (int64_t)words * 32;
+        const int32_t stride = gridDim.x * kTilesPerIter;
+        // the next step's column loads are issued before this step's tests
+        int32_t nx[kTilesPerIter][4];
+        auto load = [&](int32_t t0) {
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-        const int64_t t = ts + 256 * j + threadIdx.x;
-        cv[j] = t < nnz ? __builtin_nontemporal_load(col + t) : -1;
-    }
-    uint32_t c = 0;
+            for (int u = 0; u < kTilesPerIter; ++u)
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-        const uint64_t b = __ballot(cv[j] >= 0 && kept(mask, cv[j]));
-        if (lane == 0) tile_bits[(int64_t)blockIdx.x * kGroups + j * 4 + w] = b;
-        c += __popcll(b);
+                for (int i = 0; i < 4; ++i) {
+                    const int64_t p = (int64_t)(t0 + u) * kTile + T + kCountThreads * i;
+                    nx[u][i] = (t0 + u < nt && p < nnz) ? __builtin_nontemporal_load(col + p) : -1;
+                }
+        };
+        load(blockIdx.x * kTilesPerIter);
+        for (int32_t t0 = blockIdx.x * kTilesPerIter; t0 < nt; t0 += stride) {
+            int32_t cv[kTilesPerIter][4];
+#pragma unroll
+            for (int u = 0; u < kTilesPerIter; ++u)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) cv[u][i] = nx[u][i];
+            if (t0 + stride < nt) load(t0 + stride);
+#pragma unroll
+            for (int u = 0; u < kTilesPerIter; ++u) {
+                uint32_t c = 0;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int64_t v = cv[u][i];
+                    const bool k = v >= lo && v < hi && ((s_mask[(v - lo) >> 5] >> (v & 31)) & 1u);
+                    const uint64_t b = __ballot(k);
+                    c += __popcll(b);
+                    if (lane == 0 && t0 + u < nt) {
+                        const int64_t g = (int64_t)(t0 + u) * 64 + wv + kCountWaves * i;  // (o >> 6) of the entries
+                        tile_bits[g] = w0 == 0 ? b : (tile_bits[g] | b);
+                    }
+                }
+                if (lane == 0) s_cnt[u][wv] = c;
+            }
+            __syncthreads();
+            if (T < kTilesPerIter && t0 + T < nt) {
+                uint32_t c = 0;
+                for (int v = 0; v < kCountWaves; ++v) c += s_cnt[T][v];
+                tile_cnt[t0 + T] = w0 == 0 ? c : tile_cnt[t0 + T] + c;
+            }
+            __syncthreads();  // s_cnt is reused by the next step
+        }
     }
-    if (lane == 0) s[w] = c;
-    __syncthreads();
-    if (threadIdx.x == 0) tile_cnt[blockIdx.x] = s[0] + s[1] + s[2] + s[3];
 }
 
 __global__ __launch_bounds__(1024) void slice_scan_kernel(int32_t nt, const uint32_t *__restrict__ tile_cnt,
@@ -193,7 +243,7 @@ size_t slice_ws_bytes(int64_t nnz) {
     return 2 * align_up(nt * sizeof(uint32_t), 256) + align_up(nt * kGroups * sizeof(uint64_t), 256);
 }
 
-hipError_t slice_launch(int32_t n_rows, int64_t nnz, const int32_t *rowptr, const int32_t *col,
+hipError_t slice_launch(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr, const int32_t *col,
                         const float *val, const uint32_t *mask, int32_t *rowptr_out,
                         int32_t *col_out, float *val_out, int64_t capacity, int64_t *nnz_out,
                         void *ws, hipStream_t stream, const double *colw) {
@@ -207,7 +257,12 @@ hipError_t slice_launch(int32_t n_rows, int64_t nnz, const int32_t *rowptr, cons
     uint32_t *tile_cnt = static_cast<uint32_t *>(ws);
     uint32_t *tile_off = reinterpret_cast<uint32_t *>(static_cast<char *>(ws) + tb);
     uint64_t *tile_bits = reinterpret_cast<uint64_t *>(static_cast<char *>(ws) + 2 * tb);
-    slice_count_kernel<<<nt, 256, 0, stream>>>(col, nnz, mask, tile_cnt, tile_bits);
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess)
+        (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    const int32_t n_words = (int32_t)ceil_div((int64_t)n_cols, 32);
+    const unsigned cgrid = (unsigned)std::max<int64_t>(1, std::min<int64_t>(cus, ceil_div(nt, kTilesPerIter)));
+    slice_count_kernel<<<cgrid, kCountThreads, 0, stream>>>(col, nnz, mask, n_words, nt, tile_cnt, tile_bits);
     slice_scan_kernel<<<1, 1024, 0, stream>>>(nt, tile_cnt, tile_off, nnz_out);
     slice_emit_kernel<<<nt, 256, 0, stream>>>(rowptr, n_rows, col, val, nnz, tile_bits, tile_off, rowptr_out,
                                               col_out, val_out, capacity, colw);
