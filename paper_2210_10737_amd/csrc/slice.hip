@@ -38,13 +38,13 @@ static_assert(kGroups == 64, "one wave scans the (chunk, wave) ballots of a tile
 // Count pass with the mask in LDS: random 4-byte lookups into a bit set of
 // up to 306 KB would each touch an L2 line (larger than L1); in LDS they
 // cost a few cycles. Persistent blocks of 1024 threads (one per CU, 128 KB
-// of LDS each) walk the column range in pieces of 2^20 columns: load that
+// of LDS each) walk the column range in pieces of 1,277,952 columns: load that
 // piece of the mask, then test every tile's entries against it, taking
 // kTilesPerIter tiles per step so each thread has 16 column loads in flight.
 // A tile's ballots and count from later pieces are OR-ed / added by the same
 // threads that wrote them (the tile-to-block assignment is the same in every
 // piece).
-constexpr int kMaskLdsWords = 32768;  // 128 KB: 2^20 columns per piece
+constexpr int kMaskLdsWords = 39936;  // 156 KB of LDS: 1,277,952 columns per piece
 constexpr int kCountThreads = 1024;
 constexpr int kTilesPerIter = 4;
 constexpr int kCountWaves = kCountThreads / 64;
