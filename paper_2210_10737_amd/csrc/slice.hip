@@ -35,12 +35,13 @@ __device__ __forceinline__ bool kept(const uint32_t *__restrict__ mask, int32_t 
 constexpr int kGroups = kPer * 4;
 static_assert(kGroups == 64, "one wave scans the (chunk, wave) ballots of a tile");
 
-// Count pass with the mask in LDS: random 4-byte lookups into a bit set of
-// up to 306 KB would each touch an L2 line (larger than L1); in LDS they
-// cost a few cycles. Persistent blocks of 1024 threads (one per CU, 128 KB
-// of LDS each) walk the column range in pieces of 1,277,952 columns: load that
+// Count pass with the mask in LDS: random 4-byte lookups into a large bit
+// set would each touch an L2 line (the set outgrows L1); in LDS they cost a
+// few cycles. Persistent blocks of 1024 threads (one per CU, 156 KB of LDS
+// each) walk the column range in pieces of 1,277,952 columns: load that
 // piece of the mask, then test every tile's entries against it, taking
-// kTilesPerIter tiles per step so each thread has 16 column loads in flight.
+// kTilesPerIter tiles per step with the next step's 16 column loads per
+// thread already in flight.
 // A tile's ballots and count from later pieces are OR-ed / added by the same
 // threads that wrote them (the tile-to-block assignment is the same in every
 // piece).
