@@ -257,21 +257,29 @@ __global__ __launch_bounds__(kSpmmLongWaves * 64) void spmm_long_kernel(
     }
 }
 
-// Short rows: one wave per row, kSpmmRowWaves consecutive rows per block;
-// rows longer than kLongRow are left to spmm_long_kernel when skip_long.
+// Short rows: one wave per row, kSpmmRowWaves rows per block; rows longer
+// than kLongRow are left to spmm_long_kernel when skip_long. With `order`,
+// the rows are taken in that order after its first *long_count entries (the
+// long rows): a processing order only, each row's sum is unchanged.
 template <int LPE, int NV>
 __global__ __launch_bounds__(kSpmmRowWaves * 64) void spmm_rows_kernel(
     const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col, const float *__restrict__ val,
     const float *__restrict__ B, int64_t ldb, float *__restrict__ Y, int64_t ldy, int32_t n_rows,
-    int32_t d, int32_t skip_long) {
+    int32_t d, int32_t skip_long, const int32_t *__restrict__ order, const int32_t *__restrict__ long_count) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int sl = lane % LPE;
     bool act[NV];
 #pragma unroll
     for (int q = 0; q < NV; ++q) act[q] = 4 * sl + 4 * kWave * q < d;
-    const int32_t r = blockIdx.x * kSpmmRowWaves + wave;
-    if (r >= n_rows) return;
+    int32_t r = blockIdx.x * kSpmmRowWaves + wave;
+    if (order) {
+        const int64_t i = (int64_t)__builtin_amdgcn_readfirstlane(*long_count) + r;
+        if (i >= n_rows) return;
+        r = __builtin_amdgcn_readfirstlane(order[i]);
+    } else if (r >= n_rows) {
+        return;
+    }
     const int32_t s = __builtin_amdgcn_readfirstlane(rowptr[r]);
     const int32_t e = __builtin_amdgcn_readfirstlane(rowptr[r + 1]);
     if (skip_long && e - s > kLongRow) return;
@@ -282,20 +290,104 @@ __global__ __launch_bounds__(kSpmmRowWaves * 64) void spmm_rows_kernel(
     store_row<LPE, NV>(Y + (int64_t)r * ldy, d, lane, acc);
 }
 
+constexpr int kClasses = 32;
+
 struct SpmmWs {
     int32_t long_count;  // rows in the long-row list
     int32_t long_next;   // next long row to hand out (one counter per feature pass)
-    int32_t pad[62];
+    int32_t pad[30];
+    int32_t cls_count[kClasses];   // rows per length class (ordered mode)
+    int32_t cls_cursor[kClasses];  // next free slot of each class in the order
+    int32_t pad2[32];
 };
 
 inline int64_t long_rows_bound(int32_t n_rows, int64_t nnz) {
     return std::min<int64_t>(n_rows, nnz / (kLongRow + 1));
 }
 
+// Length class of a row: 0 for at most one entry, else ceil(log2(len)), so
+// rows longer than kLongRow = 1024 are exactly the classes >= 11.
+__device__ __forceinline__ int row_class(int32_t len) { return len <= 1 ? 0 : 32 - __clz(len - 1); }
+constexpr int kLongClass = 11;
+static_assert(kLongRow == 1024, "class boundary of the long rows");
+
+__global__ __launch_bounds__(128) void zero_header_kernel(SpmmWs *h) {
+    reinterpret_cast<int32_t *>(h)[threadIdx.x] = 0;
+}
+
+// Rows per length class: an LDS histogram per block, one atomic per class.
+__global__ __launch_bounds__(kCollectThreads) void class_hist_kernel(const int32_t *__restrict__ rowptr,
+                                                                    int32_t n_rows, SpmmWs *h) {
+    __shared__ int32_t hist[kClasses];
+    if (threadIdx.x < kClasses) hist[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kCollectThreads * kCollectPerThread;
+#pragma unroll
+    for (int i = 0; i < kCollectPerThread; ++i) {
+        const int64_t r = base + threadIdx.x + (int64_t)kCollectThreads * i;
+        if (r < n_rows) atomicAdd(&hist[row_class(rowptr[r + 1] - rowptr[r])], 1);
+    }
+    __syncthreads();
+    if (threadIdx.x < kClasses && hist[threadIdx.x]) atomicAdd(&h->cls_count[threadIdx.x], hist[threadIdx.x]);
+}
+
+// Class start offsets with the longest class first; the long rows (classes
+// >= kLongClass) come out as the first long_count entries of the order.
+__global__ __launch_bounds__(64) void class_scan_kernel(SpmmWs *h) {
+    const int c = threadIdx.x;
+    if (c >= kClasses) return;
+    int32_t start = 0, lng = 0;
+    for (int k = c + 1; k < kClasses; ++k) start += h->cls_count[k];
+    for (int k = kLongClass; k < kClasses; ++k) lng += h->cls_count[k];
+    h->cls_cursor[c] = start;
+    if (c == 0) {
+        h->long_count = lng;
+        h->long_next = 0;
+    }
+}
+
+// Places every row in its class's range (the order within a class follows
+// the atomics and does not matter: it only decides which wave takes a row).
+__global__ __launch_bounds__(kCollectThreads) void class_scatter_kernel(const int32_t *__restrict__ rowptr,
+                                                                       int32_t n_rows, SpmmWs *h,
+                                                                       int32_t *__restrict__ order) {
+    __shared__ int32_t hist[kClasses];
+    __shared__ int32_t slot[kClasses];
+    if (threadIdx.x < kClasses) hist[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kCollectThreads * kCollectPerThread;
+    int cls[kCollectPerThread];
+#pragma unroll
+    for (int i = 0; i < kCollectPerThread; ++i) {
+        const int64_t r = base + threadIdx.x + (int64_t)kCollectThreads * i;
+        cls[i] = r < n_rows ? row_class(rowptr[r + 1] - rowptr[r]) : -1;
+        if (cls[i] >= 0) atomicAdd(&hist[cls[i]], 1);
+    }
+    __syncthreads();
+    if (threadIdx.x < kClasses)
+        slot[threadIdx.x] = hist[threadIdx.x] ? atomicAdd(&h->cls_cursor[threadIdx.x], hist[threadIdx.x]) : 0;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kCollectPerThread; ++i)
+        if (cls[i] >= 0)
+            order[atomicAdd(&slot[cls[i]], 1)] = (int32_t)(base + threadIdx.x + (int64_t)kCollectThreads * i);
+}
+
+// Rows are taken longest class first when rows are long on average: the
+// heavy rows then start first and the kernels end on short rows. Results do
+// not depend on it. RSC_SPMM_ORDER=0/1 overrides.
+inline bool use_order(int32_t n_rows, int64_t nnz) {
+    if (const char *env = getenv("RSC_SPMM_ORDER")) return atoi(env) != 0;
+    return n_rows > 0 && nnz >= 128LL * n_rows;
+}
+
 }  // namespace
 
 size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz) {
-    return sizeof(SpmmWs) + align_up(sizeof(int32_t) * (size_t)std::max<int64_t>(1, long_rows_bound(n_rows, nnz)), 256);
+    // room for the full processing order (ordered mode may be switched on by
+    // the environment) or the long-row list
+    const int64_t entries = std::max<int64_t>({1, (int64_t)n_rows, long_rows_bound(n_rows, nnz)});
+    return sizeof(SpmmWs) + align_up(sizeof(int32_t) * (size_t)entries, 256);
 }
 
 int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) {
@@ -324,14 +416,21 @@ hipError_t spmm_launch(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr,
                        int64_t n_src_hint) {
     if (n_rows == 0) return hipSuccess;
     SpmmWs *h = static_cast<SpmmWs *>(ws);
-    int32_t *list = reinterpret_cast<int32_t *>(h + 1);
+    int32_t *list = reinterpret_cast<int32_t *>(h + 1);  // long-row list, or the whole processing order
     const int64_t lbound = long_rows_bound(n_rows, nnz_bound);
     const int32_t n_long_blocks = (int32_t)std::min<int64_t>(lbound, kSpmmLongBlocks);
-    if (n_long_blocks > 0) {
+    const bool ordered = use_order(n_rows, nnz_bound);
+    const unsigned cgrid = (unsigned)ceil_div(n_rows, kCollectThreads * kCollectPerThread);
+    if (ordered) {
+        zero_header_kernel<<<1, 128, 0, stream>>>(h);
+        class_hist_kernel<<<cgrid, kCollectThreads, 0, stream>>>(rowptr, n_rows, h);
+        class_scan_kernel<<<1, 64, 0, stream>>>(h);
+        class_scatter_kernel<<<cgrid, kCollectThreads, 0, stream>>>(rowptr, n_rows, h, list);
+    } else if (n_long_blocks > 0) {
         zero_counters_kernel<<<1, 1, 0, stream>>>(&h->long_count);
-        collect_long_rows_kernel<<<(unsigned)ceil_div(n_rows, kCollectThreads * kCollectPerThread),
-                                   kCollectThreads, 0, stream>>>(rowptr, n_rows, &h->long_count, list);
+        collect_long_rows_kernel<<<cgrid, kCollectThreads, 0, stream>>>(rowptr, n_rows, &h->long_count, list);
     }
+    const int32_t *order = ordered ? list : nullptr;
     const unsigned grid = (unsigned)ceil_div(n_rows, kSpmmRowWaves);
     const int32_t slice = spmm_slice_width(n_rows, nnz_hint, n_src_hint, d);
     for (int32_t f0 = 0; f0 < d;) {
@@ -344,7 +443,8 @@ hipError_t spmm_launch(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr,
                 rowptr, col, val, B + f0, ldb, Y + f0, ldy, dl, &h->long_count, &h->long_next, list);  \
         }                                                                                              \
         spmm_rows_kernel<LPE_, NV_><<<grid, kSpmmRowWaves * 64, 0, stream>>>(                          \
-            rowptr, col, val, B + f0, ldb, Y + f0, ldy, n_rows, dl, n_long_blocks > 0 ? 1 : 0);        \
+            rowptr, col, val, B + f0, ldb, Y + f0, ldy, n_rows, dl, n_long_blocks > 0 ? 1 : 0, order,  \
+            &h->long_count);                                                                           \
     } while (0)
         switch (slice) {
             case 16: RSC_SPMM_LAUNCH(4, 1); break;

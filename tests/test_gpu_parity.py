@@ -184,6 +184,37 @@ def test_spmm_deterministic(gen_graph):
     assert np.array_equal(Y1.view(np.uint32), Y2.view(np.uint32))
 
 
+@pytest.mark.parametrize("d", [5, 64, 256, 300])
+def test_spmm_processing_order_is_bitwise_neutral(gen_graph, d):
+    """Taking rows longest class first (RSC_SPMM_ORDER=1) changes only which
+    wave takes which row: the result equals the index-order schedule bit for
+    bit, also with feature slices."""
+    import os
+    A = to_dev(gen_graph, 2500)
+    Bh, _ = padded(2500, d, seed=19)
+    B = dense_dev(Bh)
+    old = os.environ.get("RSC_SPMM_ORDER")
+    out = {}
+    try:
+        for mode in ("0", "1"):
+            os.environ["RSC_SPMM_ORDER"] = mode
+            out[mode] = [rsc.spmm(A, B, d=d).cpu().numpy()]
+            for sl in ("32", "64"):
+                os.environ["RSC_SPMM_SLICE"] = sl
+                out[mode].append(rsc.spmm(A, B, d=d).cpu().numpy())
+                del os.environ["RSC_SPMM_SLICE"]
+    finally:
+        os.environ.pop("RSC_SPMM_SLICE", None)
+        if old is None:
+            os.environ.pop("RSC_SPMM_ORDER", None)
+        else:
+            os.environ["RSC_SPMM_ORDER"] = old
+    for y0, y1 in zip(out["0"], out["1"]):
+        assert np.array_equal(y0.view(np.uint32), y1.view(np.uint32))
+    Yo, S = oracle.spmm(gen_graph.rowptr, gen_graph.col, gen_graph.val, Bh, d=d, with_mag=True)
+    assert rel_err(out["1"][0], Yo, S) <= TOL_EXACT
+
+
 def test_spmm_empty():
     A = synth.Csr(5, np.zeros(6, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
     Y = rsc.spmm(to_dev(A, 3), dense_dev(np.ones((3, 8), np.float32))).cpu().numpy()
