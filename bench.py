@@ -505,6 +505,12 @@ def main() -> int:
         "ops_ms": {"warm": {kk: stats(v) for kk, v in per.items()},
                    "cold": {kk: stats(v) for kk, v in cold.items()}},
         "copy_ceiling_GBs": round(copy_gbs, 1),
+        # each op's algorithmic bytes over its p50 time, against the HBM peak
+        "ops_roofline": {
+            kind: {"bytes": int(b), "p50_ms": round(float(np.median(per[kind])), 4),
+                   "GBs": round(b / (float(np.median(per[kind])) * 1e-3) / 1e9, 1),
+                   "frac": round(b / (float(np.median(per[kind])) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+            for kind, b in (("exact", b_exact), ("sampled", b_sampled), ("refresh", b_refresh)) if per[kind]},
         "roofline": {
             "bound": "hbm",
             "kernel": "spmm_kernel (exact SpMM)",
