@@ -13,10 +13,15 @@
 //   * 8 gathers are issued before their FMAs for memory-level parallelism;
 //   * products are accumulated in fp32 over each run of <= 64 entries and the
 //     run sum is folded into an fp64 accumulator; one fp32 rounding per output;
-//   * rows with more than kLongRow entries are taken by persistent 4-wave
+//   * rows with more than kLongRow entries are taken by persistent 8-wave
 //     blocks: the waves take interleaved runs of 64 entries and their fp64
 //     sums are combined in LDS in fixed wave order. No float atomics, so the
-//     result is bitwise reproducible.
+//     result is bitwise reproducible;
+//   * B may be processed in feature slices of 16..128 floats (several passes,
+//     several entries per load instruction) when the slice of the referenced
+//     B rows gets close to cache size;
+//   * on graphs with long rows on average, rows are taken longest length
+//     class first (a scheduling order only).
 #include <cstdlib>
 
 #include "rsc_internal.h"
