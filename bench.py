@@ -66,10 +66,15 @@ def refresh_random_bytes(n: int, nnz: int, nnz_kept: int, k: int, d: int) -> int
 
 
 def kernel_source_digest() -> str:
-    h = hashlib.sha256()
-    with open(os.path.join(ROOT, "paper_2210_10737_amd", "csrc", "spmm.hip"), "rb") as fh:
-        h.update(fh.read())
-    return h.hexdigest()[:16]
+    """Digest of the SpMM kernel source with comments and blank lines removed
+    (a comment edit does not invalidate the counter record)."""
+    import re
+    with open(os.path.join(ROOT, "paper_2210_10737_amd", "csrc", "spmm.hip")) as fh:
+        src = fh.read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    lines = [re.sub(r"//.*", "", line).rstrip() for line in src.splitlines()]
+    code = "\n".join(line for line in lines if line.strip())
+    return hashlib.sha256(code.encode()).hexdigest()[:16]
 
 
 def load_traffic(digest: str, launch_bytes: int):
