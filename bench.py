@@ -211,6 +211,39 @@ def train_bench(args) -> int:
         model.close()
         del model, opt
         torch.cuda.empty_cache()
+    ablation = None
+    if args.ablation_steps > 0:
+        # caching / switching ablation (Table 4's layout): a whole run of
+        # `ablation_steps` steps per setting, timed end to end; "no cache"
+        # selects and slices against each step's own gradient (k_l still
+        # allocated every `refresh` steps), "switch" runs the last 20 % of
+        # the steps exact
+        def run(enabled, cache_on, total):
+            cfg = RscConfig(budget=(pct, 100), alpha=(2, 100), refresh_interval=args.refresh, enabled=enabled,
+                            total_steps=total, cache=cache_on)
+            model = GCN(Ad, p["in_features"], p["hidden"], p["classes"], cfg, seed=args.seed + 2)
+            opt = torch.optim.Adam(model.parameters(), lr=0.01)
+            model.train_step(X, Y, opt, 0)    # untimed: first-call costs
+            model.controller.last_refresh = None
+            model.controller.history.clear()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for s_ in range(args.ablation_steps):
+                model.train_step(X, Y, opt, s_)
+            torch.cuda.synchronize()
+            ms_ = (time.perf_counter() - t0) * 1e3 / args.ablation_steps
+            model.close()
+            del model, opt
+            torch.cuda.empty_cache()
+            return ms_
+        T = args.ablation_steps
+        base = run(False, True, None)
+        ablation = {"steps": T, "exact_ms_per_step": round(base, 3)}
+        for cache_on in (False, True):
+            for switch_on in (False, True):
+                ms_ = run(True, cache_on, T if switch_on else None)
+                ablation[f"cache={'yes' if cache_on else 'no'},switch={'yes' if switch_on else 'no'}"] = {
+                    "ms_per_step": round(ms_, 3), "speedup": round(base / ms_, 3)}
     staleness = None
     if args.staleness_steps > 0:
         # untimed diagnostic run: AUC / overlap of each layer's selection
@@ -241,6 +274,7 @@ def train_bench(args) -> int:
                    "hidden": p["hidden"], "classes": p["classes"], "budget_pct": pct,
                    "refresh_interval": args.refresh, "alpha_pct": 2, "seed": args.seed},
         "exact": results["exact"], "rsc": results["rsc"],
+        "ablation": ablation,
         "staleness": staleness,
     }
     print(json.dumps(out), flush=True)
@@ -266,6 +300,8 @@ def main() -> int:
                     help="topk: the k pairs with the largest scores, unscaled (section 2.2.1); random: k "
                          "i.i.d. draws with p_i proportional to the pair score, scaled by 1/(k p_i) "
                          "(Eq. 2 with Eq. 3)")
+    ap.add_argument("--ablation-steps", type=int, default=50,
+                    help="gcn2-train only: steps per setting of the caching / switching ablation (0 = skip)")
     ap.add_argument("--staleness-steps", type=int, default=60,
                     help="gcn2-train only: steps of the untimed selection-staleness run (0 = skip)")
     ap.add_argument("--graph", action="store_true",

@@ -19,7 +19,12 @@ from . import col_sqnorms, greedy, pair_keys, slice_csr, topk
 
 
 class RscReference:
-    def __init__(self, rowptr, col, val, n, widths, budget, alpha, refresh_interval):
+    """cache=False: every approximated step selects (O4, O5) and slices (O6)
+    against that step's own gradient with the current k_l before the
+    product, instead of reusing the slice of the last refresh (the
+    no-caching arm of section 3.3.1's comparison)."""
+
+    def __init__(self, rowptr, col, val, n, widths, budget, alpha, refresh_interval, cache=True):
         self.n = n
         self.A = sp.csr_matrix((val.astype(np.float64), col, rowptr), shape=(n, n))
         self.AT = self.A.T.tocsr()
@@ -33,9 +38,18 @@ class RscReference:
         self.k = [n] * len(widths)
         self.idx = [None] * len(widths)
         self.slices = [None] * len(widths)
+        self.cache = cache
+
+    def _select(self, l, key):
+        rowptr, col, val = self.csr_t
+        self.idx[l], mask = topk(key, self.k[l])
+        ro, co, vo = slice_csr(rowptr, col, val, mask)
+        self.slices[l] = sp.csr_matrix((vo.astype(np.float64), co, ro), shape=(self.n, self.n))
 
     def _backward_spmm(self, l, g, mode):
         if mode == "sampled":
+            if not self.cache:
+                self._select(l, pair_keys(self.cn2, g.astype(np.float32))["key"])
             return self.slices[l] @ g
         return self.AT @ g
 
@@ -62,11 +76,8 @@ class RscReference:
                 fro_b2.append(float(o["rn2"].sum()))
             self.k, _ = greedy(keys, self.colnnz, self.nnz, self.widths, self.fro_a2, fro_b2,
                                self.budget, self.alpha)
-            rowptr, col, val = self.csr_t
             for l in range(2):
-                self.idx[l], mask = topk(keys[l], self.k[l])
-                ro, co, vo = slice_csr(rowptr, col, val, mask)
-                self.slices[l] = sp.csr_matrix((vo.astype(np.float64), co, ro), shape=(self.n, self.n))
+                self._select(l, keys[l])
             self.last = step
         out["k"] = list(self.k)
         out["idx"] = [None if i is None else i.copy() for i in self.idx]

@@ -6,6 +6,9 @@ three modes, chosen per step by `RscController`:
 
 * "sampled": on the layer's cached top-k slice (rsc_spmm_sampled) — the
   approximation of section 3.1, reused across steps (section 3.3.1);
+* "resample": without caching, each approximated step scores, selects and
+  slices against its own gradient (rsc_cache_refresh with the current k_l)
+  before the sampled product;
 * "score": exactly, and the pairs (column i of A_hat^T, row i of grad P_l)
   are scored into the layer's cache (rsc_cache_score) — a refresh step;
   after the backward the controller allocates k_l across layers with the
@@ -46,7 +49,11 @@ class _Aggregate(torch.autograd.Function):
         layer = ctx.layer
         g = grad_P.contiguous()
         t = layer._tick()
-        if layer.mode == "sampled":
+        if layer.mode == "resample":
+            # no caching: this step's own top-k and slice, then the sampled product
+            layer.cache.refresh(g, layer.k, step=layer.step)
+            grad_J = layer.cache.spmm_sampled(g)
+        elif layer.mode == "sampled":
             grad_J = layer.cache.spmm_sampled(g)
         else:
             grad_J = spmm(layer.AT, g, ws=layer.ws)
@@ -70,6 +77,8 @@ class AggregationLayer:
         self.ws = torch.empty(max(spmm_workspace_bytes(A), spmm_workspace_bytes(self.AT)),
                               dtype=torch.uint8, device=A.rowptr.device)
         self.mode = "exact"
+        self.k = A.n_cols       # columns kept by the approximation (set by the allocation)
+        self.step = 0
         self.timings = None  # set to a list to record (kind, start, end) events of each SpMM
 
     def _tick(self):
@@ -97,6 +106,8 @@ class RscConfig:
     switch_fraction: tuple = (8, 10)  # approximate for this share of the steps (section 5.1)
     total_steps: int | None = None
     enabled: bool = True
+    cache: bool = True               # reuse each slice until the next refresh (section 3.3.1); if
+                                     # False every approximated step selects and slices anew
     track_staleness: bool = False    # record AUC / overlap of successive selections
 
 
@@ -161,16 +172,17 @@ class RscController:
         elif self.last_refresh is None or step - self.last_refresh >= cfg.refresh_interval:
             mode = "score"
         else:
-            mode = "sampled"
+            mode = "sampled" if cfg.cache else "resample"
         for layer in self.layers:
             layer.mode = mode
+            layer.step = step
         self.history.append(StepRecord(step, mode))
         return mode
 
     def end(self, step: int) -> None:
         rec = self.history[-1]
         if rec.mode != "score":
-            rec.k = list(self.k) if rec.mode == "sampled" else [self.n] * len(self.layers)
+            rec.k = list(self.k) if rec.mode in ("sampled", "resample") else [self.n] * len(self.layers)
             return
         torch.cuda.synchronize()  # time the allocation alone, not the backward before it
         t0 = time.perf_counter()
@@ -195,6 +207,7 @@ class RscController:
                                              self.fro_a2, fro_b2, self.cfg.budget, self.cfg.alpha)
         for layer, k in zip(self.layers, self.k):
             layer.cache.select(k, step)
+            layer.k = k
         rec.greedy_s = time.perf_counter() - t0
         if self.order is not None:
             for l, layer in enumerate(self.layers):

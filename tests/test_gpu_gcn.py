@@ -66,6 +66,37 @@ def test_rsc_step_matches_reference(budget):
     model.close()
 
 
+def test_no_cache_reselects_every_step():
+    """cache=False: each approximated step selects and slices against its own
+    gradient (the no-caching arm); matches the reference run the same way."""
+    A = synth.make_graph("tiny", 0)
+    n = A.n
+    X = synth.dense_normal(n, 32, seed=1)
+    Y = (np.random.default_rng(3).random((n, 16)) < 0.5).astype(np.float32)
+    cfg = RscConfig(budget=(1, 2), alpha=(2, 100), refresh_interval=3, cache=False)
+    model = GCN(rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n), 32, 64, 16, cfg, seed=2)
+    ref = RscReference(A.rowptr, A.col, A.val, n, [64, 16], (1, 2), (2, 100), 3, cache=False)
+    W1 = model.W1.detach().cpu().numpy().astype(np.float64)
+    W2 = model.W2.detach().cpu().numpy().astype(np.float64)
+    Xd, Yd = torch.from_numpy(X).cuda(), torch.from_numpy(Y).cuda()
+    modes = []
+    for step in range(4):
+        model.W1.grad = None
+        model.W2.grad = None
+        loss = float(model.train_step(Xd, Yd, None, step).detach())
+        r = ref.step(X.astype(np.float64), W1, W2, Y.astype(np.float64), step)
+        rec = model.controller.history[-1]
+        modes.append(rec.mode)
+        assert abs(loss - r["loss"]) <= 1e-5 * abs(r["loss"])
+        for g, gr in ((model.W1.grad.cpu().numpy(), r["gW1"]), (model.W2.grad.cpu().numpy(), r["gW2"])):
+            assert np.max(np.abs(g - gr)) <= 1e-4 * np.max(np.abs(gr))
+        assert rec.k == r["k"]
+        for l, layer in enumerate((model.agg1, model.agg2)):
+            assert np.array_equal(rsc.cache_snapshot(layer.cache, step)["idx"], r["idx"][l]), (step, l)
+    assert modes == ["score", "resample", "resample", "score"]
+    model.close()
+
+
 @pytest.mark.parametrize("name,d", [("tiny", 64), ("gcn2", 100)])
 def test_device_greedy_profile_bitwise(name, d):
     """Device ranking (stable radix sort) and block profile against the
