@@ -59,26 +59,38 @@ __global__ __launch_bounds__(256) void pair_scores_kernel(const double *__restri
                                                           uint64_t *__restrict__ key,
                                                           float *__restrict__ score,
                                                           double *__restrict__ rn2) {
+    constexpr int kLoads = kRows * kTileF / 4 / 256;  // float4 loads per thread per tile
     __shared__ float tile[kRows][kTileF + 1];
     const int t = threadIdx.x;
     const int64_t row0 = (int64_t)blockIdx.x * kRows;
-    double acc = 0.0;
-    for (int32_t f0 = 0; f0 < d; f0 += kTileF) {
+    float4 v[kLoads];
+    // the next tile's loads are issued before the current tile is summed
+    auto load = [&](int32_t f0) {
 #pragma unroll
-        for (int it = 0; it < kRows * kTileF / 4 / 256; ++it) {
+        for (int it = 0; it < kLoads; ++it) {
             const int idx = t + 256 * it;
             const int rl = idx >> 3, fq = idx & 7;
             const int64_t row = row0 + rl;
             const int32_t f = f0 + 4 * fq;
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            v[it] = make_float4(0.f, 0.f, 0.f, 0.f);
             // ld % 4 == 0 and ld >= d, so a float4 starting below d stays in the row
-            if (row < n && f < d) v = *reinterpret_cast<const float4 *>(B + row * ldb + f);
-            tile[rl][4 * fq + 0] = v.x;
-            tile[rl][4 * fq + 1] = v.y;
-            tile[rl][4 * fq + 2] = v.z;
-            tile[rl][4 * fq + 3] = v.w;
+            if (row < n && f < d) v[it] = *reinterpret_cast<const float4 *>(B + row * ldb + f);
+        }
+    };
+    double acc = 0.0;
+    load(0);
+    for (int32_t f0 = 0; f0 < d; f0 += kTileF) {
+#pragma unroll
+        for (int it = 0; it < kLoads; ++it) {
+            const int idx = t + 256 * it;
+            const int rl = idx >> 3, fq = idx & 7;
+            tile[rl][4 * fq + 0] = v[it].x;
+            tile[rl][4 * fq + 1] = v[it].y;
+            tile[rl][4 * fq + 2] = v[it].z;
+            tile[rl][4 * fq + 3] = v[it].w;
         }
         __syncthreads();
+        if (f0 + kTileF < d) load(f0 + kTileF);
         const int lim = min(kTileF, d - f0);
         for (int j = 0; j < lim; ++j) {
             const double b = (double)tile[t][j];
