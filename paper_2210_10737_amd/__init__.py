@@ -8,6 +8,18 @@ built, every call raises.
 
 Paper: Liu et al., "RSC: Accelerate Graph Neural Networks Training via
 Randomized Sparse Computations", ICML 2023 (arXiv 2210.10737).
+
+Typical use (A_hat symmetric, so it serves as its own transpose):
+
+    A = DeviceCsr.from_host(rowptr, col, val, n_cols)   # int32 / int32 / float32
+    Y = spmm(A, H)                                       # exact forward
+    cache = Cache(A, A, refresh_interval=10)
+    k = k_from_fraction(A.n_cols, 30, 100)
+    if cache.get(step, with_slice=False)["needs_refresh"]:
+        cache.refresh(G, k, step)                        # scores, top-k, slice
+    G_back = cache.spmm_sampled(G)                       # sampled backward
+
+`gcn.GCN` wires these into a training step with the layer-wise allocation.
 """
 from __future__ import annotations
 
