@@ -151,6 +151,33 @@ def cpu_baseline(A, Hh, Gh, k, pct, refresh_interval, step_bytes_full, n_rows_sa
     }
 
 
+def parity_check(A, Hh, Gh, k, Y, Yb, kept, n_rows, seed):
+    """The benchmarked outputs against the oracle: the kept columns bit for
+    bit, and the exact and sampled products on a seeded sample of rows
+    (max |Y - Y_oracle| / max(S, FLT_MIN), S = sum |a||b|)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    rng = np.random.Generator(np.random.PCG64(seed + 11))
+    rows = np.sort(rng.choice(A.n, size=min(A.n, n_rows), replace=False)).astype(np.int32)
+    tiny = np.float32(np.finfo(np.float32).tiny)
+
+    def err(Yd, rowptr, col, val, Bh):
+        Yo, S = oracle.spmm(rowptr, col, val, Bh, rows=rows, with_mag=True)
+        got = Yd[torch.from_numpy(rows.astype(np.int64)).to(Yd.device)].cpu().numpy().astype(np.float64)
+        return float(np.max(np.abs(got - Yo) / np.maximum(S, tiny)))
+
+    cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)
+    idx_o, mask_o = oracle.topk(oracle.pair_keys(cn2, Gh)["key"], k)
+    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask_o)
+    return {"rows_checked": int(len(rows)),
+            "kept_columns_equal": bool(np.array_equal(np.asarray(kept), idx_o[:k])),
+            "exact_max_rel_err": err(Y, A.rowptr, A.col, A.val, Hh),
+            "sampled_max_rel_err": err(Yb, ro, co, vo, Gh),
+            "tolerance": {"exact": 1e-5, "sampled": 1e-4}}
+
+
 def train_bench(args) -> int:
     """Two-layer GCN training on the gcn2 workload (716,847 nodes, 300 input
     features, hidden 512, 100 labels, multi-label BCE, Adam): exact training
@@ -307,6 +334,9 @@ def main() -> int:
     ap.add_argument("--graph", action="store_true",
                     help="replay the exact + sampled SpMM of each step from one captured HIP graph "
                          "(refreshes stay eager)")
+    ap.add_argument("--parity-rows", type=int, default=2000,
+                    help="after timing, check this many sampled output rows and the kept columns against "
+                         "the oracle (0 = skip)")
     ap.add_argument("--cold-reps", type=int, default=5,
                     help="after the timed steps, repetitions of each op that follow a 1 GiB cache flush")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -527,7 +557,7 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": args.workload, "aggregator": args.aggregator, "graph": w.description,
                    "n": n, "nnz": nnz, "d": d,
-                   "budget_pct": pct, "k": k, "selector": args.selector, "graph": bool(args.graph),
+                   "budget_pct": pct, "k": k, "selector": args.selector, "hip_graph": bool(args.graph),
                    "refresh_interval": args.refresh,
                    "seed": args.seed},
         "exact_spmm_ms": round(exact_ms, 4),
@@ -566,6 +596,8 @@ def main() -> int:
             "kernel_src_digest": digest,
         },
     }
+    if args.parity_rows > 0 and args.aggregator == "gcn" and args.selector == "topk":
+        out["parity"] = parity_check(A, Hh, Gh, k, Y, Yb, idx, args.parity_rows, args.seed)
     traffic = load_traffic(digest, b_exact) if args.workload == "copurchase" and args.aggregator == "gcn" else None
     if traffic is not None:
         out["roofline"]["traffic"] = round(traffic["total_bytes"])
