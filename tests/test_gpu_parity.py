@@ -58,7 +58,7 @@ def _gpu(gpu):
 
 
 # ------------------------------------------------------------------ SpMM
-SPMM_D = [1, 3, 4, 64, 100, 256, 300, 512, 600]
+SPMM_D = [1, 3, 4, 64, 100, 256, 300, 512, 600, 1030]
 
 
 @pytest.fixture(scope="module")
