@@ -25,7 +25,14 @@
  * Pins (tests/test_oracle_pins.py): dense brute force, B = I, permutation
  * matrices, closed forms on regular graphs, Cauchy-Schwarz on the score mass,
  * an independent selection method, slice identities, a hand-worked greedy
- * example with its derivation, and the greedy's invariants.
+ * example with its derivation, and the greedy's invariants; for SpMM_MEAN the
+ * dense definition and the appendix example; for the randomized sampler the
+ * generator's published outputs, weights re-derived independently, draw
+ * frequencies, infinite scores and unbiasedness; for the scaled slice the
+ * dense definition.
+ * Parity unpinned: the sampler's draw boundary rule (W_i > u rather than >=)
+ * decides a draw only when u equals a CDF boundary, which no seeded input
+ * reaches.
  */
 #include <math.h>
 #include <stdint.h>
