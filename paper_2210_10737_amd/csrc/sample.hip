@@ -38,12 +38,20 @@ struct SampleWs {
 
 __global__ void sample_init_kernel(SampleWs *h) { h->max_key = 0ull; }
 
+// max over the keys: a block-wide max, then one atomic per block (the grid
+// is kept small: every atomic hits the same address)
 __global__ __launch_bounds__(256) void max_key_kernel(const uint64_t *__restrict__ key, int32_t n, SampleWs *h) {
+    __shared__ unsigned long long s[4];
     unsigned long long m = 0ull;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         m = max(m, (unsigned long long)key[i]);
     for (int off = 32; off > 0; off >>= 1) m = max(m, (unsigned long long)__shfl_down(m, off));
-    if ((threadIdx.x & 63) == 0 && m) atomicMax(&h->max_key, m);
+    if ((threadIdx.x & 63) == 0) s[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        m = max(max(s[0], s[1]), max(s[2], s[3]));
+        if (m) atomicMax(&h->max_key, m);
+    }
 }
 
 // w_i and the per-tile sums of w
@@ -187,7 +195,7 @@ hipError_t sample_launch(const uint64_t *key, int32_t n, int32_t k, uint64_t see
     const unsigned g = (unsigned)std::min<int64_t>(ceil_div(n, 256), 4096);
     sample_init_kernel<<<1, 1, 0, stream>>>(h);
     zero_i32_kernel<<<g, 256, 0, stream>>>(count, n);
-    max_key_kernel<<<std::min<unsigned>(g, 1024), 256, 0, stream>>>(key, n, h);
+    max_key_kernel<<<std::min<unsigned>(g, 256), 256, 0, stream>>>(key, n, h);
     int bits = 38;  // weight resolution S
     if (n > (1 << 24)) {
         int lg = 0;
