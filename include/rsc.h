@@ -214,7 +214,8 @@ rsc_status_t rsc_sample_columns(const uint64_t *key, int32_t n, int32_t k, uint6
  *     the current slice in place; used when k comes from the keys of several
  *     operands, as in the layer-wise allocation of section 3.2.
  *   rsc_cache_select: top k of the keys last scored, then the slice; records
- *     `step` as the refresh step.
+ *     `step` as the refresh step (RSC_ERR_INVALID_ARGUMENT if nothing was
+ *     scored yet).
  *   rsc_cache_refresh_random: scores against B, then the randomized sampler
  *     (rsc_sample_columns: k_draws draws with `seed`) instead of top-k, and
  *     the slice with each kept column scaled by its colw; rsc_cache_get then

@@ -137,6 +137,7 @@ struct rsc_cache {
     void *ws_sample = nullptr;
     size_t ws_sample_bytes = 0;
     bool random = false;       // the current slice comes from rsc_cache_refresh_random
+    bool scored = false;       // keys have been computed at least once
     int32_t *idx = nullptr;
     uint32_t *mask = nullptr;
     int32_t *s_rowptr = nullptr;
@@ -409,12 +410,14 @@ rsc_status_t rsc_cache_score(rsc_cache_t *c, const float *B, int32_t d, int64_t 
     if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
     RSC_TRY(check_dense(B, c->n, d, ldb, "B"));
     RSC_HIP(rsc::pair_scores_launch(c->cn2, B, c->n, d, ldb, c->key, nullptr, c->rn2, stream), "cache scores");
+    c->scored = true;
     return RSC_OK;
 }
 
 rsc_status_t rsc_cache_select(rsc_cache_t *c, int32_t k, int64_t step, hipStream_t stream) {
     if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
     if (k < 0 || k > c->n) return fail(RSC_ERR_INVALID_ARGUMENT, "k = %d outside [0, %d]", k, c->n);
+    if (!c->scored) return fail(RSC_ERR_INVALID_ARGUMENT, "cache select before any score");
     RSC_HIP(rsc::topk_launch(c->key, c->n, k, c->idx, c->mask, c->ws_topk, stream), "cache topk");
     RSC_HIP(rsc::slice_launch(c->X.n_rows, c->X.n_cols, c->X.nnz, c->X.rowptr, c->X.col, c->X.val, c->mask, c->s_rowptr,
                               c->s_col, c->s_val, c->X.nnz, c->d_nnz, c->ws_slice, stream),
@@ -425,6 +428,7 @@ rsc_status_t rsc_cache_select(rsc_cache_t *c, int32_t k, int64_t step, hipStream
     c->last_step = step;
     c->version += 1;
     c->nnz_known = false;
+    c->random = false;
     return RSC_OK;
 }
 

@@ -123,3 +123,26 @@ def test_cache_random_zero_draws_and_unrefreshed_cache():
     assert snap["nnz"] == 0 and not snap["rowptr"].any()
     assert not cache.spmm_sampled(B).any()
     cache.close()
+
+
+def test_cache_switches_between_random_and_topk_slices():
+    """A top-k refresh after a randomized one reports its index list again;
+    selecting before anything was scored is an error."""
+    A = synth.random_csr(600, 500, 25, seed=81)
+    AT = synth.transpose(A, 500)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, 500)
+    cache = rsc.Cache(X, rsc.DeviceCsr.from_host(AT.rowptr, AT.col, AT.val, 600))
+    with pytest.raises(rsc.RscError):
+        cache.select(10, step=0)
+    B = synth.dense_normal(500, 24, seed=82)
+    Bd = torch.from_numpy(B).cuda()
+    cache.refresh_random(Bd, 100, seed=3, step=0)
+    assert rsc.cache_snapshot(cache)["idx_ptr"] is None
+    cache.refresh(Bd, 120, step=1)
+    snap = rsc.cache_snapshot(cache, 1)
+    cn2, _ = oracle.col_sqnorms(AT.rowptr, AT.val)
+    idx, mask = oracle.topk(oracle.pair_keys(cn2, B)["key"], 120)
+    assert snap["idx_ptr"] is not None and np.array_equal(snap["idx"], idx)
+    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+    assert np.array_equal(snap["val"].view(np.uint32), vo.view(np.uint32))
+    cache.close()
