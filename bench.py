@@ -344,7 +344,7 @@ def main() -> int:
                          "size, so hardware byte counters can be scaled)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+        print(f"bench.py measures one GPU; the library has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         return 2
 
