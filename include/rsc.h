@@ -96,7 +96,9 @@ rsc_status_t rsc_csr_validate(const rsc_csr_t *A, int64_t *bad_row_host, hipStre
  * into fp64; one rounding to fp32 per output. The features may be processed
  * in several passes of 32/64 columns of B (chosen from n_rows, nnz, n_cols
  * and d only, with the environment variable RSC_SPMM_SLICE = 16/32/64/128/256
- * as an override); the pass layout sets the summation order. Deterministic:
+ * as an override); the pass layout sets the summation order. Rows may be
+ * taken longest first (when rows are long on average; RSC_SPMM_ORDER = 0/1
+ * overrides), which never changes a result. Deterministic:
  * equal arguments give bitwise equal Y, and rsc_spmm_sampled with every
  * column kept reproduces rsc_spmm bitwise.
  * ws / ws_bytes: scratch of at least rsc_spmm_workspace_bytes(A) bytes,
