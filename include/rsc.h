@@ -98,9 +98,15 @@ rsc_status_t rsc_csr_validate(const rsc_csr_t *A, int64_t *bad_row_host, hipStre
  * and d only, with the environment variable RSC_SPMM_SLICE = 16/32/64/128/256
  * as an override); the pass layout sets the summation order. Rows may be
  * taken longest first (when rows are long on average; RSC_SPMM_ORDER = 0/1
- * overrides), which never changes a result. Deterministic:
- * equal arguments give bitwise equal Y, and rsc_spmm_sampled with every
- * column kept reproduces rsc_spmm bitwise.
+ * overrides), which never changes a result. Column-blocked mode: when a
+ * 64-float slice of B spans 2..8 ranges of about 4.5 MiB and rows hold at
+ * least 64 entries per range on average, the columns are cut into P equal
+ * index ranges processed one after another (the gathered B rows then stay
+ * in L2); each row's entries in one range are summed as above and rounded
+ * to an fp32 partial, and the P partials are added in fp64 in range order
+ * and rounded once (RSC_SPMM_BLOCKED = 0 switches it off, 2..8 forces that
+ * P). Deterministic: equal arguments give bitwise equal Y, and
+ * rsc_spmm_sampled with every column kept reproduces rsc_spmm bitwise.
  * ws / ws_bytes: scratch of at least rsc_spmm_workspace_bytes(A) bytes,
  * 256-byte aligned, private to this call until it completes on `stream`. */
 size_t rsc_spmm_workspace_bytes(const rsc_csr_t *A);

@@ -185,7 +185,7 @@ rsc_status_t rsc_csr_validate(const rsc_csr_t *A, int64_t *bad_row_host, hipStre
 // ------------------------------------------------------------------- A1
 size_t rsc_spmm_workspace_bytes(const rsc_csr_t *A) {
     if (!A || A->n_rows < 0 || A->nnz < 0) return 0;
-    return rsc::spmm_ws_bytes(A->n_rows, A->nnz);
+    return rsc::spmm_ws_bytes(A->n_rows, A->nnz, A->n_cols);
 }
 
 rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb, float *Y,
@@ -193,11 +193,11 @@ rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb
     RSC_TRY(check_csr(A, "A"));
     RSC_TRY(check_dense(B, A->n_cols, d, ldb, "B"));
     RSC_TRY(check_dense(Y, A->n_rows, d, ldy, "Y"));
-    RSC_TRY(check_ws(ws, ws_bytes, rsc::spmm_ws_bytes(A->n_rows, A->nnz), "spmm"));
+    RSC_TRY(check_ws(ws, ws_bytes, rsc::spmm_ws_bytes(A->n_rows, A->nnz, A->n_cols), "spmm"));
     RSC_TRY(check_device());
     RSC_TRY(maybe_validate(A, "A", stream));
-    RSC_HIP(rsc::spmm_launch(A->n_rows, A->nnz, A->rowptr, A->col, A->val, B, d, ldb, Y, ldy, ws, stream,
-                             A->nnz, A->n_cols),
+    RSC_HIP(rsc::spmm_launch(A->n_rows, A->n_cols, A->nnz, A->rowptr, A->col, A->val, B, d, ldb, Y, ldy, ws,
+                             ws_bytes, stream, A->nnz, A->n_cols),
             "spmm launch");
     return RSC_OK;
 }
@@ -353,7 +353,7 @@ rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_
     const int64_t n = std::max<int32_t>(c->n, 1), m = std::max<int64_t>(X->nnz, 1);
     c->ws_topk_bytes = rsc::topk_ws_bytes(c->n);
     c->ws_slice_bytes = rsc::slice_ws_bytes(X->nnz);
-    c->ws_spmm_bytes = rsc::spmm_ws_bytes(X->n_rows, X->nnz);
+    c->ws_spmm_bytes = rsc::spmm_ws_bytes(X->n_rows, X->nnz, X->n_cols);
     c->ws_sample_bytes = rsc::sample_ws_bytes(c->n);
     struct {
         void **p;
@@ -501,8 +501,8 @@ rsc_status_t rsc_spmm_sampled(rsc_cache_t *c, const float *B, int32_t d, int64_t
     // never depend on which calls came before).
     const int64_t kk = std::min<int64_t>(c->k, c->n);
     const int64_t nnz_hint = c->n > 0 ? c->X.nnz * kk / c->n : 0;
-    RSC_HIP(rsc::spmm_launch(c->X.n_rows, c->X.nnz, c->s_rowptr, c->s_col, c->s_val, B, d, ldb, Y, ldy,
-                             c->ws_spmm, stream, nnz_hint, kk),
+    RSC_HIP(rsc::spmm_launch(c->X.n_rows, c->X.n_cols, c->X.nnz, c->s_rowptr, c->s_col, c->s_val, B, d, ldb, Y,
+                             ldy, c->ws_spmm, c->ws_spmm_bytes, stream, nnz_hint, kk),
             "spmm_sampled launch");
     return RSC_OK;
 }

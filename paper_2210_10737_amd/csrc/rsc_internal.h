@@ -12,13 +12,14 @@ namespace rsc {
 constexpr int kWave = 64;
 
 // ---- SpMM --------------------------------------------------------------
-size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz);
+size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz, int32_t n_cols);
 // nnz_bound sizes the long-row list; nnz_hint (expected entries) and
-// n_src_hint (distinct B rows the entries reference) choose the feature slice.
+// n_src_hint (distinct B rows the entries reference) choose the feature slice
+// and the column-blocked mode, which runs only if ws_bytes holds its buffers.
 int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d);
-hipError_t spmm_launch(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr, const int32_t *col,
-                       const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
-                       int64_t ldy, void *ws, hipStream_t stream, int64_t nnz_hint,
+hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const int32_t *rowptr,
+                       const int32_t *col, const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
+                       int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream, int64_t nnz_hint,
                        int64_t n_src_hint);
 
 // ---- scores ------------------------------------------------------------

@@ -21,7 +21,10 @@
 //     several entries per load instruction) when the slice of the referenced
 //     B rows gets close to cache size;
 //   * on graphs with long rows on average, rows are taken longest length
-//     class first (a scheduling order only).
+//     class first (a scheduling order only);
+//   * when the referenced B rows span a few L2-sized ranges, the columns are
+//     cut into those ranges and processed one range at a time, with fp32
+//     partial rows combined in fixed range order (column-blocked mode).
 #include <cstdlib>
 
 #include "rsc_internal.h"
@@ -45,16 +48,17 @@ typedef float vf4 __attribute__((ext_vector_type(4)));
 __global__ void zero_counters_kernel(int32_t *p) { p[0] = 0; p[1] = 0; }
 __global__ void zero_next_kernel(int32_t *p) { *p = 0; }
 
-// Appends every row longer than kLongRow to `list`. Each thread checks
-// kCollectPerThread rows (coalesced rowptr reads); a block-wide scan gives
-// each long row its place, and one atomic per block reserves the block's
-// range, so the list costs a few hundred atomics rather than one per row.
-// The list order only decides which block takes which row.
+// Appends every row longer than kLongRow to `list`; row r spans
+// [ptr[r], ptr[r + off]) (off = 1 for a CSR row pointer). Each thread checks
+// kCollectPerThread rows (coalesced reads); a block-wide scan gives each long
+// row its place, and one atomic per block reserves the block's range, so the
+// list costs a few hundred atomics rather than one per row. The list order
+// only decides which block takes which row.
 constexpr int kCollectThreads = 1024;
 constexpr int kCollectPerThread = 4;
 
 __global__ __launch_bounds__(kCollectThreads) void collect_long_rows_kernel(
-    const int32_t *__restrict__ rowptr, int32_t n_rows, int32_t *count, int32_t *list) {
+    const int32_t *__restrict__ ptr, int64_t off, int32_t n_rows, int32_t *count, int32_t *list) {
     __shared__ int32_t s_wave[kCollectThreads / 64];
     __shared__ int32_t s_base;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -64,7 +68,7 @@ __global__ __launch_bounds__(kCollectThreads) void collect_long_rows_kernel(
 #pragma unroll
     for (int i = 0; i < kCollectPerThread; ++i) {
         const int64_t r = base + t + (int64_t)kCollectThreads * i;
-        is_long[i] = r < n_rows && rowptr[r + 1] - rowptr[r] > kLongRow;
+        is_long[i] = r < n_rows && ptr[r + off] - ptr[r] > kLongRow;
         mine += is_long[i];
     }
     // exclusive scan of `mine` over the block: within the wave, then across waves
@@ -213,10 +217,11 @@ __device__ __forceinline__ void store_row(float *__restrict__ yrow, int32_t d, i
 // Long rows: persistent blocks of kSpmmLongWaves waves take rows from the list
 // through an atomic counter; within a row the waves take interleaved runs of
 // 64 entries and their fp64 sums are added in LDS in fixed wave order.
+// Row r spans [ptr[r], ptr[r + off]) and is written to row r of Y.
 // B and Y point at the first feature of the current slice; d is its width.
 template <int LPE, int NV>
 __global__ __launch_bounds__(kSpmmLongWaves * 64) void spmm_long_kernel(
-    const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col, const float *__restrict__ val,
+    const int32_t *__restrict__ ptr, int64_t off, const int32_t *__restrict__ col, const float *__restrict__ val,
     const float *__restrict__ B, int64_t ldb, float *__restrict__ Y, int64_t ldy, int32_t d,
     const int32_t *__restrict__ long_count, int32_t *__restrict__ long_next,
     const int32_t *__restrict__ long_rows) {
@@ -235,8 +240,8 @@ __global__ __launch_bounds__(kSpmmLongWaves * 64) void spmm_long_kernel(
         const int32_t j = __builtin_amdgcn_readfirstlane(s_job);
         if (j >= nl) break;  // block-uniform: every wave read the same s_job
         const int32_t r = __builtin_amdgcn_readfirstlane(long_rows[j]);
-        const int32_t s = __builtin_amdgcn_readfirstlane(rowptr[r]);
-        const int32_t e = __builtin_amdgcn_readfirstlane(rowptr[r + 1]);
+        const int32_t s = __builtin_amdgcn_readfirstlane(ptr[r]);
+        const int32_t e = __builtin_amdgcn_readfirstlane(ptr[r + off]);
         double acc[NV][4];
 #pragma unroll
         for (int q = 0; q < NV; ++q) acc[q][0] = acc[q][1] = acc[q][2] = acc[q][3] = 0.0;
@@ -265,10 +270,11 @@ __global__ __launch_bounds__(kSpmmLongWaves * 64) void spmm_long_kernel(
 // Short rows: one wave per row, kSpmmRowWaves rows per block; rows longer
 // than kLongRow are left to spmm_long_kernel when skip_long. With `order`,
 // the rows are taken in that order after its first *long_count entries (the
-// long rows): a processing order only, each row's sum is unchanged.
+// long rows): a processing order only, each row's sum is unchanged. Row r
+// spans [ptr[r], ptr[r + off]).
 template <int LPE, int NV>
 __global__ __launch_bounds__(kSpmmRowWaves * 64) void spmm_rows_kernel(
-    const int32_t *__restrict__ rowptr, const int32_t *__restrict__ col, const float *__restrict__ val,
+    const int32_t *__restrict__ ptr, int64_t off, const int32_t *__restrict__ col, const float *__restrict__ val,
     const float *__restrict__ B, int64_t ldb, float *__restrict__ Y, int64_t ldy, int32_t n_rows,
     int32_t d, int32_t skip_long, const int32_t *__restrict__ order, const int32_t *__restrict__ long_count) {
     const int lane = threadIdx.x & (kWave - 1);
@@ -285,8 +291,8 @@ __global__ __launch_bounds__(kSpmmRowWaves * 64) void spmm_rows_kernel(
     } else if (r >= n_rows) {
         return;
     }
-    const int32_t s = __builtin_amdgcn_readfirstlane(rowptr[r]);
-    const int32_t e = __builtin_amdgcn_readfirstlane(rowptr[r + 1]);
+    const int32_t s = __builtin_amdgcn_readfirstlane(ptr[r]);
+    const int32_t e = __builtin_amdgcn_readfirstlane(ptr[(int64_t)r + off]);
     if (skip_long && e - s > kLongRow) return;
     double acc[NV][4];
 #pragma unroll
@@ -386,13 +392,120 @@ inline bool use_order(int32_t n_rows, int64_t nnz) {
     return n_rows > 0 && nnz >= 128LL * n_rows;
 }
 
+// ---- column-blocked mode ------------------------------------------------
+// When the columns of B fit L2 in a few pieces, the product is taken one
+// piece at a time: the columns are cut into P equal ranges, and "virtual row"
+// (b, r) = the entries of row r whose column lies in range b (contiguous in
+// the row, since columns are sorted). The virtual rows are processed
+// block-major, so at any moment the whole GPU gathers from one range of B
+// rows (a few MB, resident in each XCD's L2) instead of from all of them.
+// Each virtual row writes a partial row; a combine pass adds the P partials
+// of row r in fixed order b = 0..P-1 in fp64 and rounds once.
+constexpr int kBlockW = 64;                         // features per blocked pass
+constexpr double kBlockBytes = 4.5 * 1024 * 1024;   // B bytes per column range (~ one XCD's L2)
+constexpr int kMaxBlocks = 8;                       // partial outputs at most 8 x Y per pass
+
+// Number of column ranges P for a product with n_rows rows, about nnz
+// entries and n_src distinct B rows referenced; 1 = not blocked. Blocked when
+// the referenced 64-float slice of B spans 2..8 L2-sized ranges and rows are
+// long enough that each piece still holds a full 64-entry run on average.
+// RSC_SPMM_BLOCKED=0 switches the mode off, =2..8 forces that P.
+inline int32_t column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src) {
+    if (n_rows <= 0 || (int64_t)(kMaxBlocks + 1) * n_rows > INT32_MAX) return 1;  // virtual rows are int32
+    if (const char *env = getenv("RSC_SPMM_BLOCKED")) {
+        const int v = atoi(env);
+        if (v == 0) return 1;
+        if (v >= 2 && v <= kMaxBlocks) return v;
+    }
+    const int64_t P = (int64_t)std::ceil((double)n_src * kBlockW * 4 / kBlockBytes);
+    if (P < 2 || P > kMaxBlocks) return 1;
+    if (nnz < 64LL * P * n_rows) return 1;
+    return (int32_t)P;
+}
+
+// S[b * n_rows + r] = first entry of row r with column >= b * n_cols / P
+// (b = 0: rowptr[r]; b = P: rowptr[r + 1]); binary search in the sorted row.
+// Piece b of row r ("virtual row" v = b * n_rows + r) is then
+// [S[v], S[v + n_rows]): the row kernels take S with offset n_rows as their
+// row pointer, and consecutive virtual rows run through one column range.
+__global__ __launch_bounds__(256) void split_rows_kernel(const int32_t *__restrict__ rowptr,
+                                                         const int32_t *__restrict__ col, int32_t n_rows,
+                                                         int32_t n_cols, int32_t P, int32_t *__restrict__ S) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (int64_t)n_rows * (P + 1)) return;
+    const int32_t b = (int32_t)(t / n_rows);
+    const int64_t r = t - (int64_t)b * n_rows;
+    const int32_t s = rowptr[r], e = rowptr[r + 1];
+    int32_t pos;
+    if (b == 0) {
+        pos = s;
+    } else if (b == P) {
+        pos = e;
+    } else {
+        const int64_t bound = (int64_t)b * n_cols / P;
+        int32_t lo = s, hi = e;
+        while (lo < hi) {
+            const int32_t mid = lo + (hi - lo) / 2;
+            if (col[mid] < bound) lo = mid + 1; else hi = mid;
+        }
+        pos = lo;
+    }
+    S[t] = pos;
+}
+
+// Y[r][f] = fl32(sum over b = 0..P-1 of part[b * n_rows + r][f]) in fp64;
+// one thread per 4 features of a row.
+__global__ __launch_bounds__(256) void combine_blocks_kernel(const float *__restrict__ part, int64_t ldp,
+                                                             int32_t n_rows, int32_t P, int32_t d,
+                                                             float *__restrict__ Y, int64_t ldy) {
+    const int32_t q = (d + 3) / 4;
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (int64_t)n_rows * q) return;
+    const int64_t r = t / q;
+    const int32_t f = 4 * (int32_t)(t - r * q);
+    const int32_t m = min(4, d - f);
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int32_t b = 0; b < P; ++b) {
+        const float *p = part + ((int64_t)b * n_rows + r) * ldp + f;
+        if (m == 4) {
+            const vf4 x = __builtin_nontemporal_load(reinterpret_cast<const vf4 *>(p));
+            acc[0] += (double)x.x;
+            acc[1] += (double)x.y;
+            acc[2] += (double)x.z;
+            acc[3] += (double)x.w;
+        } else {
+            for (int i = 0; i < m; ++i) acc[i] += (double)p[i];
+        }
+    }
+    float *y = Y + r * ldy + f;
+    if (m == 4) {
+        const vf4 o = {(float)acc[0], (float)acc[1], (float)acc[2], (float)acc[3]};
+        __builtin_nontemporal_store(o, reinterpret_cast<vf4 *>(y));
+    } else {
+        for (int i = 0; i < m; ++i) y[i] = (float)acc[i];
+    }
+}
+
 }  // namespace
 
-size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz) {
-    // room for the full processing order (ordered mode may be switched on by
-    // the environment) or the long-row list
+namespace {
+// bytes of the row list (long rows, or the whole processing order)
+size_t list_bytes(int32_t n_rows, int64_t nnz) {
     const int64_t entries = std::max<int64_t>({1, (int64_t)n_rows, long_rows_bound(n_rows, nnz)});
-    return sizeof(SpmmWs) + align_up(sizeof(int32_t) * (size_t)entries, 256);
+    return align_up(sizeof(int32_t) * (size_t)entries, 256);
+}
+// bytes of the blocked mode's split points and partial rows for P ranges
+size_t blocked_bytes(int32_t n_rows, int32_t P) {
+    if (P <= 1) return 0;
+    return align_up(sizeof(int32_t) * (size_t)n_rows * (P + 1), 256) +
+           align_up(sizeof(float) * (size_t)P * n_rows * kBlockW, 256);
+}
+}  // namespace
+
+size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz, int32_t n_cols) {
+    // header, the row list, then the blocked mode's buffers when the full
+    // product would be blocked (a slice of it never needs more ranges)
+    return sizeof(SpmmWs) + list_bytes(n_rows, nnz) + blocked_bytes(n_rows, column_blocks(n_rows, nnz, n_cols));
 }
 
 int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) {
@@ -415,13 +528,50 @@ int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) 
     return 32;
 }
 
-hipError_t spmm_launch(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr, const int32_t *col,
-                       const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
-                       int64_t ldy, void *ws, hipStream_t stream, int64_t nnz_hint,
+hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const int32_t *rowptr,
+                       const int32_t *col, const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
+                       int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream, int64_t nnz_hint,
                        int64_t n_src_hint) {
     if (n_rows == 0) return hipSuccess;
     SpmmWs *h = static_cast<SpmmWs *>(ws);
     int32_t *list = reinterpret_cast<int32_t *>(h + 1);  // long-row list, or the whole processing order
+    // The blocked mode is chosen from the expected entries and referenced B
+    // rows (the same for the exact product and a full-budget slice of it);
+    // it runs only when the workspace holds its buffers.
+    const int32_t P = column_blocks(n_rows, nnz_hint, n_src_hint);
+    const size_t head = sizeof(SpmmWs) + list_bytes(n_rows, nnz_bound);
+    if (P > 1 && head + blocked_bytes(n_rows, P) <= ws_bytes) {
+        char *p = static_cast<char *>(ws) + head;
+        int32_t *S = reinterpret_cast<int32_t *>(p);
+        float *part = reinterpret_cast<float *>(p + align_up(sizeof(int32_t) * (size_t)n_rows * (P + 1), 256));
+        const int64_t ns = (int64_t)n_rows * (P + 1);
+        const int32_t nv = P * n_rows;  // virtual rows, block-major
+        split_rows_kernel<<<(unsigned)ceil_div(ns, 256), 256, 0, stream>>>(rowptr, col, n_rows, n_cols, P, S);
+        // long pieces (a piece of a row longer than kLongRow) go to the
+        // persistent 8-wave blocks as in the unblocked mode
+        const int32_t n_long = (int32_t)std::min<int64_t>(long_rows_bound(n_rows, nnz_bound), kSpmmLongBlocks);
+        if (n_long > 0) {
+            zero_counters_kernel<<<1, 1, 0, stream>>>(&h->long_count);
+            collect_long_rows_kernel<<<(unsigned)ceil_div(nv, kCollectThreads * kCollectPerThread), kCollectThreads,
+                                       0, stream>>>(S, n_rows, nv, &h->long_count, list);
+        }
+        const unsigned vgrid = (unsigned)ceil_div(nv, kSpmmRowWaves);
+        for (int32_t f0 = 0; f0 < d; f0 += kBlockW) {
+            const int32_t dl = std::min<int32_t>(d - f0, kBlockW);
+            if (n_long > 0) {
+                if (f0 > 0) zero_next_kernel<<<1, 1, 0, stream>>>(&h->long_next);
+                spmm_long_kernel<16, 1><<<n_long, kSpmmLongWaves * 64, 0, stream>>>(
+                    S, n_rows, col, val, B + f0, ldb, part, kBlockW, dl, &h->long_count, &h->long_next, list);
+            }
+            spmm_rows_kernel<16, 1><<<vgrid, kSpmmRowWaves * 64, 0, stream>>>(
+                S, n_rows, col, val, B + f0, ldb, part, kBlockW, nv, dl, n_long > 0 ? 1 : 0, nullptr,
+                &h->long_count);
+            const int64_t nc = (int64_t)n_rows * ((dl + 3) / 4);
+            combine_blocks_kernel<<<(unsigned)ceil_div(nc, 256), 256, 0, stream>>>(part, kBlockW, n_rows, P, dl,
+                                                                                  Y + f0, ldy);
+        }
+        return hipGetLastError();
+    }
     const int64_t lbound = long_rows_bound(n_rows, nnz_bound);
     const int32_t n_long_blocks = (int32_t)std::min<int64_t>(lbound, kSpmmLongBlocks);
     const bool ordered = use_order(n_rows, nnz_bound);
@@ -433,7 +583,7 @@ hipError_t spmm_launch(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr,
         class_scatter_kernel<<<cgrid, kCollectThreads, 0, stream>>>(rowptr, n_rows, h, list);
     } else if (n_long_blocks > 0) {
         zero_counters_kernel<<<1, 1, 0, stream>>>(&h->long_count);
-        collect_long_rows_kernel<<<cgrid, kCollectThreads, 0, stream>>>(rowptr, n_rows, &h->long_count, list);
+        collect_long_rows_kernel<<<cgrid, kCollectThreads, 0, stream>>>(rowptr, 1, n_rows, &h->long_count, list);
     }
     const int32_t *order = ordered ? list : nullptr;
     const unsigned grid = (unsigned)ceil_div(n_rows, kSpmmRowWaves);
@@ -445,10 +595,10 @@ hipError_t spmm_launch(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr,
         if (n_long_blocks > 0) {                                                                       \
             if (f0 > 0) zero_next_kernel<<<1, 1, 0, stream>>>(&h->long_next);                          \
             spmm_long_kernel<LPE_, NV_><<<n_long_blocks, kSpmmLongWaves * 64, 0, stream>>>(             \
-                rowptr, col, val, B + f0, ldb, Y + f0, ldy, dl, &h->long_count, &h->long_next, list);  \
+                rowptr, 1, col, val, B + f0, ldb, Y + f0, ldy, dl, &h->long_count, &h->long_next, list);  \
         }                                                                                              \
         spmm_rows_kernel<LPE_, NV_><<<grid, kSpmmRowWaves * 64, 0, stream>>>(                          \
-            rowptr, col, val, B + f0, ldb, Y + f0, ldy, n_rows, dl, n_long_blocks > 0 ? 1 : 0, order,  \
+            rowptr, 1, col, val, B + f0, ldb, Y + f0, ldy, n_rows, dl, n_long_blocks > 0 ? 1 : 0, order,  \
             &h->long_count);                                                                           \
     } while (0)
         switch (slice) {

@@ -1,0 +1,128 @@
+"""Column-blocked SpMM mode (the columns cut into P index ranges processed
+one after another, partial rows added in fixed range order). Forced with
+RSC_SPMM_BLOCKED = 2..8 on seeded random shapes, and chosen automatically on
+a graph whose B slice spans two L2-sized ranges: exact and sampled SpMM
+against the oracle, a full-budget slice equal to the exact product bit for
+bit, and the automatic choice equal to the forced one."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2210_10737_amd as rsc
+import synth
+
+pytestmark = pytest.mark.gpu
+FLT_MIN = np.float32(np.finfo(np.float32).tiny)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu(gpu):
+    yield
+
+
+class blocked:
+    """Sets RSC_SPMM_BLOCKED for the duration of a with-block."""
+
+    def __init__(self, value):
+        self.value = value
+
+    def __enter__(self):
+        self.old = os.environ.get("RSC_SPMM_BLOCKED")
+        if self.value is None:
+            os.environ.pop("RSC_SPMM_BLOCKED", None)
+        else:
+            os.environ["RSC_SPMM_BLOCKED"] = str(self.value)
+
+    def __exit__(self, *exc):
+        if self.old is None:
+            os.environ.pop("RSC_SPMM_BLOCKED", None)
+        else:
+            os.environ["RSC_SPMM_BLOCKED"] = self.old
+
+
+def rel_err(Y, Yo, S):
+    return float(np.max(np.abs(np.asarray(Y, np.float64) - Yo) / np.maximum(S, FLT_MIN))) if Yo.size else 0.0
+
+
+def shape(seed):
+    rng = np.random.default_rng(5000 + seed)
+    n_rows = int(rng.integers(1, 2500))
+    n_cols = int(rng.integers(1, 3000))
+    kinds = rng.choice(["short", "runs", "long", "empty"], size=n_rows, p=[0.5, 0.3, 0.1, 0.1])
+    lens = np.where(kinds == "short", rng.integers(0, 20, n_rows),
+                    np.where(kinds == "runs", rng.integers(60, 300, n_rows),
+                             np.where(kinds == "long", rng.integers(1000, 3000, n_rows), 0)))
+    lens = np.minimum(lens, n_cols)
+    A = synth.bucket_csr(lens, n_cols, seed=seed)
+    d = int(rng.choice([1, 5, 16, 64, 65, 100, 256, 300]))
+    ld = (d + 3) // 4 * 4 + 4 * int(rng.integers(0, 3))
+    k = int(rng.choice([0, 1, n_cols // 4, n_cols]))
+    P = int(rng.choice([2, 3, 5, 8]))
+    return A, n_cols, d, ld, k, P
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_forced_blocks_match_oracle(seed):
+    A, n_cols, d, ld, k, P = shape(seed)
+    B = synth.dense_normal(n_cols, d, seed=seed + 11, ld=ld)
+    Bd = torch.from_numpy(B).cuda()
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
+    Yo, S = oracle.spmm(A.rowptr, A.col, A.val, B, d=d, with_mag=True)
+    with blocked(P):
+        Y = rsc.spmm(X, Bd, d=d).cpu().numpy()
+        AT = synth.transpose(A, n_cols)
+        cache = rsc.Cache(X, rsc.DeviceCsr.from_host(AT.rowptr, AT.col, AT.val, A.n))
+        cache.refresh(Bd, k, step=0, d=d)
+        Ys = cache.spmm_sampled(Bd, d=d).cpu().numpy()
+        snap = rsc.cache_snapshot(cache)
+        cache.close()
+    assert rel_err(Y, Yo, S) <= 1e-5, (seed, P, d, ld)
+    Yso, Ss = oracle.spmm(snap["rowptr"], snap["col"], snap["val"], B, d=d, with_mag=True)
+    assert rel_err(Ys, Yso, Ss) <= 1e-4, (seed, P)
+    if k == n_cols:
+        assert np.array_equal(Ys.view(np.uint32), Y.view(np.uint32)), (seed, P)
+    with blocked(0):
+        Y0 = rsc.spmm(X, Bd, d=d).cpu().numpy()
+    assert rel_err(Y0, Yo, S) <= 1e-5
+
+
+def test_blocked_is_reproducible_and_keeps_empty_rows_zero():
+    lens = np.array([0, 700, 0, 1500, 64, 0, 2000], np.int64)
+    A = synth.bucket_csr(lens, 2100, seed=3)
+    B = torch.from_numpy(synth.dense_normal(2100, 96, seed=4)).cuda()
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, 2100)
+    with blocked(8):
+        Y1 = rsc.spmm(X, B)
+        Y2 = rsc.spmm(X, B)
+    assert torch.equal(Y1, Y2)
+    assert torch.count_nonzero(Y1[torch.from_numpy(lens == 0).cuda()]) == 0
+    Yo, S = oracle.spmm(A.rowptr, A.col, A.val, B.cpu().numpy(), with_mag=True)
+    assert rel_err(Y1.cpu().numpy(), Yo, S) <= 1e-5
+
+
+def test_automatic_choice_on_long_rows():
+    # 20,000 columns x 64 floats = 4.9 MiB of B per pass: two ranges; rows of
+    # ~200 entries (>= 64 per range on average) switch the mode on.
+    n = 20000
+    rng = np.random.default_rng(9)
+    lens = rng.integers(150, 260, n)
+    A = synth.bucket_csr(lens, n, seed=12)
+    B = synth.dense_normal(n, 128, seed=13)
+    Bd = torch.from_numpy(B).cuda()
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n)
+    with blocked(None):
+        Y = rsc.spmm(X, Bd)
+        cache = rsc.Cache(X, X)
+        cache.refresh(Bd, n, step=0)
+        Yk = cache.spmm_sampled(Bd)
+        cache.close()
+    with blocked(2):
+        Y2 = rsc.spmm(X, Bd)
+    assert torch.equal(Y, Y2)                  # the automatic mode took P = 2
+    assert torch.equal(Yk, Y)                  # full budget == exact, bitwise
+    rows = np.arange(0, n, 97, dtype=np.int32)
+    Yo, S = oracle.spmm(A.rowptr, A.col, A.val, B, rows=rows, with_mag=True)
+    assert rel_err(Y.cpu().numpy()[rows], Yo, S) <= 1e-5
