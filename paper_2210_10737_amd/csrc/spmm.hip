@@ -271,8 +271,9 @@ __global__ __launch_bounds__(kSpmmLongWaves * 64) void spmm_long_kernel(
 // than kLongRow are left to spmm_long_kernel when skip_long. With `order`,
 // the rows are taken in that order after its first *long_count entries (the
 // long rows): a processing order only, each row's sum is unchanged. Row r
-// spans [ptr[r], ptr[r + off]).
-template <int LPE, int NV>
+// spans [ptr[r], ptr[r + off]); kCsr says off == 1 (a CSR row pointer, both
+// bounds then come from one 8-byte scalar load).
+template <int LPE, int NV, bool kCsr>
 __global__ __launch_bounds__(kSpmmRowWaves * 64) void spmm_rows_kernel(
     const int32_t *__restrict__ ptr, int64_t off, const int32_t *__restrict__ col, const float *__restrict__ val,
     const float *__restrict__ B, int64_t ldb, float *__restrict__ Y, int64_t ldy, int32_t n_rows,
@@ -292,7 +293,7 @@ __global__ __launch_bounds__(kSpmmRowWaves * 64) void spmm_rows_kernel(
         return;
     }
     const int32_t s = __builtin_amdgcn_readfirstlane(ptr[r]);
-    const int32_t e = __builtin_amdgcn_readfirstlane(ptr[(int64_t)r + off]);
+    const int32_t e = __builtin_amdgcn_readfirstlane(kCsr ? ptr[r + 1] : ptr[(int64_t)r + off]);
     if (skip_long && e - s > kLongRow) return;
     double acc[NV][4];
 #pragma unroll
@@ -563,7 +564,7 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
                 spmm_long_kernel<16, 1><<<n_long, kSpmmLongWaves * 64, 0, stream>>>(
                     S, n_rows, col, val, B + f0, ldb, part, kBlockW, dl, &h->long_count, &h->long_next, list);
             }
-            spmm_rows_kernel<16, 1><<<vgrid, kSpmmRowWaves * 64, 0, stream>>>(
+            spmm_rows_kernel<16, 1, false><<<vgrid, kSpmmRowWaves * 64, 0, stream>>>(
                 S, n_rows, col, val, B + f0, ldb, part, kBlockW, nv, dl, n_long > 0 ? 1 : 0, nullptr,
                 &h->long_count);
             const int64_t nc = (int64_t)n_rows * ((dl + 3) / 4);
@@ -597,7 +598,7 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
             spmm_long_kernel<LPE_, NV_><<<n_long_blocks, kSpmmLongWaves * 64, 0, stream>>>(             \
                 rowptr, 1, col, val, B + f0, ldb, Y + f0, ldy, dl, &h->long_count, &h->long_next, list);  \
         }                                                                                              \
-        spmm_rows_kernel<LPE_, NV_><<<grid, kSpmmRowWaves * 64, 0, stream>>>(                          \
+        spmm_rows_kernel<LPE_, NV_, true><<<grid, kSpmmRowWaves * 64, 0, stream>>>(                    \
             rowptr, 1, col, val, B + f0, ldb, Y + f0, ldy, n_rows, dl, n_long_blocks > 0 ? 1 : 0, order,  \
             &h->long_count);                                                                           \
     } while (0)
