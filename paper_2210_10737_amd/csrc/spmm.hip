@@ -525,7 +525,7 @@ int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) 
     const double mib = 1024.0 * 1024.0;
     const double ws32 = (double)n_src * 32 * 4 / mib, ws64 = 2 * ws32;
     if (ws32 > 64.0) return full;
-    if (ws64 <= 20.0 && ws32 > 8.0) return 64;
+    if (ws64 <= 30.0 && ws32 > 8.0) return 64;
     return 32;
 }
 
