@@ -265,7 +265,7 @@ int64_t orc_greedy(int32_t L, int32_t n, int64_t nnz, const uint64_t *const *key
     int32_t step = (int32_t)(((int64_t)n * a_num) / a_den);
     if (step < 1) step = 1;
     int64_t bud = total;
-    while (bud * (int64_t)C_den > (int64_t)C_num * total) {
+    while ((__int128)bud * C_den > (__int128)C_num * total) {  /* exact: both sides may pass 2^63 */
         int32_t best = -1;
         double best_inc = 0.0;
         for (int32_t l = 0; l < L; ++l) {
