@@ -27,7 +27,9 @@
  *     surface at the caller's next synchronisation.
  *   - Stateless calls are reentrant; a cache handle must not be used from
  *     two host threads at once, and two calls that share a workspace must
- *     not overlap on the device.
+ *     not overlap on the device. The calls on one cache share its internal
+ *     buffers and workspaces, so they must be ordered on the device (one
+ *     stream, or events between streams).
  */
 #ifndef RSC_H
 #define RSC_H

@@ -46,14 +46,18 @@ rsc_status_t hip_fail(hipError_t e, const char *what) {
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 rsc_status_t check_device() {
-    static int count = -1;
-    if (count < 0) {
+    static const int count = [] {  // counted once, thread-safe initialisation
         int c = 0;
         if (hipGetDeviceCount(&c) != hipSuccess) c = 0;
-        count = c;
-    }
+        return c;
+    }();
     if (count <= 0) return fail(RSC_ERR_NO_DEVICE, "no HIP device visible");
     return RSC_OK;
+}
+
+// bud / total > C_num / C_den without overflow (both sides can pass 2^63)
+bool over_budget(int64_t bud, int64_t total, int32_t C_num, int32_t C_den) {
+    return (__int128)bud * C_den > (__int128)C_num * total;
 }
 
 rsc_status_t check_csr(const rsc_csr_t *A, const char *name) {
@@ -577,7 +581,7 @@ rsc_status_t rsc_greedy_allocate(int32_t L, int32_t n, int64_t nnz, const uint64
     int32_t step = (int32_t)(((int64_t)n * alpha_num) / alpha_den);
     if (step < 1) step = 1;
     int64_t bud = total;
-    while (bud * (int64_t)C_den > (int64_t)C_num * total) {
+    while (over_budget(bud, total, C_num, C_den)) {
         int32_t best = -1;
         double best_inc = 0.0;
         for (int32_t l = 0; l < L; ++l) {
@@ -648,7 +652,7 @@ rsc_status_t rsc_greedy_allocate_profiles(int32_t L, int32_t n, int64_t nnz, int
         total += nnz * (int64_t)d_host[l];
     }
     int64_t bud = total;
-    while (bud * (int64_t)C_den > (int64_t)C_num * total) {
+    while (over_budget(bud, total, C_num, C_den)) {
         int32_t best = -1;
         double best_inc = 0.0;
         for (int32_t l = 0; l < L; ++l) {

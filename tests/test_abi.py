@@ -239,3 +239,15 @@ def test_selection_auc_brute_force():
     # identical ranking: the previous top-k is ranked first -> AUC 1
     assert selection_auc(np.arange(20), np.arange(5)) == 1.0
     assert selection_auc(np.arange(20)[::-1].copy(), np.arange(5)) == 0.0
+
+
+def test_greedy_budget_comparison_wide_range():
+    """bud * C_den and C_num * total pass 2^63 here (nnz = 2^31 - 1, d = 2^20,
+    C = 1 / 2^30); the library must take the same decisions as the oracle's
+    exact integer comparison."""
+    keys = [np.array([9, 7, 5, 3], np.uint64) << np.uint64(52)]
+    colnnz = np.ones(4, np.int32)
+    args = (keys, colnnz, 2**31 - 1, [2**20], 1.0, [1.0], (1, 2**30), (1, 4))
+    k_lib, b_lib = rsc.greedy_allocate(*args)
+    k_orc, b_orc = oracle.greedy(*args)
+    assert k_lib == k_orc == [0] and b_lib == b_orc
