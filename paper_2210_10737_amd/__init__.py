@@ -446,6 +446,8 @@ def greedy_allocate(keys, colnnz, nnz: int, d, fro_a2: float, fro_b2, C, alpha):
     colnnz = np.ascontiguousarray(colnnz, dtype=np.int32)
     d_arr = np.ascontiguousarray(d, dtype=np.int32)
     fb = np.ascontiguousarray(fro_b2, dtype=np.float64)
+    if any(len(k) != n for k in keys) or len(colnnz) != n or len(d_arr) != L or len(fb) != L:
+        raise ValueError("keys and colnnz need n entries each; d and fro_b2 one per layer")
     k_out = np.zeros(L, dtype=np.int32)
     bud = ctypes.c_int64()
     _check(lib().rsc_greedy_allocate(L, n, nnz, ctypes.cast(ptrs, ctypes.c_void_p), colnnz.ctypes.data,
@@ -482,6 +484,10 @@ def greedy_allocate_profiles(masses, counts, n: int, nnz: int, d, fro_a2: float,
     cp = (ctypes.c_void_p * L)(*[c.ctypes.data for c in counts])
     d_arr = np.ascontiguousarray(d, dtype=np.int32)
     fb = np.ascontiguousarray(fro_b2, dtype=np.float64)
+    nb = lib().rsc_greedy_blocks(n, alpha[0], alpha[1])
+    if len(counts) != L or any(len(m) < nb for m in masses) or any(len(c) < nb for c in counts) \
+            or len(d_arr) != L or len(fb) != L:
+        raise ValueError("one mass and count profile of the greedy's block count per layer; d and fro_b2 per layer")
     k_out = np.zeros(L, dtype=np.int32)
     bud = ctypes.c_int64()
     _check(lib().rsc_greedy_allocate_profiles(L, n, nnz, alpha[0], alpha[1], ctypes.cast(mp, ctypes.c_void_p),

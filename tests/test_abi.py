@@ -251,3 +251,13 @@ def test_greedy_budget_comparison_wide_range():
     k_lib, b_lib = rsc.greedy_allocate(*args)
     k_orc, b_orc = oracle.greedy(*args)
     assert k_lib == k_orc == [0] and b_lib == b_orc
+
+
+def test_greedy_binding_rejects_short_arrays():
+    keys = [np.array([9, 7, 5, 3], np.uint64)]
+    with pytest.raises(ValueError):
+        rsc.greedy_allocate(keys, np.ones(3, np.int32), 4, [8], 1.0, [1.0], (1, 2), (1, 4))
+    with pytest.raises(ValueError):
+        rsc.greedy_allocate(keys, np.ones(4, np.int32), 4, [8, 8], 1.0, [1.0], (1, 2), (1, 4))
+    with pytest.raises(ValueError):
+        rsc.greedy_allocate_profiles([np.zeros(1)], [np.zeros(1, np.int64)], 4, 4, [8], 1.0, [1.0], (1, 2), (1, 4))
