@@ -7,8 +7,8 @@
 // number of kept entries before it, and Rowptr'[i] is that count at position
 // Rowptr[i]. So the slice is one stream compaction over the nnz entries:
 //   1. per tile of 4096 entries: the kept flags as 64 wave ballots (reads
-//      col; the mask is an n-bit set that stays in L2), stored for step 3,
-//      and their count;
+//      col; the n-bit mask is tested from LDS, loaded piece by piece), stored
+//      for step 3, and their count;
 //   2. one block scans the tile counts (and stores nnz');
 //   3. per tile: load col/val into registers, scan the tile's ballot counts,
 //      compact the kept entries in LDS and write them out coalesced at their
