@@ -261,3 +261,24 @@ def test_greedy_binding_rejects_short_arrays():
         rsc.greedy_allocate(keys, np.ones(4, np.int32), 4, [8, 8], 1.0, [1.0], (1, 2), (1, 4))
     with pytest.raises(ValueError):
         rsc.greedy_allocate_profiles([np.zeros(1)], [np.zeros(1, np.int64)], 4, 4, [8], 1.0, [1.0], (1, 2), (1, 4))
+
+
+def test_plain_c_consumer(tmp_path):
+    """include/rsc.h compiles as C11 and a C program linked against
+    librsc.so runs its host-only entry points; its greedy result equals the
+    oracle's on the same input."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    exe = tmp_path / "c_abi_consumer"
+    libdir = os.path.dirname(rsc.LIB_PATH)
+    subprocess.run([gcc, "-std=c11", "-Wall", "-Werror", "-Wno-unused-function", "-D__HIP_PLATFORM_AMD__",
+                    "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include",
+                    os.path.join(ROOT, "tests", "c_abi_consumer.c"), "-L", libdir, "-lrsc",
+                    f"-Wl,-rpath,{libdir}", "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()
+    keys = [np.array([9, 7, 5, 3], np.uint64) << np.uint64(52), np.array([8, 6, 4, 2], np.uint64) << np.uint64(52)]
+    k, bud = oracle.greedy(keys, [3, 1, 2, 4], 10, [4, 2], 1.0, [1.0, 1.0], (1, 2), (1, 4))
+    assert [int(out[0]), int(out[1])] == k and int(out[2]) == bud
