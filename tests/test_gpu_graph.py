@@ -54,3 +54,39 @@ def test_graph_replays_match_eager(name, d):
         assert torch.equal(Yb, want_b), f"sampled, replay {r}"
     del g
     cache.close()
+
+
+def test_graph_replays_blocked_mode():
+    """The column-blocked SpMM (forced to 4 ranges) captured and replayed:
+    split, long-piece list, row and combine kernels, all launch-only."""
+    import os
+    old = os.environ.get("RSC_SPMM_BLOCKED")
+    os.environ["RSC_SPMM_BLOCKED"] = "4"
+    try:
+        A = synth.make_graph("tiny", 0)
+        X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, A.n)
+        ws = torch.empty(rsc.spmm_workspace_bytes(X), dtype=torch.uint8, device="cuda")
+        H = torch.from_numpy(synth.dense_normal(A.n, 96, seed=2)).cuda()
+        Y = rsc.spmm(X, H, ws=ws)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            rsc.spmm(X, H, out=Y, ws=ws)
+        torch.cuda.current_stream().wait_stream(s)
+        with torch.cuda.graph(g):
+            rsc.spmm(X, H, out=Y, ws=ws)
+        for r in range(3):
+            H.copy_(torch.from_numpy(synth.dense_normal(A.n, 96, seed=20 + r)).cuda())
+            g.replay()
+            torch.cuda.synchronize()
+            want = rsc.spmm(X, H)
+            torch.cuda.synchronize()
+            assert torch.equal(Y, want), f"replay {r}"
+        del g
+    finally:
+        if old is None:
+            del os.environ["RSC_SPMM_BLOCKED"]
+        else:
+            os.environ["RSC_SPMM_BLOCKED"] = old
