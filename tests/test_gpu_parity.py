@@ -8,6 +8,8 @@ S = sum |a||b| in fp64) must be <= 1e-5 for exact and <= 1e-4 for sampled
 SpMM. The kernel accumulates fp32 over runs of <= 64 entries and folds them
 in fp64, so its error is about 64 * 2^-24 * S ~ 4e-6 S in the worst case.
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -219,6 +221,39 @@ def test_spmm_empty():
     A = synth.Csr(5, np.zeros(6, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
     Y = rsc.spmm(to_dev(A, 3), dense_dev(np.ones((3, 8), np.float32))).cpu().numpy()
     assert np.all(Y == 0)
+
+
+def test_degenerate_shapes():
+    """No rows; no columns (every row empty, B without rows), also in the
+    column-blocked mode; one entry in one column through the cache at k = 0
+    and k = 1."""
+    A0 = synth.Csr(0, np.zeros(1, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
+    assert rsc.spmm(to_dev(A0, 5), dense_dev(np.ones((5, 8), np.float32))).shape == (0, 8)
+    A1 = synth.Csr(4, np.zeros(5, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
+    B0 = torch.empty((0, 8), dtype=torch.float32, device="cuda")
+    for blocks in (None, "3"):
+        old = os.environ.get("RSC_SPMM_BLOCKED")
+        if blocks:
+            os.environ["RSC_SPMM_BLOCKED"] = blocks
+        try:
+            Y = torch.full((4, 8), 7.0, device="cuda")
+            rsc.spmm(to_dev(A1, 0), B0, out=Y)
+            assert not Y.any()
+        finally:
+            if old is None:
+                os.environ.pop("RSC_SPMM_BLOCKED", None)
+            else:
+                os.environ["RSC_SPMM_BLOCKED"] = old
+    A2 = synth.Csr(1, np.array([0, 1], np.int32), np.array([0], np.int32), np.array([0.5], np.float32))
+    X = to_dev(A2, 1)
+    B = dense_dev(np.full((1, 4), 3.0, np.float32))
+    cache = rsc.Cache(X, X)
+    cache.refresh(B, 0, step=0)
+    assert not cache.spmm_sampled(B).any()
+    cache.refresh(B, 1, step=1)
+    assert torch.equal(cache.spmm_sampled(B), rsc.spmm(X, B))
+    assert torch.equal(rsc.spmm(X, B), torch.full((1, 4), 1.5, device="cuda"))
+    cache.close()
 
 
 # ------------------------------------------------------------------ scores
