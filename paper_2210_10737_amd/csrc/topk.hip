@@ -13,6 +13,8 @@
 //    than r equal keys precede it, writing mask words from wave ballots and
 //    idx at the running count of kept keys. Everything is integer, so the
 //    result is exact and deterministic.
+// Up to 16,384 keys the whole selection runs in one block with the keys in
+// LDS (one launch; the small graphs are launch-bound).
 #include "rsc_internal.h"
 
 namespace rsc {
@@ -226,6 +228,89 @@ __global__ __launch_bounds__(256) void topk_emit_kernel(const uint64_t *__restri
     }
 }
 
+// Small inputs (n <= kSmallN) in one block of 1024 threads, the keys held in
+// LDS: the same six radix passes (LDS histogram, a block scan picks the
+// digit), then thread t takes keys [16 t, 16 t + 16): block scans of its
+// (== T) count and of its kept count give the ranks, idx is written at the
+// running kept count and each 16-bit piece of the mask is paired with its
+// neighbour's into a word. One launch instead of fifteen; same result.
+constexpr int kSmallN = 16384;
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallPer = kSmallN / kSmallThreads;  // 16 keys per thread in the emit
+static_assert(kSmallPer == 16, "two threads' 16-bit pieces make one mask word");
+
+__global__ __launch_bounds__(kSmallThreads) void topk_small_kernel(const uint64_t *__restrict__ key, int32_t n,
+                                                                   int32_t k, int32_t *__restrict__ idx,
+                                                                   uint32_t *__restrict__ mask) {
+    __shared__ uint64_t s_key[kSmallN];
+    __shared__ uint32_t s_hist[kBins];
+    __shared__ int64_t s_scan[kSmallThreads];
+    __shared__ uint64_t s_prefix, s_pmask;
+    __shared__ int64_t s_krem;
+    const int t = threadIdx.x;
+    for (int i = t; i < n; i += kSmallThreads) s_key[i] = key[i];
+    uint64_t prefix = 0, pmask = 0;
+    int64_t k_rem = k;
+    for (int pass = 0; pass < kPasses; ++pass) {
+        const int shift = kShift[pass];
+        const int nb = 1 << kWidth[pass];
+        const uint64_t dmask = (uint64_t)(nb - 1);
+        for (int b = t; b < kBins; b += kSmallThreads) s_hist[b] = 0;
+        __syncthreads();  // keys loaded (first pass), histogram cleared
+        for (int i = t; i < n; i += kSmallThreads) {
+            const uint64_t kv = s_key[i];
+            if ((kv & pmask) == prefix) atomicAdd(&s_hist[(kv >> shift) & dmask], 1u);
+        }
+        __syncthreads();
+        // thread t owns bins nb-1-(t*per+j), descending; the exclusive scan
+        // gives the keys in all higher bins
+        const int per = nb / kSmallThreads;  // 2 or 1
+        int64_t sum = 0;
+        for (int j = 0; j < per; ++j) sum += s_hist[nb - 1 - (t * per + j)];
+        int64_t total;
+        int64_t run = block_exclusive_scan_1024(sum, s_scan, &total);
+        for (int j = 0; j < per; ++j) {
+            const int b = nb - 1 - (t * per + j);
+            const int64_t c = s_hist[b];
+            if (run < k_rem && run + c >= k_rem) {  // exactly one (thread, bin)
+                s_prefix = prefix | ((uint64_t)b << shift);
+                s_pmask = pmask | (dmask << shift);
+                s_krem = k_rem - run;
+            }
+            run += c;
+        }
+        __syncthreads();
+        prefix = s_prefix;
+        pmask = s_pmask;
+        k_rem = s_krem;
+        __syncthreads();  // every thread has read the state before the next pass writes it
+    }
+    const uint64_t T = prefix;
+    const int64_t r = k_rem;  // keys equal to T that are kept (the lowest indices)
+    const int lo = min(n, t * kSmallPer), hi = min(n, lo + kSmallPer);
+    int64_t eq = 0;
+    for (int i = lo; i < hi; ++i) eq += s_key[i] == T;
+    int64_t total;
+    int64_t eq_before = block_exclusive_scan_1024(eq, s_scan, &total);
+    uint32_t bits = 0;
+    int64_t kept = 0;
+    for (int i = lo; i < hi; ++i) {
+        const uint64_t kv = s_key[i];
+        bool sel = kv > T;
+        if (kv == T) sel = eq_before++ < r;
+        if (sel) {
+            bits |= 1u << (i - lo);
+            ++kept;
+        }
+    }
+    int64_t pos = block_exclusive_scan_1024(kept, s_scan, &total);
+    for (int i = lo; i < hi; ++i)
+        if ((bits >> (i - lo)) & 1u) idx[pos++] = i;
+    const uint32_t hi16 = __shfl_down(bits, 1);  // the odd neighbour's piece
+    const int64_t word = t / 2;
+    if ((t & 1) == 0 && word < ((int64_t)n + 31) / 32) mask[word] = bits | (hi16 << 16);
+}
+
 __global__ __launch_bounds__(256) void fill_u32_kernel(uint32_t *p, int64_t count, uint32_t v) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
          i += (int64_t)gridDim.x * blockDim.x)
@@ -246,6 +331,10 @@ hipError_t topk_launch(const uint64_t *key, int32_t n, int32_t k, int32_t *idx, 
     if (k == 0) {
         fill_u32_kernel<<<(unsigned)std::min<int64_t>(ceil_div(nwords, 256), 1024), 256, 0, stream>>>(
             mask, nwords, 0u);
+        return hipGetLastError();
+    }
+    if (n <= kSmallN) {
+        topk_small_kernel<<<1, kSmallThreads, 0, stream>>>(key, n, k, idx, mask);
         return hipGetLastError();
     }
     TopkWs *h = static_cast<TopkWs *>(ws);

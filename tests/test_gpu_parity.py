@@ -319,6 +319,18 @@ def test_topk_ties_nan_inf():
     _topk_case(top, 4)
 
 
+@pytest.mark.parametrize("n", [16383, 16384, 16385])
+def test_topk_single_block_boundary(n):
+    """Both sides of the one-block path's size limit (16,384 keys), with
+    heavy ties, NaN keys and the maximum key."""
+    rng = np.random.default_rng(n)
+    key = rng.integers(0, 5, size=n).astype(np.uint64) * np.uint64(1 << 60)
+    key[::97] = np.uint64(0xFFFFFFFFFFFFFFFF)
+    for k in (1, 170, n // 2, n - 1, n):
+        _topk_case(key, k)
+    _topk_case(np.arange(1, n + 1).astype(np.uint64), 777)
+
+
 def test_topk_on_real_keys():
     A = synth.make_graph("tiny", 0)
     cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)
