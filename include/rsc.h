@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define RSC_ABI_VERSION 4
+#define RSC_ABI_VERSION 5
 
 typedef enum {
     RSC_OK = 0,
@@ -114,6 +114,31 @@ rsc_status_t rsc_csr_validate(const rsc_csr_t *A, int64_t *bad_row_host, hipStre
 size_t rsc_spmm_workspace_bytes(const rsc_csr_t *A);
 rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb, float *Y,
                       int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Plan for repeated exact products with one sparse operand (a training
+ * run's static A_hat). Same product, same kernels, same summation order as
+ * rsc_spmm: rsc_spmm_plan_run gives Y bitwise equal to rsc_spmm on the same
+ * arguments. What the plan adds is per-matrix preparation, done once:
+ *   - its own workspace, so runs need none;
+ *   - for operands with more than 262,144 columns, a copy of col whose bit
+ *     31 marks the "hub" columns, the columns of highest entry count that
+ *     together hold just under half of the entries (entry-weighted median of
+ *     the column counts, on a scale of 8 steps per octave). When one feature
+ *     pass gathers from more than 512 MiB of B rows (far beyond the on-chip
+ *     caches), the other columns' rows are gathered non-temporally, so the
+ *     hubs' rows stay in L2. This changes cache allocation only, never a
+ *     value; RSC_SPMM_HINT=0 switches the policy off.
+ * rsc_spmm_plan_create [sync] borrows A's arrays (they must outlive the plan
+ * and not change) and allocates 4 nnz bytes for the copy plus the
+ * workspace; RSC_ERR_OUT_OF_MEMORY if that fails. Runs of one plan share its
+ * workspace, so they must be ordered on the device. (The sampled products
+ * of rsc_cache_* do not take the hint: on the cached slices it measured
+ * slower.) */
+typedef struct rsc_spmm_plan rsc_spmm_plan_t;
+rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_spmm_plan_t **out);
+rsc_status_t rsc_spmm_plan_run(rsc_spmm_plan_t *plan, const float *B, int32_t d, int64_t ldb, float *Y,
+                               int64_t ldy, hipStream_t stream);
+rsc_status_t rsc_spmm_plan_destroy(rsc_spmm_plan_t *plan);
 
 /* MEAN aggregator operand (appendix A.3: SpMM_MEAN(A, H) = D^-1 A H, D the
  * degree matrix of A, D_ii = stored entries of row i). Writes A's values

@@ -40,6 +40,7 @@ STATUS = {0: "RSC_OK", 1: "RSC_ERR_INVALID_ARGUMENT", 2: "RSC_ERR_UNSUPPORTED",
 EXPORTED = [
     "rsc_status_string", "rsc_last_error", "rsc_abi_version", "rsc_csr_validate",
     "rsc_spmm_workspace_bytes", "rsc_spmm", "rsc_degree_scale",
+    "rsc_spmm_plan_create", "rsc_spmm_plan_run", "rsc_spmm_plan_destroy",
     "rsc_col_sqnorms", "rsc_pair_scores",
     "rsc_topk_workspace_bytes", "rsc_topk_select",
     "rsc_slice_workspace_bytes", "rsc_slice_csr",
@@ -109,6 +110,9 @@ def lib():
             "rsc_abi_version": ([], i32),
             "rsc_spmm_workspace_bytes": ([csrp], sz),
             "rsc_spmm": ([csrp, vp, i32, i64, vp, i64, vp, sz, vp], ctypes.c_int),
+            "rsc_spmm_plan_create": ([csrp, vp, ctypes.POINTER(vp)], ctypes.c_int),
+            "rsc_spmm_plan_run": ([vp, vp, i32, i64, vp, i64, vp], ctypes.c_int),
+            "rsc_spmm_plan_destroy": ([vp], ctypes.c_int),
             "rsc_col_sqnorms": ([csrp, vp, vp, vp], ctypes.c_int),
             "rsc_degree_scale": ([csrp, vp, i32, vp, vp], ctypes.c_int),
             "rsc_pair_scores": ([vp, vp, i32, i32, i64, vp, vp, vp, vp], ctypes.c_int),
@@ -229,6 +233,36 @@ def spmm(A: DeviceCsr, B: torch.Tensor, d: int | None = None, out: torch.Tensor 
     _check(lib().rsc_spmm(ctypes.byref(s), B.data_ptr(), d, _ld(B), Y.data_ptr(), _ld(Y),
                           ws.data_ptr(), ws.numel(), _stream()))
     return Y
+
+
+class SpmmPlan:
+    """Repeated exact products with one sparse operand (rsc_spmm_plan_*):
+    the same result as spmm(A, B) bit for bit, with the plan's own workspace
+    and, on large operands, the column cache hint. A's tensors must outlive
+    the plan."""
+
+    def __init__(self, A: DeviceCsr):
+        self.A = A
+        h = ctypes.c_void_p()
+        _check(lib().rsc_spmm_plan_create(ctypes.byref(A.struct()), _stream(), ctypes.byref(h)))
+        self._h = h
+
+    def run(self, B: torch.Tensor, d: int | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
+        d = B.shape[1] if d is None else d
+        Y = _new_out(self.A.n_rows, d, B.device) if out is None else out
+        _check(lib().rsc_spmm_plan_run(self._h, B.data_ptr(), d, _ld(B), Y.data_ptr(), _ld(Y), _stream()))
+        return Y
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            _check(lib().rsc_spmm_plan_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def degree_scale(A: DeviceCsr, by_column: bool = False, deg_rowptr: torch.Tensor | None = None) -> DeviceCsr:

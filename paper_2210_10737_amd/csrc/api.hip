@@ -118,6 +118,11 @@ rsc_status_t validate(const rsc_csr_t *A, const char *name, int64_t *bad_row, hi
     return RSC_OK;
 }
 
+// Whether a product with this many B rows can ever take the column cache hint
+// (the SpMM uses it when one feature pass gathers from more than 512 MiB of
+// B rows, and a pass is at most 512 floats wide).
+bool hint_worthwhile(int32_t n_src) { return (double)n_src * 512 * sizeof(float) > 512.0 * 1024 * 1024; }
+
 // with RSC_VALIDATE=1, the device check of a caller's CSR before any launch
 rsc_status_t maybe_validate(const rsc_csr_t *A, const char *name, hipStream_t stream) {
     return validate_env() ? validate(A, name, nullptr, stream) : RSC_OK;
@@ -203,6 +208,77 @@ rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb
     RSC_HIP(rsc::spmm_launch(A->n_rows, A->n_cols, A->nnz, A->rowptr, A->col, A->val, B, d, ldb, Y, ldy, ws,
                              ws_bytes, stream, A->nnz, A->n_cols),
             "spmm launch");
+    return RSC_OK;
+}
+
+struct rsc_spmm_plan {
+    rsc_csr_t A{};
+    int32_t *colf = nullptr;  // A's columns with the hub hint in bit 31 (large graphs only)
+    void *ws = nullptr;
+    size_t ws_bytes = 0;
+};
+
+static void plan_free(rsc_spmm_plan_t *p) {
+    if (!p) return;
+    if (p->colf) (void)hipFree(p->colf);
+    if (p->ws) (void)hipFree(p->ws);
+    delete p;
+}
+
+rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_spmm_plan_t **out) {
+    if (!out) return fail(RSC_ERR_INVALID_ARGUMENT, "out is NULL");
+    *out = nullptr;
+    RSC_TRY(check_csr(A, "A"));
+    RSC_TRY(check_device());
+    RSC_TRY(maybe_validate(A, "A", stream));
+    rsc_spmm_plan_t *p = new rsc_spmm_plan_t();
+    p->A = *A;
+    p->ws_bytes = std::max<size_t>(rsc::spmm_ws_bytes(A->n_rows, A->nnz, A->n_cols), 256);
+    if (hipMalloc(&p->ws, p->ws_bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        plan_free(p);
+        return fail(RSC_ERR_OUT_OF_MEMORY, "plan workspace of %zu bytes", p->ws_bytes);
+    }
+    if (hint_worthwhile(A->n_cols) && A->nnz > 0) {
+        int32_t *deg = nullptr;
+        void *ws_hub = nullptr;
+        hipError_t e = hipMalloc((void **)&p->colf, sizeof(int32_t) * (size_t)A->nnz);
+        if (e == hipSuccess) e = hipMalloc((void **)&deg, sizeof(int32_t) * (size_t)A->n_cols);
+        if (e == hipSuccess) e = hipMalloc(&ws_hub, rsc::hub_ws_bytes(A->n_cols));
+        if (e == hipSuccess) e = rsc::degree_count_launch(A->col, A->nnz, A->n_cols, deg, stream);
+        if (e == hipSuccess) e = rsc::hub_bits_launch(deg, nullptr, A->n_cols, ws_hub, stream);
+        if (e == hipSuccess) e = rsc::flag_cols_launch(A->col, A->nnz, rsc::hub_bits_of(ws_hub), p->colf, stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        if (deg) (void)hipFree(deg);
+        if (ws_hub) (void)hipFree(ws_hub);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            plan_free(p);
+            return e == hipErrorOutOfMemory ? fail(RSC_ERR_OUT_OF_MEMORY, "plan allocation failed")
+                                            : hip_fail(e, "plan create");
+        }
+    }
+    *out = p;
+    return RSC_OK;
+}
+
+rsc_status_t rsc_spmm_plan_run(rsc_spmm_plan_t *p, const float *B, int32_t d, int64_t ldb, float *Y, int64_t ldy,
+                               hipStream_t stream) {
+    if (!p) return fail(RSC_ERR_INVALID_ARGUMENT, "plan is NULL");
+    const rsc_csr_t *A = &p->A;
+    RSC_TRY(check_dense(B, A->n_cols, d, ldb, "B"));
+    RSC_TRY(check_dense(Y, A->n_rows, d, ldy, "Y"));
+    RSC_HIP(rsc::spmm_launch(A->n_rows, A->n_cols, A->nnz, A->rowptr, p->colf ? p->colf : A->col, A->val, B, d,
+                             ldb, Y, ldy, p->ws, p->ws_bytes, stream, A->nnz, A->n_cols, p->colf != nullptr),
+            "plan run");
+    return RSC_OK;
+}
+
+rsc_status_t rsc_spmm_plan_destroy(rsc_spmm_plan_t *p) {
+    if (!p) return RSC_OK;
+    hipError_t e = hipDeviceSynchronize();
+    plan_free(p);
+    if (e != hipSuccess) return hip_fail(e, "plan destroy");
     return RSC_OK;
 }
 

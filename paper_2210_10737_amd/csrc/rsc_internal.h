@@ -16,11 +16,13 @@ size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz, int32_t n_cols);
 // nnz_bound sizes the long-row list; nnz_hint (expected entries) and
 // n_src_hint (distinct B rows the entries reference) choose the feature slice
 // and the column-blocked mode, which runs only if ws_bytes holds its buffers.
+// hint_cols: col carries the hub hint in bit 31 (a plan's own copy only);
+// kernels always mask that bit off.
 int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d);
 hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const int32_t *rowptr,
                        const int32_t *col, const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
                        int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream, int64_t nnz_hint,
-                       int64_t n_src_hint);
+                       int64_t n_src_hint, bool hint_cols = false);
 
 // ---- scores ------------------------------------------------------------
 hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,
@@ -39,6 +41,19 @@ hipError_t slice_launch(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
                         const float *val, const uint32_t *mask, int32_t *rowptr_out,
                         int32_t *col_out, float *val_out, int64_t capacity, int64_t *nnz_out,
                         void *ws, hipStream_t stream, const double *colw = nullptr);
+
+// ---- column hub hint for the SpMM gathers --------------------------------
+// hub_bits_launch: from per-column degrees (optionally only the columns kept
+// by mask), the entry-weighted median split; writes the n-bit hub set into
+// the workspace (hub_bits_of). flag_cols_launch: col with bit 31 = hub bit.
+// Used by SpMM plans; the sampled products do not take the hint (measured
+// slower on the cached slices).
+size_t hub_ws_bytes(int32_t n);
+uint32_t *hub_bits_of(void *ws);
+hipError_t hub_bits_launch(const int32_t *deg, const uint32_t *mask, int32_t n, void *ws, hipStream_t stream);
+hipError_t degree_count_launch(const int32_t *col, int64_t nnz, int32_t n_cols, int32_t *deg, hipStream_t stream);
+hipError_t flag_cols_launch(const int32_t *col, int64_t nnz, const uint32_t *bits, int32_t *colf,
+                            hipStream_t stream);
 
 // ---- randomized column-row sampling ------------------------------------
 size_t sample_ws_bytes(int32_t n);

@@ -44,12 +44,18 @@ namespace {
 
 constexpr int kUnroll = 8;
 typedef float vf4 __attribute__((ext_vector_type(4)));
+constexpr int32_t kColMask = 0x7FFFFFFF;  // bit 31 of a column index: cache hint
+
+__device__ __forceinline__ float4 load_nt(const float4 *p) {
+    const vf4 x = __builtin_nontemporal_load(reinterpret_cast<const vf4 *>(p));
+    return make_float4(x.x, x.y, x.z, x.w);
+}
 
 __global__ void zero_counters_kernel(int32_t *p) { p[0] = 0; p[1] = 0; }
 __global__ void zero_next_kernel(int32_t *p) { *p = 0; }
 
 // Appends every row longer than kLongRow to `list`; row r spans
-// [ptr[r], ptr[r + off]) (off = 1 for a CSR row pointer). Each thread checks
+// [ptr[r], ptr[r + end_off]) (end_off = 1 for a CSR row pointer). Each thread checks
 // kCollectPerThread rows (coalesced reads); a block-wide scan gives each long
 // row its place, and one atomic per block reserves the block's range, so the
 // list costs a few hundred atomics rather than one per row. The list order
@@ -58,7 +64,7 @@ constexpr int kCollectThreads = 1024;
 constexpr int kCollectPerThread = 4;
 
 __global__ __launch_bounds__(kCollectThreads) void collect_long_rows_kernel(
-    const int32_t *__restrict__ ptr, int64_t off, int32_t n_rows, int32_t *count, int32_t *list) {
+    const int32_t *__restrict__ ptr, int64_t end_off, int32_t n_rows, int32_t *count, int32_t *list) {
     __shared__ int32_t s_wave[kCollectThreads / 64];
     __shared__ int32_t s_base;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -68,7 +74,7 @@ __global__ __launch_bounds__(kCollectThreads) void collect_long_rows_kernel(
 #pragma unroll
     for (int i = 0; i < kCollectPerThread; ++i) {
         const int64_t r = base + t + (int64_t)kCollectThreads * i;
-        is_long[i] = r < n_rows && ptr[r + off] - ptr[r] > kLongRow;
+        is_long[i] = r < n_rows && ptr[r + end_off] - ptr[r] > kLongRow;
         mine += is_long[i];
     }
     // exclusive scan of `mine` over the block: within the wave, then across waves
@@ -108,7 +114,11 @@ struct Layout {
 // Within a run, entry-group g takes entries g, g + G, g + 2G, ...; the group
 // partials are combined by a butterfly over the groups (fixed order, every
 // lane ends with the same sum) before the run is folded into fp64.
-template <int LPE, int NV>
+// Bit 31 of a column index is a cache hint (set by a plan or a cache on
+// their own copies; a caller's indices are < 2^31): with kHint, gathers of
+// columns without it bypass cache allocation (non-temporal), so the rows of
+// the columns that carry half the entries stay in L2. Values are unchanged.
+template <int LPE, int NV, bool kHint>
 __device__ __forceinline__ void accumulate_runs(const int32_t *__restrict__ col,
                                                 const float *__restrict__ val,
                                                 const float *__restrict__ B, int64_t ldb,
@@ -140,12 +150,19 @@ __device__ __forceinline__ void accumulate_runs(const int32_t *__restrict__ col,
                     for (int q = 0; q < NV; ++q) b[u][q] = make_float4(0.f, 0.f, 0.f, 0.f);
                     v[u] = 0.f;
                     if (t + u < cnt) {  // wave-uniform
-                        const int32_t c = __builtin_amdgcn_readlane(my_c, t + u);
+                        const int32_t cf = __builtin_amdgcn_readlane(my_c, t + u);
+                        const int32_t c = cf & kColMask;
                         v[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_v), t + u));
                         const float4 *brow = reinterpret_cast<const float4 *>(B + (int64_t)c * ldb) + lane;
+                        if (kHint && cf >= 0) {  // not a hub column: stream it past the caches
 #pragma unroll
-                        for (int q = 0; q < NV; ++q)
-                            if (act[q]) b[u][q] = brow[q * kWave];
+                            for (int q = 0; q < NV; ++q)
+                                if (act[q]) b[u][q] = load_nt(brow + q * kWave);
+                        } else {
+#pragma unroll
+                            for (int q = 0; q < NV; ++q)
+                                if (act[q]) b[u][q] = brow[q * kWave];
+                        }
                     }
                 }
 #pragma unroll
@@ -169,12 +186,14 @@ __device__ __forceinline__ void accumulate_runs(const int32_t *__restrict__ col,
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u) {
                     const int j = (t0 + u) * G + g;  // entry of this group within the run
-                    const int32_t c = __shfl(my_c, j & (kWave - 1));
+                    const int32_t cf = __shfl(my_c, j & (kWave - 1));
+                    const int32_t c = cf & kColMask;
                     const float vv = __shfl(my_v, j & (kWave - 1));
                     b[u] = make_float4(0.f, 0.f, 0.f, 0.f);
                     v[u] = 0.f;
                     if (t0 + u < kSteps && j < cnt && act[0]) {
-                        b[u] = reinterpret_cast<const float4 *>(B + (int64_t)c * ldb)[sl];
+                        const float4 *brow = reinterpret_cast<const float4 *>(B + (int64_t)c * ldb) + sl;
+                        b[u] = (kHint && cf >= 0) ? load_nt(brow) : *brow;
                         v[u] = vv;
                     }
                 }
@@ -219,7 +238,7 @@ __device__ __forceinline__ void store_row(float *__restrict__ yrow, int32_t d, i
 // 64 entries and their fp64 sums are added in LDS in fixed wave order.
 // Row r spans [ptr[r], ptr[r + off]) and is written to row r of Y.
 // B and Y point at the first feature of the current slice; d is its width.
-template <int LPE, int NV>
+template <int LPE, int NV, bool kHint>
 __global__ __launch_bounds__(kSpmmLongWaves * 64) void spmm_long_kernel(
     const int32_t *__restrict__ ptr, int64_t off, const int32_t *__restrict__ col, const float *__restrict__ val,
     const float *__restrict__ B, int64_t ldb, float *__restrict__ Y, int64_t ldy, int32_t d,
@@ -245,7 +264,7 @@ __global__ __launch_bounds__(kSpmmLongWaves * 64) void spmm_long_kernel(
         double acc[NV][4];
 #pragma unroll
         for (int q = 0; q < NV; ++q) acc[q][0] = acc[q][1] = acc[q][2] = acc[q][3] = 0.0;
-        accumulate_runs<LPE, NV>(col, val, B, ldb, (int64_t)s + kWave * wave, e, kWave * kSpmmLongWaves, act,
+        accumulate_runs<LPE, NV, kHint>(col, val, B, ldb, (int64_t)s + kWave * wave, e, kWave * kSpmmLongWaves, act,
                                  lane, acc);
 #pragma unroll
         for (int q = 0; q < NV; ++q)
@@ -273,7 +292,7 @@ __global__ __launch_bounds__(kSpmmLongWaves * 64) void spmm_long_kernel(
 // long rows): a processing order only, each row's sum is unchanged. Row r
 // spans [ptr[r], ptr[r + off]); kCsr says off == 1 (a CSR row pointer, both
 // bounds then come from one 8-byte scalar load).
-template <int LPE, int NV, bool kCsr>
+template <int LPE, int NV, bool kCsr, bool kHint>
 __global__ __launch_bounds__(kSpmmRowWaves * 64) void spmm_rows_kernel(
     const int32_t *__restrict__ ptr, int64_t off, const int32_t *__restrict__ col, const float *__restrict__ val,
     const float *__restrict__ B, int64_t ldb, float *__restrict__ Y, int64_t ldy, int32_t n_rows,
@@ -298,7 +317,7 @@ __global__ __launch_bounds__(kSpmmRowWaves * 64) void spmm_rows_kernel(
     double acc[NV][4];
 #pragma unroll
     for (int q = 0; q < NV; ++q) acc[q][0] = acc[q][1] = acc[q][2] = acc[q][3] = 0.0;
-    accumulate_runs<LPE, NV>(col, val, B, ldb, s, e, kWave, act, lane, acc);
+    accumulate_runs<LPE, NV, kHint>(col, val, B, ldb, s, e, kWave, act, lane, acc);
     store_row<LPE, NV>(Y + (int64_t)r * ldy, d, lane, acc);
 }
 
@@ -388,6 +407,15 @@ __global__ __launch_bounds__(kCollectThreads) void class_scatter_kernel(const in
 // Rows are taken longest class first when rows are long on average: the
 // heavy rows then start first and the kernels end on short rows. Results do
 // not depend on it. RSC_SPMM_ORDER=0/1 overrides.
+// Gathered rows beyond this many bytes per feature pass take the column
+// cache hint (twice the 256 MB MALL).
+constexpr double kHintBytes = 512.0 * 1024 * 1024;
+
+inline bool use_hint() {
+    if (const char *env = getenv("RSC_SPMM_HINT")) return atoi(env) != 0;
+    return true;
+}
+
 inline bool use_order(int32_t n_rows, int64_t nnz) {
     if (const char *env = getenv("RSC_SPMM_ORDER")) return atoi(env) != 0;
     return n_rows > 0 && nnz >= 128LL * n_rows;
@@ -447,7 +475,7 @@ __global__ __launch_bounds__(256) void split_rows_kernel(const int32_t *__restri
         int32_t lo = s, hi = e;
         while (lo < hi) {
             const int32_t mid = lo + (hi - lo) / 2;
-            if (col[mid] < bound) lo = mid + 1; else hi = mid;
+            if ((col[mid] & kColMask) < bound) lo = mid + 1; else hi = mid;
         }
         pos = lo;
     }
@@ -532,7 +560,7 @@ int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) 
 hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const int32_t *rowptr,
                        const int32_t *col, const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
                        int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream, int64_t nnz_hint,
-                       int64_t n_src_hint) {
+                       int64_t n_src_hint, bool hint_cols) {
     if (n_rows == 0) return hipSuccess;
     SpmmWs *h = static_cast<SpmmWs *>(ws);
     int32_t *list = reinterpret_cast<int32_t *>(h + 1);  // long-row list, or the whole processing order
@@ -561,10 +589,10 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
             const int32_t dl = std::min<int32_t>(d - f0, kBlockW);
             if (n_long > 0) {
                 if (f0 > 0) zero_next_kernel<<<1, 1, 0, stream>>>(&h->long_next);
-                spmm_long_kernel<16, 1><<<n_long, kSpmmLongWaves * 64, 0, stream>>>(
+                spmm_long_kernel<16, 1, false><<<n_long, kSpmmLongWaves * 64, 0, stream>>>(
                     S, n_rows, col, val, B + f0, ldb, part, kBlockW, dl, &h->long_count, &h->long_next, list);
             }
-            spmm_rows_kernel<16, 1, false><<<vgrid, kSpmmRowWaves * 64, 0, stream>>>(
+            spmm_rows_kernel<16, 1, false, false><<<vgrid, kSpmmRowWaves * 64, 0, stream>>>(
                 S, n_rows, col, val, B + f0, ldb, part, kBlockW, nv, dl, n_long > 0 ? 1 : 0, nullptr,
                 &h->long_count);
             const int64_t nc = (int64_t)n_rows * ((dl + 3) / 4);
@@ -589,18 +617,29 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
     const int32_t *order = ordered ? list : nullptr;
     const unsigned grid = (unsigned)ceil_div(n_rows, kSpmmRowWaves);
     const int32_t slice = spmm_slice_width(n_rows, nnz_hint, n_src_hint, d);
+    // the hint pays off only when the gathered rows far outgrow the on-chip
+    // caches (MALL included); below that, bypassing them loses reuse
+    const bool hint = hint_cols && use_hint() &&
+                      (double)n_src_hint * std::min(d, slice) * sizeof(float) > kHintBytes;
     for (int32_t f0 = 0; f0 < d;) {
         const int32_t dl = std::min<int32_t>(d - f0, slice);
-#define RSC_SPMM_LAUNCH(LPE_, NV_)                                                                     \
+#define RSC_SPMM_LAUNCH_H(LPE_, NV_, H_)                                                               \
     do {                                                                                               \
         if (n_long_blocks > 0) {                                                                       \
             if (f0 > 0) zero_next_kernel<<<1, 1, 0, stream>>>(&h->long_next);                          \
-            spmm_long_kernel<LPE_, NV_><<<n_long_blocks, kSpmmLongWaves * 64, 0, stream>>>(             \
+            spmm_long_kernel<LPE_, NV_, H_><<<n_long_blocks, kSpmmLongWaves * 64, 0, stream>>>(         \
                 rowptr, 1, col, val, B + f0, ldb, Y + f0, ldy, dl, &h->long_count, &h->long_next, list);  \
         }                                                                                              \
-        spmm_rows_kernel<LPE_, NV_, true><<<grid, kSpmmRowWaves * 64, 0, stream>>>(                    \
+        spmm_rows_kernel<LPE_, NV_, true, H_><<<grid, kSpmmRowWaves * 64, 0, stream>>>(                \
             rowptr, 1, col, val, B + f0, ldb, Y + f0, ldy, n_rows, dl, n_long_blocks > 0 ? 1 : 0, order,  \
             &h->long_count);                                                                           \
+    } while (0)
+#define RSC_SPMM_LAUNCH(LPE_, NV_)                   \
+    do {                                             \
+        if (hint)                                    \
+            RSC_SPMM_LAUNCH_H(LPE_, NV_, true);      \
+        else                                         \
+            RSC_SPMM_LAUNCH_H(LPE_, NV_, false);     \
     } while (0)
         switch (slice) {
             case 16: RSC_SPMM_LAUNCH(4, 1); break;
@@ -611,6 +650,7 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
                 if (dl <= 4 * kWave) RSC_SPMM_LAUNCH(64, 1); else RSC_SPMM_LAUNCH(64, 2);
         }
 #undef RSC_SPMM_LAUNCH
+#undef RSC_SPMM_LAUNCH_H
         f0 += dl;
     }
     return hipGetLastError();

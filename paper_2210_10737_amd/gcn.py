@@ -31,8 +31,7 @@ from dataclasses import dataclass, field
 import numpy as np
 import torch
 
-from . import (Cache, DeviceCsr, _check, _stream, copy_to_host, greedy_allocate_profiles, lib, spmm,
-               spmm_workspace_bytes)
+from . import Cache, DeviceCsr, SpmmPlan, _check, _stream, copy_to_host, greedy_allocate_profiles, lib
 
 
 class _Aggregate(torch.autograd.Function):
@@ -40,7 +39,7 @@ class _Aggregate(torch.autograd.Function):
     def forward(ctx, J: torch.Tensor, layer: "AggregationLayer") -> torch.Tensor:
         ctx.layer = layer
         t = layer._tick()
-        P = spmm(layer.A, J.contiguous(), ws=layer.ws)
+        P = layer.plan.run(J.contiguous())
         layer._tock(t, "forward")
         return P
 
@@ -56,7 +55,7 @@ class _Aggregate(torch.autograd.Function):
         elif layer.mode == "sampled":
             grad_J = layer.cache.spmm_sampled(g)
         else:
-            grad_J = spmm(layer.AT, g, ws=layer.ws)
+            grad_J = layer.plan_t.run(g)
         layer._tock(t, "backward")
         if layer.mode == "score":
             layer.cache.score(g)
@@ -74,8 +73,9 @@ class AggregationLayer:
         # the backward multiplies by A_hat^T: its columns are scored and sliced;
         # the CSR of its transpose (A_hat) gives the column norms
         self.cache = Cache(self.AT, self.A, refresh_interval=refresh_interval)
-        self.ws = torch.empty(max(spmm_workspace_bytes(A), spmm_workspace_bytes(self.AT)),
-                              dtype=torch.uint8, device=A.rowptr.device)
+        # exact products with the static operands go through plans (prepared once)
+        self.plan = SpmmPlan(A)
+        self.plan_t = self.plan if self.AT is A else SpmmPlan(self.AT)
         self.mode = "exact"
         self.k = A.n_cols       # columns kept by the approximation (set by the allocation)
         self.step = 0
@@ -223,6 +223,8 @@ class RscController:
     def close(self):
         for layer in self.layers:
             layer.cache.close()
+            layer.plan.close()
+            layer.plan_t.close()
 
 
 class GCN(torch.nn.Module):

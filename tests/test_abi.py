@@ -34,7 +34,7 @@ def test_header_matches_exports():
     L = rsc.lib()
     for name in declared:
         assert getattr(L, name) is not None
-    assert L.rsc_abi_version() == 4
+    assert L.rsc_abi_version() == 5
 
 
 def test_status_strings():
@@ -282,3 +282,14 @@ def test_plain_c_consumer(tmp_path):
     keys = [np.array([9, 7, 5, 3], np.uint64) << np.uint64(52), np.array([8, 6, 4, 2], np.uint64) << np.uint64(52)]
     k, bud = oracle.greedy(keys, [3, 1, 2, 4], 10, [4, 2], 1.0, [1.0, 1.0], (1, 2), (1, 4))
     assert [int(out[0]), int(out[1])] == k and int(out[2]) == bud
+
+
+def test_plan_argument_checks():
+    L = rsc.lib()
+    out = ctypes.c_void_p(7)
+    A = rsc.CsrStruct(4, 4, 0, None, None, None)
+    assert L.rsc_spmm_plan_create(ctypes.byref(A), None, None) == 1          # out is NULL
+    assert L.rsc_spmm_plan_create(ctypes.byref(A), None, ctypes.byref(out)) == 1  # rowptr is NULL
+    assert out.value is None
+    assert L.rsc_spmm_plan_run(None, None, 4, 4, None, 4, None) == 1
+    assert L.rsc_spmm_plan_destroy(None) == 0

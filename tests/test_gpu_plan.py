@@ -1,0 +1,99 @@
+"""SpMM plans (rsc_spmm_plan_*) and the column cache hint: a plan's product
+equals rsc_spmm bitwise, on small operands (no hinted copy) and on operands
+with more than 262,144 columns (hinted copy; the hint active when a pass
+gathers from more than 512 MiB of B rows), also with the hint switched off
+and with the column-blocked mode forced; and it matches the oracle."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2210_10737_amd as rsc
+import synth
+
+pytestmark = pytest.mark.gpu
+FLT_MIN = np.float32(np.finfo(np.float32).tiny)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu(gpu):
+    yield
+
+
+class env:
+    def __init__(self, **kv):
+        self.kv = kv
+
+    def __enter__(self):
+        self.old = {k: os.environ.get(k) for k in self.kv}
+        for k, v in self.kv.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = str(v)
+
+    def __exit__(self, *exc):
+        for k, v in self.old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+def rel_err(Y, Yo, S):
+    return float(np.max(np.abs(np.asarray(Y, np.float64) - Yo) / np.maximum(S, FLT_MIN))) if Yo.size else 0.0
+
+
+def wide_graph(seed=1):
+    """20,000 rows over 300,000 columns, power-law-like row lengths, columns
+    drawn with a skewed popularity (so there are hub columns)."""
+    rng = np.random.default_rng(seed)
+    n_rows, n_cols = 20_000, 300_000
+    lens = np.minimum((rng.pareto(1.5, n_rows) * 40 + 5).astype(np.int64), 3000)
+    w = 1.0 / (np.arange(n_cols) + 10.0) ** 0.8
+    w = w[rng.permutation(n_cols)]
+    w /= w.sum()
+    draws = rng.choice(n_cols, size=int(lens.sum()), p=w)
+    cols = [np.unique(c) for c in np.split(draws, np.cumsum(lens)[:-1])]
+    rowptr = np.zeros(n_rows + 1, np.int64)
+    rowptr[1:] = np.cumsum([len(c) for c in cols])
+    col = np.concatenate(cols).astype(np.int32)
+    val = rng.uniform(-1, 1, len(col)).astype(np.float32)
+    return synth.Csr(n_rows, rowptr.astype(np.int32), col, val), n_cols
+
+
+@pytest.mark.parametrize("d", [1, 64, 100, 256, 300, 512])
+def test_plan_equals_spmm_small(d):
+    A = synth.make_graph("tiny", 0)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, A.n)
+    B = torch.from_numpy(synth.dense_normal(A.n, d, seed=d, ld=(d + 3) // 4 * 4)).cuda()
+    plan = rsc.SpmmPlan(X)
+    for _ in range(2):
+        assert torch.equal(plan.run(B, d=d), rsc.spmm(X, B, d=d))
+    plan.close()
+
+
+@pytest.fixture(scope="module")
+def wide():
+    return wide_graph()
+
+
+@pytest.mark.parametrize("d,mode", [(512, None), (256, None), (512, "nohint"), (64, "blocked")])
+def test_plan_equals_spmm_wide(wide, d, mode):
+    A, n_cols = wide
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
+    Bh = synth.dense_normal(n_cols, d, seed=7)
+    B = torch.from_numpy(Bh).cuda()
+    kv = {"RSC_SPMM_HINT": 0 if mode == "nohint" else None, "RSC_SPMM_BLOCKED": 3 if mode == "blocked" else None}
+    with env(**kv):
+        plan = rsc.SpmmPlan(X)
+        Yp = plan.run(B)
+        Yp2 = plan.run(B)
+        Ys = rsc.spmm(X, B)
+        plan.close()
+    assert torch.equal(Yp, Ys) and torch.equal(Yp, Yp2)
+    rows = np.arange(0, A.n, 13, dtype=np.int32)
+    Yo, S = oracle.spmm(A.rowptr, A.col, A.val, Bh, rows=rows, with_mag=True)
+    assert rel_err(Yp.cpu().numpy()[rows], Yo, S) <= 1e-5
