@@ -12,7 +12,9 @@ Randomized Sparse Computations", ICML 2023 (arXiv 2210.10737).
 Typical use (A_hat symmetric, so it serves as its own transpose):
 
     A = DeviceCsr.from_host(rowptr, col, val, n_cols)   # int32 / int32 / float32
-    Y = spmm(A, H)                                       # exact forward
+    Y = spmm(A, H)                                       # exact forward (one-off)
+    plan = SpmmPlan(A)                                   # or: prepare the static operand once,
+    Y = plan.run(H)                                      # same Y bit for bit, every step
     cache = Cache(A, A, refresh_interval=10)
     k = k_from_fraction(A.n_cols, 30, 100)
     if cache.get(step, with_slice=False)["needs_refresh"]:
