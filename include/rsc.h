@@ -118,8 +118,12 @@ rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb
 /* Plan for repeated exact products with one sparse operand (a training
  * run's static A_hat). Same product, same kernels, same summation order as
  * rsc_spmm: rsc_spmm_plan_run gives Y bitwise equal to rsc_spmm on the same
- * arguments. What the plan adds is per-matrix preparation, done once:
+ * arguments (with the RSC_SPMM_* switches as they were when the plan was
+ * made; a plan whose workspace cannot hold a later switch's column-blocked
+ * buffers runs unblocked). What the plan adds is per-matrix preparation,
+ * done once:
  *   - its own workspace, so runs need none;
+ *   - when the product runs column-blocked, the split bounds of the rows;
  *   - for operands with more than 262,144 columns, a copy of col whose bit
  *     31 marks the "hub" columns, the columns of highest entry count that
  *     together hold just under half of the entries (entry-weighted median of
@@ -129,8 +133,9 @@ rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb
  *     hubs' rows stay in L2. This changes cache allocation only, never a
  *     value; RSC_SPMM_HINT=0 switches the policy off.
  * rsc_spmm_plan_create [sync] borrows A's arrays (they must outlive the plan
- * and not change) and allocates 4 nnz bytes for the copy plus the
- * workspace; RSC_ERR_OUT_OF_MEMORY if that fails. Runs of one plan share its
+ * and not change) and allocates 4 nnz bytes for the copy, 4 (P+1) n_rows
+ * bytes for the split bounds and the workspace; RSC_ERR_OUT_OF_MEMORY if
+ * that fails. Runs of one plan share its
  * workspace, so they must be ordered on the device. (The sampled products
  * of rsc_cache_* do not take the hint: on the cached slices it measured
  * slower.) */

@@ -214,6 +214,8 @@ rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb
 struct rsc_spmm_plan {
     rsc_csr_t A{};
     int32_t *colf = nullptr;  // A's columns with the hub hint in bit 31 (large graphs only)
+    int32_t *split = nullptr;  // column-blocked mode's split bounds (when the product is blocked)
+    int32_t P = 0;
     void *ws = nullptr;
     size_t ws_bytes = 0;
 };
@@ -221,6 +223,7 @@ struct rsc_spmm_plan {
 static void plan_free(rsc_spmm_plan_t *p) {
     if (!p) return;
     if (p->colf) (void)hipFree(p->colf);
+    if (p->split) (void)hipFree(p->split);
     if (p->ws) (void)hipFree(p->ws);
     delete p;
 }
@@ -238,6 +241,18 @@ rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_sp
         (void)hipGetLastError();
         plan_free(p);
         return fail(RSC_ERR_OUT_OF_MEMORY, "plan workspace of %zu bytes", p->ws_bytes);
+    }
+    const int32_t P = rsc::spmm_column_blocks(A->n_rows, A->nnz, A->n_cols);
+    if (P > 1) {
+        hipError_t e = hipMalloc((void **)&p->split, sizeof(int32_t) * (size_t)A->n_rows * (P + 1));
+        if (e == hipSuccess) e = rsc::spmm_split_launch(A->n_rows, A->n_cols, A->rowptr, A->col, P, p->split, stream);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            plan_free(p);
+            return e == hipErrorOutOfMemory ? fail(RSC_ERR_OUT_OF_MEMORY, "plan split bounds")
+                                            : hip_fail(e, "plan split");
+        }
+        p->P = P;
     }
     if (hint_worthwhile(A->n_cols) && A->nnz > 0) {
         int32_t *deg = nullptr;
@@ -258,6 +273,11 @@ rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_sp
                                             : hip_fail(e, "plan create");
         }
     }
+    if (hipStreamSynchronize(stream) != hipSuccess) {
+        const hipError_t e = hipGetLastError();
+        plan_free(p);
+        return hip_fail(e, "plan create");
+    }
     *out = p;
     return RSC_OK;
 }
@@ -269,7 +289,8 @@ rsc_status_t rsc_spmm_plan_run(rsc_spmm_plan_t *p, const float *B, int32_t d, in
     RSC_TRY(check_dense(B, A->n_cols, d, ldb, "B"));
     RSC_TRY(check_dense(Y, A->n_rows, d, ldy, "Y"));
     RSC_HIP(rsc::spmm_launch(A->n_rows, A->n_cols, A->nnz, A->rowptr, p->colf ? p->colf : A->col, A->val, B, d,
-                             ldb, Y, ldy, p->ws, p->ws_bytes, stream, A->nnz, A->n_cols, p->colf != nullptr),
+                             ldb, Y, ldy, p->ws, p->ws_bytes, stream, A->nnz, A->n_cols, p->colf != nullptr,
+                             p->split, p->P),
             "plan run");
     return RSC_OK;
 }

@@ -22,7 +22,14 @@ int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d);
 hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const int32_t *rowptr,
                        const int32_t *col, const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
                        int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream, int64_t nnz_hint,
-                       int64_t n_src_hint, bool hint_cols = false);
+                       int64_t n_src_hint, bool hint_cols = false, const int32_t *pre_split = nullptr,
+                       int32_t pre_P = 0);
+// The column-blocked mode's range count for a product (1 = not blocked) and
+// its split bounds S[(P + 1) * n_rows] (pre_split/pre_P above: bounds a plan
+// computed once; used when P matches, else recomputed in the workspace).
+int32_t spmm_column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src);
+hipError_t spmm_split_launch(int32_t n_rows, int32_t n_cols, const int32_t *rowptr, const int32_t *col, int32_t P,
+                             int32_t *S, hipStream_t stream);
 
 // ---- scores ------------------------------------------------------------
 hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,

@@ -531,6 +531,15 @@ size_t blocked_bytes(int32_t n_rows, int32_t P) {
 }
 }  // namespace
 
+int32_t spmm_column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src) { return column_blocks(n_rows, nnz, n_src); }
+
+hipError_t spmm_split_launch(int32_t n_rows, int32_t n_cols, const int32_t *rowptr, const int32_t *col, int32_t P,
+                             int32_t *S, hipStream_t stream) {
+    const int64_t ns = (int64_t)n_rows * (P + 1);
+    if (ns > 0) split_rows_kernel<<<(unsigned)ceil_div(ns, 256), 256, 0, stream>>>(rowptr, col, n_rows, n_cols, P, S);
+    return hipGetLastError();
+}
+
 size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz, int32_t n_cols) {
     // header, the row list, then the blocked mode's buffers when the full
     // product would be blocked (a slice of it never needs more ranges)
@@ -560,7 +569,7 @@ int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) 
 hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const int32_t *rowptr,
                        const int32_t *col, const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
                        int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream, int64_t nnz_hint,
-                       int64_t n_src_hint, bool hint_cols) {
+                       int64_t n_src_hint, bool hint_cols, const int32_t *pre_split, int32_t pre_P) {
     if (n_rows == 0) return hipSuccess;
     SpmmWs *h = static_cast<SpmmWs *>(ws);
     int32_t *list = reinterpret_cast<int32_t *>(h + 1);  // long-row list, or the whole processing order
@@ -571,11 +580,16 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
     const size_t head = sizeof(SpmmWs) + list_bytes(n_rows, nnz_bound);
     if (P > 1 && head + blocked_bytes(n_rows, P) <= ws_bytes) {
         char *p = static_cast<char *>(ws) + head;
-        int32_t *S = reinterpret_cast<int32_t *>(p);
         float *part = reinterpret_cast<float *>(p + align_up(sizeof(int32_t) * (size_t)n_rows * (P + 1), 256));
-        const int64_t ns = (int64_t)n_rows * (P + 1);
         const int32_t nv = P * n_rows;  // virtual rows, block-major
-        split_rows_kernel<<<(unsigned)ceil_div(ns, 256), 256, 0, stream>>>(rowptr, col, n_rows, n_cols, P, S);
+        // split bounds: a plan's, computed once, or this call's, in the workspace
+        const int32_t *S = pre_split;
+        if (!pre_split || pre_P != P) {
+            int32_t *Sw = reinterpret_cast<int32_t *>(p);
+            const hipError_t e = spmm_split_launch(n_rows, n_cols, rowptr, col, P, Sw, stream);
+            if (e != hipSuccess) return e;
+            S = Sw;
+        }
         // long pieces (a piece of a row longer than kLongRow) go to the
         // persistent 8-wave blocks as in the unblocked mode
         const int32_t n_long = (int32_t)std::min<int64_t>(long_rows_bound(n_rows, nnz_bound), kSpmmLongBlocks);

@@ -97,3 +97,28 @@ def test_plan_equals_spmm_wide(wide, d, mode):
     rows = np.arange(0, A.n, 13, dtype=np.int32)
     Yo, S = oracle.spmm(A.rowptr, A.col, A.val, Bh, rows=rows, with_mag=True)
     assert rel_err(Yp.cpu().numpy()[rows], Yo, S) <= 1e-5
+
+
+def test_plan_keeps_split_bounds():
+    """A product that runs column-blocked (20,000 columns, ~200 entries per
+    row: two ranges): the plan's precomputed split bounds give rsc_spmm's
+    result. Switched off later, the plan runs unblocked like rsc_spmm; asked
+    for more ranges than its workspace was sized for, it runs unblocked too
+    (rsc_spmm would size a larger workspace), so that result only agrees
+    within rounding."""
+    n = 20000
+    rng = np.random.default_rng(9)
+    A = synth.bucket_csr(rng.integers(150, 260, n), n, seed=12)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n)
+    B = torch.from_numpy(synth.dense_normal(n, 128, seed=13)).cuda()
+    with env(RSC_SPMM_BLOCKED=None):
+        plan = rsc.SpmmPlan(X)
+        assert torch.equal(plan.run(B), rsc.spmm(X, B))
+    for blocks in (0, 2):
+        with env(RSC_SPMM_BLOCKED=blocks):
+            assert torch.equal(plan.run(B), rsc.spmm(X, B)), blocks
+    with env(RSC_SPMM_BLOCKED=4):
+        Y4 = plan.run(B)
+    with env(RSC_SPMM_BLOCKED=0):
+        assert torch.equal(Y4, rsc.spmm(X, B))
+    plan.close()
