@@ -90,3 +90,33 @@ def test_graph_replays_blocked_mode():
             del os.environ["RSC_SPMM_BLOCKED"]
         else:
             os.environ["RSC_SPMM_BLOCKED"] = old
+
+
+def test_graph_replays_plan_run():
+    """An SpMM plan's run (its own workspace, no allocation) captured and
+    replayed, on an operand wide enough for the hinted column copy."""
+    rng = np.random.default_rng(4)
+    n_rows, n_cols = 4000, 300_000
+    A = synth.bucket_csr(rng.integers(0, 400, n_rows), n_cols, seed=5)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
+    plan = rsc.SpmmPlan(X)
+    H = torch.from_numpy(synth.dense_normal(n_cols, 512, seed=6)).cuda()
+    Y = plan.run(H)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        plan.run(H, out=Y)
+    torch.cuda.current_stream().wait_stream(s)
+    with torch.cuda.graph(g):
+        plan.run(H, out=Y)
+    for r in range(3):
+        H.mul_(-0.5)
+        g.replay()
+        torch.cuda.synchronize()
+        want = rsc.spmm(X, H)
+        torch.cuda.synchronize()
+        assert torch.equal(Y, want), f"replay {r}"
+    del g
+    plan.close()
