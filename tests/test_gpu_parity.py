@@ -448,6 +448,9 @@ def test_full_workload(name, d, pct):
     rows = np.unique(np.concatenate([rng.choice(n, 2000, replace=False),
                                      np.argsort(deg)[-16:]])).astype(np.int32)
     Y = rsc.spmm(X, Bd)
+    plan = rsc.SpmmPlan(X)      # hinted column copy on the wide operands (copurchase, gcn2)
+    assert torch.equal(plan.run(Bd), Y)
+    plan.close()
     Ys_rows = Y[torch.from_numpy(rows).long().cuda()].cpu().numpy()
     del Y
     Yo, S = oracle.spmm(A.rowptr, A.col, A.val, Bh, rows=rows, with_mag=True)
