@@ -213,9 +213,9 @@ rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb
 
 struct rsc_spmm_plan {
     rsc_csr_t A{};
-    int32_t *colf = nullptr;  // A's columns with the hub hint in bit 31 (large graphs only)
+    int32_t *colf = nullptr;   // A's columns with the hub hint in bit 31 (large graphs only)
     int32_t *split = nullptr;  // column-blocked mode's split bounds (when the product is blocked)
-    int32_t P = 0;
+    rsc::SpmmPrepared prep;    // what the runs skip: split bounds, row list (in ws) and its length
     void *ws = nullptr;
     size_t ws_bytes = 0;
 };
@@ -242,17 +242,35 @@ rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_sp
         plan_free(p);
         return fail(RSC_ERR_OUT_OF_MEMORY, "plan workspace of %zu bytes", p->ws_bytes);
     }
-    const int32_t P = rsc::spmm_column_blocks(A->n_rows, A->nnz, A->n_cols);
-    if (P > 1) {
-        hipError_t e = hipMalloc((void **)&p->split, sizeof(int32_t) * (size_t)A->n_rows * (P + 1));
-        if (e == hipSuccess) e = rsc::spmm_split_launch(A->n_rows, A->n_cols, A->rowptr, A->col, P, p->split, stream);
+    // the per-call preparation of the product, done once: split bounds and
+    // long-piece list (column-blocked), or the long-row list / row order
+    const int32_t P = std::max(1, rsc::spmm_column_blocks(A->n_rows, A->nnz, A->n_cols));
+    {
+        hipError_t e = hipSuccess;
+        if (P > 1) {
+            e = hipMalloc((void **)&p->split, sizeof(int32_t) * (size_t)A->n_rows * (P + 1));
+            if (e == hipSuccess) e = rsc::spmm_split_launch(A->n_rows, A->n_cols, A->rowptr, A->col, P, p->split, stream);
+            if (e == hipSuccess) e = rsc::spmm_blocked_prepare(A->n_rows, A->nnz, p->split, P, p->ws, stream);
+        } else {
+            p->prep.ordered = rsc::spmm_use_order(A->n_rows, A->nnz);
+            e = rsc::spmm_rows_prepare(A->n_rows, A->nnz, A->rowptr, p->ws, stream);
+        }
+        int32_t long_rows = 0;
+        const bool has_list = P > 1 || p->prep.ordered || std::min<int64_t>(A->n_rows, A->nnz / 1025) > 0;
+        if (e == hipSuccess && has_list && A->n_rows > 0)
+            e = hipMemcpyAsync(&long_rows, rsc::spmm_long_count_of(p->ws), sizeof long_rows, hipMemcpyDeviceToHost,
+                               stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);
         if (e != hipSuccess) {
             (void)hipGetLastError();
             plan_free(p);
-            return e == hipErrorOutOfMemory ? fail(RSC_ERR_OUT_OF_MEMORY, "plan split bounds")
-                                            : hip_fail(e, "plan split");
+            return e == hipErrorOutOfMemory ? fail(RSC_ERR_OUT_OF_MEMORY, "plan preparation")
+                                            : hip_fail(e, "plan preparation");
         }
-        p->P = P;
+        p->prep.split = p->split;
+        p->prep.P = P;
+        p->prep.long_rows = long_rows;
+        p->prep.ready = true;
     }
     if (hint_worthwhile(A->n_cols) && A->nnz > 0) {
         int32_t *deg = nullptr;
@@ -288,10 +306,15 @@ rsc_status_t rsc_spmm_plan_run(rsc_spmm_plan_t *p, const float *B, int32_t d, in
     const rsc_csr_t *A = &p->A;
     RSC_TRY(check_dense(B, A->n_cols, d, ldb, "B"));
     RSC_TRY(check_dense(Y, A->n_rows, d, ldy, "Y"));
-    RSC_HIP(rsc::spmm_launch(A->n_rows, A->n_cols, A->nnz, A->rowptr, p->colf ? p->colf : A->col, A->val, B, d,
-                             ldb, Y, ldy, p->ws, p->ws_bytes, stream, A->nnz, A->n_cols, p->colf != nullptr,
-                             p->split, p->P),
-            "plan run");
+    bool used = false;
+    const hipError_t e = rsc::spmm_launch(A->n_rows, A->n_cols, A->nnz, A->rowptr, p->colf ? p->colf : A->col,
+                                          A->val, B, d, ldb, Y, ldy, p->ws, p->ws_bytes, stream, A->nnz, A->n_cols,
+                                          p->colf != nullptr, &p->prep, &used);
+    // a run whose decisions differed (an environment switch changed since the
+    // plan was made) rebuilt its own row list in the plan's workspace: from
+    // then on every run prepares for itself
+    if (!used && A->n_rows > 0) p->prep.ready = false;
+    RSC_HIP(e, "plan run");
     return RSC_OK;
 }
 

@@ -19,17 +19,37 @@ size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz, int32_t n_cols);
 // hint_cols: col carries the hub hint in bit 31 (a plan's own copy only);
 // kernels always mask that bit off.
 int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d);
+// What an SpMM plan prepared once for its operand: the column-blocked split
+// bounds (split, P; P = 1 for an unblocked product) and, in the plan's own
+// workspace, the long-row (or long-piece) list or the length-class order,
+// with long_rows their count and ordered the row-order decision taken.
+// A launch uses them only while its own decisions match (ready); one that
+// did not (*used_prep false) rebuilt the list in that workspace.
+struct SpmmPrepared {
+    const int32_t *split = nullptr;
+    int32_t P = 1;
+    bool ordered = false;
+    bool ready = false;
+    int32_t long_rows = 0;
+};
 hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const int32_t *rowptr,
                        const int32_t *col, const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
                        int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream, int64_t nnz_hint,
-                       int64_t n_src_hint, bool hint_cols = false, const int32_t *pre_split = nullptr,
-                       int32_t pre_P = 0);
+                       int64_t n_src_hint, bool hint_cols = false, const SpmmPrepared *prep = nullptr,
+                       bool *used_prep = nullptr);
 // The column-blocked mode's range count for a product (1 = not blocked) and
-// its split bounds S[(P + 1) * n_rows] (pre_split/pre_P above: bounds a plan
-// computed once; used when P matches, else recomputed in the workspace).
+// its split bounds S[(P + 1) * n_rows]; the row-order decision; and the
+// preparation a launch would do, run once into a plan's workspace (then
+// *spmm_long_count_of(ws) holds the list's length on the device).
 int32_t spmm_column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src);
 hipError_t spmm_split_launch(int32_t n_rows, int32_t n_cols, const int32_t *rowptr, const int32_t *col, int32_t P,
                              int32_t *S, hipStream_t stream);
+bool spmm_use_order(int32_t n_rows, int64_t nnz);
+hipError_t spmm_rows_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr, void *ws,
+                             hipStream_t stream);
+hipError_t spmm_blocked_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t *S, int32_t P, void *ws,
+                                hipStream_t stream);
+const int32_t *spmm_long_count_of(const void *ws);
 
 // ---- scores ------------------------------------------------------------
 hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,

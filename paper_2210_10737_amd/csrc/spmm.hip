@@ -566,10 +566,46 @@ int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) 
     return 32;
 }
 
+bool spmm_use_order(int32_t n_rows, int64_t nnz) { return use_order(n_rows, nnz); }
+
+hipError_t spmm_rows_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr, void *ws,
+                             hipStream_t stream) {
+    if (n_rows == 0) return hipSuccess;
+    SpmmWs *h = static_cast<SpmmWs *>(ws);
+    int32_t *list = reinterpret_cast<int32_t *>(h + 1);
+    const int64_t lbound = long_rows_bound(n_rows, nnz_bound);
+    const unsigned cgrid = (unsigned)ceil_div(n_rows, kCollectThreads * kCollectPerThread);
+    if (use_order(n_rows, nnz_bound)) {
+        zero_header_kernel<<<1, 128, 0, stream>>>(h);
+        class_hist_kernel<<<cgrid, kCollectThreads, 0, stream>>>(rowptr, n_rows, h);
+        class_scan_kernel<<<1, 64, 0, stream>>>(h);
+        class_scatter_kernel<<<cgrid, kCollectThreads, 0, stream>>>(rowptr, n_rows, h, list);
+    } else if (lbound > 0) {
+        zero_counters_kernel<<<1, 1, 0, stream>>>(&h->long_count);
+        collect_long_rows_kernel<<<cgrid, kCollectThreads, 0, stream>>>(rowptr, 1, n_rows, &h->long_count, list);
+    }
+    return hipGetLastError();
+}
+
+hipError_t spmm_blocked_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t *S, int32_t P, void *ws,
+                                hipStream_t stream) {
+    SpmmWs *h = static_cast<SpmmWs *>(ws);
+    int32_t *list = reinterpret_cast<int32_t *>(h + 1);
+    const int32_t nv = P * n_rows;
+    zero_counters_kernel<<<1, 1, 0, stream>>>(&h->long_count);
+    if (long_rows_bound(n_rows, nnz_bound) > 0 && nv > 0)
+        collect_long_rows_kernel<<<(unsigned)ceil_div(nv, kCollectThreads * kCollectPerThread), kCollectThreads, 0,
+                                   stream>>>(S, n_rows, nv, &h->long_count, list);
+    return hipGetLastError();
+}
+
+const int32_t *spmm_long_count_of(const void *ws) { return &static_cast<const SpmmWs *>(ws)->long_count; }
+
 hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const int32_t *rowptr,
                        const int32_t *col, const float *val, const float *B, int32_t d, int64_t ldb, float *Y,
                        int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream, int64_t nnz_hint,
-                       int64_t n_src_hint, bool hint_cols, const int32_t *pre_split, int32_t pre_P) {
+                       int64_t n_src_hint, bool hint_cols, const SpmmPrepared *prep, bool *used_prep) {
+    if (used_prep) *used_prep = false;
     if (n_rows == 0) return hipSuccess;
     SpmmWs *h = static_cast<SpmmWs *>(ws);
     int32_t *list = reinterpret_cast<int32_t *>(h + 1);  // long-row list, or the whole processing order
@@ -582,27 +618,32 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
         char *p = static_cast<char *>(ws) + head;
         float *part = reinterpret_cast<float *>(p + align_up(sizeof(int32_t) * (size_t)n_rows * (P + 1), 256));
         const int32_t nv = P * n_rows;  // virtual rows, block-major
-        // split bounds: a plan's, computed once, or this call's, in the workspace
-        const int32_t *S = pre_split;
-        if (!pre_split || pre_P != P) {
-            int32_t *Sw = reinterpret_cast<int32_t *>(p);
-            const hipError_t e = spmm_split_launch(n_rows, n_cols, rowptr, col, P, Sw, stream);
+        // split bounds and the long-piece list: a plan's, prepared once (the
+        // list then already sits in this workspace), or this call's
+        const bool pre = prep && prep->ready && prep->P == P && prep->split;
+        if (used_prep) *used_prep = pre;
+        const int32_t *S = pre ? prep->split : reinterpret_cast<const int32_t *>(p);
+        int32_t n_long;
+        if (pre) {
+            n_long = std::min<int32_t>(prep->long_rows, kSpmmLongBlocks);
+        } else {
+            const hipError_t e = spmm_split_launch(n_rows, n_cols, rowptr, col, P, reinterpret_cast<int32_t *>(p),
+                                                   stream);
             if (e != hipSuccess) return e;
-            S = Sw;
-        }
-        // long pieces (a piece of a row longer than kLongRow) go to the
-        // persistent 8-wave blocks as in the unblocked mode
-        const int32_t n_long = (int32_t)std::min<int64_t>(long_rows_bound(n_rows, nnz_bound), kSpmmLongBlocks);
-        if (n_long > 0) {
-            zero_counters_kernel<<<1, 1, 0, stream>>>(&h->long_count);
-            collect_long_rows_kernel<<<(unsigned)ceil_div(nv, kCollectThreads * kCollectPerThread), kCollectThreads,
-                                       0, stream>>>(S, n_rows, nv, &h->long_count, list);
+            // long pieces (a piece of a row longer than kLongRow) go to the
+            // persistent 8-wave blocks as in the unblocked mode
+            n_long = (int32_t)std::min<int64_t>(long_rows_bound(n_rows, nnz_bound), kSpmmLongBlocks);
+            if (n_long > 0) {
+                zero_counters_kernel<<<1, 1, 0, stream>>>(&h->long_count);
+                collect_long_rows_kernel<<<(unsigned)ceil_div(nv, kCollectThreads * kCollectPerThread),
+                                           kCollectThreads, 0, stream>>>(S, n_rows, nv, &h->long_count, list);
+            }
         }
         const unsigned vgrid = (unsigned)ceil_div(nv, kSpmmRowWaves);
         for (int32_t f0 = 0; f0 < d; f0 += kBlockW) {
             const int32_t dl = std::min<int32_t>(d - f0, kBlockW);
             if (n_long > 0) {
-                if (f0 > 0) zero_next_kernel<<<1, 1, 0, stream>>>(&h->long_next);
+                if (f0 > 0 || pre) zero_next_kernel<<<1, 1, 0, stream>>>(&h->long_next);
                 spmm_long_kernel<16, 1, false><<<n_long, kSpmmLongWaves * 64, 0, stream>>>(
                     S, n_rows, col, val, B + f0, ldb, part, kBlockW, dl, &h->long_count, &h->long_next, list);
             }
@@ -615,18 +656,18 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
         }
         return hipGetLastError();
     }
-    const int64_t lbound = long_rows_bound(n_rows, nnz_bound);
-    const int32_t n_long_blocks = (int32_t)std::min<int64_t>(lbound, kSpmmLongBlocks);
     const bool ordered = use_order(n_rows, nnz_bound);
-    const unsigned cgrid = (unsigned)ceil_div(n_rows, kCollectThreads * kCollectPerThread);
-    if (ordered) {
-        zero_header_kernel<<<1, 128, 0, stream>>>(h);
-        class_hist_kernel<<<cgrid, kCollectThreads, 0, stream>>>(rowptr, n_rows, h);
-        class_scan_kernel<<<1, 64, 0, stream>>>(h);
-        class_scatter_kernel<<<cgrid, kCollectThreads, 0, stream>>>(rowptr, n_rows, h, list);
-    } else if (n_long_blocks > 0) {
-        zero_counters_kernel<<<1, 1, 0, stream>>>(&h->long_count);
-        collect_long_rows_kernel<<<cgrid, kCollectThreads, 0, stream>>>(rowptr, 1, n_rows, &h->long_count, list);
+    // a plan's row list (long rows, or the whole order) prepared once sits in
+    // this workspace already; else this call builds it
+    const bool pre = prep && prep->ready && prep->P == 1 && prep->ordered == ordered;
+    if (used_prep) *used_prep = pre;
+    int32_t n_long_blocks;
+    if (pre) {
+        n_long_blocks = std::min<int32_t>(prep->long_rows, kSpmmLongBlocks);
+    } else {
+        n_long_blocks = (int32_t)std::min<int64_t>(long_rows_bound(n_rows, nnz_bound), kSpmmLongBlocks);
+        const hipError_t e = spmm_rows_prepare(n_rows, nnz_bound, rowptr, ws, stream);
+        if (e != hipSuccess) return e;
     }
     const int32_t *order = ordered ? list : nullptr;
     const unsigned grid = (unsigned)ceil_div(n_rows, kSpmmRowWaves);
@@ -640,7 +681,7 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
 #define RSC_SPMM_LAUNCH_H(LPE_, NV_, H_)                                                               \
     do {                                                                                               \
         if (n_long_blocks > 0) {                                                                       \
-            if (f0 > 0) zero_next_kernel<<<1, 1, 0, stream>>>(&h->long_next);                          \
+            if (f0 > 0 || pre) zero_next_kernel<<<1, 1, 0, stream>>>(&h->long_next);                   \
             spmm_long_kernel<LPE_, NV_, H_><<<n_long_blocks, kSpmmLongWaves * 64, 0, stream>>>(         \
                 rowptr, 1, col, val, B + f0, ldb, Y + f0, ldy, dl, &h->long_count, &h->long_next, list);  \
         }                                                                                              \

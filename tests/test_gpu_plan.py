@@ -80,13 +80,14 @@ def wide():
     return wide_graph()
 
 
-@pytest.mark.parametrize("d,mode", [(512, None), (256, None), (512, "nohint"), (64, "blocked")])
+@pytest.mark.parametrize("d,mode", [(512, None), (256, None), (512, "nohint"), (64, "blocked"), (300, "ordered")])
 def test_plan_equals_spmm_wide(wide, d, mode):
     A, n_cols = wide
     X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
     Bh = synth.dense_normal(n_cols, d, seed=7)
     B = torch.from_numpy(Bh).cuda()
-    kv = {"RSC_SPMM_HINT": 0 if mode == "nohint" else None, "RSC_SPMM_BLOCKED": 3 if mode == "blocked" else None}
+    kv = {"RSC_SPMM_HINT": 0 if mode == "nohint" else None, "RSC_SPMM_BLOCKED": 3 if mode == "blocked" else None,
+          "RSC_SPMM_ORDER": 1 if mode == "ordered" else None}
     with env(**kv):
         plan = rsc.SpmmPlan(X)
         Yp = plan.run(B)
@@ -122,3 +123,20 @@ def test_plan_keeps_split_bounds():
     with env(RSC_SPMM_BLOCKED=0):
         assert torch.equal(Y4, rsc.spmm(X, B))
     plan.close()
+
+
+def test_plan_row_list_survives_switches(wide):
+    """The plan builds its long-row list (or the length-class order) once;
+    runs under a different row-order switch rebuild it themselves, and every
+    run equals rsc_spmm."""
+    A, n_cols = wide
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
+    B = torch.from_numpy(synth.dense_normal(n_cols, 64, seed=21)).cuda()
+    want = rsc.spmm(X, B)
+    for first in (0, 1):
+        with env(RSC_SPMM_ORDER=first):
+            plan = rsc.SpmmPlan(X)
+        for order in (first, 1 - first, first):
+            with env(RSC_SPMM_ORDER=order):
+                assert torch.equal(plan.run(B), want), (first, order)
+        plan.close()
