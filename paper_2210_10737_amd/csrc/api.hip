@@ -157,6 +157,9 @@ struct rsc_cache {
     void *ws_topk = nullptr, *ws_slice = nullptr, *ws_spmm = nullptr;
     size_t ws_topk_bytes = 0, ws_slice_bytes = 0, ws_spmm_bytes = 0;
     hipEvent_t ev = nullptr;
+    int32_t *s_split = nullptr;  // the slice's column-blocked split bounds (when its product is blocked)
+    int32_t split_P = 0;          // ranges s_split has room for
+    rsc::SpmmPrepared prep;       // the slice product's row list, prepared at each refresh (in ws_spmm)
     int32_t k = 0;
     int64_t last_step = 0;
     uint64_t version = 0;
@@ -435,7 +438,7 @@ rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, const doubl
 static void cache_free(rsc_cache_t *c) {
     if (!c) return;
     void *dev[] = {c->cn2, c->colnnz, c->key, c->rn2, c->count, c->colw, c->idx, c->mask, c->s_rowptr,
-                   c->s_col, c->s_val, c->d_nnz, c->ws_topk, c->ws_slice, c->ws_spmm, c->ws_sample};
+                   c->s_col, c->s_val, c->d_nnz, c->ws_topk, c->ws_slice, c->ws_spmm, c->ws_sample, c->s_split};
     for (void *p : dev) {
         if (!p) continue;
         if (c->alloc.alloc)
@@ -479,6 +482,8 @@ rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_
     c->ws_slice_bytes = rsc::slice_ws_bytes(X->nnz);
     c->ws_spmm_bytes = rsc::spmm_ws_bytes(X->n_rows, X->nnz, X->n_cols);
     c->ws_sample_bytes = rsc::sample_ws_bytes(c->n);
+    // a slice's product is column-blocked with at most the full product's ranges
+    c->split_P = std::max(1, rsc::spmm_column_blocks(X->n_rows, X->nnz, X->n_cols));
     struct {
         void **p;
         size_t bytes;
@@ -499,6 +504,7 @@ rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_
         {&c->ws_slice, c->ws_slice_bytes},
         {&c->ws_spmm, c->ws_spmm_bytes},
         {&c->ws_sample, c->ws_sample_bytes},
+        {(void **)&c->s_split, sizeof(int32_t) * ((size_t)X->n_rows + 1) * (c->split_P + 1)},
     };
     for (auto &a : allocs) {
         const size_t bytes = std::max<size_t>(a.bytes, 256);
@@ -530,6 +536,33 @@ rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_
     return RSC_OK;
 }
 
+// After a new slice: what every sampled product would build first (split
+// bounds and long-piece list when blocked, else the long-row list or the
+// row order), built once into ws_spmm. Asynchronous (the list's length stays
+// on the device; launches use its bound).
+static hipError_t cache_prepare(rsc_cache_t *c, hipStream_t stream) {
+    c->prep = rsc::SpmmPrepared{};
+    const rsc_csr_t &X = c->X;
+    if (X.n_rows == 0) return hipSuccess;
+    const int64_t kk = std::min<int64_t>(c->k, c->n);
+    const int64_t nnz_hint = c->n > 0 ? X.nnz * kk / c->n : 0;
+    const int32_t P = std::max(1, rsc::spmm_column_blocks(X.n_rows, nnz_hint, kk));
+    hipError_t e;
+    if (P > 1) {
+        if (P > c->split_P || rsc::spmm_blocked_fits(X.n_rows, X.nnz, P) > c->ws_spmm_bytes) return hipSuccess;
+        e = rsc::spmm_split_launch(X.n_rows, X.n_cols, c->s_rowptr, c->s_col, P, c->s_split, stream);
+        if (e == hipSuccess) e = rsc::spmm_blocked_prepare(X.n_rows, X.nnz, c->s_split, P, c->ws_spmm, stream);
+        c->prep.split = c->s_split;
+    } else {
+        c->prep.ordered = rsc::spmm_use_order(X.n_rows, X.nnz);
+        e = rsc::spmm_rows_prepare(X.n_rows, X.nnz, c->s_rowptr, c->ws_spmm, stream);
+    }
+    c->prep.P = P;
+    c->prep.long_rows = -1;
+    c->prep.ready = e == hipSuccess;
+    return e;
+}
+
 rsc_status_t rsc_cache_score(rsc_cache_t *c, const float *B, int32_t d, int64_t ldb, hipStream_t stream) {
     if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
     RSC_TRY(check_dense(B, c->n, d, ldb, "B"));
@@ -553,6 +586,7 @@ rsc_status_t rsc_cache_select(rsc_cache_t *c, int32_t k, int64_t step, hipStream
     c->version += 1;
     c->nnz_known = false;
     c->random = false;
+    RSC_HIP(cache_prepare(c, stream), "cache slice preparation");
     return RSC_OK;
 }
 
@@ -574,6 +608,7 @@ rsc_status_t rsc_cache_refresh_random(rsc_cache_t *c, const float *B, int32_t d,
     c->version += 1;
     c->nnz_known = false;
     c->random = true;
+    RSC_HIP(cache_prepare(c, stream), "cache slice preparation");
     return RSC_OK;
 }
 
@@ -625,9 +660,12 @@ rsc_status_t rsc_spmm_sampled(rsc_cache_t *c, const float *B, int32_t d, int64_t
     // never depend on which calls came before).
     const int64_t kk = std::min<int64_t>(c->k, c->n);
     const int64_t nnz_hint = c->n > 0 ? c->X.nnz * kk / c->n : 0;
-    RSC_HIP(rsc::spmm_launch(c->X.n_rows, c->X.n_cols, c->X.nnz, c->s_rowptr, c->s_col, c->s_val, B, d, ldb, Y,
-                             ldy, c->ws_spmm, c->ws_spmm_bytes, stream, nnz_hint, kk),
-            "spmm_sampled launch");
+    bool used = false;
+    const hipError_t e = rsc::spmm_launch(c->X.n_rows, c->X.n_cols, c->X.nnz, c->s_rowptr, c->s_col, c->s_val, B, d,
+                                          ldb, Y, ldy, c->ws_spmm, c->ws_spmm_bytes, stream, nnz_hint, kk, false,
+                                          &c->prep, &used);
+    if (!used) c->prep.ready = false;  // the launch rebuilt its own list in ws_spmm
+    RSC_HIP(e, "spmm_sampled launch");
     return RSC_OK;
 }
 

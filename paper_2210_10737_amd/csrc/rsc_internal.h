@@ -22,7 +22,8 @@ int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d);
 // What an SpMM plan prepared once for its operand: the column-blocked split
 // bounds (split, P; P = 1 for an unblocked product) and, in the plan's own
 // workspace, the long-row (or long-piece) list or the length-class order,
-// with long_rows their count and ordered the row-order decision taken.
+// with long_rows their count (-1: not known on the host, the launch uses the
+// bound) and ordered the row-order decision taken.
 // A launch uses them only while its own decisions match (ready); one that
 // did not (*used_prep false) rebuilt the list in that workspace.
 struct SpmmPrepared {
@@ -49,6 +50,7 @@ hipError_t spmm_rows_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t *r
                              hipStream_t stream);
 hipError_t spmm_blocked_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t *S, int32_t P, void *ws,
                                 hipStream_t stream);
+size_t spmm_blocked_fits(int32_t n_rows, int64_t nnz_bound, int32_t P);  // workspace bytes the blocked mode needs
 const int32_t *spmm_long_count_of(const void *ws);
 
 // ---- scores ------------------------------------------------------------

@@ -599,6 +599,10 @@ hipError_t spmm_blocked_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t
     return hipGetLastError();
 }
 
+size_t spmm_blocked_fits(int32_t n_rows, int64_t nnz_bound, int32_t P) {
+    return sizeof(SpmmWs) + list_bytes(n_rows, nnz_bound) + blocked_bytes(n_rows, P);
+}
+
 const int32_t *spmm_long_count_of(const void *ws) { return &static_cast<const SpmmWs *>(ws)->long_count; }
 
 hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const int32_t *rowptr,
@@ -625,7 +629,8 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
         const int32_t *S = pre ? prep->split : reinterpret_cast<const int32_t *>(p);
         int32_t n_long;
         if (pre) {
-            n_long = std::min<int32_t>(prep->long_rows, kSpmmLongBlocks);
+            n_long = (int32_t)std::min<int64_t>(
+                prep->long_rows >= 0 ? prep->long_rows : long_rows_bound(n_rows, nnz_bound), kSpmmLongBlocks);
         } else {
             const hipError_t e = spmm_split_launch(n_rows, n_cols, rowptr, col, P, reinterpret_cast<int32_t *>(p),
                                                    stream);
@@ -663,7 +668,8 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
     if (used_prep) *used_prep = pre;
     int32_t n_long_blocks;
     if (pre) {
-        n_long_blocks = std::min<int32_t>(prep->long_rows, kSpmmLongBlocks);
+        n_long_blocks = (int32_t)std::min<int64_t>(
+            prep->long_rows >= 0 ? prep->long_rows : long_rows_bound(n_rows, nnz_bound), kSpmmLongBlocks);
     } else {
         n_long_blocks = (int32_t)std::min<int64_t>(long_rows_bound(n_rows, nnz_bound), kSpmmLongBlocks);
         const hipError_t e = spmm_rows_prepare(n_rows, nnz_bound, rowptr, ws, stream);
