@@ -160,6 +160,7 @@ struct rsc_cache {
     int32_t *s_split = nullptr;  // the slice's column-blocked split bounds (when its product is blocked)
     int32_t split_P = 0;          // ranges s_split has room for
     rsc::SpmmPrepared prep;       // the slice product's row list, prepared at each refresh (in ws_spmm)
+    int32_t x_long_rows = -1;     // rows of X longer than the long-row threshold (0: no slice has any)
     int32_t k = 0;
     int64_t last_step = 0;
     uint64_t version = 0;
@@ -527,11 +528,23 @@ rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_
     hipError_t e = hipHostMalloc((void **)&c->h_nnz, sizeof(int64_t), hipHostMallocDefault);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev, hipEventDisableTiming);
     if (e == hipSuccess) e = rsc::col_sqnorms_launch(XT->n_rows, XT->rowptr, XT->val, c->cn2, c->colnnz, stream);
+    // whether X has long rows at all: a slice's rows are parts of X's, so if
+    // none is long, the sampled products need no long-row pass
+    int32_t x_long = 0;
+    const bool any_long_possible =
+        rsc::spmm_use_order(X->n_rows, X->nnz) || std::min<int64_t>(X->n_rows, X->nnz / 1025) > 0;
+    if (e == hipSuccess && any_long_possible && X->n_rows > 0) {
+        e = rsc::spmm_rows_prepare(X->n_rows, X->nnz, X->rowptr, c->ws_spmm, stream);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(&x_long, rsc::spmm_long_count_of(c->ws_spmm), sizeof x_long, hipMemcpyDeviceToHost,
+                               stream);
+    }
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
     if (e != hipSuccess) {
         cache_free(c);
         return hip_fail(e, "cache create");
     }
+    c->x_long_rows = x_long;
     *out = c;
     return RSC_OK;
 }
@@ -558,7 +571,7 @@ static hipError_t cache_prepare(rsc_cache_t *c, hipStream_t stream) {
         e = rsc::spmm_rows_prepare(X.n_rows, X.nnz, c->s_rowptr, c->ws_spmm, stream);
     }
     c->prep.P = P;
-    c->prep.long_rows = -1;
+    c->prep.long_rows = c->x_long_rows == 0 ? 0 : -1;  // else the length stays on the device
     c->prep.ready = e == hipSuccess;
     return e;
 }
