@@ -124,6 +124,8 @@ rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb
  * done once:
  *   - its own workspace, so runs need none;
  *   - when the product runs column-blocked, the split bounds of the rows;
+ *   - the long-row list (or the length-class row order) and its length,
+ *     which every rsc_spmm call builds first;
  *   - for operands with more than 262,144 columns, a copy of col whose bit
  *     31 marks the "hub" columns, the columns of highest entry count that
  *     together hold just under half of the entries (entry-weighted median of
@@ -135,10 +137,10 @@ rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb
  * rsc_spmm_plan_create [sync] borrows A's arrays (they must outlive the plan
  * and not change) and allocates 4 nnz bytes for the copy, 4 (P+1) n_rows
  * bytes for the split bounds and the workspace; RSC_ERR_OUT_OF_MEMORY if
- * that fails. Runs of one plan share its
- * workspace, so they must be ordered on the device. (The sampled products
- * of rsc_cache_* do not take the hint: on the cached slices it measured
- * slower.) */
+ * that fails. Runs of one plan share its workspace, so they must be
+ * ordered on the device. The sampled-matrix cache prepares each new slice's
+ * row list the same way at refresh time; its sampled products do not take
+ * the column hint (on the cached slices it measured slower). */
 typedef struct rsc_spmm_plan rsc_spmm_plan_t;
 rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_spmm_plan_t **out);
 rsc_status_t rsc_spmm_plan_run(rsc_spmm_plan_t *plan, const float *B, int32_t d, int64_t ldb, float *Y,
