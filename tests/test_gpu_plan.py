@@ -140,3 +140,35 @@ def test_plan_row_list_survives_switches(wide):
             with env(RSC_SPMM_ORDER=order):
                 assert torch.equal(plan.run(B), want), (first, order)
         plan.close()
+
+
+@pytest.mark.parametrize("switch", ["RSC_SPMM_ORDER", "RSC_SPMM_BLOCKED", "RSC_SPMM_SLICE"])
+def test_cache_prepared_list_survives_switches(switch):
+    """The cache prepares each slice's row list at refresh; sampled products
+    run under other switch settings rebuild their own, and every product
+    stays within tolerance of the oracle (and bitwise stable per setting)."""
+    rng = np.random.default_rng(77)
+    n = 3000
+    lens = np.minimum(np.where(rng.random(n) < 0.05, rng.integers(1100, 2900, n), rng.integers(0, 300, n)), n)
+    A = synth.bucket_csr(lens, n, seed=31)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n)
+    AT = synth.transpose(A, n)
+    Bh = synth.dense_normal(n, 96, seed=32)
+    B = torch.from_numpy(Bh).cuda()
+    values = {"RSC_SPMM_ORDER": (1, 0, 1), "RSC_SPMM_BLOCKED": (2, 0, 3, 2), "RSC_SPMM_SLICE": (32, 256, 32)}[switch]
+    with env(**{switch: values[0]}):
+        cache = rsc.Cache(X, rsc.DeviceCsr.from_host(AT.rowptr, AT.col, AT.val, n))
+        cache.refresh(B, n // 2, step=0)
+        snap = rsc.cache_snapshot(cache)
+        first = cache.spmm_sampled(B)
+    Yo, S = oracle.spmm(snap["rowptr"], snap["col"], snap["val"], Bh, with_mag=True)
+    seen = {}
+    for v in values:
+        with env(**{switch: v}):
+            Ys = cache.spmm_sampled(B)
+        assert rel_err(Ys.cpu().numpy(), Yo, S) <= 1e-4, (switch, v)
+        if v in seen:
+            assert torch.equal(Ys, seen[v]), (switch, v)
+        seen[v] = Ys
+    assert torch.equal(seen[values[0]], first)
+    cache.close()
