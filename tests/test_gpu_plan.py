@@ -2,7 +2,9 @@
 equals rsc_spmm bitwise, on small operands (no hinted copy) and on operands
 with more than 262,144 columns (hinted copy; the hint active when a pass
 gathers from more than 512 MiB of B rows), also with the hint switched off
-and with the column-blocked mode forced; and it matches the oracle."""
+and with the column-blocked mode forced; and it matches the oracle. Plans
+and caches prepare their row lists once; runs under changed environment
+switches rebuild their own and stay correct."""
 import os
 
 import numpy as np
