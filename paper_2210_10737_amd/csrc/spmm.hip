@@ -24,7 +24,12 @@
 //     class first (a scheduling order only);
 //   * when the referenced B rows span a few L2-sized ranges, the columns are
 //     cut into those ranges and processed one range at a time, with fp32
-//     partial rows combined in fixed range order (column-blocked mode).
+//     partial rows combined in fixed range order (column-blocked mode);
+//   * bit 31 of a column index (set only in a plan's own copy of col) marks
+//     hub columns; when the gathered rows far outgrow the caches, the other
+//     columns' rows are loaded non-temporally so the hubs' stay in L2;
+//   * the per-call preparation (long-row list or row order, split bounds)
+//     can be done once by a plan or at a cache refresh and reused.
 #include <cstdlib>
 
 #include "rsc_internal.h"
