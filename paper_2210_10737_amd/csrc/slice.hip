@@ -24,10 +24,6 @@ namespace {
 constexpr int kTile = 4096;          // entries per tile
 constexpr int kPer = kTile / 256;    // 256-entry chunks per tile
 
-__device__ __forceinline__ bool kept(const uint32_t *__restrict__ mask, int32_t c) {
-    return (mask[c >> 5] >> (c & 31)) & 1u;
-}
-
 // Entry o of a tile (0 <= o < kTile) is position o & 255 of chunk o >> 8;
 // within a chunk, wave (o >> 6) & 3, lane o & 63. The kept flags of one
 // (chunk, wave) are one 64-bit ballot, stored per tile in that order

@@ -23,6 +23,13 @@ namespace {
 constexpr int kBins = 2048;
 constexpr int kTile = 4096;     // keys per tile: 4 waves x 16 groups of 64
 constexpr int kPasses = 6;
+
+// Of eq keys equal to the threshold, how many are taken when want more are
+// still wanted: want clamped to [0, eq], in integers.
+__device__ __forceinline__ int64_t clamp_take(int64_t want, int64_t eq) {
+    return want < 0 ? 0 : (want < eq ? want : eq);
+}
+
 __constant__ const int kShift[kPasses] = {53, 42, 31, 20, 10, 0};
 __constant__ const int kWidth[kPasses] = {11, 11, 11, 11, 10, 10};
 
@@ -167,7 +174,7 @@ __global__ __launch_bounds__(1024) void topk_tile_scan_kernel(int32_t nt, const 
     int64_t sel_local = 0;
     for (int32_t i = lo; i < hi; ++i) {
         eq_before[i] = (uint32_t)run;
-        const int64_t take = min<int64_t>(max<int64_t>(r - run, 0), tile_eq[i]);
+        const int64_t take = clamp_take(r - run, tile_eq[i]);
         sel_local += tile_gt[i] + take;
         run += tile_eq[i];
     }
@@ -175,7 +182,7 @@ __global__ __launch_bounds__(1024) void topk_tile_scan_kernel(int32_t nt, const 
     for (int32_t i = lo; i < hi; ++i) {
         sel_before[i] = (uint32_t)srun;
         const int64_t eb = eq_before[i];
-        const int64_t take = min<int64_t>(max<int64_t>(r - eb, 0), tile_eq[i]);
+        const int64_t take = clamp_take(r - eb, tile_eq[i]);
         srun += tile_gt[i] + take;
     }
 }
@@ -205,7 +212,7 @@ __global__ __launch_bounds__(256) void topk_emit_kernel(const uint64_t *__restri
     __syncthreads();
     int64_t eq_base = eq_before[blockIdx.x], sel_base = sel_before[blockIdx.x];
     for (int v = 0; v < w; ++v) {
-        const int64_t take = min<int64_t>(max<int64_t>(r - eq_base, 0), s_eq[v]);
+        const int64_t take = clamp_take(r - eq_base, s_eq[v]);
         sel_base += s_gt[v] + take;
         eq_base += s_eq[v];
     }
