@@ -30,6 +30,9 @@
  *     not overlap on the device. The calls on one cache share its internal
  *     buffers and workspaces, so they must be ordered on the device (one
  *     stream, or events between streams).
+ *   - A plan or cache lives on the device that was current when it was
+ *     made; a call that launches work for it with another device current
+ *     returns RSC_ERR_INVALID_ARGUMENT.
  */
 #ifndef RSC_H
 #define RSC_H
@@ -326,6 +329,8 @@ int32_t rsc_k_from_fraction(int32_t n, int32_t num, int32_t den);
  *   d_host[l]: width of layer l's dense operand; fro_a2 = ||A||_F^2;
  *   fro_b2_host[l] = ||grad H^(l+1)||_F^2.
  *   Budget C = C_num / C_den; step = max(1, floor(n * alpha_num / alpha_den)).
+ *   RSC_ERR_INVALID_ARGUMENT unless C >= 0, 0 <= alpha <= 1 (alpha is a
+ *   fraction of the n columns) and sum_l nnz d_l fits int64.
  * Pairs rank by (key desc, index asc). Starting from k_l = n, while
  * Bud * C_den > C_num * sum_l nnz d_l, the eligible layer (k_l > 0) whose
  * shrink to max(0, k_l - step) loses the least normalised score mass
@@ -352,7 +357,8 @@ rsc_status_t rsc_greedy_allocate(int32_t L, int32_t n, int64_t nnz,
  *   count[j] = sum of colnnz over the block.
  * rsc_greedy_profile computes it on the device (stable radix sort of the
  * keys); order (nullable, int32[n]) receives the ranking itself. mass and
- * count hold rsc_greedy_blocks(n, alpha_num, alpha_den) entries. ws: at
+ * count hold rsc_greedy_blocks(n, alpha_num, alpha_den) entries (-1 for
+ * n < 0 or alpha outside [0, 1], where both calls fail). ws: at
  * least rsc_greedy_profile_workspace_bytes(n) bytes, 256-byte aligned.
  * rsc_greedy_allocate_profiles runs the greedy loop on the host from the
  * layers' profiles (copied to the host); given the same keys it returns the

@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdarg>
+#include <cstdint>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -123,6 +124,32 @@ rsc_status_t validate(const rsc_csr_t *A, const char *name, int64_t *bad_row, hi
 // B rows, and a pass is at most 512 floats wide).
 bool hint_worthwhile(int32_t n_src) { return (double)n_src * 512 * sizeof(float) > 512.0 * 1024 * 1024; }
 
+// The greedy's shared argument checks: alpha is a fraction of the n columns
+// (0 <= alpha <= 1) and the full budget sum_l nnz d_l fits int64 (*total).
+rsc_status_t check_greedy(int32_t L, int32_t n, int64_t nnz, const int32_t *d_host, int32_t C_num, int32_t C_den,
+                          int32_t alpha_num, int32_t alpha_den, int64_t *total) {
+    if (L < 1 || n < 0 || nnz < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "L < 1, n < 0 or nnz < 0");
+    if (C_num < 0 || C_den <= 0 || alpha_num < 0 || alpha_den <= 0 || alpha_num > alpha_den)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "bad budget or step fraction (need C >= 0, 0 <= alpha <= 1)");
+    __int128 t = 0;
+    for (int32_t l = 0; l < L; ++l) {
+        if (d_host[l] < 1) return fail(RSC_ERR_INVALID_ARGUMENT, "d[%d] < 1", l);
+        t += (__int128)nnz * d_host[l];
+    }
+    if (t > (__int128)INT64_MAX) return fail(RSC_ERR_INVALID_ARGUMENT, "budget sum_l nnz * d_l exceeds int64");
+    *total = (int64_t)t;
+    return RSC_OK;
+}
+
+// The device a plan or cache was made on must be the current one when it is used.
+rsc_status_t check_same_device(int made_on, const char *what) {
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return fail(RSC_ERR_NO_DEVICE, "no current HIP device");
+    if (cur != made_on)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "%s was made on device %d, current device is %d", what, made_on, cur);
+    return RSC_OK;
+}
+
 // with RSC_VALIDATE=1, the device check of a caller's CSR before any launch
 rsc_status_t maybe_validate(const rsc_csr_t *A, const char *name, hipStream_t stream) {
     return validate_env() ? validate(A, name, nullptr, stream) : RSC_OK;
@@ -222,6 +249,7 @@ struct rsc_spmm_plan {
     rsc::SpmmPrepared prep;    // what the runs skip: split bounds, row list (in ws) and its length
     void *ws = nullptr;
     size_t ws_bytes = 0;
+    int device = 0;
 };
 
 static void plan_free(rsc_spmm_plan_t *p) {
@@ -240,6 +268,7 @@ rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_sp
     RSC_TRY(maybe_validate(A, "A", stream));
     rsc_spmm_plan_t *p = new rsc_spmm_plan_t();
     p->A = *A;
+    (void)hipGetDevice(&p->device);
     p->ws_bytes = std::max<size_t>(rsc::spmm_ws_bytes(A->n_rows, A->nnz, A->n_cols), 256);
     if (hipMalloc(&p->ws, p->ws_bytes) != hipSuccess) {
         (void)hipGetLastError();
@@ -310,6 +339,7 @@ rsc_status_t rsc_spmm_plan_run(rsc_spmm_plan_t *p, const float *B, int32_t d, in
     const rsc_csr_t *A = &p->A;
     RSC_TRY(check_dense(B, A->n_cols, d, ldb, "B"));
     RSC_TRY(check_dense(Y, A->n_rows, d, ldy, "Y"));
+    RSC_TRY(check_same_device(p->device, "plan"));
     bool used = false;
     const hipError_t e = rsc::spmm_launch(A->n_rows, A->n_cols, A->nnz, A->rowptr, p->colf ? p->colf : A->col,
                                           A->val, B, d, ldb, Y, ldy, p->ws, p->ws_bytes, stream, A->nnz, A->n_cols,
@@ -579,6 +609,7 @@ static hipError_t cache_prepare(rsc_cache_t *c, hipStream_t stream) {
 rsc_status_t rsc_cache_score(rsc_cache_t *c, const float *B, int32_t d, int64_t ldb, hipStream_t stream) {
     if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
     RSC_TRY(check_dense(B, c->n, d, ldb, "B"));
+    RSC_TRY(check_same_device(c->device, "cache"));
     RSC_HIP(rsc::pair_scores_launch(c->cn2, B, c->n, d, ldb, c->key, nullptr, c->rn2, stream), "cache scores");
     c->scored = true;
     return RSC_OK;
@@ -588,6 +619,7 @@ rsc_status_t rsc_cache_select(rsc_cache_t *c, int32_t k, int64_t step, hipStream
     if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
     if (k < 0 || k > c->n) return fail(RSC_ERR_INVALID_ARGUMENT, "k = %d outside [0, %d]", k, c->n);
     if (!c->scored) return fail(RSC_ERR_INVALID_ARGUMENT, "cache select before any score");
+    RSC_TRY(check_same_device(c->device, "cache"));
     RSC_HIP(rsc::topk_launch(c->key, c->n, k, c->idx, c->mask, c->ws_topk, stream), "cache topk");
     RSC_HIP(rsc::slice_launch(c->X.n_rows, c->X.n_cols, c->X.nnz, c->X.rowptr, c->X.col, c->X.val, c->mask, c->s_rowptr,
                               c->s_col, c->s_val, c->X.nnz, c->d_nnz, c->ws_slice, stream),
@@ -608,6 +640,7 @@ rsc_status_t rsc_cache_refresh_random(rsc_cache_t *c, const float *B, int32_t d,
     if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
     RSC_TRY(check_dense(B, c->n, d, ldb, "B"));
     if (k_draws < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "k_draws < 0");
+    RSC_TRY(check_same_device(c->device, "cache"));
     RSC_TRY(rsc_cache_score(c, B, d, ldb, stream));
     RSC_HIP(rsc::sample_launch(c->key, c->n, k_draws, seed, c->count, c->colw, c->mask, c->ws_sample, stream),
             "cache sample");
@@ -667,6 +700,7 @@ rsc_status_t rsc_spmm_sampled(rsc_cache_t *c, const float *B, int32_t d, int64_t
     if (c->version == 0) return fail(RSC_ERR_INVALID_ARGUMENT, "cache was never refreshed");
     RSC_TRY(check_dense(B, c->X.n_cols, d, ldb, "B"));
     RSC_TRY(check_dense(Y, c->X.n_rows, d, ldy, "Y"));
+    RSC_TRY(check_same_device(c->device, "cache"));
     // nnz of the full operand bounds the slice's and sizes the long-row list;
     // the expected kept share k/n of the entries and the k kept source rows
     // choose the feature slice (a function of the arguments only, so results
@@ -711,20 +745,16 @@ rsc_status_t rsc_greedy_allocate(int32_t L, int32_t n, int64_t nnz, const uint64
                                  const int32_t *colnnz_host, const int32_t *d_host, double fro_a2,
                                  const double *fro_b2_host, int32_t C_num, int32_t C_den, int32_t alpha_num,
                                  int32_t alpha_den, int32_t *k_out_host, int64_t *budget_out_host) {
-    if (L < 1 || n < 0 || nnz < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "L < 1, n < 0 or nnz < 0");
     if (!key_host || !colnnz_host || !d_host || !fro_b2_host || !k_out_host)
         return fail(RSC_ERR_INVALID_ARGUMENT, "NULL host array");
-    if (C_num < 0 || C_den <= 0 || alpha_num < 0 || alpha_den <= 0)
-        return fail(RSC_ERR_INVALID_ARGUMENT, "bad budget or step fraction");
-    for (int32_t l = 0; l < L; ++l) {
+    int64_t total = 0;
+    RSC_TRY(check_greedy(L, n, nnz, d_host, C_num, C_den, alpha_num, alpha_den, &total));
+    for (int32_t l = 0; l < L; ++l)
         if (!key_host[l]) return fail(RSC_ERR_INVALID_ARGUMENT, "key_host[%d] is NULL", l);
-        if (d_host[l] < 1) return fail(RSC_ERR_INVALID_ARGUMENT, "d[%d] < 1", l);
-    }
     // rank order per layer: (key desc, index asc); contribution sqrt(q) with
     // NaN keys (0) counting 0
     std::vector<std::vector<int32_t>> order(L);
     std::vector<std::vector<double>> contrib(L);
-    int64_t total = 0;
     for (int32_t l = 0; l < L; ++l) {
         const uint64_t *key = key_host[l];
         auto &o = order[l];
@@ -747,10 +777,8 @@ rsc_status_t rsc_greedy_allocate(int32_t L, int32_t n, int64_t nnz, const uint64
             }
         }
         k_out_host[l] = n;
-        total += nnz * (int64_t)d_host[l];
     }
-    int32_t step = (int32_t)(((int64_t)n * alpha_num) / alpha_den);
-    if (step < 1) step = 1;
+    const int32_t step = rsc::greedy_step(n, alpha_num, alpha_den);
     int64_t bud = total;
     while (over_budget(bud, total, C_num, C_den)) {
         int32_t best = -1;
@@ -781,15 +809,15 @@ rsc_status_t rsc_greedy_allocate(int32_t L, int32_t n, int64_t nnz, const uint64
 size_t rsc_greedy_profile_workspace_bytes(int32_t n) { return n < 0 ? 0 : rsc::greedy_profile_ws_bytes(n); }
 
 int32_t rsc_greedy_blocks(int32_t n, int32_t alpha_num, int32_t alpha_den) {
-    if (n < 0 || alpha_num < 0 || alpha_den <= 0) return -1;
+    if (n < 0 || alpha_num < 0 || alpha_den <= 0 || alpha_num > alpha_den) return -1;
     return rsc::greedy_blocks(n, rsc::greedy_step(n, alpha_num, alpha_den));
 }
 
 rsc_status_t rsc_greedy_profile(const uint64_t *key, const int32_t *colnnz, int32_t n, int32_t alpha_num,
                                 int32_t alpha_den, double *mass, int64_t *count, int32_t *order, void *ws,
                                 size_t ws_bytes, hipStream_t stream) {
-    if (n < 0 || alpha_num < 0 || alpha_den <= 0)
-        return fail(RSC_ERR_INVALID_ARGUMENT, "n < 0 or bad step fraction");
+    if (n < 0 || alpha_num < 0 || alpha_den <= 0 || alpha_num > alpha_den)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "n < 0 or bad step fraction (need 0 <= alpha <= 1)");
     if (n > 0 && (!key || !colnnz || !mass || !count))
         return fail(RSC_ERR_INVALID_ARGUMENT, "key/colnnz/mass/count is NULL");
     if (!aligned(key, 8) || !aligned(mass, 8) || !aligned(count, 8) || !aligned(colnnz, 4) || !aligned(order, 4))
@@ -807,21 +835,14 @@ rsc_status_t rsc_greedy_allocate_profiles(int32_t L, int32_t n, int64_t nnz, int
                                           const int64_t *const *count_host, const int32_t *d_host,
                                           double fro_a2, const double *fro_b2_host, int32_t C_num,
                                           int32_t C_den, int32_t *k_out_host, int64_t *budget_out_host) {
-    if (L < 1 || n < 0 || nnz < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "L < 1, n < 0 or nnz < 0");
     if (!mass_host || !count_host || !d_host || !fro_b2_host || !k_out_host)
         return fail(RSC_ERR_INVALID_ARGUMENT, "NULL host array");
-    if (C_num < 0 || C_den <= 0 || alpha_num < 0 || alpha_den <= 0)
-        return fail(RSC_ERR_INVALID_ARGUMENT, "bad budget or step fraction");
-    for (int32_t l = 0; l < L; ++l) {
-        if (!mass_host[l] || !count_host[l]) return fail(RSC_ERR_INVALID_ARGUMENT, "profile %d is NULL", l);
-        if (d_host[l] < 1) return fail(RSC_ERR_INVALID_ARGUMENT, "d[%d] < 1", l);
-    }
-    const int32_t step = rsc::greedy_step(n, alpha_num, alpha_den);
     int64_t total = 0;
-    for (int32_t l = 0; l < L; ++l) {
-        k_out_host[l] = n;
-        total += nnz * (int64_t)d_host[l];
-    }
+    RSC_TRY(check_greedy(L, n, nnz, d_host, C_num, C_den, alpha_num, alpha_den, &total));
+    for (int32_t l = 0; l < L; ++l)
+        if (!mass_host[l] || !count_host[l]) return fail(RSC_ERR_INVALID_ARGUMENT, "profile %d is NULL", l);
+    const int32_t step = rsc::greedy_step(n, alpha_num, alpha_den);
+    for (int32_t l = 0; l < L; ++l) k_out_host[l] = n;
     int64_t bud = total;
     while (over_budget(bud, total, C_num, C_den)) {
         int32_t best = -1;

@@ -187,6 +187,7 @@ __global__ __launch_bounds__(64) void greedy_profile_kernel(const double *__rest
 }  // namespace
 
 int32_t greedy_step(int32_t n, int32_t alpha_num, int32_t alpha_den) {
+    // callers pass 0 <= alpha_num <= alpha_den, so 0 <= s <= n fits int32
     const int64_t s = ((int64_t)n * alpha_num) / alpha_den;
     return (int32_t)std::max<int64_t>(1, s);
 }

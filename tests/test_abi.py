@@ -253,6 +253,26 @@ def test_greedy_budget_comparison_wide_range():
     assert k_lib == k_orc == [0] and b_lib == b_orc
 
 
+def test_greedy_rejects_step_above_n_and_budget_overflow():
+    """alpha is a fraction of the n columns (section 5.1 uses 2 %): above 1 the
+    step n * alpha would not fit int32, so the allocation, the profile's block
+    count and the profile itself refuse it; a full budget sum_l nnz d_l past
+    int64 is refused too."""
+    keys = [np.array([9, 7, 5, 3], np.uint64)]
+    with pytest.raises(rsc.RscError, match="alpha"):
+        rsc.greedy_allocate(keys, np.ones(4, np.int32), 4, [8], 1.0, [1.0], (1, 2), (5, 4))
+    assert rsc.lib().rsc_greedy_blocks(4, 5, 4) == -1
+    assert rsc.lib().rsc_greedy_blocks(4, 4, 4) == 1
+    assert rsc.lib().rsc_greedy_blocks(2**31 - 1, 3, 1) == -1
+    with pytest.raises(rsc.RscError, match="alpha"):
+        rsc.greedy_allocate_profiles([np.zeros(1)], [np.zeros(1, np.int64)], 4, 4, [8], 1.0, [1.0], (1, 2), (3, 1))
+    with pytest.raises(rsc.RscError, match="int64"):
+        rsc.greedy_allocate(keys * 2, np.ones(4, np.int32), 2**40, [2**22, 2**22], 1.0, [1.0, 1.0], (1, 2), (1, 4))
+    # one layer at 2^62 still fits
+    k, _ = rsc.greedy_allocate(keys, np.ones(4, np.int32), 2**40, [2**22], 1.0, [1.0], (1, 1), (1, 4))
+    assert k == [4]
+
+
 def test_greedy_binding_rejects_short_arrays():
     keys = [np.array([9, 7, 5, 3], np.uint64)]
     with pytest.raises(ValueError):
