@@ -28,11 +28,9 @@
  * example with its derivation, and the greedy's invariants; for SpMM_MEAN the
  * dense definition and the appendix example; for the randomized sampler the
  * generator's published outputs, weights re-derived independently, draw
- * frequencies, infinite scores and unbiasedness; for the scaled slice the
- * dense definition.
- * Parity unpinned: the sampler's draw boundary rule (W_i > u rather than >=)
- * decides a draw only when u equals a CDF boundary, which no seeded input
- * reaches.
+ * frequencies, infinite scores, unbiasedness and a draw constructed to fall
+ * exactly on a CDF boundary (the W_i > u rule: column i owns [W_{i-1}, W_i));
+ * for the scaled slice the dense definition.
  */
 #include <math.h>
 #include <stdint.h>

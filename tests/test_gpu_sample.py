@@ -48,6 +48,15 @@ def test_sample_columns_bitwise_full_size():
     assert o["count"].sum() == 215_054
 
 
+def test_sample_draw_on_a_cdf_boundary():
+    """The first draw's u equals the CDF boundary W_0 (the case constructed in
+    the oracle's pins): the device draw lands on column 1, as the oracle's."""
+    from test_oracle_pins import boundary_case
+    key, seed, _ = boundary_case()
+    o = _check(key, 1, seed)
+    assert list(o["count"]) == [0, 1]
+
+
 def test_sample_columns_degenerate():
     n = 5000
     _check(np.zeros(n, np.uint64), 100, 1)                      # nothing to draw

@@ -481,6 +481,35 @@ def test_sample_columns_frequencies():
     np.testing.assert_allclose(p, np.arange(1, 13) / 78.0, rtol=1e-9)
 
 
+def boundary_case(S=38):
+    """Two columns with weights (a, 2^S) and a seed whose first draw has
+    u = floor(z * (a + 2^S) / 2^64) equal to a = W_0, a CDF boundary: the
+    seed is the first whose first output z is below 2^51 (so a < 2^25 and
+    sqrt(q_0) = a 2^-S is exact), a is the fixed point of that floor."""
+    seed = next(s for s in range(1 << 22) if oracle.splitmix64(s, 0) < 1 << 51)
+    z = oracle.splitmix64(seed, 0)
+    a = (z << S) // ((1 << 64) - z)
+    while (z * (a + (1 << S))) >> 64 > a:
+        a += 1
+    while (z * (a + (1 << S))) >> 64 < a:
+        a -= 1
+    assert (z * (a + (1 << S))) >> 64 == a and 0 < a < 1 << 25
+    key = np.array([key_of((a * 2.0 ** -S) ** 2), key_of(1.0)], np.uint64)
+    return key, seed, a
+
+
+def test_sample_draw_on_a_cdf_boundary_goes_to_the_next_column():
+    """With u uniform on the integers [0, total), column i must own exactly
+    w_i of them for p_i = w_i / total (Eq. 3 up to the weights' rounding):
+    [W_{i-1}, W_i). A draw with u = W_0 therefore lands on column 1; the rule
+    'smallest i with W_i >= u' would give column 0 one value too many."""
+    key, seed, a = boundary_case()
+    assert np.array_equal(_weights_by_definition(key), [a, 1 << 38])
+    o = oracle.sample_columns(key, 1, seed)
+    assert list(o["w"]) == [a, 1 << 38]
+    assert list(o["count"]) == [0, 1]
+
+
 def test_slice_scaled_against_dense_definition(small_gen):
     """Scaled slice = dense(A) diag(mask * colw), each value rounded once to
     fp32; unit scales give the plain slice bit for bit, power-of-two scales
