@@ -10,10 +10,10 @@ scored (O4 keys of the fp32-rounded gradients), k_l comes from the greedy of
 section 3.2.1 (O8) and each layer's columns are selected (O5) and sliced (O6).
 Products are scipy sparse / numpy dense in fp64.
 
-Parity unpinned: the dense update (MatMul, ReLU, the loss and its gradient)
-is written from the definitions and checked only through the library
-routines it calls; the aggregation steps it uses (O3-O8) are pinned in
-tests/test_oracle_pins.py.
+Pins (tests/test_oracle_pins.py): the exact-mode gradients against central
+differences of the reported loss, the loss at zero logits (ln 2), and a
+full-budget step between refreshes against the exact gradients; the
+aggregation steps it uses (O3-O8) are pinned there too.
 """
 from __future__ import annotations
 

@@ -569,3 +569,58 @@ def test_sampled_product_is_unbiased():
     err_mean = np.linalg.norm(acc / seeds - exact)
     err_one = np.linalg.norm(one - exact)
     assert err_mean < 0.2 * err_one
+
+
+# ---------------------------------------------------------------- GCN reference step
+def _gcn_problem():
+    A = synth.erdos_renyi(40, 0.15, seed=3)
+    rng = np.random.default_rng(0)
+    n, f, h, c = A.n, 5, 4, 3
+    X = rng.standard_normal((n, f))
+    W1, W2 = rng.standard_normal((f, h)), rng.standard_normal((h, c))
+    Y = (rng.random((n, c)) < 0.5).astype(np.float64)
+    return A, X, W1, W2, Y, [h, c]
+
+
+def test_gcn_reference_gradients_are_the_loss_derivatives():
+    """The reference step's exact backward (a refresh step) gives the
+    derivatives of the loss its forward reports: central differences in fp64
+    agree. A dropped term, a transposed operand or a wrong ReLU mask in the
+    backward fails this; at zero logits the mean binary cross-entropy with
+    logits is ln 2 whatever the labels."""
+    from oracle.gcn_ref import RscReference
+    A, X, W1, W2, Y, widths = _gcn_problem()
+
+    def run(w1, w2):
+        ref = RscReference(A.rowptr, A.col, A.val, A.n, widths, (1, 2), (1, 4), 10)
+        return ref.step(X, w1, w2, Y, 0)
+
+    out = run(W1, W2)
+    assert out["mode"] == "score"
+    eps = 1e-6
+    for which, W in ((0, W1), (1, W2)):
+        num = np.zeros_like(W)
+        for ij in np.ndindex(W.shape):
+            Wp, Wm = W.copy(), W.copy()
+            Wp[ij] += eps
+            Wm[ij] -= eps
+            lp = run(Wp, W2)["loss"] if which == 0 else run(W1, Wp)["loss"]
+            lm = run(Wm, W2)["loss"] if which == 0 else run(W1, Wm)["loss"]
+            num[ij] = (lp - lm) / (2 * eps)
+        np.testing.assert_allclose(out["gW1" if which == 0 else "gW2"], num, rtol=1e-5, atol=1e-9)
+    assert abs(run(W1, np.zeros_like(W2))["loss"] - np.log(2.0)) < 1e-15
+
+
+def test_gcn_reference_full_budget_slices_give_the_exact_backward():
+    """With the budget C = 1 the greedy keeps every column (k_l = n), so the
+    cached slices are the whole operand and a step between refreshes has the
+    exact gradients."""
+    from oracle.gcn_ref import RscReference
+    A, X, W1, W2, Y, widths = _gcn_problem()
+    ref = RscReference(A.rowptr, A.col, A.val, A.n, widths, (1, 1), (1, 4), 10)
+    exact = ref.step(X, W1, W2, Y, 0)
+    sampled = ref.step(X, W1, W2, Y, 1)
+    assert exact["mode"] == "score" and sampled["mode"] == "sampled"
+    assert exact["k"] == [A.n, A.n]
+    for g in ("gW1", "gW2"):
+        np.testing.assert_allclose(sampled[g], exact[g], rtol=1e-14, atol=0)
