@@ -174,3 +174,38 @@ def test_cache_prepared_list_survives_switches(switch):
         seen[v] = Ys
     assert torch.equal(seen[values[0]], first)
     cache.close()
+
+
+def test_whole_chain_on_a_side_stream_matches_the_current_stream():
+    """Every call enqueues on the stream it is given: plan creation and runs,
+    the cache's creation, refresh, slice read-back and sampled product, all
+    issued inside a side stream, give the same bits as on the default stream
+    (a launch or copy on another stream would race with the producer of B
+    here, which is enqueued just before on the same stream)."""
+    A = synth.make_graph("tiny", 0)
+    d, k = 64, 1500
+
+    def chain():
+        X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, A.n)
+        H0 = torch.from_numpy(synth.dense_normal(A.n, d, seed=4)).cuda()
+        plan = rsc.SpmmPlan(X)
+        cache = rsc.Cache(X, X, refresh_interval=10)
+        H = H0 * 2.0 - 1.0                 # produced on this stream right before use
+        Y = plan.run(H)
+        cache.refresh(H, k, step=0)
+        nnz = cache.get(0)["slice"].nnz
+        Yb = cache.spmm_sampled(H)
+        out = (Y.cpu().numpy(), Yb.cpu().numpy(), nnz)
+        plan.close()
+        cache.close()
+        return out
+
+    ref = chain()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        got = chain()
+    torch.cuda.current_stream().wait_stream(side)
+    assert got[2] == ref[2]
+    assert np.array_equal(got[0].view(np.uint32), ref[0].view(np.uint32))
+    assert np.array_equal(got[1].view(np.uint32), ref[1].view(np.uint32))
