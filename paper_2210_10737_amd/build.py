@@ -22,7 +22,7 @@ FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     # packed fp32 instructions are disabled for all device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    "-Wall", "-Wshadow", "-Wno-unused-function",
+    "-Wall", "-Wextra", "-Wshadow",
     f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}",
 ]
 
