@@ -152,6 +152,100 @@ def cpu_baseline(A, Hh, Gh, k, pct, refresh_interval, step_bytes_full, n_rows_sa
     }
 
 
+ROCSPARSE = "/opt/rocm/lib/librocsparse.so"
+
+
+def vendor_baseline(X, H, Y, plan, reps: int = 10):
+    """The vendor library's sparse-dense product on the same operands as the
+    exact SpMM, timed beside it (context, like the CPU baseline; the product
+    path never calls it): rocsparse_spmm on the CSR (int32 indices, fp32),
+    row-major B and C, the preprocess stage run before timing, with the
+    library's default CSR algorithm and its nnz-split one. Returns None when
+    the library cannot be loaded."""
+    import ctypes
+    import statistics
+
+    import torch
+    try:
+        L = ctypes.CDLL(ROCSPARSE)
+    except OSError:
+        return None
+    vp, i64 = ctypes.c_void_p, ctypes.c_int64
+    # enumerator values of the rocSPARSE C API
+    OP_NONE, IDX_I32, BASE_ZERO, F32, ORDER_ROW = 111, 2, 0, 151, 0
+    STAGE_BUFFER, STAGE_PREPROCESS, STAGE_COMPUTE = 1, 2, 3
+    algs = {"default": 0, "csr_nnz_split": 5}
+
+    def median_ms(fn):
+        for _ in range(2):
+            fn()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return statistics.median(ts)
+
+    n, d = X.n_rows, H.shape[1]
+    out = {"library": "rocSPARSE", "call": "rocsparse_spmm, CSR int32 / fp32, row-major B and C",
+           "ours_ms": round(median_ms(lambda: plan.run(H, out=Y)), 4), "algorithms": {}}
+    C = torch.empty((n, d), dtype=torch.float32, device="cuda")
+    h, mA, mB, mC = vp(), vp(), vp(), vp()
+    if L.rocsparse_create_handle(ctypes.byref(h)) != 0:
+        return None
+    try:
+        ver = ctypes.c_int(0)
+        L.rocsparse_get_version(h, ctypes.byref(ver))
+        out["version"] = f"{ver.value // 100000}.{ver.value // 100 % 1000}.{ver.value % 100}"
+        st = L.rocsparse_set_stream(h, vp(torch.cuda.current_stream().cuda_stream))
+        st = st or L.rocsparse_create_csr_descr(ctypes.byref(mA), i64(n), i64(X.n_cols), i64(X.nnz),
+                                                vp(X.rowptr.data_ptr()), vp(X.col.data_ptr()),
+                                                vp(X.val.data_ptr()), IDX_I32, IDX_I32, BASE_ZERO, F32)
+        st = st or L.rocsparse_create_dnmat_descr(ctypes.byref(mB), i64(X.n_cols), i64(d), i64(H.stride(0)),
+                                                  vp(H.data_ptr()), F32, ORDER_ROW)
+        st = st or L.rocsparse_create_dnmat_descr(ctypes.byref(mC), i64(n), i64(d), i64(d), vp(C.data_ptr()),
+                                                  F32, ORDER_ROW)
+        if st != 0:
+            out["error"] = f"descriptor setup: rocSPARSE status {st}"
+            return out
+        alpha, beta = ctypes.c_float(1.0), ctypes.c_float(0.0)
+        for name, alg in algs.items():
+            size = ctypes.c_size_t(0)
+
+            def call(stage, buf):
+                return L.rocsparse_spmm(h, OP_NONE, OP_NONE, ctypes.byref(alpha), mA, mB, ctypes.byref(beta), mC,
+                                        F32, alg, stage, ctypes.byref(size), buf)
+
+            st = call(STAGE_BUFFER, None)
+            buf = torch.empty(max(size.value, 256), dtype=torch.uint8, device="cuda")
+            st = st or call(STAGE_PREPROCESS, vp(buf.data_ptr()))
+            st = st or call(STAGE_COMPUTE, vp(buf.data_ptr()))
+            if st != 0:
+                out["algorithms"][name] = {"error": f"rocSPARSE status {st}"}
+                continue
+            torch.cuda.synchronize()
+            diff = float((C - Y).abs().max() / Y.abs().max().clamp_min(1e-30))
+            ms = median_ms(lambda: call(STAGE_COMPUTE, vp(buf.data_ptr())))
+            out["algorithms"][name] = {"ms": round(ms, 4), "buffer_bytes": size.value,
+                                       "max_abs_diff_over_max_abs": diff}
+            del buf
+        best = min((a["ms"] for a in out["algorithms"].values() if "ms" in a), default=None)
+        out["vendor_best_over_ours"] = None if best is None else round(best / out["ours_ms"], 3)
+        return out
+    finally:
+        torch.cuda.synchronize()
+        if mA.value:
+            L.rocsparse_destroy_spmat_descr(mA)
+        for m in (mB, mC):
+            if m.value:
+                L.rocsparse_destroy_dnmat_descr(m)
+        L.rocsparse_destroy_handle(h)
+        del C
+
+
 def parity_check(A, Hh, Gh, k, Y, Yb, kept, n_rows, seed):
     """The benchmarked outputs against the oracle: the kept columns bit for
     bit, and the exact and sampled products on a seeded sample of rows
@@ -340,6 +434,8 @@ def main() -> int:
                          "the oracle (0 = skip)")
     ap.add_argument("--cold-reps", type=int, default=5,
                     help="after the timed steps, repetitions of each op that follow a 1 GiB cache flush")
+    ap.add_argument("--no-vendor-baseline", action="store_true",
+                    help="skip timing the vendor library's SpMM (rocSPARSE) on the exact product's operands")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB once (a plain copy of known "
                          "size, so hardware byte counters can be scaled)")
@@ -607,6 +703,7 @@ def main() -> int:
     if traffic is not None:
         out["roofline"]["traffic"] = round(traffic["total_bytes"])
         out["roofline"]["traffic_detail"] = traffic
+    out["vendor_baseline"] = None if args.no_vendor_baseline else vendor_baseline(X, H, Y, plan)
     cache.close()
     plan.close()
     del X, XB, XT, H, G, Y, Yb, plan

@@ -168,7 +168,13 @@ def _check(status: int) -> None:
 
 
 def _stream() -> int:
-    return torch.cuda.current_stream().cuda_stream
+    """The current HIP stream of the current device, as a raw handle. torch's
+    raw-stream getter costs ~0.1 us per call against ~3 us for building a
+    torch.cuda.Stream object, which matters for launch-bound products."""
+    try:
+        return torch._C._cuda_getCurrentRawStream(torch._C._cuda_getDevice())
+    except AttributeError:
+        return torch.cuda.current_stream().cuda_stream
 
 
 def _ptr(t: torch.Tensor | None) -> int | None:

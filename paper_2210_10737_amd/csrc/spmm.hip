@@ -17,9 +17,10 @@
 //     blocks: the waves take interleaved runs of 64 entries and their fp64
 //     sums are combined in LDS in fixed wave order. No float atomics, so the
 //     result is bitwise reproducible;
-//   * B may be processed in feature slices of 16..128 floats (several passes,
-//     several entries per load instruction) when the slice of the referenced
-//     B rows gets close to cache size;
+//   * features up to 128 wide take a layout of 16..128 floats (several
+//     entries per load instruction), and B may be processed in several such
+//     feature slices when the slice of the referenced B rows gets close to
+//     cache size;
 //   * on graphs with long rows on average, rows are taken longest length
 //     class first (a scheduling order only);
 //   * when the referenced B rows span a few L2-sized ranges, the columns are
@@ -183,7 +184,10 @@ __device__ __forceinline__ void accumulate_runs(const int32_t *__restrict__ col,
         } else {
             static_assert(NV == 1, "sliced layouts hold one float4 per lane");
             constexpr int kSteps = kWave / G;  // steps that cover the 64-entry run
-#pragma unroll
+            // one window of kUnroll steps at a time: unrolling the step loop
+            // too keeps every window's (col, val) live at once (130 VGPRs for
+            // G = 2) and costs occupancy
+#pragma unroll 1
             for (int t0 = 0; t0 < kSteps; t0 += kUnroll) {
                 if (t0 * G >= cnt) break;  // wave-uniform
                 float4 b[kUnroll];
@@ -554,20 +558,24 @@ size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz, int32_t n_cols) {
 int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) {
     // Feature-slice width (floats) of one pass. Slices of 16/32/64/128 use
     // 4/8/16/32 lanes per gathered entry; 256 (512 for d > 256) is one pass.
-    // Gathers are limited by the rate of L2-miss requests, so a narrower slice
-    // pays off when the slice of the referenced B rows comes close to L2 size
-    // and rows are long enough to amortise the extra passes over rowptr/col/val.
+    // Features up to 128 wide take the narrowest layout that holds them in one
+    // pass (several entries per load instruction instead of idle lanes).
+    // Gathers are limited by the rate of L2-miss requests, so several narrower
+    // passes pay off when the slice of the referenced B rows comes close to L2
+    // size and rows are long enough to amortise the extra passes over
+    // rowptr/col/val; only for widths of whole 128-byte lines (d % 32 == 0),
+    // since a slice that straddles lines doubles the requests.
     if (const char *env = getenv("RSC_SPMM_SLICE")) {
         const int v = atoi(env);
         if (v == 16 || v == 32 || v == 64 || v == 128) return v;
         if (v == 256 || v == 512) return d > 256 ? 512 : 256;
     }
-    const int32_t full = d > 256 ? 512 : 256;
-    if (d <= 32 || n_rows <= 0 || nnz < 128LL * n_rows) return full;
+    const int32_t fit = d <= 16 ? 16 : d <= 32 ? 32 : d <= 64 ? 64 : d <= 128 ? 128 : d <= 256 ? 256 : 512;
+    if (d <= 32 || d % 32 != 0 || n_rows <= 0 || nnz < 128LL * n_rows) return fit;
     const double mib = 1024.0 * 1024.0;
     const double ws32 = (double)n_src * 32 * 4 / mib, ws64 = 2 * ws32;
-    if (ws32 > 64.0) return full;
-    if (ws64 <= 30.0 && ws32 > 8.0) return 64;
+    if (ws32 > 64.0) return fit;
+    if (ws64 <= 30.0 && ws32 > 8.0) return std::min(64, fit);
     return 32;
 }
 
