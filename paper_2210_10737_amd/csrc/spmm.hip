@@ -184,16 +184,17 @@ __device__ __forceinline__ void accumulate_runs(const int32_t *__restrict__ col,
         } else {
             static_assert(NV == 1, "sliced layouts hold one float4 per lane");
             constexpr int kSteps = kWave / G;  // steps that cover the 64-entry run
+            constexpr int kWin = G >= 8 ? 4 : kUnroll;  // steps per window (gathers in flight)
             // one window of kUnroll steps at a time: unrolling the step loop
             // too keeps every window's (col, val) live at once (130 VGPRs for
             // G = 2) and costs occupancy
 #pragma unroll 1
-            for (int t0 = 0; t0 < kSteps; t0 += kUnroll) {
+            for (int t0 = 0; t0 < kSteps; t0 += kWin) {
                 if (t0 * G >= cnt) break;  // wave-uniform
-                float4 b[kUnroll];
-                float v[kUnroll];
+                float4 b[kWin];
+                float v[kWin];
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u) {
+                for (int u = 0; u < kWin; ++u) {
                     const int j = (t0 + u) * G + g;  // entry of this group within the run
                     const int32_t cf = __shfl(my_c, j & (kWave - 1));
                     const int32_t c = cf & kColMask;
@@ -207,7 +208,7 @@ __device__ __forceinline__ void accumulate_runs(const int32_t *__restrict__ col,
                     }
                 }
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u) {
+                for (int u = 0; u < kWin; ++u) {
                     a[0][0] = fmaf(v[u], b[u].x, a[0][0]);
                     a[0][1] = fmaf(v[u], b[u].y, a[0][1]);
                     a[0][2] = fmaf(v[u], b[u].z, a[0][2]);
