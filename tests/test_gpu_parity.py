@@ -60,7 +60,7 @@ def _gpu(gpu):
 
 
 # ------------------------------------------------------------------ SpMM
-SPMM_D = [1, 3, 4, 64, 100, 256, 300, 512, 600, 1030]
+SPMM_D = [1, 3, 4, 16, 17, 32, 48, 64, 65, 100, 128, 129, 256, 300, 512, 600, 1030]
 
 
 @pytest.fixture(scope="module")
