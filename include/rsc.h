@@ -98,10 +98,12 @@ rsc_status_t rsc_csr_validate(const rsc_csr_t *A, int64_t *bad_row_host, hipStre
  *   Y: n_rows x d, leading dimension ldy; every row is written (empty rows
  *      get zeros).
  * Accumulation: fp32 over runs of at most 64 consecutive entries, folded
- * into fp64; one rounding to fp32 per output. The features may be processed
- * in several passes of 32/64 columns of B (chosen from n_rows, nnz, n_cols
- * and d only, with the environment variable RSC_SPMM_SLICE = 16/32/64/128/256
- * as an override); the pass layout sets the summation order. Rows may be
+ * into fp64; one rounding to fp32 per output. Features up to 128 wide take
+ * a lane layout that gathers several entries per load, and the features may
+ * be processed in several passes of 32/64 columns of B (both chosen from
+ * n_rows, nnz, n_cols and d only, with the environment variable
+ * RSC_SPMM_SLICE = 16/32/64/128/256 as an override); the layout sets the
+ * summation order. Rows may be
  * taken longest first (when rows are long on average; RSC_SPMM_ORDER = 0/1
  * overrides), which never changes a result. Column-blocked mode: when a
  * 64-float slice of B spans 2..8 ranges of about 4.5 MiB and rows hold at
