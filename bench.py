@@ -15,11 +15,12 @@ measured step time, in GB/s. `roofline` describes the dominant kernel (the
 exact SpMM): algorithmic bytes per launch over its average duration measured
 with HIP events on the stream the kernels run on, against the 8 TB/s HBM
 peak. `cpu_baseline` times the oracle (all its OpenMP threads) on a bounded
-sample of the same step.
+sample of the same step. `vendor_baseline` times rocSPARSE's SpMM on the
+exact product's operands beside the library's (context only).
 
 usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload copurchase]
                        [--budget-pct 30] [--aggregator gcn|mean] [--selector topk|random]
-                       [--no-cpu-baseline]
+                       [--no-cpu-baseline] [--no-vendor-baseline]
        python bench.py --workload gcn2-train [--budget-pct 10]   (training-step comparison)
 """
 from __future__ import annotations
