@@ -10,7 +10,8 @@
 //     coalesced, non-temporal load and broadcast from the owning lane with
 //     v_readlane into scalar registers, so each gathered B row is addressed
 //     by a scalar base plus the lane offset;
-//   * 8 gathers are issued before their FMAs for memory-level parallelism;
+//   * 8 gather instructions (4 in the layouts that take 8 or 16 entries per
+//     instruction) are issued before their FMAs for memory-level parallelism;
 //   * products are accumulated in fp32 over each run of <= 64 entries and the
 //     run sum is folded into an fp64 accumulator; one fp32 rounding per output;
 //   * rows with more than kLongRow entries are taken by persistent 8-wave
