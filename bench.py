@@ -156,6 +156,91 @@ def cpu_baseline(A, Hh, Gh, k, pct, refresh_interval, step_bytes_full, n_rows_sa
 ROCSPARSE = "/opt/rocm/lib/librocsparse.so"
 
 
+class RocsparseSpmm:
+    """rocSPARSE's generic SpMM (rocsparse_spmm) set up on one CSR operand X
+    (int32 indices, fp32) and one row-major dense B: run(alg) writes
+    C = X B into a row-major n_rows x d tensor, after the algorithm's
+    preprocess stage. The vendor library, used as a timing baseline and a
+    cross-check only; raises OSError when the library cannot be loaded and
+    RuntimeError on a rocSPARSE error status."""
+
+    # enumerator values of the rocSPARSE C API
+    OP_NONE, IDX_I32, BASE_ZERO, F32, ORDER_ROW = 111, 2, 0, 151, 0
+    STAGE_BUFFER, STAGE_PREPROCESS, STAGE_COMPUTE = 1, 2, 3
+    ALGS = {"default": 0, "csr_nnz_split": 5}
+
+    def __init__(self, X, B):
+        import ctypes
+
+        import torch
+        self.ct, self.torch = ctypes, torch
+        self.L = ctypes.CDLL(ROCSPARSE)
+        vp, i64 = ctypes.c_void_p, ctypes.c_int64
+        self.h, self.mA, self.mB, self.mC = vp(), vp(), vp(), vp()
+        self.C = torch.empty((X.n_rows, B.shape[1]), dtype=torch.float32, device=B.device)
+        self._check(self.L.rocsparse_create_handle(ctypes.byref(self.h)), "create handle")
+        try:
+            ver = ctypes.c_int(0)
+            self.L.rocsparse_get_version(self.h, ctypes.byref(ver))
+            self.version = f"{ver.value // 100000}.{ver.value // 100 % 1000}.{ver.value % 100}"
+            self._check(self.L.rocsparse_set_stream(self.h, vp(torch.cuda.current_stream().cuda_stream)), "stream")
+            self._check(self.L.rocsparse_create_csr_descr(
+                ctypes.byref(self.mA), i64(X.n_rows), i64(X.n_cols), i64(X.nnz), vp(X.rowptr.data_ptr()),
+                vp(X.col.data_ptr()), vp(X.val.data_ptr()), self.IDX_I32, self.IDX_I32, self.BASE_ZERO, self.F32),
+                "CSR descriptor")
+            self._check(self.L.rocsparse_create_dnmat_descr(
+                ctypes.byref(self.mB), i64(X.n_cols), i64(B.shape[1]), i64(B.stride(0)), vp(B.data_ptr()), self.F32,
+                self.ORDER_ROW), "B descriptor")
+            self._check(self.L.rocsparse_create_dnmat_descr(
+                ctypes.byref(self.mC), i64(X.n_rows), i64(B.shape[1]), i64(B.shape[1]), vp(self.C.data_ptr()),
+                self.F32, self.ORDER_ROW), "C descriptor")
+        except RuntimeError:
+            self.close()
+            raise
+        self.alpha, self.beta = ctypes.c_float(1.0), ctypes.c_float(0.0)
+        self.bufs, self.sizes = {}, {}
+
+    @staticmethod
+    def _check(status, what):
+        if status != 0:
+            raise RuntimeError(f"rocSPARSE {what}: status {status}")
+
+    def _call(self, alg, stage, buf):
+        ct = self.ct
+        size = ct.c_size_t(0)
+        st = self.L.rocsparse_spmm(self.h, self.OP_NONE, self.OP_NONE, ct.byref(self.alpha), self.mA, self.mB,
+                                   ct.byref(self.beta), self.mC, self.F32, self.ALGS[alg], stage, ct.byref(size),
+                                   buf)
+        return st, size.value
+
+    def prepare(self, alg):
+        """Buffer and preprocess stages of one algorithm (once per algorithm)."""
+        if alg not in self.bufs:
+            st, size = self._call(alg, self.STAGE_BUFFER, None)
+            self._check(st, "buffer size")
+            buf = self.torch.empty(max(size, 256), dtype=self.torch.uint8, device=self.C.device)
+            self._check(self._call(alg, self.STAGE_PREPROCESS, self.ct.c_void_p(buf.data_ptr()))[0], "preprocess")
+            self.bufs[alg], self.sizes[alg] = buf, size
+        return self.sizes[alg]
+
+    def run(self, alg="csr_nnz_split"):
+        self.prepare(alg)
+        self._check(self._call(alg, self.STAGE_COMPUTE, self.ct.c_void_p(self.bufs[alg].data_ptr()))[0], "compute")
+        return self.C
+
+    def close(self):
+        self.torch.cuda.synchronize()
+        if self.mA.value:
+            self.L.rocsparse_destroy_spmat_descr(self.mA)
+        for m in (self.mB, self.mC):
+            if m.value:
+                self.L.rocsparse_destroy_dnmat_descr(m)
+        if self.h.value:
+            self.L.rocsparse_destroy_handle(self.h)
+        self.h, self.mA, self.mB, self.mC = (self.ct.c_void_p() for _ in range(4))
+        self.bufs.clear()
+
+
 def vendor_baseline(X, H, Y, plan, reps: int = 10):
     """The vendor library's sparse-dense product on the same operands as the
     exact SpMM, timed beside it (context, like the CPU baseline; the product
@@ -163,19 +248,9 @@ def vendor_baseline(X, H, Y, plan, reps: int = 10):
     row-major B and C, the preprocess stage run before timing, with the
     library's default CSR algorithm and its nnz-split one. Returns None when
     the library cannot be loaded."""
-    import ctypes
     import statistics
 
     import torch
-    try:
-        L = ctypes.CDLL(ROCSPARSE)
-    except OSError:
-        return None
-    vp, i64 = ctypes.c_void_p, ctypes.c_int64
-    # enumerator values of the rocSPARSE C API
-    OP_NONE, IDX_I32, BASE_ZERO, F32, ORDER_ROW = 111, 2, 0, 151, 0
-    STAGE_BUFFER, STAGE_PREPROCESS, STAGE_COMPUTE = 1, 2, 3
-    algs = {"default": 0, "csr_nnz_split": 5}
 
     def median_ms(fn):
         for _ in range(2):
@@ -190,61 +265,34 @@ def vendor_baseline(X, H, Y, plan, reps: int = 10):
             ts.append(e0.elapsed_time(e1))
         return statistics.median(ts)
 
-    n, d = X.n_rows, H.shape[1]
-    out = {"library": "rocSPARSE", "call": "rocsparse_spmm, CSR int32 / fp32, row-major B and C",
-           "ours_ms": round(median_ms(lambda: plan.run(H, out=Y)), 4), "algorithms": {}}
-    C = torch.empty((n, d), dtype=torch.float32, device="cuda")
-    h, mA, mB, mC = vp(), vp(), vp(), vp()
-    if L.rocsparse_create_handle(ctypes.byref(h)) != 0:
-        return None
+    ours = median_ms(lambda: plan.run(H, out=Y))
     try:
-        ver = ctypes.c_int(0)
-        L.rocsparse_get_version(h, ctypes.byref(ver))
-        out["version"] = f"{ver.value // 100000}.{ver.value // 100 % 1000}.{ver.value % 100}"
-        st = L.rocsparse_set_stream(h, vp(torch.cuda.current_stream().cuda_stream))
-        st = st or L.rocsparse_create_csr_descr(ctypes.byref(mA), i64(n), i64(X.n_cols), i64(X.nnz),
-                                                vp(X.rowptr.data_ptr()), vp(X.col.data_ptr()),
-                                                vp(X.val.data_ptr()), IDX_I32, IDX_I32, BASE_ZERO, F32)
-        st = st or L.rocsparse_create_dnmat_descr(ctypes.byref(mB), i64(X.n_cols), i64(d), i64(H.stride(0)),
-                                                  vp(H.data_ptr()), F32, ORDER_ROW)
-        st = st or L.rocsparse_create_dnmat_descr(ctypes.byref(mC), i64(n), i64(d), i64(d), vp(C.data_ptr()),
-                                                  F32, ORDER_ROW)
-        if st != 0:
-            out["error"] = f"descriptor setup: rocSPARSE status {st}"
-            return out
-        alpha, beta = ctypes.c_float(1.0), ctypes.c_float(0.0)
-        for name, alg in algs.items():
-            size = ctypes.c_size_t(0)
-
-            def call(stage, buf):
-                return L.rocsparse_spmm(h, OP_NONE, OP_NONE, ctypes.byref(alpha), mA, mB, ctypes.byref(beta), mC,
-                                        F32, alg, stage, ctypes.byref(size), buf)
-
-            st = call(STAGE_BUFFER, None)
-            buf = torch.empty(max(size.value, 256), dtype=torch.uint8, device="cuda")
-            st = st or call(STAGE_PREPROCESS, vp(buf.data_ptr()))
-            st = st or call(STAGE_COMPUTE, vp(buf.data_ptr()))
-            if st != 0:
-                out["algorithms"][name] = {"error": f"rocSPARSE status {st}"}
+        v = RocsparseSpmm(X, H)
+    except OSError:
+        return None
+    except RuntimeError as e:
+        return {"library": "rocSPARSE", "error": str(e)}
+    out = {"library": "rocSPARSE", "version": v.version,
+           "call": "rocsparse_spmm, CSR int32 / fp32, row-major B and C", "ours_ms": round(ours, 4),
+           "algorithms": {}}
+    try:
+        for alg in RocsparseSpmm.ALGS:
+            try:
+                buf_bytes = v.prepare(alg)
+                C = v.run(alg)
+                torch.cuda.synchronize()
+                diff = float((C - Y).abs().max() / Y.abs().max().clamp_min(1e-30))
+                ms = median_ms(lambda: v.run(alg))
+            except RuntimeError as e:
+                out["algorithms"][alg] = {"error": str(e)}
                 continue
-            torch.cuda.synchronize()
-            diff = float((C - Y).abs().max() / Y.abs().max().clamp_min(1e-30))
-            ms = median_ms(lambda: call(STAGE_COMPUTE, vp(buf.data_ptr())))
-            out["algorithms"][name] = {"ms": round(ms, 4), "buffer_bytes": size.value,
-                                       "max_abs_diff_over_max_abs": diff}
-            del buf
-        best = min((a["ms"] for a in out["algorithms"].values() if "ms" in a), default=None)
-        out["vendor_best_over_ours"] = None if best is None else round(best / out["ours_ms"], 3)
-        return out
+            out["algorithms"][alg] = {"ms": round(ms, 4), "buffer_bytes": buf_bytes,
+                                      "max_abs_diff_over_max_abs": diff}
     finally:
-        torch.cuda.synchronize()
-        if mA.value:
-            L.rocsparse_destroy_spmat_descr(mA)
-        for m in (mB, mC):
-            if m.value:
-                L.rocsparse_destroy_dnmat_descr(m)
-        L.rocsparse_destroy_handle(h)
-        del C
+        v.close()
+    best = min((a["ms"] for a in out["algorithms"].values() if "ms" in a), default=None)
+    out["vendor_best_over_ours"] = None if best is None else round(best / ours, 3)
+    return out
 
 
 def parity_check(A, Hh, Gh, k, Y, Yb, kept, n_rows, seed):
