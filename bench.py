@@ -174,6 +174,7 @@ class RocsparseSpmm:
 
         import torch
         self.ct, self.torch = ctypes, torch
+        self.X, self.B = X, B   # the descriptors hold raw pointers: keep the tensors alive
         self.L = ctypes.CDLL(ROCSPARSE)
         vp, i64 = ctypes.c_void_p, ctypes.c_int64
         self.h, self.mA, self.mB, self.mC = vp(), vp(), vp(), vp()
@@ -239,6 +240,7 @@ class RocsparseSpmm:
             self.L.rocsparse_destroy_handle(self.h)
         self.h, self.mA, self.mB, self.mC = (self.ct.c_void_p() for _ in range(4))
         self.bufs.clear()
+        self.X = self.B = None
 
 
 def vendor_baseline(X, H, Y, plan, reps: int = 10):
