@@ -177,8 +177,25 @@ def _stream() -> int:
         return torch.cuda.current_stream().cuda_stream
 
 
+def _device_index() -> int:
+    try:
+        return torch._C._cuda_getDevice()
+    except AttributeError:
+        return torch.cuda.current_device()
+
+
+def _dp(t: torch.Tensor) -> int:
+    """Device address of a tensor that lives on the current GPU (the library
+    launches on the current device's stream, so a host tensor or one on
+    another GPU would hand the kernels an address they cannot use)."""
+    dev = t.device
+    if dev.type != "cuda" or dev.index != _device_index():
+        raise ValueError(f"tensor on {dev}: the library runs on the current device cuda:{_device_index()}")
+    return t.data_ptr()
+
+
 def _ptr(t: torch.Tensor | None) -> int | None:
-    return None if t is None else t.data_ptr()
+    return None if t is None else _dp(t)
 
 
 def _ld(t: torch.Tensor) -> int:
@@ -220,9 +237,9 @@ class DeviceCsr:
         return cls(len(rowptr) - 1, int(n_cols), rp, c, v)
 
     def struct(self) -> CsrStruct:
-        return CsrStruct(self.n_rows, self.n_cols, self.nnz, self.rowptr.data_ptr(),
-                         self.col.data_ptr() if self.nnz else None,
-                         self.val.data_ptr() if self.nnz else None)
+        return CsrStruct(self.n_rows, self.n_cols, self.nnz, _dp(self.rowptr),
+                         _dp(self.col) if self.nnz else None,
+                         _dp(self.val) if self.nnz else None)
 
 
 # ---------------------------------------------------------------- A1
@@ -238,8 +255,8 @@ def spmm(A: DeviceCsr, B: torch.Tensor, d: int | None = None, out: torch.Tensor 
     s = A.struct()
     need = lib().rsc_spmm_workspace_bytes(ctypes.byref(s))
     ws = _workspace(need, B.device) if ws is None else ws
-    _check(lib().rsc_spmm(ctypes.byref(s), B.data_ptr(), d, _ld(B), Y.data_ptr(), _ld(Y),
-                          ws.data_ptr(), ws.numel(), _stream()))
+    _check(lib().rsc_spmm(ctypes.byref(s), _dp(B), d, _ld(B), _dp(Y), _ld(Y),
+                          _dp(ws), ws.numel(), _stream()))
     return Y
 
 
@@ -258,7 +275,7 @@ class SpmmPlan:
     def run(self, B: torch.Tensor, d: int | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
         d = B.shape[1] if d is None else d
         Y = _new_out(self.A.n_rows, d, B.device) if out is None else out
-        _check(lib().rsc_spmm_plan_run(self._h, B.data_ptr(), d, _ld(B), Y.data_ptr(), _ld(Y), _stream()))
+        _check(lib().rsc_spmm_plan_run(self._h, _dp(B), d, _ld(B), _dp(Y), _ld(Y), _stream()))
         return Y
 
     def close(self) -> None:
@@ -278,7 +295,7 @@ def degree_scale(A: DeviceCsr, by_column: bool = False, deg_rowptr: torch.Tensor
     M^T and deg_rowptr = M's rowptr, M^T D^-1 (by_column=True)."""
     out = torch.empty_like(A.val)
     _check(lib().rsc_degree_scale(ctypes.byref(A.struct()), _ptr(deg_rowptr), 1 if by_column else 0,
-                                  out.data_ptr() if A.nnz else None, _stream()))
+                                  _dp(out) if A.nnz else None, _stream()))
     return DeviceCsr(A.n_rows, A.n_cols, A.rowptr, A.col, out, nnz=A.nnz)
 
 
@@ -287,7 +304,7 @@ def col_sqnorms(XT: DeviceCsr):
     """(cn2 float64[n], colnnz int32[n]) from the CSR of X^T."""
     cn2 = torch.empty(XT.n_rows, dtype=torch.float64, device=XT.rowptr.device)
     colnnz = torch.empty(XT.n_rows, dtype=torch.int32, device=XT.rowptr.device)
-    _check(lib().rsc_col_sqnorms(ctypes.byref(XT.struct()), cn2.data_ptr(), colnnz.data_ptr(), _stream()))
+    _check(lib().rsc_col_sqnorms(ctypes.byref(XT.struct()), _dp(cn2), _dp(colnnz), _stream()))
     return cn2, colnnz
 
 
@@ -301,7 +318,7 @@ def pair_scores(cn2: torch.Tensor, B: torch.Tensor, d: int | None = None, with_s
     key = torch.empty(n, dtype=torch.int64, device=B.device)
     score = torch.empty(n, dtype=torch.float32, device=B.device) if with_score else None
     rn2 = torch.empty(n, dtype=torch.float64, device=B.device) if with_rn2 else None
-    _check(lib().rsc_pair_scores(cn2.data_ptr(), B.data_ptr(), n, d, _ld(B), key.data_ptr(),
+    _check(lib().rsc_pair_scores(_dp(cn2), _dp(B), n, d, _ld(B), _dp(key),
                                  _ptr(score), _ptr(rn2), _stream()))
     out = [key] + ([score] if with_score else []) + ([rn2] if with_rn2 else [])
     return out[0] if len(out) == 1 else tuple(out)
@@ -315,7 +332,7 @@ def topk_select(key: torch.Tensor, k: int, ws: torch.Tensor | None = None):
     mask = torch.empty(max((n + 31) // 32, 1), dtype=torch.int32, device=key.device)
     need = lib().rsc_topk_workspace_bytes(n)
     ws = _workspace(need, key.device) if ws is None else ws
-    _check(lib().rsc_topk_select(key.data_ptr(), n, k, idx.data_ptr(), mask.data_ptr(), ws.data_ptr(),
+    _check(lib().rsc_topk_select(_dp(key), n, k, _dp(idx), _dp(mask), _dp(ws),
                                  ws.numel(), _stream()))
     return idx[:k], mask[: (n + 31) // 32]
 
@@ -335,8 +352,8 @@ def slice_csr(A: DeviceCsr, mask: torch.Tensor, capacity: int | None = None,
     s = A.struct()
     need = lib().rsc_slice_workspace_bytes(ctypes.byref(s))
     ws = _workspace(need, dev) if ws is None else ws
-    _check(lib().rsc_slice_csr(ctypes.byref(s), _ptr(mask), _ptr(colw), rp.data_ptr(), co.data_ptr(),
-                               vo.data_ptr(), cap, nnz_out.data_ptr(), ws.data_ptr(), ws.numel(), _stream()))
+    _check(lib().rsc_slice_csr(ctypes.byref(s), _ptr(mask), _ptr(colw), _dp(rp), _dp(co),
+                               _dp(vo), cap, _dp(nnz_out), _dp(ws), ws.numel(), _stream()))
     return DeviceCsr(A.n_rows, A.n_cols, rp, co, vo, nnz=cap), nnz_out
 
 
@@ -349,8 +366,8 @@ def sample_columns(key: torch.Tensor, k: int, seed: int, ws: torch.Tensor | None
     mask = torch.empty(max((n + 31) // 32, 1), dtype=torch.int32, device=key.device)
     need = lib().rsc_sample_workspace_bytes(n)
     ws = _workspace(need, key.device) if ws is None else ws
-    _check(lib().rsc_sample_columns(key.data_ptr(), n, k, seed, count.data_ptr(), colw.data_ptr(),
-                                    mask.data_ptr(), ws.data_ptr(), ws.numel(), _stream()))
+    _check(lib().rsc_sample_columns(_dp(key), n, k, seed, _dp(count), _dp(colw),
+                                    _dp(mask), _dp(ws), ws.numel(), _stream()))
     return count[:n], colw[:n], mask[: (n + 31) // 32]
 
 
@@ -381,18 +398,18 @@ class Cache:
 
     def refresh(self, B: torch.Tensor, k: int, step: int, d: int | None = None) -> None:
         d = B.shape[1] if d is None else d
-        _check(lib().rsc_cache_refresh(self._h, B.data_ptr(), d, _ld(B), k, step, _stream()))
+        _check(lib().rsc_cache_refresh(self._h, _dp(B), d, _ld(B), k, step, _stream()))
 
     def score(self, B: torch.Tensor, d: int | None = None) -> None:
         d = B.shape[1] if d is None else d
-        _check(lib().rsc_cache_score(self._h, B.data_ptr(), d, _ld(B), _stream()))
+        _check(lib().rsc_cache_score(self._h, _dp(B), d, _ld(B), _stream()))
 
     def select(self, k: int, step: int) -> None:
         _check(lib().rsc_cache_select(self._h, k, step, _stream()))
 
     def refresh_random(self, B: torch.Tensor, k_draws: int, seed: int, step: int, d: int | None = None) -> None:
         d = B.shape[1] if d is None else d
-        _check(lib().rsc_cache_refresh_random(self._h, B.data_ptr(), d, _ld(B), k_draws, seed, step, _stream()))
+        _check(lib().rsc_cache_refresh_random(self._h, _dp(B), d, _ld(B), k_draws, seed, step, _stream()))
 
     def get(self, step: int, with_slice: bool = True):
         """dict(slice=CsrStruct or None, idx_ptr, k, needs_refresh, version).
@@ -411,7 +428,7 @@ class Cache:
     def spmm_sampled(self, B: torch.Tensor, d: int | None = None, out: torch.Tensor | None = None):
         d = B.shape[1] if d is None else d
         Y = _new_out(self.X.n_rows, d, B.device) if out is None else out
-        _check(lib().rsc_spmm_sampled(self._h, B.data_ptr(), d, _ld(B), Y.data_ptr(), _ld(Y), _stream()))
+        _check(lib().rsc_spmm_sampled(self._h, _dp(B), d, _ld(B), _dp(Y), _ld(Y), _stream()))
         return Y
 
     def buffers(self):
@@ -509,8 +526,8 @@ def greedy_profile(key: torch.Tensor, colnnz: torch.Tensor, alpha, with_order: b
     order = torch.empty(max(n, 1), dtype=torch.int32, device=key.device) if with_order else None
     need = lib().rsc_greedy_profile_workspace_bytes(n)
     ws = _workspace(need, key.device) if ws is None else ws
-    _check(lib().rsc_greedy_profile(key.data_ptr(), colnnz.data_ptr(), n, alpha[0], alpha[1],
-                                    mass.data_ptr(), count.data_ptr(), _ptr(order), ws.data_ptr(),
+    _check(lib().rsc_greedy_profile(_dp(key), _dp(colnnz), n, alpha[0], alpha[1],
+                                    _dp(mass), _dp(count), _ptr(order), _dp(ws),
                                     ws.numel(), _stream()))
     out = (mass[:nb], count[:nb])
     return out + (order[:n],) if with_order else out

@@ -209,3 +209,23 @@ def test_whole_chain_on_a_side_stream_matches_the_current_stream():
     assert got[2] == ref[2]
     assert np.array_equal(got[0].view(np.uint32), ref[0].view(np.uint32))
     assert np.array_equal(got[1].view(np.uint32), ref[1].view(np.uint32))
+
+
+def test_binding_refuses_tensors_off_the_current_device():
+    """The binding hands the kernels raw addresses on the current device's
+    stream; a host tensor is refused before anything is launched."""
+    A = synth.make_graph("tiny", 0)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, A.n)
+    H = torch.from_numpy(synth.dense_normal(A.n, 8, seed=1))        # host memory
+    with pytest.raises(ValueError, match="current device"):
+        rsc.spmm(X, H)
+    plan = rsc.SpmmPlan(X)
+    with pytest.raises(ValueError, match="current device"):
+        plan.run(H)
+    Y = plan.run(H.cuda())
+    with pytest.raises(ValueError, match="current device"):
+        plan.run(H.cuda(), out=torch.empty_like(Y).cpu())
+    plan.close()
+    Xh = rsc.DeviceCsr(A.n, A.n, torch.from_numpy(A.rowptr), torch.from_numpy(A.col), torch.from_numpy(A.val))
+    with pytest.raises(ValueError, match="current device"):
+        rsc.spmm(Xh, H.cuda())
