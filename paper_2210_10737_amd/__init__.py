@@ -188,9 +188,8 @@ def _dp(t: torch.Tensor) -> int:
     """Device address of a tensor that lives on the current GPU (the library
     launches on the current device's stream, so a host tensor or one on
     another GPU would hand the kernels an address they cannot use)."""
-    dev = t.device
-    if dev.type != "cuda" or dev.index != _device_index():
-        raise ValueError(f"tensor on {dev}: the library runs on the current device cuda:{_device_index()}")
+    if t.get_device() != _device_index():   # -1 for host tensors
+        raise ValueError(f"tensor on {t.device}: the library runs on the current device cuda:{_device_index()}")
     return t.data_ptr()
 
 
