@@ -116,7 +116,8 @@ __global__ __launch_bounds__(1024) void slice_scan_kernel(int32_t nt, const uint
     const int32_t per = (nt + 1023) / 1024;
     const int32_t lo = min(nt, t * per), hi = min(nt, lo + per);
     int64_t s = 0;
-    for (int32_t i = lo; i < hi; ++i) s += tile_cnt[i];
+#pragma unroll 8
+    for (int32_t i = lo; i < hi; ++i) s += tile_cnt[i];  // unrolled: 8 loads in flight, not 1
     sh[t] = s;
     __syncthreads();
     for (int off = 1; off < 1024; off <<= 1) {
@@ -126,6 +127,7 @@ __global__ __launch_bounds__(1024) void slice_scan_kernel(int32_t nt, const uint
         __syncthreads();
     }
     int64_t run = sh[t] - s;
+#pragma unroll 8
     for (int32_t i = lo; i < hi; ++i) {
         tile_off[i] = (uint32_t)run;
         run += tile_cnt[i];
