@@ -444,11 +444,13 @@ inline bool use_order(int32_t n_rows, int64_t nnz) {
 constexpr int kBlockW = 64;                         // features per blocked pass
 constexpr double kBlockBytes = 4.5 * 1024 * 1024;   // B bytes per column range (~ one XCD's L2)
 constexpr int kMaxBlocks = 8;                       // partial outputs at most 8 x Y per pass
+constexpr int kPieceMin = 56;                       // mean entries per piece of a row for blocking
 
 // Number of column ranges P for a product with n_rows rows, about nnz
 // entries and n_src distinct B rows referenced; 1 = not blocked. Blocked when
 // the referenced 64-float slice of B spans 2..8 L2-sized ranges and rows are
-// long enough that each piece still holds a full 64-entry run on average.
+// long enough that each piece still holds most of a 64-entry run on average
+// (kPieceMin entries).
 // RSC_SPMM_BLOCKED=0 switches the mode off, =2..8 forces that P.
 inline int32_t column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src) {
     if (n_rows <= 0 || (int64_t)(kMaxBlocks + 1) * n_rows > INT32_MAX) return 1;  // virtual rows are int32
@@ -459,7 +461,7 @@ inline int32_t column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src) {
     }
     const int64_t P = (int64_t)std::ceil((double)n_src * kBlockW * 4 / kBlockBytes);
     if (P < 2 || P > kMaxBlocks) return 1;
-    if (nnz < 64LL * P * n_rows) return 1;
+    if (nnz < (int64_t)kPieceMin * P * n_rows) return 1;
     return (int32_t)P;
 }
 
