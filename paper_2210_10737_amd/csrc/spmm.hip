@@ -347,6 +347,12 @@ inline int64_t long_rows_bound(int32_t n_rows, int64_t nnz) {
     return std::min<int64_t>(n_rows, nnz / (kLongRow + 1));
 }
 
+// Pieces longer than kLongRow in the column-blocked mode with P ranges: up to
+// P per row, and no more than nnz / (kLongRow + 1) in all.
+inline int64_t long_pieces_bound(int32_t n_rows, int64_t nnz, int32_t P) {
+    return std::min<int64_t>((int64_t)P * n_rows, nnz / (kLongRow + 1));
+}
+
 // Length class of a row: 0 for at most one entry, else ceil(log2(len)), so
 // rows longer than kLongRow = 1024 are exactly the classes >= 11.
 __device__ __forceinline__ int row_class(int32_t len) { return len <= 1 ? 0 : 32 - __clz(len - 1); }
@@ -531,10 +537,15 @@ __global__ __launch_bounds__(256) void combine_blocks_kernel(const float *__rest
 }  // namespace
 
 namespace {
-// bytes of the row list (long rows, or the whole processing order)
+// entries of the row list: the whole processing order (n_rows), or the long
+// rows, or the long pieces of a column-blocked product with up to kMaxBlocks
+// ranges (one layout for every P, so a workspace never depends on the range
+// count an environment switch picks)
+int64_t list_entries(int32_t n_rows, int64_t nnz) {
+    return std::max<int64_t>({1, (int64_t)n_rows, long_pieces_bound(n_rows, nnz, kMaxBlocks)});
+}
 size_t list_bytes(int32_t n_rows, int64_t nnz) {
-    const int64_t entries = std::max<int64_t>({1, (int64_t)n_rows, long_rows_bound(n_rows, nnz)});
-    return align_up(sizeof(int32_t) * (size_t)entries, 256);
+    return align_up(sizeof(int32_t) * (size_t)list_entries(n_rows, nnz), 256);
 }
 // bytes of the blocked mode's split points and partial rows for P ranges
 size_t blocked_bytes(int32_t n_rows, int32_t P) {
@@ -609,6 +620,8 @@ hipError_t spmm_blocked_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t
     SpmmWs *h = static_cast<SpmmWs *>(ws);
     int32_t *list = reinterpret_cast<int32_t *>(h + 1);
     const int32_t nv = P * n_rows;
+    if (P > kMaxBlocks || long_pieces_bound(n_rows, nnz_bound, P) > list_entries(n_rows, nnz_bound))
+        return hipErrorInvalidValue;
     zero_counters_kernel<<<1, 1, 0, stream>>>(&h->long_count);
     if (long_rows_bound(n_rows, nnz_bound) > 0 && nv > 0)
         collect_long_rows_kernel<<<(unsigned)ceil_div(nv, kCollectThreads * kCollectPerThread), kCollectThreads, 0,
@@ -636,6 +649,9 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
     const int32_t P = column_blocks(n_rows, nnz_hint, n_src_hint);
     const size_t head = sizeof(SpmmWs) + list_bytes(n_rows, nnz_bound);
     if (P > 1 && head + blocked_bytes(n_rows, P) <= ws_bytes) {
+        // the long-piece list must hold every piece the collect pass can find
+        if (P > kMaxBlocks || long_pieces_bound(n_rows, nnz_bound, P) > list_entries(n_rows, nnz_bound))
+            return hipErrorInvalidValue;
         char *p = static_cast<char *>(ws) + head;
         float *part = reinterpret_cast<float *>(p + align_up(sizeof(int32_t) * (size_t)n_rows * (P + 1), 256));
         const int32_t nv = P * n_rows;  // virtual rows, block-major

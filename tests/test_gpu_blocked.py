@@ -71,16 +71,24 @@ def test_forced_blocks_match_oracle(seed):
     Bd = torch.from_numpy(B).cuda()
     X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
     Yo, S = oracle.spmm(A.rowptr, A.col, A.val, B, d=d, with_mag=True)
+    AT = synth.transpose(A, n_cols)
     with blocked(P):
         Y = rsc.spmm(X, Bd, d=d).cpu().numpy()
-        AT = synth.transpose(A, n_cols)
         cache = rsc.Cache(X, rsc.DeviceCsr.from_host(AT.rowptr, AT.col, AT.val, A.n))
         cache.refresh(Bd, k, step=0, d=d)
         Ys = cache.spmm_sampled(Bd, d=d).cpu().numpy()
         snap = rsc.cache_snapshot(cache)
         cache.close()
     assert rel_err(Y, Yo, S) <= 1e-5, (seed, P, d, ld)
-    Yso, Ss = oracle.spmm(snap["rowptr"], snap["col"], snap["val"], B, d=d, with_mag=True)
+    # the oracle's own chain: column norms of X (rows of X^T), keys, top-k, slice
+    cn2, _ = oracle.col_sqnorms(AT.rowptr, AT.val)
+    key = oracle.pair_keys(cn2, B, d=d)["key"]
+    idx, mask = oracle.topk(key, k)
+    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+    assert np.array_equal(snap["idx"], idx), (seed, P)
+    assert np.array_equal(snap["rowptr"], ro) and np.array_equal(snap["col"], co), (seed, P)
+    assert np.array_equal(snap["val"].view(np.uint32), vo.view(np.uint32)), (seed, P)
+    Yso, Ss = oracle.spmm(ro, co, vo, B, d=d, with_mag=True)
     assert rel_err(Ys, Yso, Ss) <= 1e-4, (seed, P)
     if k == n_cols:
         assert np.array_equal(Ys.view(np.uint32), Y.view(np.uint32)), (seed, P)
@@ -126,3 +134,30 @@ def test_automatic_choice_on_long_rows():
     rows = np.arange(0, n, 97, dtype=np.int32)
     Yo, S = oracle.spmm(A.rowptr, A.col, A.val, B, rows=rows, with_mag=True)
     assert rel_err(Y.cpu().numpy()[rows], Yo, S) <= 1e-5
+
+
+@pytest.mark.parametrize("n_rows,n_cols,row_len,d", [
+    (100, 40_000, 10_000, 96),     # P = 3: 300 long pieces from 100 rows
+    (20_000, 20_000, 2_200, 64),   # P = 2: 40,000 pieces of 1,100 entries from 20,000 rows
+])
+def test_long_pieces_outnumber_rows(n_rows, n_cols, row_len, d):
+    # Regression: the long-piece list of the column-blocked mode must hold up
+    # to P pieces per row (not one per row) when rows average over 1,024
+    # entries per range. The automatic rule picks the blocked mode here.
+    A = synth.bucket_csr(np.full(n_rows, row_len), n_cols, seed=21)
+    B = synth.dense_normal(n_cols, d, seed=22)
+    Bd = torch.from_numpy(B).cuda()
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
+    with blocked(None):
+        Y = rsc.spmm(X, Bd)
+        plan = rsc.SpmmPlan(X)
+        Yp = plan.run(Bd)
+        plan.close()
+    with blocked(0):
+        Yu = rsc.spmm(X, Bd)
+    torch.cuda.synchronize()
+    assert not torch.equal(Y, Yu)              # the blocked mode ran (different partial rounding)
+    assert torch.equal(Y, Yp)                  # the plan's prepared list gives the same product
+    Yo, S = oracle.spmm(A.rowptr, A.col, A.val, B, with_mag=True)
+    assert rel_err(Y.cpu().numpy(), Yo, S) <= 1e-5
+    assert rel_err(Yu.cpu().numpy(), Yo, S) <= 1e-5
