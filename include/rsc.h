@@ -150,6 +150,10 @@ typedef struct rsc_spmm_plan rsc_spmm_plan_t;
 rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_spmm_plan_t **out);
 rsc_status_t rsc_spmm_plan_run(rsc_spmm_plan_t *plan, const float *B, int32_t d, int64_t ldb, float *Y,
                                int64_t ldy, hipStream_t stream);
+/* rsc_spmm_plan_destroy waits (on the host) for the plan's own runs on
+ * every stream they used (runs captured into a HIP graph excepted: the
+ * caller synchronises those launches), then frees the plan's memory,
+ * stream-ordered; work on other streams is not waited for. NULL is a no-op. */
 rsc_status_t rsc_spmm_plan_destroy(rsc_spmm_plan_t *plan);
 
 /* MEAN aggregator operand (appendix A.3: SpMM_MEAN(A, H) = D^-1 A H, D the
@@ -315,7 +319,12 @@ rsc_status_t rsc_spmm_sampled(rsc_cache_t *cache, const float *B, int32_t d, int
  * output pointer may be NULL. */
 rsc_status_t rsc_cache_buffers(rsc_cache_t *cache, const double **cn2, const int32_t **colnnz,
                                const uint64_t **key, const double **rn2, const uint32_t **mask);
-/* Waits for outstanding cache work, then frees its buffers. NULL is a no-op. */
+/* Waits (on the host) for the work this cache's own calls enqueued, on
+ * every stream they used, then frees its buffers (stream-ordered, on a
+ * library-owned stream of the cache's device; through the allocator for a
+ * cache made by rsc_cache_create_ex). Work on other streams is not waited
+ * for. Calls captured into a HIP graph are not tracked: synchronise the
+ * graph's launches before destroying the cache. NULL is a no-op. */
 rsc_status_t rsc_cache_destroy(rsc_cache_t *cache);
 
 /* ---------------------------------------------------------------- A8 --- */

@@ -8,6 +8,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -106,11 +107,11 @@ rsc_status_t validate(const rsc_csr_t *A, const char *name, int64_t *bad_row, hi
         return RSC_OK;
     }
     unsigned long long *d_bad = nullptr, h_bad = 0;
-    RSC_HIP(hipMalloc((void **)&d_bad, sizeof(unsigned long long)), "validate alloc");
+    RSC_HIP(hipMallocAsync((void **)&d_bad, sizeof(unsigned long long), stream), "validate alloc");
     hipError_t e = rsc::csr_validate_launch(A->n_rows, A->n_cols, A->nnz, A->rowptr, A->col, d_bad, stream);
     if (e == hipSuccess) e = hipMemcpyAsync(&h_bad, d_bad, sizeof h_bad, hipMemcpyDeviceToHost, stream);
+    (void)hipFreeAsync(d_bad, stream);
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
-    (void)hipFree(d_bad);
     if (e != hipSuccess) return hip_fail(e, "validate");
     if (h_bad != ~0ull) {
         if (bad_row) *bad_row = (int64_t)h_bad;
@@ -148,6 +149,90 @@ rsc_status_t check_same_device(int made_on, const char *what) {
     if (cur != made_on)
         return fail(RSC_ERR_INVALID_ARGUMENT, "%s was made on device %d, current device is %d", what, made_on, cur);
     return RSC_OK;
+}
+
+// Completion markers of the work a plan or cache has enqueued: one event per
+// stream it was used on, recorded after each call (not while the stream is
+// being captured into a graph: a captured call runs when the caller launches
+// the graph, which the caller synchronises). Destroying the handle waits for
+// these events only, so work on other streams is never waited for.
+struct StreamFence {
+    std::vector<std::pair<hipStream_t, hipEvent_t>> ev;
+
+    hipError_t record(hipStream_t s) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        hipError_t e = hipStreamIsCapturing(s, &cs);
+        if (e != hipSuccess) return e;
+        if (cs != hipStreamCaptureStatusNone) return hipSuccess;
+        for (auto &p : ev)
+            if (p.first == s) return hipEventRecord(p.second, s);
+        hipEvent_t x = nullptr;
+        e = hipEventCreateWithFlags(&x, hipEventDisableTiming);
+        if (e != hipSuccess) return e;
+        ev.emplace_back(s, x);
+        return hipEventRecord(x, s);
+    }
+
+    // waits for every recorded event and releases them; the first error
+    hipError_t wait_and_release() {
+        hipError_t first = hipSuccess;
+        for (auto &p : ev) {
+            const hipError_t e = hipEventSynchronize(p.second);
+            if (first == hipSuccess) first = e;
+            (void)hipEventDestroy(p.second);
+        }
+        ev.clear();
+        return first;
+    }
+};
+
+// Device memory of plans and caches (and the validation flag) comes from the
+// stream-ordered allocator: hipFree would wait for every stream on the
+// device, hipFreeAsync only orders the free on one stream. After a handle's
+// own work has completed, its memory is freed on a library-owned stream of
+// its device (non-blocking, default priority), so destroying it never waits
+// for work on other streams; on a failed create, on the creation stream.
+constexpr int kMaxDevices = 64;
+std::mutex g_stream_mu;
+hipStream_t g_free_stream[kMaxDevices] = {};
+
+hipError_t free_stream_of_current_device(hipStream_t *out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_stream_mu);
+    if (!g_free_stream[dev]) {
+        e = hipStreamCreateWithFlags(&g_free_stream[dev], hipStreamNonBlocking);
+        if (e != hipSuccess) return e;
+    }
+    *out = g_free_stream[dev];
+    return hipSuccess;
+}
+
+// Pinned host words for the caches' slice-size readback, taken from chunks
+// that are never released (hipHostFree would also wait for the whole device).
+std::mutex g_pin_mu;
+std::vector<int64_t *> g_pin_free;
+
+hipError_t take_pinned_word(int64_t **out) {
+    std::lock_guard<std::mutex> lock(g_pin_mu);
+    if (g_pin_free.empty()) {
+        constexpr int kChunk = 64;
+        int64_t *chunk = nullptr;
+        const hipError_t e = hipHostMalloc((void **)&chunk, kChunk * sizeof(int64_t), hipHostMallocPortable);
+        if (e != hipSuccess) return e;
+        for (int i = kChunk - 1; i >= 0; --i) g_pin_free.push_back(chunk + i);
+    }
+    *out = g_pin_free.back();
+    g_pin_free.pop_back();
+    return hipSuccess;
+}
+
+void return_pinned_word(int64_t *p) {
+    if (!p) return;
+    std::lock_guard<std::mutex> lock(g_pin_mu);
+    g_pin_free.push_back(p);
 }
 
 // with RSC_VALIDATE=1, the device check of a caller's CSR before any launch
@@ -193,6 +278,8 @@ struct rsc_cache {
     uint64_t version = 0;
     bool nnz_known = false;
     int64_t nnz_slice = 0;
+    StreamFence fence;            // completion of the calls' work, per stream
+    hipStream_t free_stream = nullptr;  // the library's stream for this device's frees
 };
 
 extern "C" {
@@ -250,13 +337,16 @@ struct rsc_spmm_plan {
     void *ws = nullptr;
     size_t ws_bytes = 0;
     int device = 0;
+    StreamFence fence;         // completion of the runs, per stream
+    hipStream_t free_stream = nullptr;  // the library's stream for this device's frees
 };
 
-static void plan_free(rsc_spmm_plan_t *p) {
+// frees the plan's memory, ordered on `s` (stream-ordered frees)
+static void plan_free(rsc_spmm_plan_t *p, hipStream_t s) {
     if (!p) return;
-    if (p->colf) (void)hipFree(p->colf);
-    if (p->split) (void)hipFree(p->split);
-    if (p->ws) (void)hipFree(p->ws);
+    if (p->colf) (void)hipFreeAsync(p->colf, s);
+    if (p->split) (void)hipFreeAsync(p->split, s);
+    if (p->ws) (void)hipFreeAsync(p->ws, s);
     delete p;
 }
 
@@ -270,9 +360,9 @@ rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_sp
     p->A = *A;
     (void)hipGetDevice(&p->device);
     p->ws_bytes = std::max<size_t>(rsc::spmm_ws_bytes(A->n_rows, A->nnz, A->n_cols), 256);
-    if (hipMalloc(&p->ws, p->ws_bytes) != hipSuccess) {
+    if (hipMallocAsync(&p->ws, p->ws_bytes, stream) != hipSuccess) {
         (void)hipGetLastError();
-        plan_free(p);
+        plan_free(p, stream);
         return fail(RSC_ERR_OUT_OF_MEMORY, "plan workspace of %zu bytes", p->ws_bytes);
     }
     // the per-call preparation of the product, done once: split bounds and
@@ -281,7 +371,7 @@ rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_sp
     {
         hipError_t e = hipSuccess;
         if (P > 1) {
-            e = hipMalloc((void **)&p->split, sizeof(int32_t) * (size_t)A->n_rows * (P + 1));
+            e = hipMallocAsync((void **)&p->split, sizeof(int32_t) * (size_t)A->n_rows * (P + 1), stream);
             if (e == hipSuccess) e = rsc::spmm_split_launch(A->n_rows, A->n_cols, A->rowptr, A->col, P, p->split, stream);
             if (e == hipSuccess) e = rsc::spmm_blocked_prepare(A->n_rows, A->nnz, p->split, P, p->ws, stream);
         } else {
@@ -296,7 +386,7 @@ rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_sp
         if (e == hipSuccess) e = hipStreamSynchronize(stream);
         if (e != hipSuccess) {
             (void)hipGetLastError();
-            plan_free(p);
+            plan_free(p, stream);
             return e == hipErrorOutOfMemory ? fail(RSC_ERR_OUT_OF_MEMORY, "plan preparation")
                                             : hip_fail(e, "plan preparation");
         }
@@ -308,26 +398,30 @@ rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_sp
     if (hint_worthwhile(A->n_cols) && A->nnz > 0) {
         int32_t *deg = nullptr;
         void *ws_hub = nullptr;
-        hipError_t e = hipMalloc((void **)&p->colf, sizeof(int32_t) * (size_t)A->nnz);
-        if (e == hipSuccess) e = hipMalloc((void **)&deg, sizeof(int32_t) * (size_t)A->n_cols);
-        if (e == hipSuccess) e = hipMalloc(&ws_hub, rsc::hub_ws_bytes(A->n_cols));
+        hipError_t e = hipMallocAsync((void **)&p->colf, sizeof(int32_t) * (size_t)A->nnz, stream);
+        if (e == hipSuccess) e = hipMallocAsync((void **)&deg, sizeof(int32_t) * (size_t)A->n_cols, stream);
+        if (e == hipSuccess) e = hipMallocAsync(&ws_hub, rsc::hub_ws_bytes(A->n_cols), stream);
         if (e == hipSuccess) e = rsc::degree_count_launch(A->col, A->nnz, A->n_cols, deg, stream);
         if (e == hipSuccess) e = rsc::hub_bits_launch(deg, nullptr, A->n_cols, ws_hub, stream);
         if (e == hipSuccess) e = rsc::flag_cols_launch(A->col, A->nnz, rsc::hub_bits_of(ws_hub), p->colf, stream);
+        if (deg) (void)hipFreeAsync(deg, stream);
+        if (ws_hub) (void)hipFreeAsync(ws_hub, stream);
         if (e == hipSuccess) e = hipStreamSynchronize(stream);
-        if (deg) (void)hipFree(deg);
-        if (ws_hub) (void)hipFree(ws_hub);
         if (e != hipSuccess) {
             (void)hipGetLastError();
-            plan_free(p);
+            plan_free(p, stream);
             return e == hipErrorOutOfMemory ? fail(RSC_ERR_OUT_OF_MEMORY, "plan allocation failed")
                                             : hip_fail(e, "plan create");
         }
     }
-    if (hipStreamSynchronize(stream) != hipSuccess) {
-        const hipError_t e = hipGetLastError();
-        plan_free(p);
-        return hip_fail(e, "plan create");
+    {
+        hipError_t e = free_stream_of_current_device(&p->free_stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            plan_free(p, stream);
+            return hip_fail(e, "plan create");
+        }
     }
     *out = p;
     return RSC_OK;
@@ -349,13 +443,14 @@ rsc_status_t rsc_spmm_plan_run(rsc_spmm_plan_t *p, const float *B, int32_t d, in
     // then on every run prepares for itself
     if (!used && A->n_rows > 0) p->prep.ready = false;
     RSC_HIP(e, "plan run");
+    RSC_HIP(p->fence.record(stream), "plan run event");
     return RSC_OK;
 }
 
 rsc_status_t rsc_spmm_plan_destroy(rsc_spmm_plan_t *p) {
     if (!p) return RSC_OK;
-    hipError_t e = hipDeviceSynchronize();
-    plan_free(p);
+    const hipError_t e = p->fence.wait_and_release();  // the plan's own runs only
+    plan_free(p, p->free_stream);
     if (e != hipSuccess) return hip_fail(e, "plan destroy");
     return RSC_OK;
 }
@@ -466,7 +561,8 @@ rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, const doubl
 }
 
 // ------------------------------------------------------------------- A6 / A7
-static void cache_free(rsc_cache_t *c) {
+// frees the cache's memory: through its allocator, or ordered on `s`
+static void cache_free(rsc_cache_t *c, hipStream_t s) {
     if (!c) return;
     void *dev[] = {c->cn2, c->colnnz, c->key, c->rn2, c->count, c->colw, c->idx, c->mask, c->s_rowptr,
                    c->s_col, c->s_val, c->d_nnz, c->ws_topk, c->ws_slice, c->ws_spmm, c->ws_sample, c->s_split};
@@ -475,9 +571,9 @@ static void cache_free(rsc_cache_t *c) {
         if (c->alloc.alloc)
             c->alloc.free(p, c->alloc_stream, c->alloc.ctx);
         else
-            (void)hipFree(p);
+            (void)hipFreeAsync(p, s);
     }
-    if (c->h_nnz) (void)hipHostFree(c->h_nnz);
+    return_pinned_word(c->h_nnz);
     if (c->ev) (void)hipEventDestroy(c->ev);
     delete c;
 }
@@ -542,21 +638,22 @@ rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_
         if (c->alloc.alloc) {
             *a.p = c->alloc.alloc(bytes, stream, c->alloc.ctx);
             if (!*a.p) {
-                cache_free(c);
+                cache_free(c, stream);
                 return fail(RSC_ERR_OUT_OF_MEMORY, "allocator returned NULL for %zu bytes", bytes);
             }
             if (!aligned(*a.p, 256)) {
-                cache_free(c);
+                cache_free(c, stream);
                 return fail(RSC_ERR_UNSUPPORTED, "allocator returned memory that is not 256-byte aligned");
             }
-        } else if (hipMalloc(a.p, bytes) != hipSuccess) {
+        } else if (hipMallocAsync(a.p, bytes, stream) != hipSuccess) {
             (void)hipGetLastError();
-            cache_free(c);
+            cache_free(c, stream);
             return fail(RSC_ERR_OUT_OF_MEMORY, "cache allocation of %zu bytes failed", a.bytes);
         }
     }
-    hipError_t e = hipHostMalloc((void **)&c->h_nnz, sizeof(int64_t), hipHostMallocDefault);
+    hipError_t e = take_pinned_word(&c->h_nnz);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev, hipEventDisableTiming);
+    if (e == hipSuccess) e = free_stream_of_current_device(&c->free_stream);
     if (e == hipSuccess) e = rsc::col_sqnorms_launch(XT->n_rows, XT->rowptr, XT->val, c->cn2, c->colnnz, stream);
     // whether X has long rows at all: a slice's rows are parts of X's, so if
     // none is long, the sampled products need no long-row pass
@@ -571,7 +668,7 @@ rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_
     }
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
     if (e != hipSuccess) {
-        cache_free(c);
+        cache_free(c, stream);
         return hip_fail(e, "cache create");
     }
     c->x_long_rows = x_long;
@@ -612,6 +709,7 @@ rsc_status_t rsc_cache_score(rsc_cache_t *c, const float *B, int32_t d, int64_t 
     RSC_TRY(check_same_device(c->device, "cache"));
     RSC_HIP(rsc::pair_scores_launch(c->cn2, B, c->n, d, ldb, c->key, nullptr, c->rn2, stream), "cache scores");
     c->scored = true;
+    RSC_HIP(c->fence.record(stream), "cache event");
     return RSC_OK;
 }
 
@@ -632,6 +730,7 @@ rsc_status_t rsc_cache_select(rsc_cache_t *c, int32_t k, int64_t step, hipStream
     c->nnz_known = false;
     c->random = false;
     RSC_HIP(cache_prepare(c, stream), "cache slice preparation");
+    RSC_HIP(c->fence.record(stream), "cache event");
     return RSC_OK;
 }
 
@@ -655,6 +754,7 @@ rsc_status_t rsc_cache_refresh_random(rsc_cache_t *c, const float *B, int32_t d,
     c->nnz_known = false;
     c->random = true;
     RSC_HIP(cache_prepare(c, stream), "cache slice preparation");
+    RSC_HIP(c->fence.record(stream), "cache event");
     return RSC_OK;
 }
 
@@ -713,6 +813,7 @@ rsc_status_t rsc_spmm_sampled(rsc_cache_t *c, const float *B, int32_t d, int64_t
                                           &c->prep, &used);
     if (!used) c->prep.ready = false;  // the launch rebuilt its own list in ws_spmm
     RSC_HIP(e, "spmm_sampled launch");
+    RSC_HIP(c->fence.record(stream), "cache event");
     return RSC_OK;
 }
 
@@ -729,8 +830,8 @@ rsc_status_t rsc_cache_buffers(rsc_cache_t *c, const double **cn2, const int32_t
 
 rsc_status_t rsc_cache_destroy(rsc_cache_t *c) {
     if (!c) return RSC_OK;
-    hipError_t e = hipDeviceSynchronize();
-    cache_free(c);
+    const hipError_t e = c->fence.wait_and_release();  // the cache's own work only
+    cache_free(c, c->free_stream);
     if (e != hipSuccess) return hip_fail(e, "cache destroy");
     return RSC_OK;
 }
