@@ -120,6 +120,22 @@ size_t rsc_spmm_workspace_bytes(const rsc_csr_t *A);
 rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb, float *Y,
                       int64_t ldy, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* rsc_spmm for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same product with no workspace argument and no allocation. Its scratch is
+ * a static 32 MiB device array inside the library, one per GPU, held until
+ * the process ends; a product needs 512 bytes plus 4 max(n_rows,
+ * min(8 n_rows, nnz / 1025)) bytes of it (about 8.3M rows at most), beyond
+ * which the call returns RSC_ERR_CAPACITY without launching. A product whose
+ * column-blocked buffers do not also fit runs unblocked (then Y may differ
+ * from rsc_spmm's within rounding; otherwise it is bitwise equal). Every
+ * call on one GPU uses that GPU's scratch, which keeps the last call's
+ * contents (the call clears what it needs): calls that overlap on one GPU
+ * (two streams, or two host threads) race and give wrong results, so order
+ * them on the device. RSC_VALIDATE does not apply (the check allocates). */
+rsc_status_t rsc_spmm_noalloc(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb, float *Y,
+                              int64_t ldy, hipStream_t stream);
+
 /* Plan for repeated exact products with one sparse operand (a training
  * run's static A_hat). Same product, same kernels, same summation order as
  * rsc_spmm: rsc_spmm_plan_run gives Y bitwise equal to rsc_spmm on the same

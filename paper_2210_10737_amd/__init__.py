@@ -41,7 +41,7 @@ STATUS = {0: "RSC_OK", 1: "RSC_ERR_INVALID_ARGUMENT", 2: "RSC_ERR_UNSUPPORTED",
 
 EXPORTED = [
     "rsc_status_string", "rsc_last_error", "rsc_abi_version", "rsc_csr_validate",
-    "rsc_spmm_workspace_bytes", "rsc_spmm", "rsc_degree_scale",
+    "rsc_spmm_workspace_bytes", "rsc_spmm", "rsc_spmm_noalloc", "rsc_degree_scale",
     "rsc_spmm_plan_create", "rsc_spmm_plan_run", "rsc_spmm_plan_destroy",
     "rsc_col_sqnorms", "rsc_pair_scores",
     "rsc_topk_workspace_bytes", "rsc_topk_select",
@@ -112,6 +112,7 @@ def lib():
             "rsc_abi_version": ([], i32),
             "rsc_spmm_workspace_bytes": ([csrp], sz),
             "rsc_spmm": ([csrp, vp, i32, i64, vp, i64, vp, sz, vp], ctypes.c_int),
+            "rsc_spmm_noalloc": ([csrp, vp, i32, i64, vp, i64, vp], ctypes.c_int),
             "rsc_spmm_plan_create": ([csrp, vp, ctypes.POINTER(vp)], ctypes.c_int),
             "rsc_spmm_plan_run": ([vp, vp, i32, i64, vp, i64, vp], ctypes.c_int),
             "rsc_spmm_plan_destroy": ([vp], ctypes.c_int),
@@ -256,6 +257,16 @@ def spmm(A: DeviceCsr, B: torch.Tensor, d: int | None = None, out: torch.Tensor 
     ws = _workspace(need, B.device) if ws is None else ws
     _check(lib().rsc_spmm(ctypes.byref(s), _dp(B), d, _ld(B), _dp(Y), _ld(Y),
                           _dp(ws), ws.numel(), _stream()))
+    return Y
+
+
+def spmm_noalloc(A: DeviceCsr, B: torch.Tensor, d: int | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Y = A @ B[:, :d] through rsc_spmm_noalloc: no workspace, no device
+    allocation inside the library (its scratch is static). With ``out`` given
+    nothing is allocated here either."""
+    d = B.shape[1] if d is None else d
+    Y = _new_out(A.n_rows, d, B.device) if out is None else out
+    _check(lib().rsc_spmm_noalloc(ctypes.byref(A.struct()), _dp(B), d, _ld(B), _dp(Y), _ld(Y), _stream()))
     return Y
 
 

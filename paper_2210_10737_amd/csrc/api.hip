@@ -329,6 +329,38 @@ rsc_status_t rsc_spmm(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb
     return RSC_OK;
 }
 
+// ------------------------------------------------------------------- A1 without allocation
+// Scratch of rsc_spmm_noalloc: a static device array, one copy per GPU the
+// library runs on, held until the process ends. Its name is a host-side
+// stand-in in host code; the device address of the current GPU's copy comes
+// from hipGetSymbolAddress (looked up once per device, with that device
+// current) and only that address is passed to kernels.
+constexpr size_t kNoallocScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxScratchDevices] = {};
+
+rsc_status_t scratch_of_current_device(void **out) {
+    int dev = -1;
+    RSC_HIP(hipGetDevice(&dev), "current device");
+    if (dev < 0 || dev >= kMaxScratchDevices)
+        return fail(RSC_ERR_UNSUPPORTED, "device %d: the no-allocation SpMM supports devices 0..%d", dev,
+                    kMaxScratchDevices - 1);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        RSC_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "no-allocation SpMM scratch address");
+        if (!p || !aligned(p, 256)) return fail(RSC_ERR_INTERNAL, "scratch address is not 256-byte aligned");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return RSC_OK;
+}
+}  // namespace
+
 struct rsc_spmm_plan {
     rsc_csr_t A{};
     int32_t *colf = nullptr;   // A's columns with the hub hint in bit 31 (large graphs only)
@@ -444,6 +476,26 @@ rsc_status_t rsc_spmm_plan_run(rsc_spmm_plan_t *p, const float *B, int32_t d, in
     if (!used && A->n_rows > 0) p->prep.ready = false;
     RSC_HIP(e, "plan run");
     RSC_HIP(p->fence.record(stream), "plan run event");
+    return RSC_OK;
+}
+
+rsc_status_t rsc_spmm_noalloc(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb, float *Y, int64_t ldy,
+                              hipStream_t stream) {
+    RSC_TRY(check_csr(A, "A"));
+    RSC_TRY(check_dense(B, A->n_cols, d, ldb, "B"));
+    RSC_TRY(check_dense(Y, A->n_rows, d, ldy, "Y"));
+    const size_t need = rsc::spmm_core_ws_bytes(A->n_rows, A->nnz);
+    if (need > kNoallocScratchBytes)
+        return fail(RSC_ERR_CAPACITY,
+                    "rsc_spmm_noalloc: %d rows and %lld entries need %zu bytes of scratch; the static scratch "
+                    "holds %zu",
+                    A->n_rows, (long long)A->nnz, need, kNoallocScratchBytes);
+    RSC_TRY(check_device());
+    void *ws = nullptr;
+    RSC_TRY(scratch_of_current_device(&ws));
+    RSC_HIP(rsc::spmm_launch(A->n_rows, A->n_cols, A->nnz, A->rowptr, A->col, A->val, B, d, ldb, Y, ldy, ws,
+                             kNoallocScratchBytes, stream, A->nnz, A->n_cols),
+            "spmm_noalloc launch");
     return RSC_OK;
 }
 

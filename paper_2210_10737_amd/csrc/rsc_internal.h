@@ -51,6 +51,9 @@ hipError_t spmm_rows_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t *r
 hipError_t spmm_blocked_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t *S, int32_t P, void *ws,
                                 hipStream_t stream);
 size_t spmm_blocked_fits(int32_t n_rows, int64_t nnz_bound, int32_t P);  // workspace bytes the blocked mode needs
+// workspace bytes an unblocked product needs (header and row list); with at
+// least this much a launch runs, blocked only if the blocked buffers also fit
+size_t spmm_core_ws_bytes(int32_t n_rows, int64_t nnz_bound);
 const int32_t *spmm_long_count_of(const void *ws);
 
 // ---- scores ------------------------------------------------------------

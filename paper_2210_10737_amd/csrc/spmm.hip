@@ -629,6 +629,8 @@ hipError_t spmm_blocked_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t
     return hipGetLastError();
 }
 
+size_t spmm_core_ws_bytes(int32_t n_rows, int64_t nnz_bound) { return sizeof(SpmmWs) + list_bytes(n_rows, nnz_bound); }
+
 size_t spmm_blocked_fits(int32_t n_rows, int64_t nnz_bound, int32_t P) {
     return sizeof(SpmmWs) + list_bytes(n_rows, nnz_bound) + blocked_bytes(n_rows, P);
 }
