@@ -36,7 +36,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-COUNTERS = os.path.join(ROOT, "profiles", "spmm_copurchase_counters.json")
+
+
+def counters_path(workload: str) -> str:
+    """The committed rocprofv3 counter record of a workload's SpMM calls."""
+    return os.path.join(ROOT, "profiles", f"spmm_{workload}_counters.json")
 
 
 def spmm_bytes(n: int, nnz: int, n_src: int, d: int) -> int:
@@ -68,31 +72,44 @@ def refresh_random_bytes(n: int, nnz: int, nnz_kept: int, k: int, d: int) -> int
 
 
 def kernel_source_digest() -> str:
-    """Digest of the SpMM kernel source with comments and blank lines removed
-    (a comment edit does not invalidate the counter record)."""
+    """Digest of the SpMM and gather-probe kernel sources with comments and
+    blank lines removed (a comment edit does not invalidate a counter
+    record)."""
     import re
-    with open(os.path.join(ROOT, "paper_2210_10737_amd", "csrc", "spmm.hip")) as fh:
-        src = fh.read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    lines = [re.sub(r"//.*", "", line).rstrip() for line in src.splitlines()]
-    code = "\n".join(line for line in lines if line.strip())
-    return hashlib.sha256(code.encode()).hexdigest()[:16]
+    code = []
+    for name in ("spmm.hip", "probe.hip"):
+        with open(os.path.join(ROOT, "paper_2210_10737_amd", "csrc", name)) as fh:
+            src = fh.read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        lines = [re.sub(r"//.*", "", line).rstrip() for line in src.splitlines()]
+        code.append("\n".join(line for line in lines if line.strip()))
+    return hashlib.sha256("\n".join(code).encode()).hexdigest()[:16]
 
 
-def load_traffic(digest: str, launch_bytes: int):
-    """HBM traffic of the exact SpMM from the committed rocprofv3 counter
-    record, if it was taken on the current kernel source; else None."""
+COUNTER_CONFIG_KEYS = ("workload", "n", "nnz", "d", "budget_pct", "aggregator", "selector")
+
+
+def load_traffic(config: dict, digest: str, op_bytes: dict):
+    """Bytes past L2 per call of each operation (FETCH_SIZE + WRITE_SIZE,
+    scaled by a 1 GiB copy) and L2 hit rates, from the workload's committed
+    rocprofv3 counter record, if it was taken on the current kernel source
+    and the same configuration; else None."""
+    path = counters_path(config["workload"])
     try:
-        rec = json.load(open(COUNTERS))
+        rec = json.load(open(path))
     except (OSError, ValueError):
         return None
     if rec.get("kernel_src_digest") != digest:
         return None
-    return {"fetch_bytes": rec["fetch_bytes_per_launch"], "write_bytes": rec["write_bytes_per_launch"],
-            "total_bytes": rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"],
-            "over_algorithmic": (rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]) / launch_bytes,
-            "l2_hit_rate": rec.get("l2_hit_rate"),
-            "source": os.path.relpath(COUNTERS, ROOT)}
+    if any(rec.get("config", {}).get(k_) != config.get(k_) for k_ in COUNTER_CONFIG_KEYS):
+        return None
+    out = {"source": os.path.relpath(path, ROOT), "ops": {}}
+    for op, r in rec["ops"].items():
+        tot = r["fetch_bytes"] + r["write_bytes"]
+        out["ops"][op] = {"fetch_bytes": round(r["fetch_bytes"]), "write_bytes": round(r["write_bytes"]),
+                          "total_bytes": round(tot), "l2_hit_rate": r.get("l2_hit_rate"),
+                          "over_algorithmic": round(tot / op_bytes[op], 3) if op_bytes.get(op) else None}
+    return out
 
 
 def _cpu_model() -> str:
@@ -297,6 +314,37 @@ def vendor_baseline(X, H, Y, plan, reps: int = 10):
     return out
 
 
+def gather_ceiling(plan, H, d, reps: int = 5):
+    """Times the plan's gather probe (rsc_spmm_plan_gather_probe: the exact
+    product's B-row gathers alone) at 4, 8 and 16 loads in flight per wave,
+    median of `reps` each after one untimed run; the fastest setting is the
+    ceiling. HIP events on the current stream, which the library launches on."""
+    import statistics
+
+    import torch
+    n_entries = plan.A.nnz
+    sink = torch.empty(max((n_entries + 63) // 64, 1), dtype=torch.float32, device=H.device)
+    per, slice_w = {}, None
+    for inflight in (4, 8, 16):
+        slice_w = plan.gather_probe(H, d=d, inflight=inflight, sink=sink)
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            plan.gather_probe(H, d=d, inflight=inflight, sink=sink)
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        per[inflight] = statistics.median(ts)
+    best = min(per, key=per.get)
+    ms = per[best]
+    return {"ms": round(ms, 4), "inflight": best, "slice_floats": slice_w,
+            "ms_by_inflight": {str(k_): round(v, 4) for k_, v in per.items()},
+            "logical_gather_GBs": round(4.0 * n_entries * d / (ms * 1e-3) / 1e9, 1),
+            "what": "the exact product's B-row gathers alone: same column stream (the plan's hinted copy), "
+                    "feature passes and cache policy; no values, row walk or output"}
+
+
 def parity_check(A, Hh, Gh, k, Y, Yb, kept, n_rows, seed):
     """The benchmarked outputs against the oracle: the kept columns bit for
     bit, and the exact and sampled products on a seeded sample of rows
@@ -487,6 +535,10 @@ def main() -> int:
                     help="after the timed steps, repetitions of each op that follow a 1 GiB cache flush")
     ap.add_argument("--no-vendor-baseline", action="store_true",
                     help="skip timing the vendor library's SpMM (rocSPARSE) on the exact product's operands")
+    ap.add_argument("--marked-ops", type=int, default=0,
+                    help="after timing, run this many rounds of exact SpMM, refresh, sampled SpMM and gather "
+                         "probe, each operation between two launches of a 3-byte uint8 fill (markers for "
+                         "attributing profiler counters to operations)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB once (a plain copy of known "
                          "size, so hardware byte counters can be scaled)")
@@ -647,6 +699,11 @@ def main() -> int:
         return {"mean": round(float(np.mean(v)), 4), "p10": round(float(q[0]), 4),
                 "p50": round(float(q[1]), 4), "p90": round(float(q[2]), 4), "n": len(v)}
 
+    # the gather ceiling: the exact product's gathers alone (same column
+    # stream, feature passes and cache policy; no values, rows or output),
+    # at 4, 8 and 16 loads in flight per wave; the fastest is the ceiling
+    probe = gather_ceiling(plan, H, d)
+
     # cold-cache repetitions, outside the timed steps: before each, write a
     # 1 GiB scratch buffer (more than the 4 MB L2s and the 256 MB MALL)
     scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
@@ -736,12 +793,17 @@ def main() -> int:
             for kind, b in (("exact", b_exact), ("sampled", b_sampled), ("refresh", b_refresh)) if per[kind]},
         "roofline": {
             "bound": "hbm",
-            "kernel": "spmm_kernel (exact SpMM)",
+            "kernel": "spmm_long_kernel + spmm_rows_kernel (the exact SpMM, one plan run)",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "frac_of_copy_ceiling": round(achieved / copy_gbs, 4),
+            # the same algorithmic bytes over the gather probe's time: the rate
+            # the product would reach if it took no longer than its gathers
+            "gather_ceiling_GBs": round(b_exact / (probe["ms"] * 1e-3) / 1e9, 2),
+            "frac_of_gather_ceiling": round(probe["ms"] / exact_ms, 4),
+            "gather_ceiling": probe,
             "algorithmic_bytes_per_launch": b_exact,
             "avg_launch_ms": round(exact_ms, 4),
             "traffic": None,
@@ -750,11 +812,35 @@ def main() -> int:
     }
     if args.parity_rows > 0 and args.aggregator == "gcn" and args.selector == "topk":
         out["parity"] = parity_check(A, Hh, Gh, k, Y, Yb, idx, args.parity_rows, args.seed)
-    traffic = load_traffic(digest, b_exact) if args.workload == "copurchase" and args.aggregator == "gcn" else None
-    if traffic is not None:
-        out["roofline"]["traffic"] = round(traffic["total_bytes"])
+    cfg = {"workload": args.workload, "n": n, "nnz": nnz, "d": d, "budget_pct": pct,
+           "aggregator": args.aggregator, "selector": args.selector}
+    traffic = load_traffic(cfg, digest, {"exact": b_exact, "sampled": b_sampled, "refresh": b_refresh,
+                                         "probe": b_exact})
+    if traffic is not None and "exact" in traffic["ops"]:
+        ex = traffic["ops"]["exact"]
+        out["roofline"]["traffic"] = ex["total_bytes"]
+        out["roofline"]["l2_hit_rate"] = ex["l2_hit_rate"]
         out["roofline"]["traffic_detail"] = traffic
     out["vendor_baseline"] = None if args.no_vendor_baseline else vendor_baseline(X, H, Y, plan)
+    if args.marked_ops > 0:
+        # for per-dispatch profiler counters: each operation's kernels between
+        # two launches of a 3-byte uint8 fill, in the order exact SpMM,
+        # refresh, sampled SpMM, gather probe
+        mk = torch.zeros(3, dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
+        for r in range(args.marked_ops):
+            mk.fill_(1)
+            plan.run(H, out=Y)
+            mk.fill_(2)
+            cache.refresh(G, k, step=args.warmup + args.steps) if args.selector == "topk" else \
+                cache.refresh_random(G, k, seed=args.seed * 1_000_003 + r, step=args.warmup + args.steps)
+            mk.fill_(3)
+            cache.spmm_sampled(G, out=Yb)
+            mk.fill_(4)
+            plan.gather_probe(H, d=d, inflight=probe["inflight"])
+            mk.fill_(5)
+        torch.cuda.synchronize()
+        out["marked_ops"] = args.marked_ops
     cache.close()
     plan.close()
     del X, XB, XT, H, G, Y, Yb, plan

@@ -172,6 +172,22 @@ rsc_status_t rsc_spmm_plan_run(rsc_spmm_plan_t *plan, const float *B, int32_t d,
  * stream-ordered; work on other streams is not waited for. NULL is a no-op. */
 rsc_status_t rsc_spmm_plan_destroy(rsc_spmm_plan_t *plan);
 
+/* Measurement helper, not a step of the method: the gather-only pass of the
+ * plan's exact product. Streams the plan's column indices (its hinted copy
+ * when it has one) in stored order, 64 entries per wave, and loads each
+ * referenced row of B with the lane layout, feature passes and cache policy
+ * an unblocked run of the plan takes for this d (rows are not walked, no
+ * values are read, no Y is written); the loaded values are summed and one
+ * float per 64 entries is written to sink (sink_count >= ceil(nnz / 64)),
+ * only so that no load is dropped. inflight (4, 8 or 16): loads each wave
+ * issues before consuming any. Its duration bounds how fast the product's
+ * own gather pattern can run, the "gather ceiling" of the product.
+ * *slice_out (nullable) receives the feature-pass width used. Runs are
+ * tracked for rsc_spmm_plan_destroy like rsc_spmm_plan_run. */
+rsc_status_t rsc_spmm_plan_gather_probe(rsc_spmm_plan_t *plan, const float *B, int32_t d, int64_t ldb,
+                                        int32_t inflight, float *sink, int64_t sink_count,
+                                        int32_t *slice_out, hipStream_t stream);
+
 /* MEAN aggregator operand (appendix A.3: SpMM_MEAN(A, H) = D^-1 A H, D the
  * degree matrix of A, D_ii = stored entries of row i). Writes A's values
  * divided by a degree into val_out (nnz entries, same structure as A), each

@@ -42,7 +42,7 @@ STATUS = {0: "RSC_OK", 1: "RSC_ERR_INVALID_ARGUMENT", 2: "RSC_ERR_UNSUPPORTED",
 EXPORTED = [
     "rsc_status_string", "rsc_last_error", "rsc_abi_version", "rsc_csr_validate",
     "rsc_spmm_workspace_bytes", "rsc_spmm", "rsc_spmm_noalloc", "rsc_degree_scale",
-    "rsc_spmm_plan_create", "rsc_spmm_plan_run", "rsc_spmm_plan_destroy",
+    "rsc_spmm_plan_create", "rsc_spmm_plan_run", "rsc_spmm_plan_destroy", "rsc_spmm_plan_gather_probe",
     "rsc_col_sqnorms", "rsc_pair_scores",
     "rsc_topk_workspace_bytes", "rsc_topk_select",
     "rsc_slice_workspace_bytes", "rsc_slice_csr",
@@ -116,6 +116,7 @@ def lib():
             "rsc_spmm_plan_create": ([csrp, vp, ctypes.POINTER(vp)], ctypes.c_int),
             "rsc_spmm_plan_run": ([vp, vp, i32, i64, vp, i64, vp], ctypes.c_int),
             "rsc_spmm_plan_destroy": ([vp], ctypes.c_int),
+            "rsc_spmm_plan_gather_probe": ([vp, vp, i32, i64, i32, vp, i64, ctypes.POINTER(i32), vp], ctypes.c_int),
             "rsc_col_sqnorms": ([csrp, vp, vp, vp], ctypes.c_int),
             "rsc_degree_scale": ([csrp, vp, i32, vp, vp], ctypes.c_int),
             "rsc_pair_scores": ([vp, vp, i32, i32, i64, vp, vp, vp, vp], ctypes.c_int),
@@ -287,6 +288,18 @@ class SpmmPlan:
         Y = _new_out(self.A.n_rows, d, B.device) if out is None else out
         _check(lib().rsc_spmm_plan_run(self._h, _dp(B), d, _ld(B), _dp(Y), _ld(Y), _stream()))
         return Y
+
+    def gather_probe(self, B: torch.Tensor, d: int | None = None, inflight: int = 8,
+                     sink: torch.Tensor | None = None) -> int:
+        """The gather-only pass of this plan's product (rsc_spmm_plan_gather_probe,
+        a measurement helper); returns the feature-pass width it used."""
+        d = B.shape[1] if d is None else d
+        need = (self.A.nnz + 63) // 64
+        sink = torch.empty(max(need, 1), dtype=torch.float32, device=B.device) if sink is None else sink
+        sl = ctypes.c_int32(0)
+        _check(lib().rsc_spmm_plan_gather_probe(self._h, _dp(B), d, _ld(B), inflight, _dp(sink), sink.numel(),
+                                                ctypes.byref(sl), _stream()))
+        return sl.value
 
     def close(self) -> None:
         if getattr(self, "_h", None) is not None and self._h.value:

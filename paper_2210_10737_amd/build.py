@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "librsc.so")
-SOURCES = ["spmm.hip", "scores.hip", "topk.hip", "slice.hip", "greedy.hip", "mean.hip", "sample.hip", "validate.hip", "hub.hip", "api.hip"]
+SOURCES = ["spmm.hip", "scores.hip", "topk.hip", "slice.hip", "greedy.hip", "mean.hip", "sample.hip", "validate.hip", "hub.hip", "probe.hip", "api.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

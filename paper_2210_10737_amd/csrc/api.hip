@@ -479,6 +479,29 @@ rsc_status_t rsc_spmm_plan_run(rsc_spmm_plan_t *p, const float *B, int32_t d, in
     return RSC_OK;
 }
 
+rsc_status_t rsc_spmm_plan_gather_probe(rsc_spmm_plan_t *p, const float *B, int32_t d, int64_t ldb, int32_t inflight,
+                                       float *sink, int64_t sink_count, int32_t *slice_out, hipStream_t stream) {
+    if (!p) return fail(RSC_ERR_INVALID_ARGUMENT, "plan is NULL");
+    const rsc_csr_t *A = &p->A;
+    RSC_TRY(check_dense(B, A->n_cols, d, ldb, "B"));
+    if (inflight != 4 && inflight != 8 && inflight != 16)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "inflight = %d (4, 8 or 16)", inflight);
+    const int64_t need = rsc::gather_probe_sink_count(A->nnz);
+    if (sink_count < need) return fail(RSC_ERR_CAPACITY, "sink holds %lld floats, %lld needed", (long long)sink_count,
+                                       (long long)need);
+    if (need > 0 && !sink) return fail(RSC_ERR_INVALID_ARGUMENT, "sink is NULL");
+    RSC_TRY(check_same_device(p->device, "plan"));
+    // the feature passes and cache policy an unblocked run of the plan takes
+    const int32_t slice = rsc::spmm_slice_width(A->n_rows, A->nnz, A->n_cols, d);
+    const bool hint = p->colf != nullptr && rsc::spmm_hint_taken(A->n_cols, d, slice);
+    if (slice_out) *slice_out = slice;
+    RSC_HIP(rsc::gather_probe_launch(p->colf ? p->colf : A->col, A->nnz, B, ldb, d, slice, hint, inflight, sink,
+                                     stream),
+            "gather probe launch");
+    RSC_HIP(p->fence.record(stream), "gather probe event");
+    return RSC_OK;
+}
+
 rsc_status_t rsc_spmm_noalloc(const rsc_csr_t *A, const float *B, int32_t d, int64_t ldb, float *Y, int64_t ldy,
                               hipStream_t stream) {
     RSC_TRY(check_csr(A, "A"));

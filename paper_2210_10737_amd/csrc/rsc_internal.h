@@ -46,6 +46,9 @@ int32_t spmm_column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src);
 hipError_t spmm_split_launch(int32_t n_rows, int32_t n_cols, const int32_t *rowptr, const int32_t *col, int32_t P,
                              int32_t *S, hipStream_t stream);
 bool spmm_use_order(int32_t n_rows, int64_t nnz);
+// whether a pass `slice` floats wide over n_src B rows takes the hub hint
+// (on a column copy that carries it)
+bool spmm_hint_taken(int64_t n_src, int32_t d, int32_t slice);
 hipError_t spmm_rows_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr, void *ws,
                              hipStream_t stream);
 hipError_t spmm_blocked_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t *S, int32_t P, void *ws,
@@ -55,6 +58,11 @@ size_t spmm_blocked_fits(int32_t n_rows, int64_t nnz_bound, int32_t P);  // work
 // least this much a launch runs, blocked only if the blocked buffers also fit
 size_t spmm_core_ws_bytes(int32_t n_rows, int64_t nnz_bound);
 const int32_t *spmm_long_count_of(const void *ws);
+
+// ---- gather-ceiling probe (measurement helper) ---------------------------
+int64_t gather_probe_sink_count(int64_t nnz);
+hipError_t gather_probe_launch(const int32_t *col, int64_t nnz, const float *B, int64_t ldb, int32_t d, int32_t slice,
+                               bool hint, int32_t inflight, float *sink, hipStream_t stream);
 
 // ---- scores ------------------------------------------------------------
 hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,

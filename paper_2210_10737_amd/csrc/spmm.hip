@@ -596,6 +596,10 @@ int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) 
 
 bool spmm_use_order(int32_t n_rows, int64_t nnz) { return use_order(n_rows, nnz); }
 
+bool spmm_hint_taken(int64_t n_src, int32_t d, int32_t slice) {
+    return use_hint() && (double)n_src * std::min(d, slice) * sizeof(float) > kHintBytes;
+}
+
 hipError_t spmm_rows_prepare(int32_t n_rows, int64_t nnz_bound, const int32_t *rowptr, void *ws,
                              hipStream_t stream) {
     if (n_rows == 0) return hipSuccess;
@@ -715,8 +719,7 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
     const int32_t slice = spmm_slice_width(n_rows, nnz_hint, n_src_hint, d);
     // the hint pays off only when the gathered rows far outgrow the on-chip
     // caches (MALL included); below that, bypassing them loses reuse
-    const bool hint = hint_cols && use_hint() &&
-                      (double)n_src_hint * std::min(d, slice) * sizeof(float) > kHintBytes;
+    const bool hint = hint_cols && spmm_hint_taken(n_src_hint, d, slice);
     for (int32_t f0 = 0; f0 < d;) {
         const int32_t dl = std::min<int32_t>(d - f0, slice);
 #define RSC_SPMM_LAUNCH_H(LPE_, NV_, H_)                                                               \

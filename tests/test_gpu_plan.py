@@ -229,3 +229,33 @@ def test_binding_refuses_tensors_off_the_current_device():
     Xh = rsc.DeviceCsr(A.n, A.n, torch.from_numpy(A.rowptr), torch.from_numpy(A.col), torch.from_numpy(A.val))
     with pytest.raises(ValueError, match="current device"):
         rsc.spmm(Xh, H.cuda())
+
+
+@pytest.mark.parametrize("d", [64, 100, 256, 512])
+@pytest.mark.parametrize("wide", [False, True])
+def test_gather_probe_gathers_the_plan_rows(d, wide):
+    # The gather-ceiling probe loads exactly the B rows of the column stream:
+    # the float it writes per 64 entries equals the sum of those rows' last
+    # feature pass (the sink is rewritten by every pass).
+    if wide:
+        A, n_cols = wide_graph(3)
+    else:
+        A = synth.random_csr(3000, 2500, 400, seed=8, hub_rows=5, hub_len=2400)
+        n_cols = 2500
+    B = synth.dense_normal(n_cols, d, seed=9)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
+    plan = rsc.SpmmPlan(X)
+    Bd = torch.from_numpy(B).cuda()
+    nnz = int(A.rowptr[-1])
+    chunks = (nnz + 63) // 64
+    for inflight in (4, 8, 16):
+        sink = torch.full((chunks,), float("nan"), device="cuda")
+        slice_w = plan.gather_probe(Bd, inflight=inflight, sink=sink)
+        got = sink.cpu().numpy().astype(np.float64)
+        f_last = ((d - 1) // slice_w) * slice_w
+        part = B[:, f_last:d].astype(np.float64)
+        pad = np.zeros(chunks * 64 - nnz)
+        want = np.concatenate([part.sum(axis=1)[A.col], pad]).reshape(chunks, 64).sum(axis=1)
+        mag = np.concatenate([np.abs(part).sum(axis=1)[A.col], pad]).reshape(chunks, 64).sum(axis=1)
+        assert np.all(np.abs(got - want) <= 1e-4 * mag + 1e-30), (d, wide, inflight, slice_w)
+    plan.close()
