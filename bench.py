@@ -123,48 +123,95 @@ def _cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(A, Hh, Gh, k, pct, refresh_interval, step_bytes_full, n_rows_sample,
-                 min_s: float = 10.0, max_reps: int = 8):
-    """Oracle timing on a bounded sample: the refresh (pair keys, top-k,
-    slice) on the whole graph, and both SpMMs on the first n_rows_sample rows
-    (the step time is extrapolated linearly in rows); repeated until about
-    min_s seconds of CPU work, each op's median taken."""
-    import numpy as np
+def _oracle_ops(A, Hh, Gh, k, rows):
+    """One pass of the hot path through the oracle, each operation timed on
+    its own (seconds): the exact SpMM, the column square-norms cn2, the pair
+    keys (row norms of the backward operand), the top-k selection (full
+    sort), the CSR slice, and the sampled SpMM on the slice. With `rows` the
+    two SpMMs compute only those rows."""
     import oracle
+    t = {}
+    t0 = time.perf_counter()
+    oracle.spmm(A.rowptr, A.col, A.val, Hh, rows=rows)
+    t["exact_spmm"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)   # A_hat is symmetric: its transpose's CSR is its own
+    t["cn2"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    key = oracle.pair_keys(cn2, Gh)["key"]
+    t["keys"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    idx, mask = oracle.topk(key, k)
+    t["select"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+    t["slice"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.spmm(ro, co, vo, Gh, rows=rows)
+    t["sampled_spmm"] = time.perf_counter() - t0
+    return t
+
+
+def cpu_baseline(A, Hh, Gh, k, pct, refresh_interval, step_bytes_full, n_rows_sample,
+                 min_s: float = 10.0, max_reps: int = 5):
+    """Oracle timing on the GPU machine's host cores: every operation of the hot
+    path timed separately (exact SpMM, cn2, keys, select, slice, sampled
+    SpMM), repeated until about min_s seconds of CPU work (at most max_reps),
+    median per operation, with all the oracle's threads; the SpMMs on the
+    first n_rows_sample rows (scaled linearly to the whole graph when that is
+    fewer than all). The step time is exact + sampled SpMM plus one refresh
+    (keys, select, slice) per refresh_interval steps; cn2 is computed once per
+    graph and reported apart. Then the tiny workload (4,096 nodes) the same
+    way on one thread and on all of them, in this process."""
+    import numpy as np
+
+    import oracle
+    import synth
     n = A.n
-    rows = np.arange(n_rows_sample, dtype=np.int32)
-    cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)
-    te, tr, ts = [], [], []
+    rows = None if n_rows_sample >= n else np.arange(n_rows_sample, dtype=np.int32)
+    scale = 1.0 if rows is None else n / n_rows_sample
+    cores = oracle.num_threads()
+    reps = []
     t_all = time.perf_counter()
-    while len(te) < max_reps and (time.perf_counter() - t_all < min_s or not te):
-        t0 = time.perf_counter()
-        oracle.spmm(A.rowptr, A.col, A.val, Hh, rows=rows)
-        te.append(time.perf_counter() - t0)
-        t0 = time.perf_counter()
-        key = oracle.pair_keys(cn2, Gh)["key"]
-        idx, mask = oracle.topk(key, k)
-        ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
-        tr.append(time.perf_counter() - t0)
-        t0 = time.perf_counter()
-        oracle.spmm(ro, co, vo, Gh, rows=rows)
-        ts.append(time.perf_counter() - t0)
+    while len(reps) < max_reps and (time.perf_counter() - t_all < min_s or not reps):
+        reps.append(_oracle_ops(A, Hh, Gh, k, rows))
     measured = time.perf_counter() - t_all
-    scale = n / n_rows_sample
-    t_exact, t_refresh, t_sampled = (float(np.median(x)) for x in (te, tr, ts))
-    step_s = (t_exact + t_sampled) * scale + t_refresh / refresh_interval
+    med = {op: float(np.median([r[op] for r in reps])) for op in reps[0]}
+    for op in ("exact_spmm", "sampled_spmm"):
+        med[op] *= scale
+    refresh_s = med["keys"] + med["select"] + med["slice"]
+    step_s = med["exact_spmm"] + med["sampled_spmm"] + refresh_s / refresh_interval
+
+    # the tiny workload on one core and on all of them (same process)
+    w = synth.WORKLOADS["tiny"]
+    At = synth.make_graph("tiny", 0)
+    Ht = synth.dense_normal(At.n, w.d, seed=1)
+    Gt = synth.dense_normal(At.n, w.d, seed=3)
+    kt = (At.n * w.budgets_pct[0]) // 100
+    tiny = {}
+    try:
+        for label, threads in (("one_core", 1), ("all_cores", cores)):
+            oracle.set_num_threads(threads)
+            rt = [_oracle_ops(At, Ht, Gt, kt, None) for _ in range(5)]
+            tiny[label] = {"threads": oracle.num_threads(),
+                           "ms": {op: round(float(np.median([r[op] for r in rt])) * 1e3, 3) for op in rt[0]}}
+    finally:
+        oracle.set_num_threads(cores)
     return {
         "value": round(step_bytes_full / step_s / 1e9, 3),
         "unit": "GB/s",
-        "cores": oracle.num_threads(),
+        "cores": cores,
         "kind": "oracle",
-        "sample": (f"exact and sampled SpMM on rows [0, {n_rows_sample}) of {n} "
-                   f"(x{scale:.1f} to the full graph), one refresh (keys, top-k at {pct}%, slice) "
-                   f"on the whole graph amortised over {refresh_interval} steps; {len(te)} repetitions, "
-                   f"median per op"),
+        "sample": (("exact and sampled SpMM over every row" if rows is None else
+                    f"exact and sampled SpMM on rows [0, {n_rows_sample}) of {n} (x{scale:.1f} to the full graph)")
+                   + f"; cn2, keys, top-k at {pct}% and slice on the whole graph, the refresh amortised over "
+                   f"{refresh_interval} steps; {len(reps)} repetitions, median per operation"),
         "ms_per_step": round(step_s * 1e3, 1),
-        "exact_spmm_ms": round(t_exact * scale * 1e3, 1),
-        "sampled_spmm_ms": round(t_sampled * scale * 1e3, 1),
-        "refresh_ms": round(t_refresh * 1e3, 1),
+        "ops_ms": {op: round(v * 1e3, 2) for op, v in med.items()},
+        "exact_spmm_ms": round(med["exact_spmm"] * 1e3, 1),
+        "sampled_spmm_ms": round(med["sampled_spmm"] * 1e3, 1),
+        "refresh_ms": round(refresh_s * 1e3, 1),
+        "tiny_workload": {"n": At.n, "nnz": At.nnz, "d": w.d, "budget_pct": w.budgets_pct[0], **tiny},
         "cpu_model": _cpu_model(),
         "measured_s": round(measured, 2),
     }

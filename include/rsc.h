@@ -351,6 +351,18 @@ rsc_status_t rsc_spmm_sampled(rsc_cache_t *cache, const float *B, int32_t d, int
  * output pointer may be NULL. */
 rsc_status_t rsc_cache_buffers(rsc_cache_t *cache, const double **cn2, const int32_t **colnnz,
                                const uint64_t **key, const double **rn2, const uint32_t **mask);
+/* The Frobenius normalisers of Eq. 4a: *fro_x2_host = ||X||_F^2 = the sum of
+ * the column square-norms cn2 (computed at create), *fro_b2_host =
+ * ||B||_F^2 = the sum of the row square-norms rn2 of the operand last scored
+ * (rsc_cache_score / refresh; RSC_ERR_INVALID_ARGUMENT before any score).
+ * Both are fp64 sums computed on the device in one fixed order (blocks of
+ * 8,192 consecutive terms, each thread summing 32 terms 256 apart in turn,
+ * then fixed binary trees over the threads and over the blocks), so they are
+ * bitwise reproducible; for these non-negative terms they lie within
+ * (n - 1) units of roundoff of the sequential sum. [sync]: waits for
+ * `stream`, on which the scores were enqueued. Either pointer may be NULL. */
+rsc_status_t rsc_cache_norms(rsc_cache_t *cache, double *fro_x2_host, double *fro_b2_host,
+                             hipStream_t stream);
 /* Waits (on the host) for the work this cache's own calls enqueued, on
  * every stream they used, then frees its buffers (stream-ordered, on a
  * library-owned stream of the cache's device; through the allocator for a

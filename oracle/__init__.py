@@ -54,6 +54,12 @@ def _load():
         lib.orc_greedy.argtypes = [i32, i32, i64, vp, vp, vp, f64, vp, i32, i32, i32, i32, vp]
         lib.orc_greedy.restype = i64
         lib.orc_num_threads.restype = i32
+        lib.orc_set_num_threads.argtypes = [i32]
+        lib.orc_set_num_threads.restype = i32
+        lib.orc_sum_sequential.argtypes = [i64, vp]
+        lib.orc_sum_sequential.restype = f64
+        lib.orc_selection_auc.argtypes = [i32, vp, vp, vp, vp]
+        lib.orc_selection_auc.restype = f64
         lib.orc_spmm_mean.argtypes = [i32, vp, vp, vp, vp, i32, i64, vp, i64]
         lib.orc_splitmix64.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
         lib.orc_splitmix64.restype = ctypes.c_uint64
@@ -212,6 +218,33 @@ def slice_scaled(rowptr, col, val, mask, colw):
 
 def num_threads() -> int:
     return int(_load().orc_num_threads())
+
+
+def set_num_threads(t: int) -> int:
+    """Thread count of the oracle's row loops from now on; returns it."""
+    return int(_load().orc_set_num_threads(int(t)))
+
+
+def sum_sequential(x) -> float:
+    """Plain sequential fp64 sum (Eq. 4a's Frobenius normalisers)."""
+    x = _c(x, np.float64)
+    return float(_load().orc_sum_sequential(len(x), _p(x)))
+
+
+def selection_staleness(order, prev_mask, new_mask=None):
+    """(AUC of the previous selection under the new ranking `order`, overlap
+    |S_prev & S_new| / |S_prev|) for masks of ceil(n/32) words; AUC NaN for an
+    empty or full selection, overlap None without new_mask or for an empty
+    previous selection."""
+    order = _c(order, np.int32)
+    n = len(order)
+    prev_mask = _c(prev_mask, np.uint32)
+    nm = None if new_mask is None else _c(new_mask, np.uint32)
+    both = ctypes.c_int64(0)
+    auc = _load().orc_selection_auc(n, _p(order), _p(prev_mask), _p(nm), ctypes.byref(both))
+    k = int(np.unpackbits(prev_mask.view(np.uint8), bitorder="little")[:n].sum())
+    overlap = None if (nm is None or k == 0) else both.value / k
+    return float(auc), overlap
 
 
 class CachePolicy:

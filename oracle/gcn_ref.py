@@ -10,17 +10,24 @@ scored (O4 keys of the fp32-rounded gradients), k_l comes from the greedy of
 section 3.2.1 (O8) and each layer's columns are selected (O5) and sliced (O6).
 Products are scipy sparse / numpy dense in fp64.
 
+With track_staleness, each refresh after the first also records, per layer,
+the staleness of the cached selection (section 3.3.1, Fig. 4): the AUC of
+the previous selection under the new ranking and the overlap of the two
+selections, counted by orc_selection_auc; with the k_l of every refresh this
+is the trace of Fig. 7.
+
 Pins (tests/test_oracle_pins.py): the exact-mode gradients against central
 differences of the reported loss, the loss at zero logits (ln 2), and a
 full-budget step between refreshes against the exact gradients; the
-aggregation steps it uses (O3-O8) are pinned there too.
+aggregation steps it uses (O3-O8) are pinned there too; the staleness
+record against brute force over all (selected, unselected) pairs.
 """
 from __future__ import annotations
 
 import numpy as np
 import scipy.sparse as sp
 
-from . import col_sqnorms, greedy, pair_keys, slice_csr, topk
+from . import col_sqnorms, greedy, pair_keys, rank_order, selection_staleness, slice_csr, sum_sequential, topk
 
 
 class RscReference:
@@ -29,25 +36,31 @@ class RscReference:
     product, instead of reusing the slice of the last refresh (the
     no-caching arm of section 3.3.1's comparison)."""
 
-    def __init__(self, rowptr, col, val, n, widths, budget, alpha, refresh_interval, cache=True):
+    def __init__(self, rowptr, col, val, n, widths, budget, alpha, refresh_interval, cache=True,
+                 track_staleness=False):
         self.n = n
         self.A = sp.csr_matrix((val.astype(np.float64), col, rowptr), shape=(n, n))
         self.AT = self.A.T.tocsr()
         self.csr_t = (rowptr, col, val)  # A^T of a symmetric A is A itself
         self.cn2, self.colnnz = col_sqnorms(rowptr, val)
-        self.fro_a2 = float(self.cn2.sum())
+        self.fro_a2 = sum_sequential(self.cn2)      # ||A||_F^2 (Eq. 4a)
         self.nnz = int(rowptr[-1])
         self.widths = list(widths)
         self.budget, self.alpha, self.R = budget, alpha, refresh_interval
         self.last = None
         self.k = [n] * len(widths)
         self.idx = [None] * len(widths)
+        self.masks = [None] * len(widths)
+        self.refresh_masks = [None] * len(widths)   # the selections of the last refresh
         self.slices = [None] * len(widths)
         self.cache = cache
+        self.track = track_staleness
+        self.history = []   # one record per refresh: step, k, auc, overlap
 
     def _select(self, l, key):
         rowptr, col, val = self.csr_t
         self.idx[l], mask = topk(key, self.k[l])
+        self.masks[l] = mask
         ro, co, vo = slice_csr(rowptr, col, val, mask)
         self.slices[l] = sp.csr_matrix((vo.astype(np.float64), co, ro), shape=(self.n, self.n))
 
@@ -58,7 +71,13 @@ class RscReference:
             return self.slices[l] @ g
         return self.AT @ g
 
-    def step(self, X, W1, W2, Y, step):
+    def step(self, X, W1, W2, Y, step, score_inputs=None):
+        """One training step with weights W1, W2. score_inputs (optional,
+        used at refresh steps only): (keys per layer, ||grad H||_F^2 per layer,
+        ||A||_F^2) to take instead of the values this step computes, so that a
+        run can be followed on exactly the inputs another implementation
+        scored; the ones computed here are still returned as keys_own and
+        fro_b2_own."""
         mode = "score" if (self.last is None or step - self.last >= self.R) else "sampled"
         J1 = X @ W1
         P1 = self.A @ J1
@@ -78,11 +97,23 @@ class RscReference:
             for g in (gP1, gP2):
                 o = pair_keys(self.cn2, g.astype(np.float32))
                 keys.append(o["key"])
-                fro_b2.append(float(o["rn2"].sum()))
-            self.k, _ = greedy(keys, self.colnnz, self.nnz, self.widths, self.fro_a2, fro_b2,
+                fro_b2.append(sum_sequential(o["rn2"]))     # ||grad H||_F^2 (Eq. 4a)
+            out["keys_own"], out["fro_b2_own"] = keys, fro_b2
+            fro_a2 = self.fro_a2
+            if score_inputs is not None:
+                keys, fro_b2, fro_a2 = score_inputs
+            self.k, _ = greedy(keys, self.colnnz, self.nnz, self.widths, fro_a2, fro_b2,
                                self.budget, self.alpha)
+            rec = {"step": step, "k": list(self.k), "auc": [], "overlap": []}
             for l in range(2):
+                prev = self.refresh_masks[l]
                 self._select(l, keys[l])
+                self.refresh_masks[l] = self.masks[l]
+                if self.track and prev is not None:
+                    auc, overlap = selection_staleness(rank_order(keys[l]), prev, self.masks[l])
+                    rec["auc"].append(auc)
+                    rec["overlap"].append(overlap)
+            self.history.append(rec)
             self.last = step
         out["k"] = list(self.k)
         out["idx"] = [None if i is None else i.copy() for i in self.idx]

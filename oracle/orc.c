@@ -297,6 +297,13 @@ int64_t orc_greedy(int32_t L, int32_t n, int64_t nnz, const uint64_t *const *key
 #include <omp.h>
 int32_t orc_num_threads(void) { return (int32_t)omp_get_max_threads(); }
 
+/* Sets the thread count of the following row loops (the CPU baseline times
+ * the oracle on all host cores and on one); returns the count now in force. */
+int32_t orc_set_num_threads(int32_t t) {
+    if (t >= 1) omp_set_num_threads(t);
+    return (int32_t)omp_get_max_threads();
+}
+
 /* ------------------------------------------------------------------------ */
 /* SpMM_MEAN (appendix A.3): the MEAN aggregator D^-1 A H, D the degree
  * matrix of A, read as D_ii = number of stored entries of row i (the paper's
@@ -416,4 +423,44 @@ int64_t orc_slice_scaled(int32_t n_rows, const int32_t *rowptr, const int32_t *c
         rowptr_out[i + 1] = (int32_t)w;
     }
     return w;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Eq. 4a's normalisers: ||A||_F^2 is the sum of the column square-norms cn2
+ * and ||grad H||_F^2 the sum of the row square-norms rn2. The plain
+ * sequential fp64 sum of x[0..n). */
+double orc_sum_sequential(int64_t n, const double *x) {
+    double s = 0.0;
+    for (int64_t i = 0; i < n; ++i) s += x[i];
+    return s;
+}
+
+/* Staleness of a cached selection (section 3.3.1, Fig. 4: how well the top-k
+ * pairs chosen at one refresh still match the ranking at the next). With S
+ * the previous selection (prev_mask bit i set iff i in S, |S| = k) and
+ * `order` the new ranking of the n pairs, best first, the matching score is
+ * the AUC of S under that ranking: among all pairs (i in S, j not in S), the
+ * fraction in which i is ranked before j. Counted directly: walking the
+ * ranking from the best pair, each pair outside S is preceded by every pair
+ * of S seen so far. Returns NaN when S is empty or holds every pair.
+ * *overlap_count (nullable) receives |S cap S_new| with S_new given by
+ * new_mask (nullable: then 0). */
+double orc_selection_auc(int32_t n, const int32_t *order, const uint32_t *prev_mask, const uint32_t *new_mask,
+                         int64_t *overlap_count) {
+    int64_t k = 0, seen = 0, pairs_above = 0, both = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        int in_prev = (prev_mask[i >> 5] >> (i & 31)) & 1u;
+        k += in_prev;
+        if (new_mask && in_prev && ((new_mask[i >> 5] >> (i & 31)) & 1u)) ++both;
+    }
+    if (overlap_count) *overlap_count = both;
+    if (k == 0 || k == n) return NAN;
+    for (int32_t p = 0; p < n; ++p) {
+        int32_t i = order[p];
+        if ((prev_mask[i >> 5] >> (i & 31)) & 1u)
+            ++seen;
+        else
+            pairs_above += seen;
+    }
+    return (double)pairs_above / ((double)k * (double)(n - k));
 }

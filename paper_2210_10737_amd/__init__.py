@@ -50,7 +50,7 @@ EXPORTED = [
     "rsc_cache_create", "rsc_cache_create_ex", "rsc_cache_refresh", "rsc_cache_score", "rsc_cache_select",
     "rsc_cache_refresh_random",
     "rsc_cache_get", "rsc_spmm_sampled",
-    "rsc_cache_buffers", "rsc_cache_destroy",
+    "rsc_cache_buffers", "rsc_cache_norms", "rsc_cache_destroy",
     "rsc_k_from_fraction", "rsc_greedy_allocate",
     "rsc_greedy_profile_workspace_bytes", "rsc_greedy_blocks", "rsc_greedy_profile",
     "rsc_greedy_allocate_profiles",
@@ -140,6 +140,8 @@ def lib():
             "rsc_cache_buffers": ([vp, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
                                    ctypes.POINTER(vp), ctypes.POINTER(vp)], ctypes.c_int),
             "rsc_cache_destroy": ([vp], ctypes.c_int),
+            "rsc_cache_norms": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), vp],
+                                ctypes.c_int),
             "rsc_k_from_fraction": ([i32, i32, i32], i32),
             "rsc_greedy_allocate": ([i32, i32, i64, vp, vp, vp, ctypes.c_double, vp, i32, i32, i32,
                                      i32, vp, vp], ctypes.c_int),
@@ -453,6 +455,13 @@ class Cache:
         Y = _new_out(self.X.n_rows, d, B.device) if out is None else out
         _check(lib().rsc_spmm_sampled(self._h, _dp(B), d, _ld(B), _dp(Y), _ld(Y), _stream()))
         return Y
+
+    def norms(self, scored: bool = True):
+        """(||X||_F^2, ||B||_F^2 of the last scored operand) from the device's
+        fixed-order sums (rsc_cache_norms); the second is None with scored=False."""
+        fx, fb = ctypes.c_double(), ctypes.c_double()
+        _check(lib().rsc_cache_norms(self._h, ctypes.byref(fx), ctypes.byref(fb) if scored else None, _stream()))
+        return fx.value, (fb.value if scored else None)
 
     def buffers(self):
         """Device pointers [cn2, colnnz, key, rn2, mask]."""

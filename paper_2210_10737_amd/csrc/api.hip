@@ -253,6 +253,8 @@ struct rsc_cache {
     int32_t *colnnz = nullptr;
     uint64_t *key = nullptr;
     double *rn2 = nullptr;  // row square-norms of the last scored dense operand
+    double *norms = nullptr;   // [0] = sum of cn2 (||X||_F^2), [1] = sum of rn2 of the last scored operand
+    double *sum_ws = nullptr;  // block sums of the fixed-order reductions
     int32_t *count = nullptr;  // randomized refresh: draws per column
     double *colw = nullptr;    // randomized refresh: per-column scale
     void *ws_sample = nullptr;
@@ -639,8 +641,9 @@ rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, const doubl
 // frees the cache's memory: through its allocator, or ordered on `s`
 static void cache_free(rsc_cache_t *c, hipStream_t s) {
     if (!c) return;
-    void *dev[] = {c->cn2, c->colnnz, c->key, c->rn2, c->count, c->colw, c->idx, c->mask, c->s_rowptr,
-                   c->s_col, c->s_val, c->d_nnz, c->ws_topk, c->ws_slice, c->ws_spmm, c->ws_sample, c->s_split};
+    void *dev[] = {c->cn2, c->colnnz, c->key, c->rn2, c->norms, c->sum_ws, c->count, c->colw, c->idx, c->mask,
+                   c->s_rowptr, c->s_col, c->s_val, c->d_nnz, c->ws_topk, c->ws_slice, c->ws_spmm, c->ws_sample,
+                   c->s_split};
     for (void *p : dev) {
         if (!p) continue;
         if (c->alloc.alloc)
@@ -694,6 +697,8 @@ rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_
         {(void **)&c->colnnz, sizeof(int32_t) * n},
         {(void **)&c->key, sizeof(uint64_t) * n},
         {(void **)&c->rn2, sizeof(double) * n},
+        {(void **)&c->norms, sizeof(double) * 2},
+        {(void **)&c->sum_ws, rsc::sum_ws_bytes(n)},
         {(void **)&c->count, sizeof(int32_t) * n},
         {(void **)&c->colw, sizeof(double) * n},
         {(void **)&c->idx, sizeof(int32_t) * n},
@@ -730,6 +735,7 @@ rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_
     if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev, hipEventDisableTiming);
     if (e == hipSuccess) e = free_stream_of_current_device(&c->free_stream);
     if (e == hipSuccess) e = rsc::col_sqnorms_launch(XT->n_rows, XT->rowptr, XT->val, c->cn2, c->colnnz, stream);
+    if (e == hipSuccess) e = rsc::sum_fixed_order_launch(c->cn2, c->n, c->sum_ws, c->norms, stream);
     // whether X has long rows at all: a slice's rows are parts of X's, so if
     // none is long, the sampled products need no long-row pass
     int32_t x_long = 0;
@@ -783,6 +789,7 @@ rsc_status_t rsc_cache_score(rsc_cache_t *c, const float *B, int32_t d, int64_t 
     RSC_TRY(check_dense(B, c->n, d, ldb, "B"));
     RSC_TRY(check_same_device(c->device, "cache"));
     RSC_HIP(rsc::pair_scores_launch(c->cn2, B, c->n, d, ldb, c->key, nullptr, c->rn2, stream), "cache scores");
+    RSC_HIP(rsc::sum_fixed_order_launch(c->rn2, c->n, c->sum_ws, c->norms + 1, stream), "cache norm sum");
     c->scored = true;
     RSC_HIP(c->fence.record(stream), "cache event");
     return RSC_OK;
@@ -900,6 +907,18 @@ rsc_status_t rsc_cache_buffers(rsc_cache_t *c, const double **cn2, const int32_t
     if (key) *key = c->key;
     if (rn2) *rn2 = c->rn2;
     if (mask) *mask = c->mask;
+    return RSC_OK;
+}
+
+rsc_status_t rsc_cache_norms(rsc_cache_t *c, double *fro_x2_host, double *fro_b2_host, hipStream_t stream) {
+    if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
+    if (fro_b2_host && !c->scored) return fail(RSC_ERR_INVALID_ARGUMENT, "cache norms before any score");
+    RSC_TRY(check_same_device(c->device, "cache"));
+    double h[2] = {0.0, 0.0};
+    RSC_HIP(hipMemcpyAsync(h, c->norms, sizeof h, hipMemcpyDeviceToHost, stream), "cache norms read");
+    RSC_HIP(hipStreamSynchronize(stream), "cache norms wait");
+    if (fro_x2_host) *fro_x2_host = h[0];
+    if (fro_b2_host) *fro_b2_host = h[1];
     return RSC_OK;
 }
 

@@ -67,6 +67,10 @@ hipError_t gather_probe_launch(const int32_t *col, int64_t nnz, const float *B, 
 // ---- scores ------------------------------------------------------------
 hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,
                               int32_t *colnnz, hipStream_t stream);
+// out = sum of x[0..n) in one fixed order (fp64; 0 for n = 0); ws holds
+// sum_ws_bytes(n) bytes of block sums
+size_t sum_ws_bytes(int64_t n);
+hipError_t sum_fixed_order_launch(const double *x, int64_t n, double *ws, double *out, hipStream_t stream);
 hipError_t pair_scores_launch(const double *cn2, const float *B, int32_t n, int32_t d, int64_t ldb,
                               uint64_t *key, float *score, double *rn2, hipStream_t stream);
 

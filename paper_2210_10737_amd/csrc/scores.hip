@@ -108,7 +108,61 @@ __global__ __launch_bounds__(256) void pair_scores_kernel(const double *__restri
     }
 }
 
+// Frobenius normalisers of Eq. 4a (||X||_F^2 = sum of cn2, ||B||_F^2 = sum
+// of rn2) as fp64 sums in one fixed order, so the greedy's cross-layer
+// comparison is bitwise reproducible: block b sums elements
+// [b * kSumChunk, (b + 1) * kSumChunk), each thread its 32 elements t, t + 256,
+// ... one after another, then the 256 thread sums in a fixed binary tree;
+// one block adds the block sums the same way. Summing non-negative terms in
+// any order stays within (n - 1) units of roundoff of the sequential sum.
+constexpr int kSumThreads = 256;
+constexpr int kSumPer = 32;
+constexpr int kSumChunk = kSumThreads * kSumPer;
+
+__device__ __forceinline__ double block_tree_sum(double v, double *lds) {
+    const int t = threadIdx.x;
+    lds[t] = v;
+    __syncthreads();
+    for (int h = kSumThreads / 2; h > 0; h >>= 1) {
+        if (t < h) lds[t] = lds[t] + lds[t + h];
+        __syncthreads();
+    }
+    return lds[0];
+}
+
+__global__ __launch_bounds__(kSumThreads) void sum_chunks_kernel(const double *__restrict__ x, int64_t n,
+                                                                 double *__restrict__ part) {
+    __shared__ double lds[kSumThreads];
+    const int64_t base = (int64_t)blockIdx.x * kSumChunk + threadIdx.x;
+    double acc = 0.0;
+#pragma unroll
+    for (int j = 0; j < kSumPer; ++j) {
+        const int64_t i = base + (int64_t)kSumThreads * j;
+        if (i < n) acc += x[i];
+    }
+    const double s = block_tree_sum(acc, lds);
+    if (threadIdx.x == 0) part[blockIdx.x] = s;
+}
+
+__global__ __launch_bounds__(kSumThreads) void sum_parts_kernel(const double *__restrict__ part, int64_t np,
+                                                                double *__restrict__ out) {
+    __shared__ double lds[kSumThreads];
+    double acc = 0.0;
+    for (int64_t i = threadIdx.x; i < np; i += kSumThreads) acc += part[i];
+    const double s = block_tree_sum(acc, lds);
+    if (threadIdx.x == 0) *out = s;
+}
+
 }  // namespace
+
+size_t sum_ws_bytes(int64_t n) { return sizeof(double) * (size_t)std::max<int64_t>(1, ceil_div(n, kSumChunk)); }
+
+hipError_t sum_fixed_order_launch(const double *x, int64_t n, double *ws, double *out, hipStream_t stream) {
+    const int64_t np = ceil_div(n, kSumChunk);
+    if (np > 0) sum_chunks_kernel<<<(unsigned)np, kSumThreads, 0, stream>>>(x, n, ws);
+    sum_parts_kernel<<<1, kSumThreads, 0, stream>>>(ws, np, out);
+    return hipGetLastError();
+}
 
 hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,
                               int32_t *colnnz, hipStream_t stream) {

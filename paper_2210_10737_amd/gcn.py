@@ -145,10 +145,9 @@ class RscController:
         A = layers[0].AT
         self.n = A.n_cols
         self.nnz = A.nnz
-        cn2_ptr, colnnz_ptr = layers[0].cache.buffers()[:2]
-        torch.cuda.synchronize()
-        self.colnnz_ptr = colnnz_ptr
-        self.fro_a2 = float(copy_to_host(cn2_ptr, self.n, np.float64).sum())
+        self.colnnz_ptr = layers[0].cache.buffers()[1]
+        # ||A_hat^T||_F^2 (Eq. 4a's normaliser), summed on the device in a fixed order
+        self.fro_a2 = layers[0].cache.norms(scored=False)[0]
         dev = A.rowptr.device
         nb = lib().rsc_greedy_blocks(self.n, cfg.alpha[0], cfg.alpha[1])
         self.mass = torch.empty((len(layers), max(nb, 1)), dtype=torch.float64, device=dev)
@@ -196,7 +195,7 @@ class RscController:
                                             self.count[l].data_ptr(),
                                             None if self.order is None else self.order.data_ptr(),
                                             self.ws.data_ptr(), self.ws.numel(), _stream()))
-            fro_b2.append(float(copy_to_host(ptrs[3], self.n, np.float64).sum()))
+            fro_b2.append(layer.cache.norms()[1])   # ||grad H||_F^2 of the scored gradient (device sum)
             if self.order is not None and self.prev_idx[l] is not None:
                 rec.auc.append(selection_auc(self.order.cpu().numpy(), self.prev_idx[l]))
         masses = self.mass[:, :self.nb].cpu().numpy()

@@ -179,3 +179,88 @@ def test_staleness_tracking():
     for r in recs[1:]:
         assert r.auc == [1.0, 1.0] and r.overlap == [1.0, 1.0]
     model.close()
+
+
+def test_staleness_matches_reference_with_moving_weights():
+    """NEXT-4 under training: 21 steps with Adam (the weights move), refresh
+    every 3 steps. At each refresh the fp64 reference takes the keys and
+    ||grad H||_F^2 the GPU scored (its own, from its fp64 gradients, are
+    checked against them within fp32 rounding), so both sides allocate and
+    select on identical inputs: k_l, the selections, the AUC of each
+    previous selection under the new ranking and the overlaps must then
+    agree exactly (AUC within 1e-12), and the losses and gradients of every
+    step within fp32 tolerance."""
+    A = synth.make_graph("tiny", 0)
+    n = A.n
+    X = synth.dense_normal(n, 32, seed=1)
+    Y = (np.random.default_rng(3).random((n, 16)) < 0.5).astype(np.float32)
+    cfg = RscConfig(budget=(1, 4), alpha=(2, 100), refresh_interval=3, track_staleness=True)
+    model = GCN(rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n), 32, 64, 16, cfg, seed=2)
+    ref = RscReference(A.rowptr, A.col, A.val, n, [64, 16], (1, 4), (2, 100), 3, track_staleness=True)
+    assert abs(model.controller.fro_a2 - ref.fro_a2) <= 1e-12 * ref.fro_a2
+    opt = torch.optim.Adam(model.parameters(), lr=0.01)
+    Xd, Yd = torch.from_numpy(X).cuda(), torch.from_numpy(Y).cuda()
+    X64, Y64 = X.astype(np.float64), Y.astype(np.float64)
+    layers = (model.agg1, model.agg2)
+    for step in range(21):
+        W1 = model.W1.detach().cpu().numpy().astype(np.float64)
+        W2 = model.W2.detach().cpu().numpy().astype(np.float64)
+        loss = float(model.train_step(Xd, Yd, opt, step).detach())
+        g1, g2 = model.W1.grad.cpu().numpy(), model.W2.grad.cpu().numpy()
+        rec = model.controller.history[-1]
+        inputs = None
+        if rec.mode == "score":
+            keys = [rsc.copy_to_host(layer.cache.buffers()[2], n, np.uint64) for layer in layers]
+            fro = [layer.cache.norms()[1] for layer in layers]
+            inputs = (keys, fro, model.controller.fro_a2)
+        r = ref.step(X64, W1, W2, Y64, step, score_inputs=inputs)
+        assert rec.mode == r["mode"], step
+        assert abs(loss - r["loss"]) <= 1e-5 * abs(r["loss"]), step
+        for g, gr in ((g1, r["gW1"]), (g2, r["gW2"])):
+            assert np.max(np.abs(g - gr)) <= 1e-4 * np.max(np.abs(gr)), step
+        assert rec.k == r["k"], step
+        if rec.mode == "score":
+            for l, layer in enumerate(layers):
+                assert np.array_equal(rsc.cache_snapshot(layer.cache, step)["idx"], r["idx"][l]), (step, l)
+                q_gpu = (keys[l] - np.uint64(1)).view(np.float64)
+                q_own = (r["keys_own"][l] - np.uint64(1)).view(np.float64)
+                assert np.all(np.abs(q_gpu - q_own) <= 1e-4 * np.abs(q_own) + 1e-300), (step, l)
+                assert abs(fro[l] - r["fro_b2_own"][l]) <= 1e-5 * r["fro_b2_own"][l], (step, l)
+    recs = [x for x in model.controller.history if x.mode == "score"]
+    assert [x.step for x in recs] == [h["step"] for h in ref.history] == list(range(0, 21, 3))
+    moved = False
+    for g, h in zip(recs, ref.history):
+        assert g.k == h["k"]
+        assert len(g.auc) == len(h["auc"]) and len(g.overlap) == len(h["overlap"])
+        for a, b in zip(g.auc, h["auc"]):
+            assert (np.isnan(a) and np.isnan(b)) or abs(a - b) <= 1e-12, (g.step, a, b)
+            moved |= a < 1.0
+        assert g.overlap == h["overlap"], g.step
+    assert moved                       # the weights moved: some selection went stale
+    model.close()
+
+
+@pytest.mark.parametrize("n,seed", [(1, 0), (8191, 1), (8193, 2), (716_847, 3)])
+def test_cache_norms_against_sequential_sums(n, seed):
+    """Eq. 4a's normalisers on the device (fixed-order fp64 sums) against the
+    oracle's sequential sums: within (n - 1) units of roundoff for these
+    non-negative terms, and bitwise reproducible."""
+    import oracle
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(1, 12, n)
+    A = synth.bucket_csr(np.minimum(lens, n), n, seed=seed)
+    AT = synth.transpose(A, n)
+    B = synth.dense_normal(n, 40, seed=seed + 7)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n)
+    XT = rsc.DeviceCsr.from_host(AT.rowptr, AT.col, AT.val, n)
+    cache = rsc.Cache(X, XT)
+    cache.score(torch.from_numpy(B).cuda())
+    fx, fb = cache.norms()
+    cn2, _ = oracle.col_sqnorms(AT.rowptr, AT.val)
+    rn2 = oracle.pair_keys(cn2, B)["rn2"]
+    sx, sb = oracle.sum_sequential(cn2), oracle.sum_sequential(rn2)
+    assert abs(fx - sx) <= max(n - 1, 1) * 2.0 ** -53 * sx
+    assert abs(fb - sb) <= max(n - 1, 1) * 2.0 ** -53 * sb
+    cache.score(torch.from_numpy(B).cuda())
+    assert cache.norms() == (fx, fb)
+    cache.close()

@@ -74,6 +74,16 @@ def test_csr_check(small_gen):
     assert oracle.check_csr(A.rowptr, bad, A.n, 190) == 5
     bad = A.col.copy(); bad[0] = 190                 # out of range
     assert oracle.check_csr(A.rowptr, bad, A.n, 190) == 4
+    bad = A.col.copy(); bad[0] = -1                  # negative column
+    assert oracle.check_csr(A.rowptr, bad, A.n, 190) == 4
+    rp = A.rowptr.copy(); rp[0] = 1                  # rowptr[0] != 0
+    assert oracle.check_csr(rp, A.col, A.n, 190) == 2
+    rp = A.rowptr.copy()
+    i = int(np.argmax(rp > 0))                       # first row that starts past entry 0
+    rp[i + 1] = rp[i] - 1                            # row i ends before it starts
+    assert oracle.check_csr(rp, A.col, A.n, 190) == 3
+    assert oracle.check_csr(A.rowptr, A.col, -1, 190) == 1
+    assert oracle.check_csr(A.rowptr, A.col, A.n, -5) == 1
 
 
 def test_gcn_values_closed_form_ring():
@@ -624,3 +634,102 @@ def test_gcn_reference_full_budget_slices_give_the_exact_backward():
     assert exact["k"] == [A.n, A.n]
     for g in ("gW1", "gW2"):
         np.testing.assert_allclose(sampled[g], exact[g], rtol=1e-14, atol=0)
+
+
+# ---------------------------------------------------------------- Eq. 4a normalisers
+def test_sum_sequential_order_and_bound():
+    """The Frobenius normalisers are plain left-to-right fp64 sums: the order
+    shows where cancellation decides the result, and on positive data the
+    sum stays within (n - 1) units of roundoff of the exact (correctly
+    rounded) sum."""
+    import math
+    assert oracle.sum_sequential(np.array([1.0, 1e16, -1e16])) == 0.0   # 1 absorbed first
+    assert oracle.sum_sequential(np.array([1e16, -1e16, 1.0])) == 1.0   # 1 added last
+    assert oracle.sum_sequential(np.zeros(0)) == 0.0
+    ints = np.arange(1, 100_001, dtype=np.float64)
+    assert oracle.sum_sequential(ints) == 100_000 * 100_001 / 2         # exact below 2^53
+    x = np.random.default_rng(4).random(200_001) ** 3 * 1e3
+    exact = math.fsum(x)
+    assert abs(oracle.sum_sequential(x) - exact) <= (len(x) - 1) * 2.0 ** -53 * exact
+    assert np.isinf(oracle.sum_sequential(np.array([1.0, np.inf, 2.0])))
+
+
+# ---------------------------------------------------------------- staleness (NEXT-4)
+def _brute_auc(order, prev):
+    pos = {int(i): p for p, i in enumerate(order)}
+    sel = [i for i in range(len(order)) if i in prev]
+    uns = [j for j in range(len(order)) if j not in prev]
+    if not sel or not uns:
+        return float("nan")
+    good = sum(1 for i in sel for j in uns if pos[i] < pos[j])
+    return good / (len(sel) * len(uns))
+
+
+def _mask(idx, n):
+    m = np.zeros((n + 31) // 32, np.uint32)
+    for i in idx:
+        m[i >> 5] |= np.uint32(1 << (i & 31))
+    return m
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_selection_staleness_brute_force(seed):
+    rng = np.random.default_rng(900 + seed)
+    n = int(rng.integers(2, 180))
+    key = rng.integers(1, 50, n).astype(np.uint64)          # many ties: rank by (key desc, index asc)
+    order = oracle.rank_order(key)
+    k_prev = int(rng.integers(0, n + 1))
+    prev = set(int(i) for i in rng.choice(n, k_prev, replace=False))
+    new = set(int(i) for i in rng.choice(n, int(rng.integers(0, n + 1)), replace=False))
+    auc, overlap = oracle.selection_staleness(order, _mask(prev, n), _mask(new, n))
+    want = _brute_auc(order, prev)
+    assert (np.isnan(auc) and np.isnan(want)) or auc == want
+    if prev:
+        assert overlap == len(prev & new) / len(prev)
+    else:
+        assert overlap is None
+
+
+def test_selection_staleness_special_cases():
+    n = 100
+    key = np.arange(n, 0, -1).astype(np.uint64)               # ranking 0, 1, ..., n-1
+    order = oracle.rank_order(key)
+    top = set(range(30))
+    auc, ov = oracle.selection_staleness(order, _mask(top, n), _mask(top, n))
+    assert auc == 1.0 and ov == 1.0                           # same ranking: the selection is still on top
+    bottom = set(range(70, 100))
+    auc, ov = oracle.selection_staleness(order, _mask(bottom, n), _mask(top, n))
+    assert auc == 0.0 and ov == 0.0                           # ranked last now
+    alt = set(range(0, n, 2))                                  # every other rank: above exactly half on average
+    auc, _ = oracle.selection_staleness(order, _mask(alt, n))
+    assert auc == sum(50 - i for i in range(50)) / (50 * 50)
+    assert np.isnan(oracle.selection_staleness(order, _mask(set(), n))[0])
+    assert np.isnan(oracle.selection_staleness(order, _mask(set(range(n)), n))[0])
+
+
+def test_gcn_reference_staleness_record():
+    """With tracking, each refresh after the first records per layer the AUC
+    of the previous refresh's selection under the new keys and the overlap,
+    and the k_l of every refresh (the Fig. 7 trace); the values equal the
+    brute-force count on the keys the step scored."""
+    from oracle.gcn_ref import RscReference
+    A, X, W1, W2, Y, widths = _gcn_problem()
+    ref = RscReference(A.rowptr, A.col, A.val, A.n, widths, (1, 3), (1, 10), 2, track_staleness=True)
+    prev_idx, lr = None, 5.0
+    for step in range(7):
+        out = ref.step(X, W1, W2, Y, step)
+        if out["mode"] == "score":
+            rec = ref.history[-1]
+            assert rec["step"] == step and rec["k"] == out["k"]
+            if prev_idx is None:
+                assert rec["auc"] == [] and rec["overlap"] == []
+            else:
+                for l in range(2):
+                    order = oracle.rank_order(out["keys_own"][l])
+                    assert rec["auc"][l] == _brute_auc(order, set(int(i) for i in prev_idx[l]))
+                    inter = len(set(prev_idx[l].tolist()) & set(out["idx"][l].tolist()))
+                    assert rec["overlap"][l] == inter / len(prev_idx[l])
+            prev_idx = out["idx"]
+        W1 = W1 - lr * out["gW1"]                               # the weights move between refreshes
+        W2 = W2 - lr * out["gW2"]
+    assert [r["step"] for r in ref.history] == [0, 2, 4, 6]
