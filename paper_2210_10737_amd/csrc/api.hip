@@ -630,6 +630,7 @@ rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, const doubl
         int64_t got = 0;
         RSC_HIP(hipMemcpyAsync(&got, nnz_out, sizeof got, hipMemcpyDeviceToHost, stream), "slice nnz read");
         RSC_HIP(hipStreamSynchronize(stream), "slice sync");
+        if (got < 0) return fail(RSC_ERR_INTERNAL, "slice: the single-pass scan did not complete");
         if (got > capacity)
             return fail(RSC_ERR_CAPACITY, "slice has %lld entries, capacity %lld", (long long)got,
                         (long long)capacity);
@@ -863,6 +864,7 @@ rsc_status_t rsc_cache_get(rsc_cache_t *c, int64_t step, rsc_csr_t *slice_out, c
         if (c->version) {
             if (!c->nnz_known) {
                 RSC_HIP(hipEventSynchronize(c->ev), "cache get wait");
+                if (*c->h_nnz < 0) return fail(RSC_ERR_INTERNAL, "cache slice: the single-pass scan did not complete");
                 c->nnz_slice = *c->h_nnz;
                 c->nnz_known = true;
             }

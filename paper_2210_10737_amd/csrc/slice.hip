@@ -14,8 +14,13 @@
 //      compact the kept entries in LDS and write them out coalesced at their
 //      global positions, and write Rowptr'[i] for every row whose Rowptr[i]
 //      falls in the tile.
+// The three steps also exist fused in one kernel (count, decoupled look-back
+// scan over ticketed tiles, compaction; below), taken on request; both forms
+// give the same bytes.
 // Integer-only and deterministic. With a per-column scale (the randomized
 // sampler's 1/(k p)), each kept value becomes fl32(val * colw[col]).
+#include <cstdlib>
+
 #include "rsc_internal.h"
 
 namespace rsc {
@@ -227,12 +232,183 @@ __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restri
     }
 }
 
+// ---- single pass: count, decoupled look-back scan and compaction fused ----
+// Persistent blocks of 1024 threads take tiles of 4096 entries in ticket
+// order (an atomic counter), so a tile's predecessors were all taken by
+// blocks that are already running. Per tile: load col/val (4 entries per
+// thread, coalesced), test the mask bits (from LDS when the whole mask fits,
+// else from global memory, where the n-bit set stays in L2), one ballot per
+// 64 entries; publish the tile's kept count, then the first wave looks back
+// over the predecessors' published counts (64 at a time) until it meets an
+// inclusive prefix, and publishes this tile's inclusive prefix. The kept
+// entries are then written at their global positions straight from
+// registers: the kept entries of one ballot are consecutive in the output,
+// so each wave's stores cover one contiguous range.
+// Status word of a tile: bits 63..62 = 1 (count published) or 2 (inclusive
+// prefix published), bits 61..0 the value; 0 = nothing yet.
+// Every wait is bounded: after kSpinLimit polls without progress the kernel
+// records a failure (*nnz_out = -1), takes the missing counts as 0 and
+// finishes, so no wave can wait forever.
+constexpr int kFusedThreads = 1024;
+constexpr int kFusedWaves = kFusedThreads / 64;
+constexpr int kFusedMaskWords = 36864;  // 144 KB of LDS: up to 1,179,648 columns
+constexpr uint64_t kFlagAgg = 1ull << 62, kFlagIncl = 2ull << 62, kValMask = (1ull << 62) - 1;
+constexpr int64_t kSpinLimit = 1ll << 22;
+static_assert(kTile == kFusedThreads * 4, "four entries per thread per tile");
+
+// A status word carries its own value, so relaxed device-scope atomics
+// suffice (no other data is published through it); acquire loads would also
+// invalidate the CU's vector L1 on every poll.
+__device__ __forceinline__ uint64_t load_status(const uint64_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_status(uint64_t *p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <bool kLdsMask>
+__global__ __launch_bounds__(kFusedThreads) void slice_fused_kernel(
+    const int32_t *__restrict__ rowptr, int32_t n_rows, const int32_t *__restrict__ col,
+    const float *__restrict__ val, int64_t nnz, const uint32_t *__restrict__ mask, int32_t n_words, int32_t nt,
+    uint64_t *__restrict__ status, int32_t *__restrict__ ticket, int32_t *__restrict__ rowptr_out,
+    int32_t *__restrict__ col_out, float *__restrict__ val_out, int64_t capacity, int64_t *__restrict__ nnz_out,
+    int32_t *__restrict__ failed, const double *__restrict__ colw) {
+    __shared__ uint32_t s_mask[kLdsMask ? kFusedMaskWords : 1];
+    __shared__ uint64_t s_ball[kGroups];
+    __shared__ uint32_t s_pre[kGroups + 1];
+    __shared__ int32_t s_tile, s_rows[2];
+    __shared__ int64_t s_base;
+    const int T = threadIdx.x, lane = T & 63, wv = T >> 6;
+    if constexpr (kLdsMask) {
+        for (int i = T; i < n_words; i += kFusedThreads) s_mask[i] = mask[i];
+    }
+    for (;;) {
+        if (T == 0) s_tile = atomicAdd(ticket, 1);
+        __syncthreads();  // s_tile visible; the previous tile's shared state is no longer read
+        const int32_t tile = s_tile;
+        if (tile >= nt) break;  // block-uniform
+        const int64_t ts = (int64_t)tile * kTile;
+        const int64_t te = min<int64_t>(ts + kTile, nnz);
+        const bool last = tile == nt - 1;
+        if (T == 0) s_rows[0] = lower_bound_rowptr(rowptr, n_rows, ts);
+        if (T == 1) s_rows[1] = last ? n_rows + 1 : lower_bound_rowptr(rowptr, n_rows, te);
+        int32_t rc[4];
+        float rv[4];
+        uint64_t ball[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {  // entry o = T + 1024 i of the tile: ballot group o >> 6 = 16 i + wv
+            const int64_t p = ts + T + kFusedThreads * i;
+            rc[i] = p < te ? __builtin_nontemporal_load(col + p) : -1;
+            rv[i] = p < te ? __builtin_nontemporal_load(val + p) : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int32_t c = rc[i];
+            bool k = false;
+            if (c >= 0 && (c >> 5) < n_words) {
+                const uint32_t wd = kLdsMask ? s_mask[c >> 5] : mask[c >> 5];
+                k = (wd >> (c & 31)) & 1u;
+            }
+            ball[i] = __ballot(k);
+            if (lane == 0) s_ball[kFusedWaves * i + wv] = ball[i];
+        }
+        __syncthreads();
+        if (wv == 0) {
+            // exclusive scan of the 64 ballot counts, then publish and look back
+            const uint32_t cnt = __popcll(s_ball[lane]);
+            uint32_t incl = cnt;
+            for (int off = 1; off < 64; off <<= 1) {
+                const uint32_t x = __shfl_up(incl, off);
+                if (lane >= off) incl += x;
+            }
+            s_pre[lane] = incl - cnt;
+            const uint32_t total = __shfl(incl, 63);
+            if (lane == 63) s_pre[kGroups] = incl;
+            int64_t excl = 0;
+            if (tile == 0) {
+                if (lane == 0) store_status(status, kFlagIncl | total);
+            } else {
+                if (lane == 0) store_status(status + tile, kFlagAgg | total);
+                int32_t q0 = tile - 1;  // nearest predecessor of the current window
+                int64_t polls = 0;
+                for (;;) {
+                    const int32_t q = q0 - lane;
+                    const uint64_t st = q >= 0 ? load_status(status + q) : kFlagIncl;  // before tile 0: prefix 0
+                    const uint64_t flag = st >> 62;
+                    const uint64_t incl_lanes = __ballot(flag == 2);
+                    const uint64_t empty_lanes = __ballot(flag == 0);
+                    const int first = incl_lanes ? __ffsll((long long)incl_lanes) - 1 : 64;
+                    const uint64_t need = first == 64 ? ~0ull : (2ull << first) - 1ull;  // lanes 0..first
+                    if (empty_lanes & need) {
+                        if (++polls < kSpinLimit) continue;  // a predecessor has not published yet
+                        if (lane == 0) atomicExch(failed, 1);
+                    }
+                    uint64_t v = (lane <= first && flag != 0) ? (st & kValMask) : 0;
+                    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+                    excl += (int64_t)v;
+                    if (first < 64 || (empty_lanes & need)) break;
+                    q0 -= 64;
+                }
+                if (lane == 0) store_status(status + tile, kFlagIncl | (uint64_t)(excl + total));
+            }
+            if (lane == 0) {
+                s_base = excl;
+                if (last) *nnz_out = atomicAdd(failed, 0) ? -1 : excl + total;
+            }
+        }
+        __syncthreads();
+        const int64_t base = s_base;
+        const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if ((ball[i] >> lane) & 1ull) {
+                const int64_t pos = base + s_pre[kFusedWaves * i + wv] + __popcll(ball[i] & below);
+                if (pos < capacity) {
+                    col_out[pos] = rc[i];
+                    val_out[pos] = colw ? (float)((double)rv[i] * colw[rc[i]]) : rv[i];
+                }
+            }
+        }
+        const uint32_t total = s_pre[kGroups];
+        const int32_t r0 = s_rows[0], r1 = s_rows[1];
+        for (int64_t i = (int64_t)r0 + T; i < r1; i += kFusedThreads) {
+            const int64_t off = (int64_t)rowptr[i] - ts;
+            uint32_t c;
+            if (off >= kTile || ts + off >= te) {
+                c = total;
+            } else {
+                const int g = (int)(off >> 6), l = (int)(off & 63);
+                c = s_pre[g] + __popcll(s_ball[g] & ((1ull << l) - 1ull));
+            }
+            rowptr_out[i] = (int32_t)(base + c);
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void zero_words_kernel(uint64_t *__restrict__ p, int64_t count) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = 0;
+}
+
 __global__ __launch_bounds__(256) void zero_rows_kernel(int32_t *__restrict__ p, int64_t count,
                                                         int64_t *__restrict__ nnz_out) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
          i += (int64_t)gridDim.x * blockDim.x)
         p[i] = 0;
     if (blockIdx.x == 0 && threadIdx.x == 0) *nnz_out = 0;
+}
+
+// The single-pass form runs only on request (RSC_SLICE_FUSED=1): measured on
+// the benchmark workloads it is slower than the three launches (social about
+// 0.93 against 0.43 ms, copurchase 1.36 against 0.72 ms), because each tile's
+// look-back waits on its predecessors' status words at L2 latency while a
+// persistent block holds one tile at a time, where the count and emit
+// kernels keep many tiles' loads in flight.
+bool use_fused(int32_t n_words) {
+    (void)n_words;
+    if (const char *env = getenv("RSC_SLICE_FUSED")) return atoi(env) != 0;
+    return false;
 }
 
 }  // namespace
@@ -260,6 +436,26 @@ hipError_t slice_launch(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
     if (hipGetDevice(&dev) == hipSuccess)
         (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     const int32_t n_words = (int32_t)ceil_div((int64_t)n_cols, 32);
+    if (use_fused(n_words)) {
+        // ws: [ticket, failure flag | pad to 256 B][status word per tile]
+        int32_t *ticket = static_cast<int32_t *>(ws);
+        uint64_t *status = reinterpret_cast<uint64_t *>(static_cast<char *>(ws) + 256);
+        const int64_t words = 32 + (int64_t)nt;  // the 256-byte head and the status words
+        zero_words_kernel<<<(unsigned)std::min<int64_t>(ceil_div(words, 256), 1024), 256, 0, stream>>>(
+            static_cast<uint64_t *>(ws), words);
+        const bool lds = n_words <= kFusedMaskWords;
+        const int per_cu = lds ? 1 : 2;
+        const unsigned grid = (unsigned)std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * per_cu, nt));
+        if (lds)
+            slice_fused_kernel<true><<<grid, kFusedThreads, 0, stream>>>(
+                rowptr, n_rows, col, val, nnz, mask, n_words, nt, status, ticket, rowptr_out, col_out, val_out,
+                capacity, nnz_out, ticket + 1, colw);
+        else
+            slice_fused_kernel<false><<<grid, kFusedThreads, 0, stream>>>(
+                rowptr, n_rows, col, val, nnz, mask, n_words, nt, status, ticket, rowptr_out, col_out, val_out,
+                capacity, nnz_out, ticket + 1, colw);
+        return hipGetLastError();
+    }
     const unsigned cgrid = (unsigned)std::max<int64_t>(1, std::min<int64_t>(cus, ceil_div(nt, kTilesPerIter)));
     slice_count_kernel<<<cgrid, kCountThreads, 0, stream>>>(col, nnz, mask, n_words, nt, tile_cnt, tile_bits);
     slice_scan_kernel<<<1, 1024, 0, stream>>>(nt, tile_cnt, tile_off, nnz_out);
