@@ -361,24 +361,24 @@ def vendor_baseline(X, H, Y, plan, reps: int = 10):
     return out
 
 
-def gather_ceiling(plan, H, d, reps: int = 5):
-    """Times the plan's gather probe (rsc_spmm_plan_gather_probe: the exact
-    product's B-row gathers alone) at 4, 8 and 16 loads in flight per wave,
-    median of `reps` each after one untimed run; the fastest setting is the
-    ceiling. HIP events on the current stream, which the library launches on."""
+def gather_ceiling(handle, B, d, n_entries, reps: int = 5):
+    """Times a gather probe (rsc_spmm_plan_gather_probe for a plan, the exact
+    product's B-row gathers alone; rsc_cache_gather_probe for a cache, the
+    sampled product's) at 4, 8 and 16 loads in flight per wave, median of
+    `reps` each after one untimed run; the fastest setting is the ceiling.
+    HIP events on the current stream, which the library launches on."""
     import statistics
 
     import torch
-    n_entries = plan.A.nnz
-    sink = torch.empty(max((n_entries + 63) // 64, 1), dtype=torch.float32, device=H.device)
+    sink = torch.empty(max((n_entries + 63) // 64, 1), dtype=torch.float32, device=B.device)
     per, slice_w = {}, None
     for inflight in (4, 8, 16):
-        slice_w = plan.gather_probe(H, d=d, inflight=inflight, sink=sink)
+        slice_w = handle.gather_probe(B, d=d, inflight=inflight, sink=sink)
         ts = []
         for _ in range(reps):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
-            plan.gather_probe(H, d=d, inflight=inflight, sink=sink)
+            handle.gather_probe(B, d=d, inflight=inflight, sink=sink)
             e1.record()
             e1.synchronize()
             ts.append(e0.elapsed_time(e1))
@@ -388,7 +388,7 @@ def gather_ceiling(plan, H, d, reps: int = 5):
     return {"ms": round(ms, 4), "inflight": best, "slice_floats": slice_w,
             "ms_by_inflight": {str(k_): round(v, 4) for k_, v in per.items()},
             "logical_gather_GBs": round(4.0 * n_entries * d / (ms * 1e-3) / 1e9, 1),
-            "what": "the exact product's B-row gathers alone: same column stream (the plan's hinted copy), "
+            "what": "the product's B-row gathers alone: same column stream (a plan's hinted copy), "
                     "feature passes and cache policy; no values, row walk or output"}
 
 
@@ -749,7 +749,8 @@ def main() -> int:
     # the gather ceiling: the exact product's gathers alone (same column
     # stream, feature passes and cache policy; no values, rows or output),
     # at 4, 8 and 16 loads in flight per wave; the fastest is the ceiling
-    probe = gather_ceiling(plan, H, d)
+    probe = gather_ceiling(plan, H, d, nnz)
+    probe_sampled = gather_ceiling(cache, G, d, int(cache.get(args.warmup + args.steps)["slice"].nnz))
 
     # cold-cache repetitions, outside the timed steps: before each, write a
     # 1 GiB scratch buffer (more than the 4 MB L2s and the 256 MB MALL)
@@ -838,6 +839,9 @@ def main() -> int:
                    "GBs": round(b / (float(np.median(per[kind])) * 1e-3) / 1e9, 1),
                    "frac": round(b / (float(np.median(per[kind])) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
             for kind, b in (("exact", b_exact), ("sampled", b_sampled), ("refresh", b_refresh)) if per[kind]},
+        # the sampled product against its own gathers alone (the cache's probe)
+        "sampled_gather_ceiling": dict(probe_sampled, frac_of_gather_ceiling=round(
+            probe_sampled["ms"] / float(np.median(per["sampled"])), 4)),
         "roofline": {
             "bound": "hbm",
             "kernel": "spmm_long_kernel + spmm_rows_kernel (the exact SpMM, one plan run)",

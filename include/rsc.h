@@ -351,6 +351,15 @@ rsc_status_t rsc_cache_get(rsc_cache_t *cache, int64_t step, rsc_csr_t *slice_ou
                            uint64_t *version_out);
 rsc_status_t rsc_spmm_sampled(rsc_cache_t *cache, const float *B, int32_t d, int64_t ldb,
                               float *Y, int64_t ldy, hipStream_t stream);
+/* Measurement helper, not a step of the method: the gather-only pass of
+ * rsc_spmm_sampled on the cached slice, as rsc_spmm_plan_gather_probe is for
+ * a plan (the slice's column stream, the feature passes the sampled product
+ * takes, no hint; rows not walked, no values, no Y; one float per 64 kept
+ * entries into sink, sink_count >= ceil(nnz' / 64)). Needs a refreshed
+ * cache; reads nnz' like rsc_cache_get. */
+rsc_status_t rsc_cache_gather_probe(rsc_cache_t *cache, const float *B, int32_t d, int64_t ldb,
+                                    int32_t inflight, float *sink, int64_t sink_count,
+                                    int32_t *slice_out, hipStream_t stream);
 /* Device arrays owned by the cache: cn2 (fp64) and colnnz (int32), n_cols
  * entries each; keys (uint64) and row square-norms rn2 (fp64) of the last
  * scored operand; mask (ceil(n_cols/32) words) of the last selection. Any

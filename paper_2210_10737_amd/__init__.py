@@ -50,7 +50,7 @@ EXPORTED = [
     "rsc_cache_create", "rsc_cache_create_ex", "rsc_cache_refresh", "rsc_cache_score", "rsc_cache_select",
     "rsc_cache_refresh_random",
     "rsc_cache_get", "rsc_spmm_sampled",
-    "rsc_cache_buffers", "rsc_cache_norms", "rsc_cache_destroy",
+    "rsc_cache_buffers", "rsc_cache_norms", "rsc_cache_gather_probe", "rsc_cache_destroy",
     "rsc_k_from_fraction", "rsc_greedy_allocate",
     "rsc_greedy_profile_workspace_bytes", "rsc_greedy_blocks", "rsc_greedy_profile",
     "rsc_greedy_allocate_profiles",
@@ -140,6 +140,7 @@ def lib():
             "rsc_cache_buffers": ([vp, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
                                    ctypes.POINTER(vp), ctypes.POINTER(vp)], ctypes.c_int),
             "rsc_cache_destroy": ([vp], ctypes.c_int),
+            "rsc_cache_gather_probe": ([vp, vp, i32, i64, i32, vp, i64, ctypes.POINTER(i32), vp], ctypes.c_int),
             "rsc_cache_norms": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), vp],
                                 ctypes.c_int),
             "rsc_k_from_fraction": ([i32, i32, i32], i32),
@@ -455,6 +456,20 @@ class Cache:
         Y = _new_out(self.X.n_rows, d, B.device) if out is None else out
         _check(lib().rsc_spmm_sampled(self._h, _dp(B), d, _ld(B), _dp(Y), _ld(Y), _stream()))
         return Y
+
+    def gather_probe(self, B: torch.Tensor, d: int | None = None, inflight: int = 8,
+                     sink: torch.Tensor | None = None) -> int:
+        """The gather-only pass of spmm_sampled on the cached slice
+        (rsc_cache_gather_probe, a measurement helper); returns the
+        feature-pass width it used."""
+        d = B.shape[1] if d is None else d
+        if sink is None:
+            nnz = self.get(0)["slice"].nnz
+            sink = torch.empty(max((nnz + 63) // 64, 1), dtype=torch.float32, device=B.device)
+        sl = ctypes.c_int32(0)
+        _check(lib().rsc_cache_gather_probe(self._h, _dp(B), d, _ld(B), inflight, _dp(sink), sink.numel(),
+                                            ctypes.byref(sl), _stream()))
+        return sl.value
 
     def norms(self, scored: bool = True):
         """(||X||_F^2, ||B||_F^2 of the last scored operand) from the device's

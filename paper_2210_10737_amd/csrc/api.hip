@@ -901,6 +901,31 @@ rsc_status_t rsc_spmm_sampled(rsc_cache_t *c, const float *B, int32_t d, int64_t
     return RSC_OK;
 }
 
+rsc_status_t rsc_cache_gather_probe(rsc_cache_t *c, const float *B, int32_t d, int64_t ldb, int32_t inflight,
+                                    float *sink, int64_t sink_count, int32_t *slice_out, hipStream_t stream) {
+    if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
+    if (c->version == 0) return fail(RSC_ERR_INVALID_ARGUMENT, "cache was never refreshed");
+    RSC_TRY(check_dense(B, c->X.n_cols, d, ldb, "B"));
+    if (inflight != 4 && inflight != 8 && inflight != 16)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "inflight = %d (4, 8 or 16)", inflight);
+    RSC_TRY(check_same_device(c->device, "cache"));
+    rsc_csr_t s{};
+    RSC_TRY(rsc_cache_get(c, c->last_step, &s, nullptr, nullptr, nullptr, nullptr));  // nnz' (waits once per refresh)
+    const int64_t need = rsc::gather_probe_sink_count(s.nnz);
+    if (sink_count < need) return fail(RSC_ERR_CAPACITY, "sink holds %lld floats, %lld needed", (long long)sink_count,
+                                       (long long)need);
+    if (need > 0 && !sink) return fail(RSC_ERR_INVALID_ARGUMENT, "sink is NULL");
+    // the feature passes rsc_spmm_sampled takes (decided from the call's shape)
+    const int64_t kk = std::min<int64_t>(c->k, c->n);
+    const int64_t nnz_hint = c->n > 0 ? c->X.nnz * kk / c->n : 0;
+    const int32_t slice = rsc::spmm_slice_width(c->X.n_rows, nnz_hint, kk, d);
+    if (slice_out) *slice_out = slice;
+    RSC_HIP(rsc::gather_probe_launch(s.col, s.nnz, B, ldb, d, slice, false, inflight, sink, stream),
+            "gather probe launch");
+    RSC_HIP(c->fence.record(stream), "gather probe event");
+    return RSC_OK;
+}
+
 rsc_status_t rsc_cache_buffers(rsc_cache_t *c, const double **cn2, const int32_t **colnnz, const uint64_t **key,
                                const double **rn2, const uint32_t **mask) {
     if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");

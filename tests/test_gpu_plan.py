@@ -163,7 +163,13 @@ def test_cache_prepared_list_survives_switches(switch):
         cache.refresh(B, n // 2, step=0)
         snap = rsc.cache_snapshot(cache)
         first = cache.spmm_sampled(B)
-    Yo, S = oracle.spmm(snap["rowptr"], snap["col"], snap["val"], Bh, with_mag=True)
+    # the oracle's own chain (column norms, keys, top-k, slice), then its product
+    cn2, _ = oracle.col_sqnorms(AT.rowptr, AT.val)
+    _, mask = oracle.topk(oracle.pair_keys(cn2, Bh)["key"], n // 2)
+    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+    assert np.array_equal(snap["rowptr"], ro) and np.array_equal(snap["col"], co)
+    assert np.array_equal(snap["val"].view(np.uint32), vo.view(np.uint32))
+    Yo, S = oracle.spmm(ro, co, vo, Bh, with_mag=True)
     seen = {}
     for v in values:
         with env(**{switch: v}):
@@ -259,3 +265,32 @@ def test_gather_probe_gathers_the_plan_rows(d, wide):
         mag = np.concatenate([np.abs(part).sum(axis=1)[A.col], pad]).reshape(chunks, 64).sum(axis=1)
         assert np.all(np.abs(got - want) <= 1e-4 * mag + 1e-30), (d, wide, inflight, slice_w)
     plan.close()
+
+
+@pytest.mark.parametrize("d", [64, 256])
+def test_cache_gather_probe_gathers_the_slice_rows(d):
+    # the sampled product's probe streams the cached slice's columns (the
+    # oracle's slice of the same selection) and loads exactly those rows
+    A = synth.random_csr(3000, 2500, 400, seed=18, hub_rows=5, hub_len=2400)
+    AT = synth.transpose(A, 2500)
+    B = synth.dense_normal(2500, d, seed=19)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, 2500)
+    cache = rsc.Cache(X, rsc.DeviceCsr.from_host(AT.rowptr, AT.col, AT.val, 3000))
+    Bd = torch.from_numpy(B).cuda()
+    cache.refresh(Bd, 900, step=0)
+    cn2, _ = oracle.col_sqnorms(AT.rowptr, AT.val)
+    _, mask = oracle.topk(oracle.pair_keys(cn2, B)["key"], 900)
+    _, co, _ = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+    nnz = len(co)
+    chunks = (nnz + 63) // 64
+    for inflight in (4, 8, 16):
+        sink = torch.full((max(chunks, 1),), float("nan"), device="cuda")
+        slice_w = cache.gather_probe(Bd, inflight=inflight, sink=sink)
+        got = sink[:chunks].cpu().numpy().astype(np.float64)
+        f_last = ((d - 1) // slice_w) * slice_w
+        part = B[:, f_last:d].astype(np.float64)
+        pad = np.zeros(chunks * 64 - nnz)
+        want = np.concatenate([part.sum(axis=1)[co], pad]).reshape(chunks, 64).sum(axis=1)
+        mag = np.concatenate([np.abs(part).sum(axis=1)[co], pad]).reshape(chunks, 64).sum(axis=1)
+        assert np.all(np.abs(got - want) <= 1e-4 * mag + 1e-30), (d, inflight, slice_w)
+    cache.close()

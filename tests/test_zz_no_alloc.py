@@ -88,3 +88,30 @@ def test_rejects_products_beyond_the_scratch():
     st = L.rsc_spmm_noalloc(ctypes.byref(s), B.data_ptr(), 4, 4, Y.data_ptr(), 4, None)
     assert st == 4  # RSC_ERR_CAPACITY, nothing launched
     assert b"static scratch" in L.rsc_last_error()
+
+
+def test_captured_in_a_graph_and_replayed():
+    # the callers it is for: code under graph capture. Each replay (new
+    # operand contents, eager work between) equals the eager rsc_spmm bitwise.
+    A = synth.make_graph("gcn2", 0)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, A.n)
+    H = torch.from_numpy(synth.dense_normal(A.n, 100, seed=1)).cuda()
+    Y = torch.empty((A.n, 100), device="cuda")
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        rsc.spmm_noalloc(X, H, out=Y)           # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(s)
+    with torch.cuda.graph(g):
+        rsc.spmm_noalloc(X, H, out=Y)
+    for r in range(3):
+        H.copy_(torch.from_numpy(synth.dense_normal(A.n, 100, seed=20 + r)).cuda())
+        H.mul_(1.0 + r)                          # eager work between replays
+        g.replay()
+        torch.cuda.synchronize()
+        want = rsc.spmm(X, H)
+        torch.cuda.synchronize()
+        assert torch.equal(Y, want), f"replay {r}"
+    del g
