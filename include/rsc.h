@@ -157,8 +157,8 @@ rsc_status_t rsc_spmm_noalloc(const rsc_csr_t *A, const float *B, int32_t d, int
  *     value; RSC_SPMM_HINT=0 switches the policy off.
  * rsc_spmm_plan_create [sync] borrows A's arrays (they must outlive the plan
  * and not change) and allocates 4 nnz bytes for the copy, 4 (P+1) n_rows
- * bytes for the split bounds and the workspace; RSC_ERR_OUT_OF_MEMORY if
- * that fails. Runs of one plan share its workspace, so they must be
+ * bytes for the split bounds and the workspace (stream-ordered, on `stream`);
+ * RSC_ERR_OUT_OF_MEMORY if that fails. Runs of one plan share its workspace, so they must be
  * ordered on the device. The sampled-matrix cache prepares each new slice's
  * row list the same way at refresh time; its sampled products do not take
  * the column hint (on the cached slices it measured slower). */
@@ -332,7 +332,10 @@ typedef struct {
     void *ctx;
 } rsc_allocator_t;
 /* rsc_cache_create with the cache's device buffers taken from `allocator`
- * (NULL: hipMalloc/hipFree). A pointer from alloc that is NULL gives
+ * (NULL: the stream-ordered hipMallocAsync on `stream`, freed with
+ * hipFreeAsync once the cache's work is done, so neither waits for other
+ * streams; memory freed this way returns to the device's default pool and
+ * is released at a later synchronisation). A pointer from alloc that is NULL gives
  * RSC_ERR_OUT_OF_MEMORY; one that is not 256-byte aligned gives
  * RSC_ERR_UNSUPPORTED (both after freeing what was taken). The allocator
  * struct is copied; ctx must stay valid until rsc_cache_destroy. */

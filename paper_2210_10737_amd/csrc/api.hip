@@ -243,7 +243,7 @@ rsc_status_t maybe_validate(const rsc_csr_t *A, const char *name, hipStream_t st
 }  // namespace
 
 struct rsc_cache {
-    rsc_allocator_t alloc{};   // alloc.alloc == NULL: hipMalloc / hipFree
+    rsc_allocator_t alloc{};   // alloc.alloc == NULL: hipMallocAsync / hipFreeAsync
     hipStream_t alloc_stream = nullptr;
     rsc_csr_t X{}, XT{};
     int32_t interval = 10;
