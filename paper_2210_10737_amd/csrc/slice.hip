@@ -233,28 +233,31 @@ __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restri
 }
 
 // ---- single pass: count, decoupled look-back scan and compaction fused ----
-// Persistent blocks of 1024 threads take tiles of 4096 entries in ticket
+// Persistent blocks of 256 threads take tiles of 4096 entries in ticket
 // order (an atomic counter), so a tile's predecessors were all taken by
-// blocks that are already running. Per tile: load col/val (4 entries per
-// thread, coalesced), test the mask bits (from LDS when the whole mask fits,
-// else from global memory, where the n-bit set stays in L2), one ballot per
-// 64 entries; publish the tile's kept count, then the first wave looks back
-// over the predecessors' published counts (64 at a time) until it meets an
-// inclusive prefix, and publishes this tile's inclusive prefix. The kept
-// entries are then written at their global positions straight from
-// registers: the kept entries of one ballot are consecutive in the output,
-// so each wave's stores cover one contiguous range.
+// blocks that are already running. Per tile: load col/val (16 entries per
+// thread, coalesced; entry o = 256 i + thread, ballot group o >> 6, the
+// emit kernel's layout), test the mask bits (from LDS when the mask is
+// small enough for several blocks per CU, else from global memory, where the
+// n-bit set stays in L2), one ballot per 64 entries; publish the tile's kept
+// count, then the first wave looks back over the predecessors' published
+// counts (64 at a time) until it meets an inclusive prefix, and publishes
+// this tile's inclusive prefix. The kept entries are then written at their
+// global positions straight from registers: the kept entries of one ballot
+// are consecutive in the output, so each wave's stores cover one contiguous
+// range. Several blocks per CU keep several tiles' loads and look-backs in
+// flight at once.
 // Status word of a tile: bits 63..62 = 1 (count published) or 2 (inclusive
 // prefix published), bits 61..0 the value; 0 = nothing yet.
 // Every wait is bounded: after kSpinLimit polls without progress the kernel
 // records a failure (*nnz_out = -1), takes the missing counts as 0 and
 // finishes, so no wave can wait forever.
-constexpr int kFusedThreads = 1024;
-constexpr int kFusedWaves = kFusedThreads / 64;
-constexpr int kFusedMaskWords = 36864;  // 144 KB of LDS: up to 1,179,648 columns
+constexpr int kFusedThreads = 256;
+constexpr int kFusedBlocksPerCu = 8;
+constexpr int kLdsPerCu = 160 * 1024;
 constexpr uint64_t kFlagAgg = 1ull << 62, kFlagIncl = 2ull << 62, kValMask = (1ull << 62) - 1;
 constexpr int64_t kSpinLimit = 1ll << 22;
-static_assert(kTile == kFusedThreads * 4, "four entries per thread per tile");
+static_assert(kTile == kFusedThreads * kPer, "kPer entries per thread per tile");
 
 // A status word carries its own value, so relaxed device-scope atomics
 // suffice (no other data is published through it); acquire loads would also
@@ -273,7 +276,7 @@ __global__ __launch_bounds__(kFusedThreads) void slice_fused_kernel(
     uint64_t *__restrict__ status, int32_t *__restrict__ ticket, int32_t *__restrict__ rowptr_out,
     int32_t *__restrict__ col_out, float *__restrict__ val_out, int64_t capacity, int64_t *__restrict__ nnz_out,
     int32_t *__restrict__ failed, const double *__restrict__ colw) {
-    __shared__ uint32_t s_mask[kLdsMask ? kFusedMaskWords : 1];
+    extern __shared__ uint32_t s_mask[];  // n_words words with kLdsMask, else empty
     __shared__ uint64_t s_ball[kGroups];
     __shared__ uint32_t s_pre[kGroups + 1];
     __shared__ int32_t s_tile, s_rows[2];
@@ -292,25 +295,24 @@ __global__ __launch_bounds__(kFusedThreads) void slice_fused_kernel(
         const bool last = tile == nt - 1;
         if (T == 0) s_rows[0] = lower_bound_rowptr(rowptr, n_rows, ts);
         if (T == 1) s_rows[1] = last ? n_rows + 1 : lower_bound_rowptr(rowptr, n_rows, te);
-        int32_t rc[4];
-        float rv[4];
-        uint64_t ball[4];
+        int32_t rc[kPer];
+        float rv[kPer];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {  // entry o = T + 1024 i of the tile: ballot group o >> 6 = 16 i + wv
+        for (int i = 0; i < kPer; ++i) {
             const int64_t p = ts + T + kFusedThreads * i;
             rc[i] = p < te ? __builtin_nontemporal_load(col + p) : -1;
             rv[i] = p < te ? __builtin_nontemporal_load(val + p) : 0.f;
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < kPer; ++i) {
             const int32_t c = rc[i];
             bool k = false;
             if (c >= 0 && (c >> 5) < n_words) {
                 const uint32_t wd = kLdsMask ? s_mask[c >> 5] : mask[c >> 5];
                 k = (wd >> (c & 31)) & 1u;
             }
-            ball[i] = __ballot(k);
-            if (lane == 0) s_ball[kFusedWaves * i + wv] = ball[i];
+            const uint64_t b = __ballot(k);
+            if (lane == 0) s_ball[4 * i + wv] = b;
         }
         __syncthreads();
         if (wv == 0) {
@@ -360,9 +362,10 @@ __global__ __launch_bounds__(kFusedThreads) void slice_fused_kernel(
         const int64_t base = s_base;
         const uint64_t below = (1ull << lane) - 1ull;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            if ((ball[i] >> lane) & 1ull) {
-                const int64_t pos = base + s_pre[kFusedWaves * i + wv] + __popcll(ball[i] & below);
+        for (int i = 0; i < kPer; ++i) {
+            const uint64_t b = s_ball[4 * i + wv];
+            if ((b >> lane) & 1ull) {
+                const int64_t pos = base + s_pre[4 * i + wv] + __popcll(b & below);
                 if (pos < capacity) {
                     col_out[pos] = rc[i];
                     val_out[pos] = colw ? (float)((double)rv[i] * colw[rc[i]]) : rv[i];
@@ -400,11 +403,10 @@ __global__ __launch_bounds__(256) void zero_rows_kernel(int32_t *__restrict__ p,
 }
 
 // The single-pass form runs only on request (RSC_SLICE_FUSED=1): measured on
-// the benchmark workloads it is slower than the three launches (social about
-// 0.93 against 0.43 ms, copurchase 1.36 against 0.72 ms), because each tile's
-// look-back waits on its predecessors' status words at L2 latency while a
-// persistent block holds one tile at a time, where the count and emit
-// kernels keep many tiles' loads in flight.
+// the benchmark workloads it is still slower than the three launches (social
+// about 0.50 against 0.43 ms, copurchase 1.02 against 0.72 ms): what it saves
+// (one read of col, two launches) costs less than the look-backs, each a
+// chain of dependent L2 round trips over the tiles still in flight.
 bool use_fused(int32_t n_words) {
     (void)n_words;
     if (const char *env = getenv("RSC_SLICE_FUSED")) return atoi(env) != 0;
@@ -443,11 +445,14 @@ hipError_t slice_launch(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
         const int64_t words = 32 + (int64_t)nt;  // the 256-byte head and the status words
         zero_words_kernel<<<(unsigned)std::min<int64_t>(ceil_div(words, 256), 1024), 256, 0, stream>>>(
             static_cast<uint64_t *>(ws), words);
-        const bool lds = n_words <= kFusedMaskWords;
-        const int per_cu = lds ? 1 : 2;
+        // the mask goes to LDS when at least three blocks' copies fit a CU
+        const size_t mask_bytes = sizeof(uint32_t) * (size_t)n_words;
+        const int lds_blocks = (int)std::min<size_t>(kFusedBlocksPerCu, kLdsPerCu / (mask_bytes + 2048));
+        const bool lds = lds_blocks >= 3;
+        const int per_cu = lds ? lds_blocks : kFusedBlocksPerCu;
         const unsigned grid = (unsigned)std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * per_cu, nt));
         if (lds)
-            slice_fused_kernel<true><<<grid, kFusedThreads, 0, stream>>>(
+            slice_fused_kernel<true><<<grid, kFusedThreads, mask_bytes, stream>>>(
                 rowptr, n_rows, col, val, nnz, mask, n_words, nt, status, ticket, rowptr_out, col_out, val_out,
                 capacity, nnz_out, ticket + 1, colw);
         else
