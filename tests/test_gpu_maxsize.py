@@ -95,3 +95,31 @@ def test_cache_at_int32_limit(big):
     Ys = cache.spmm_sampled(Bd).cpu().numpy()
     check_rows(Ys, ro, co, vo, B, rows, 1e-4)
     cache.close()
+
+
+def test_fused_slice_at_int32_limit(big):
+    # the single-pass slice (RSC_SLICE_FUSED=1) on 2^31 - 2 entries: 524,288
+    # tiles of look-back, row pointers and kept entries against the oracle
+    import os
+    A, X, B, Bd, rows = big
+    rng = np.random.Generator(np.random.PCG64(74))
+    mask = rng.integers(0, 2**32, (N + 31) // 32, dtype=np.uint64).astype(np.uint32)
+    mask_d = torch.from_numpy(mask.view(np.int32)).cuda()
+    old = os.environ.get("RSC_SLICE_FUSED")
+    os.environ["RSC_SLICE_FUSED"] = "1"
+    try:
+        S, nnz = rsc.slice_csr(X, mask_d)
+        torch.cuda.synchronize()
+    finally:
+        if old is None:
+            os.environ.pop("RSC_SLICE_FUSED", None)
+        else:
+            os.environ["RSC_SLICE_FUSED"] = old
+    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+    assert int(nnz.item()) == int(ro[-1])
+    assert np.array_equal(S.rowptr.cpu().numpy(), ro)
+    for r in rows:
+        a, b = int(ro[r]), int(ro[r + 1])
+        assert np.array_equal(S.col[a:b].cpu().numpy(), co[a:b])
+        assert np.array_equal(S.val[a:b].cpu().numpy().view(np.uint32), vo[a:b].view(np.uint32))
+    del S
