@@ -553,7 +553,7 @@ def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="copurchase")
     ap.add_argument("--budget-pct", type=int, default=None)
     ap.add_argument("--refresh", type=int, default=10)
@@ -614,7 +614,12 @@ def main() -> int:
     Gh = synth.dense_normal(A.n, d, seed=args.seed + 3)
     t_gen = time.perf_counter() - t_gen
     n, nnz = A.n, A.nnz
-    print(f"[bench] {args.workload}: n={n} nnz={nnz} d={d} budget={pct}% (inputs {t_gen:.1f}s)",
+    deg_all = np.diff(A.rowptr)
+    deg_stats = {"max": int(deg_all.max()), "p50": float(np.percentile(deg_all, 50)),
+                 "p99": float(np.percentile(deg_all, 99)), "mean": round(float(deg_all.mean()), 2)}
+    print(f"[bench] {args.workload}: n={n} nnz={nnz} d={d} budget={pct}% seed={args.seed} "
+          f"row lengths max/p50/p99 {deg_stats['max']}/{deg_stats['p50']:.0f}/{deg_stats['p99']:.0f} "
+          f"(inputs {t_gen:.1f}s)",
           file=sys.stderr, flush=True)
 
     if args.aggregator == "gcn":
@@ -812,6 +817,7 @@ def main() -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": args.workload, "aggregator": args.aggregator, "graph": w.description,
+                   "row_lengths": deg_stats,
                    "n": n, "nnz": nnz, "d": d,
                    "budget_pct": pct, "k": k, "selector": args.selector, "hip_graph": bool(args.graph), "exact_spmm": "plan",
                    "refresh_interval": args.refresh,
