@@ -89,3 +89,58 @@ def test_sampled_mean_backward():
     Yo, S = oracle.spmm(ro, co, vo, G, with_mag=True)
     assert np.max(np.abs(Ys.astype(np.float64) - Yo) / np.maximum(S, FLT_MIN)) <= 1e-4
     cache.close()
+
+
+def test_full_size_mean_aggregator():
+    """The bench's MEAN configuration at full size (copurchase structure with
+    unit values): every element of the exact forward D^-1 A H against the
+    oracle's definition, and of the sampled backward on the cached slice of
+    A^T D^-1, whose selection and CSR match the oracle's bit for bit."""
+    A = synth.make_graph("copurchase", 0)
+    n = A.n
+    ones = np.ones_like(A.val)
+    deg = np.diff(A.rowptr).astype(np.int64)
+    H = synth.dense_normal(n, 256, seed=1)
+    G = synth.dense_normal(n, 256, seed=3)
+    dA = rsc.DeviceCsr.from_host(A.rowptr, A.col, ones, n)
+    X = rsc.degree_scale(dA)                                             # D^-1 A
+    XB = rsc.degree_scale(dA, by_column=True, deg_rowptr=dA.rowptr)       # A^T D^-1 (A symmetric)
+    Y = rsc.spmm(X, torch.from_numpy(H).cuda())
+    worst = 0.0
+    for r0 in range(0, n, 250_000):
+        rows = np.arange(r0, min(n, r0 + 250_000), dtype=np.int32)
+        sub = synth.Csr(len(rows), (A.rowptr[r0:r0 + len(rows) + 1] - A.rowptr[r0]).astype(np.int32),
+                        A.col[A.rowptr[r0]:A.rowptr[r0 + len(rows)]], ones[A.rowptr[r0]:A.rowptr[r0 + len(rows)]])
+        Yo = oracle.spmm_mean(sub.rowptr, sub.col, sub.val, H)
+        _, S = oracle.spmm(sub.rowptr, sub.col, sub.val, np.abs(H), with_mag=True)
+        S /= np.maximum(deg[rows], 1)[:, None]
+        got = Y[r0:r0 + len(rows)].cpu().numpy().astype(np.float64)
+        worst = max(worst, float(np.max(np.abs(got - Yo) / np.maximum(S, FLT_MIN))))
+    print(f"[full] MEAN exact: max rel err {worst:.3e}", flush=True)
+    assert worst <= 1e-5
+    del Y
+    k = (n * 30) // 100
+    cache = rsc.Cache(XB, X, refresh_interval=10)
+    Gd = torch.from_numpy(G).cuda()
+    cache.refresh(Gd, k, step=0)
+    snap = rsc.cache_snapshot(cache)
+    fwd_vals = (1.0 / np.repeat(deg, deg)).astype(np.float32)              # values of D^-1 A
+    bwd_vals = (1.0 / np.maximum(deg[A.col], 1)).astype(np.float32)        # values of A^T D^-1
+    assert np.array_equal(X.val.cpu().numpy().view(np.uint32), fwd_vals.view(np.uint32))
+    assert np.array_equal(XB.val.cpu().numpy().view(np.uint32), bwd_vals.view(np.uint32))
+    cn2, _ = oracle.col_sqnorms(A.rowptr, fwd_vals)   # columns of A^T D^-1 = rows of D^-1 A
+    idx, mask = oracle.topk(oracle.pair_keys(cn2, G)["key"], k)
+    assert np.array_equal(snap["idx"], idx)
+    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, bwd_vals, mask)
+    assert np.array_equal(snap["rowptr"], ro) and np.array_equal(snap["col"], co)
+    assert np.array_equal(snap["val"].view(np.uint32), vo.view(np.uint32))
+    Ys = cache.spmm_sampled(Gd)
+    worst = 0.0
+    for r0 in range(0, n, 250_000):
+        rows = np.arange(r0, min(n, r0 + 250_000), dtype=np.int32)
+        Yo, S = oracle.spmm(ro, co, vo, G, rows=rows, with_mag=True)
+        got = Ys[r0:r0 + len(rows)].cpu().numpy().astype(np.float64)
+        worst = max(worst, float(np.max(np.abs(got - Yo) / np.maximum(S, FLT_MIN))))
+    print(f"[full] MEAN sampled: max rel err {worst:.3e}", flush=True)
+    assert worst <= 1e-4
+    cache.close()
