@@ -155,3 +155,36 @@ def test_cache_switches_between_random_and_topk_slices():
     ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
     assert np.array_equal(snap["val"].view(np.uint32), vo.view(np.uint32))
     cache.close()
+
+
+def test_full_size_randomized_refresh_copurchase():
+    """The bench's randomized-selector configuration at full size
+    (copurchase, 734,708 draws): draws, scales, mask and the scaled slice bit
+    for bit against the oracle, and every element of the sampled product."""
+    A = synth.make_graph("copurchase", 0)
+    n = A.n
+    G = synth.dense_normal(n, 256, seed=3)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n)
+    cache = rsc.Cache(X, X, refresh_interval=10)
+    Gd = torch.from_numpy(G).cuda()
+    k, seed = (n * 30) // 100, 12345
+    cache.refresh_random(Gd, k, seed=seed, step=0)
+    snap = rsc.cache_snapshot(cache)
+    cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)
+    o = oracle.sample_columns(oracle.pair_keys(cn2, G)["key"], k, seed)
+    mask_g = rsc.copy_to_host(cache.buffers()[4], (n + 31) // 32, np.uint32)
+    assert np.array_equal(mask_g, o["mask"])
+    ro, co, vo = oracle.slice_scaled(A.rowptr, A.col, A.val, o["mask"], o["colw"])
+    assert snap["nnz"] == len(co)
+    assert np.array_equal(snap["rowptr"], ro) and np.array_equal(snap["col"], co)
+    assert np.array_equal(snap["val"].view(np.uint32), vo.view(np.uint32))
+    Ys = cache.spmm_sampled(Gd)
+    worst = 0.0
+    for r0 in range(0, n, 250_000):
+        rows = np.arange(r0, min(n, r0 + 250_000), dtype=np.int32)
+        Yo, S = oracle.spmm(ro, co, vo, G, rows=rows, with_mag=True)
+        got = Ys[r0:r0 + len(rows)].cpu().numpy().astype(np.float64)
+        worst = max(worst, float(np.max(np.abs(got - Yo) / np.maximum(S, FLT_MIN))))
+    print(f"[full] randomized sampled: max rel err {worst:.3e}", flush=True)
+    assert worst <= 1e-4
+    cache.close()
