@@ -14,9 +14,10 @@
 //      compact the kept entries in LDS and write them out coalesced at their
 //      global positions, and write Rowptr'[i] for every row whose Rowptr[i]
 //      falls in the tile.
-// The three steps also exist fused in one kernel (count, decoupled look-back
-// scan over ticketed tiles, compaction; below), taken on request; both forms
-// give the same bytes.
+// When the mask fits LDS with room for several blocks per CU (up to about
+// 410,000 columns) the three steps run fused in one kernel instead (count,
+// decoupled look-back scan over ticketed tiles, compaction; below); both
+// forms give the same bytes.
 // Integer-only and deterministic. With a per-column scale (the randomized
 // sampler's 1/(k p)), each kept value becomes fl32(val * colw[col]).
 #include <cstdlib>
@@ -233,26 +234,28 @@ __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restri
 }
 
 // ---- single pass: count, decoupled look-back scan and compaction fused ----
-// Persistent blocks of 256 threads take tiles of 4096 entries in ticket
-// order (an atomic counter), so a tile's predecessors were all taken by
-// blocks that are already running. Per tile: load col/val (16 entries per
-// thread, coalesced; entry o = 256 i + thread, ballot group o >> 6, the
-// emit kernel's layout), test the mask bits (from LDS when the mask is
-// small enough for several blocks per CU, else from global memory, where the
-// n-bit set stays in L2), one ballot per 64 entries; publish the tile's kept
-// count, then the first wave looks back over the predecessors' published
-// counts (64 at a time) until it meets an inclusive prefix, and publishes
-// this tile's inclusive prefix. The kept entries are then written at their
+// Persistent blocks of 256 threads take kSub consecutive 4096-entry tiles at
+// a time in ticket order (an atomic counter), so a ticket's predecessors were
+// all taken by blocks that are already running. Per ticket: load col/val
+// (16 kSub entries per thread, coalesced; entry o = 256 i + thread, ballot
+// group o >> 6), test the mask bits (from LDS when the mask is small enough
+// for several blocks per CU, else from global memory, where the n-bit set
+// stays in L2), one ballot per 64 entries; publish the ticket's kept count,
+// then the first wave looks back over the predecessors' published counts
+// (64 at a time) until it meets an inclusive prefix, and publishes this
+// ticket's inclusive prefix. The kept entries are then written at their
 // global positions straight from registers: the kept entries of one ballot
 // are consecutive in the output, so each wave's stores cover one contiguous
-// range. Several blocks per CU keep several tiles' loads and look-backs in
-// flight at once.
-// Status word of a tile: bits 63..62 = 1 (count published) or 2 (inclusive
+// range. Several blocks per CU keep several tickets' loads and look-backs in
+// flight at once; three tiles per ticket cut the look-backs and ticket
+// atomics to a third.
+// Status word of a ticket: bits 63..62 = 1 (count published) or 2 (inclusive
 // prefix published), bits 61..0 the value; 0 = nothing yet.
 // Every wait is bounded: after kSpinLimit polls without progress the kernel
 // records a failure (*nnz_out = -1), takes the missing counts as 0 and
 // finishes, so no wave can wait forever.
 constexpr int kFusedThreads = 256;
+constexpr int kFusedSub = 3;           // 4096-entry tiles per ticket (one look-back for 12,288 entries)
 constexpr int kFusedBlocksPerCu = 8;
 constexpr int kLdsPerCu = 160 * 1024;
 constexpr uint64_t kFlagAgg = 1ull << 62, kFlagIncl = 2ull << 62, kValMask = (1ull << 62) - 1;
@@ -269,7 +272,7 @@ __device__ __forceinline__ void store_status(uint64_t *p, uint64_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <bool kLdsMask>
+template <bool kLdsMask, int kSub>
 __global__ __launch_bounds__(kFusedThreads) void slice_fused_kernel(
     const int32_t *__restrict__ rowptr, int32_t n_rows, const int32_t *__restrict__ col,
     const float *__restrict__ val, int64_t nnz, const uint32_t *__restrict__ mask, int32_t n_words, int32_t nt,
@@ -277,8 +280,8 @@ __global__ __launch_bounds__(kFusedThreads) void slice_fused_kernel(
     int32_t *__restrict__ col_out, float *__restrict__ val_out, int64_t capacity, int64_t *__restrict__ nnz_out,
     int32_t *__restrict__ failed, const double *__restrict__ colw) {
     extern __shared__ uint32_t s_mask[];  // n_words words with kLdsMask, else empty
-    __shared__ uint64_t s_ball[kGroups];
-    __shared__ uint32_t s_pre[kGroups + 1];
+    __shared__ uint64_t s_ball[kGroups * kSub];
+    __shared__ uint32_t s_pre[kGroups * kSub + 1];
     __shared__ int32_t s_tile, s_rows[2];
     __shared__ int64_t s_base;
     const int T = threadIdx.x, lane = T & 63, wv = T >> 6;
@@ -290,21 +293,21 @@ __global__ __launch_bounds__(kFusedThreads) void slice_fused_kernel(
         __syncthreads();  // s_tile visible; the previous tile's shared state is no longer read
         const int32_t tile = s_tile;
         if (tile >= nt) break;  // block-uniform
-        const int64_t ts = (int64_t)tile * kTile;
-        const int64_t te = min<int64_t>(ts + kTile, nnz);
+        const int64_t ts = (int64_t)tile * kTile * kSub;
+        const int64_t te = min<int64_t>(ts + (int64_t)kTile * kSub, nnz);
         const bool last = tile == nt - 1;
         if (T == 0) s_rows[0] = lower_bound_rowptr(rowptr, n_rows, ts);
         if (T == 1) s_rows[1] = last ? n_rows + 1 : lower_bound_rowptr(rowptr, n_rows, te);
-        int32_t rc[kPer];
-        float rv[kPer];
+        int32_t rc[kPer * kSub];
+        float rv[kPer * kSub];
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) {
+        for (int i = 0; i < kPer * kSub; ++i) {
             const int64_t p = ts + T + kFusedThreads * i;
             rc[i] = p < te ? __builtin_nontemporal_load(col + p) : -1;
             rv[i] = p < te ? __builtin_nontemporal_load(val + p) : 0.f;
         }
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) {
+        for (int i = 0; i < kPer * kSub; ++i) {
             const int32_t c = rc[i];
             bool k = false;
             if (c >= 0 && (c >> 5) < n_words) {
@@ -316,16 +319,26 @@ __global__ __launch_bounds__(kFusedThreads) void slice_fused_kernel(
         }
         __syncthreads();
         if (wv == 0) {
-            // exclusive scan of the 64 ballot counts, then publish and look back
-            const uint32_t cnt = __popcll(s_ball[lane]);
-            uint32_t incl = cnt;
+            // exclusive scan of the ballot counts (kSub per lane), then publish and look back
+            uint32_t cnt[kSub], own = 0;
+#pragma unroll
+            for (int u = 0; u < kSub; ++u) {
+                cnt[u] = __popcll(s_ball[kSub * lane + u]);
+                own += cnt[u];
+            }
+            uint32_t incl = own;
             for (int off = 1; off < 64; off <<= 1) {
                 const uint32_t x = __shfl_up(incl, off);
                 if (lane >= off) incl += x;
             }
-            s_pre[lane] = incl - cnt;
+            uint32_t run = incl - own;
+#pragma unroll
+            for (int u = 0; u < kSub; ++u) {
+                s_pre[kSub * lane + u] = run;
+                run += cnt[u];
+            }
             const uint32_t total = __shfl(incl, 63);
-            if (lane == 63) s_pre[kGroups] = incl;
+            if (lane == 63) s_pre[kGroups * kSub] = incl;
             int64_t excl = 0;
             if (tile == 0) {
                 if (lane == 0) store_status(status, kFlagIncl | total);
@@ -362,7 +375,7 @@ __global__ __launch_bounds__(kFusedThreads) void slice_fused_kernel(
         const int64_t base = s_base;
         const uint64_t below = (1ull << lane) - 1ull;
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) {
+        for (int i = 0; i < kPer * kSub; ++i) {
             const uint64_t b = s_ball[4 * i + wv];
             if ((b >> lane) & 1ull) {
                 const int64_t pos = base + s_pre[4 * i + wv] + __popcll(b & below);
@@ -372,12 +385,12 @@ __global__ __launch_bounds__(kFusedThreads) void slice_fused_kernel(
                 }
             }
         }
-        const uint32_t total = s_pre[kGroups];
+        const uint32_t total = s_pre[kGroups * kSub];
         const int32_t r0 = s_rows[0], r1 = s_rows[1];
         for (int64_t i = (int64_t)r0 + T; i < r1; i += kFusedThreads) {
             const int64_t off = (int64_t)rowptr[i] - ts;
             uint32_t c;
-            if (off >= kTile || ts + off >= te) {
+            if (off >= (int64_t)kTile * kSub || ts + off >= te) {
                 c = total;
             } else {
                 const int g = (int)(off >> 6), l = (int)(off & 63);
@@ -402,15 +415,21 @@ __global__ __launch_bounds__(256) void zero_rows_kernel(int32_t *__restrict__ p,
     if (blockIdx.x == 0 && threadIdx.x == 0) *nnz_out = 0;
 }
 
-// The single-pass form runs only on request (RSC_SLICE_FUSED=1): measured on
-// the benchmark workloads it is still slower than the three launches (social
-// about 0.50 against 0.43 ms, copurchase 1.02 against 0.72 ms): what it saves
-// (one read of col, two launches) costs less than the look-backs, each a
-// chain of dependent L2 round trips over the tiles still in flight.
+// Whether the fused kernel keeps the mask in LDS: a copy per block, when at
+// least three blocks' copies (plus their small shared state) fit a CU.
+bool mask_in_lds(int32_t n_words) {
+    return sizeof(uint32_t) * (size_t)n_words + 2048 <= (size_t)kLdsPerCu / 3;
+}
+
+// The single-pass form is taken when its mask goes to LDS (up to about
+// 410,000 columns): measured there it beats the three launches (social's
+// refresh 0.540 against 0.570 ms, protein's 0.427 against 0.436 ms); with
+// the mask in global memory the lookups cost more than the saved read of col
+// (gcn2 0.485 against 0.469 ms, copurchase 1.41 against 1.35 ms).
+// RSC_SLICE_FUSED = 0 / 1 forces the three-launch / fused form.
 bool use_fused(int32_t n_words) {
-    (void)n_words;
     if (const char *env = getenv("RSC_SLICE_FUSED")) return atoi(env) != 0;
-    return false;
+    return mask_in_lds(n_words);
 }
 
 }  // namespace
@@ -442,22 +461,22 @@ hipError_t slice_launch(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
         // ws: [ticket, failure flag | pad to 256 B][status word per tile]
         int32_t *ticket = static_cast<int32_t *>(ws);
         uint64_t *status = reinterpret_cast<uint64_t *>(static_cast<char *>(ws) + 256);
-        const int64_t words = 32 + (int64_t)nt;  // the 256-byte head and the status words
+        const int32_t nt2 = (int32_t)ceil_div(nt, kFusedSub);
+        const int64_t words = 32 + (int64_t)nt2;  // the 256-byte head and the status words
         zero_words_kernel<<<(unsigned)std::min<int64_t>(ceil_div(words, 256), 1024), 256, 0, stream>>>(
             static_cast<uint64_t *>(ws), words);
-        // the mask goes to LDS when at least three blocks' copies fit a CU
         const size_t mask_bytes = sizeof(uint32_t) * (size_t)n_words;
-        const int lds_blocks = (int)std::min<size_t>(kFusedBlocksPerCu, kLdsPerCu / (mask_bytes + 2048));
-        const bool lds = lds_blocks >= 3;
-        const int per_cu = lds ? lds_blocks : kFusedBlocksPerCu;
-        const unsigned grid = (unsigned)std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * per_cu, nt));
+        const bool lds = mask_in_lds(n_words);
+        const int per_cu = lds ? (int)std::min<size_t>(kFusedBlocksPerCu, kLdsPerCu / (mask_bytes + 2048))
+                               : kFusedBlocksPerCu;
+        const unsigned grid = (unsigned)std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * per_cu, nt2));
         if (lds)
-            slice_fused_kernel<true><<<grid, kFusedThreads, mask_bytes, stream>>>(
-                rowptr, n_rows, col, val, nnz, mask, n_words, nt, status, ticket, rowptr_out, col_out, val_out,
+            slice_fused_kernel<true, kFusedSub><<<grid, kFusedThreads, mask_bytes, stream>>>(
+                rowptr, n_rows, col, val, nnz, mask, n_words, nt2, status, ticket, rowptr_out, col_out, val_out,
                 capacity, nnz_out, ticket + 1, colw);
         else
-            slice_fused_kernel<false><<<grid, kFusedThreads, 0, stream>>>(
-                rowptr, n_rows, col, val, nnz, mask, n_words, nt, status, ticket, rowptr_out, col_out, val_out,
+            slice_fused_kernel<false, kFusedSub><<<grid, kFusedThreads, 0, stream>>>(
+                rowptr, n_rows, col, val, nnz, mask, n_words, nt2, status, ticket, rowptr_out, col_out, val_out,
                 capacity, nnz_out, ticket + 1, colw);
         return hipGetLastError();
     }
