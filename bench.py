@@ -71,13 +71,17 @@ def refresh_random_bytes(n: int, nnz: int, nnz_kept: int, k: int, d: int) -> int
             + 12 * nnz + 8 * (n + 1) + 16 * nnz_kept)
 
 
+COUNTED_SOURCES = ("spmm.hip", "probe.hip", "scores.hip", "topk.hip", "slice.hip")
+
+
 def kernel_source_digest() -> str:
-    """Digest of the SpMM and gather-probe kernel sources with comments and
-    blank lines removed (a comment edit does not invalidate a counter
-    record)."""
+    """Digest of the kernel sources the counter records measure (the SpMM,
+    the gather probe and the refresh's scores, top-k and slice), with
+    comments and blank lines removed (a comment edit does not invalidate a
+    counter record)."""
     import re
     code = []
-    for name in ("spmm.hip", "probe.hip"):
+    for name in COUNTED_SOURCES:
         with open(os.path.join(ROOT, "paper_2210_10737_amd", "csrc", name)) as fh:
             src = fh.read()
         src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)

@@ -28,13 +28,18 @@ def test_digest_ignores_comments_only(tmp_path, monkeypatch):
     fake = tmp_path / "paper_2210_10737_amd" / "csrc"
     fake.mkdir(parents=True)
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    (fake / "probe.hip").write_text(probe)
+    for name in bench.COUNTED_SOURCES:
+        (fake / name).write_text(open(os.path.join(csrc, name)).read())
     (fake / "spmm.hip").write_text("// a new comment\n\n" + text.replace("namespace rsc {", "namespace rsc {  /* x */"))
     assert bench.kernel_source_digest() == d0
     (fake / "spmm.hip").write_text(text.replace("kUnroll = 8", "kUnroll = 4"))
     assert bench.kernel_source_digest() != d0
     (fake / "spmm.hip").write_text(text)
     (fake / "probe.hip").write_text(probe.replace("kProbeWaves = 4", "kProbeWaves = 8"))
+    assert bench.kernel_source_digest() != d0
+    (fake / "probe.hip").write_text(probe)
+    slice_src = open(os.path.join(csrc, "slice.hip")).read()
+    (fake / "slice.hip").write_text(slice_src.replace("kFusedSub = 3", "kFusedSub = 2"))
     assert bench.kernel_source_digest() != d0
 
 
