@@ -365,24 +365,26 @@ def vendor_baseline(X, H, Y, plan, reps: int = 10):
     return out
 
 
-def gather_ceiling(handle, B, d, n_entries, reps: int = 5):
+def gather_ceiling(handle, B, d, n_entries, reps: int = 5, out=None):
     """Times a gather probe (rsc_spmm_plan_gather_probe for a plan, the exact
     product's B-row gathers alone; rsc_cache_gather_probe for a cache, the
     sampled product's) at 4, 8 and 16 loads in flight per wave, median of
     `reps` each after one untimed run; the fastest setting is the ceiling.
-    HIP events on the current stream, which the library launches on."""
+    With `out` (a scratch tensor of the product's output shape) the probe
+    also writes the product's output stream. HIP events on the current
+    stream, which the library launches on."""
     import statistics
 
     import torch
     sink = torch.empty(max((n_entries + 63) // 64, 1), dtype=torch.float32, device=B.device)
     per, slice_w = {}, None
     for inflight in (4, 8, 16):
-        slice_w = handle.gather_probe(B, d=d, inflight=inflight, sink=sink)
+        slice_w = handle.gather_probe(B, d=d, inflight=inflight, sink=sink, out=out)
         ts = []
         for _ in range(reps):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
-            handle.gather_probe(B, d=d, inflight=inflight, sink=sink)
+            handle.gather_probe(B, d=d, inflight=inflight, sink=sink, out=out)
             e1.record()
             e1.synchronize()
             ts.append(e0.elapsed_time(e1))
@@ -392,8 +394,10 @@ def gather_ceiling(handle, B, d, n_entries, reps: int = 5):
     return {"ms": round(ms, 4), "inflight": best, "slice_floats": slice_w,
             "ms_by_inflight": {str(k_): round(v, 4) for k_, v in per.items()},
             "logical_gather_GBs": round(4.0 * n_entries * d / (ms * 1e-3) / 1e9, 1),
-            "what": "the product's B-row gathers alone: same column stream (a plan's hinted copy), "
-                    "feature passes and cache policy; no values, row walk or output"}
+            "what": ("the product's B-row gathers alone: same column stream (a plan's hinted copy), "
+                     "feature passes and cache policy; no values, row walk or output") if out is None else
+                    ("the product's B-row gathers and its output stream (each wave writes an even share "
+                     "of the output rows after its gathers); no values or row walk")}
 
 
 def parity_check(A, Hh, Gh, k, Y, Yb, kept, n_rows, seed):
@@ -759,7 +763,13 @@ def main() -> int:
     # stream, feature passes and cache policy; no values, rows or output),
     # at 4, 8 and 16 loads in flight per wave; the fastest is the ceiling
     probe = gather_ceiling(plan, H, d, nnz)
-    probe_sampled = gather_ceiling(cache, G, d, int(cache.get(args.warmup + args.steps)["slice"].nnz))
+    nnz_s = int(cache.get(args.warmup + args.steps)["slice"].nnz)
+    probe_sampled = gather_ceiling(cache, G, d, nnz_s)
+    # the same with each product's output stream (into scratch of its shape)
+    scratch_out = torch.empty_like(Y)
+    probe_out = gather_ceiling(plan, H, d, nnz, out=scratch_out)
+    probe_sampled_out = gather_ceiling(cache, G, d, nnz_s, out=scratch_out)
+    del scratch_out
 
     # cold-cache repetitions, outside the timed steps: before each, write a
     # 1 GiB scratch buffer (more than the 4 MB L2s and the 256 MB MALL)
@@ -850,8 +860,11 @@ def main() -> int:
                    "frac": round(b / (float(np.median(per[kind])) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
             for kind, b in (("exact", b_exact), ("sampled", b_sampled), ("refresh", b_refresh)) if per[kind]},
         # the sampled product against its own gathers alone (the cache's probe)
-        "sampled_gather_ceiling": dict(probe_sampled, frac_of_gather_ceiling=round(
-            probe_sampled["ms"] / float(np.median(per["sampled"])), 4)),
+        "sampled_gather_ceiling": dict(
+            probe_sampled,
+            frac_of_gather_ceiling=round(probe_sampled["ms"] / float(np.median(per["sampled"])), 4),
+            with_output_stream=probe_sampled_out,
+            frac_of_gather_output_ceiling=round(probe_sampled_out["ms"] / float(np.median(per["sampled"])), 4)),
         "roofline": {
             "bound": "hbm",
             "kernel": "spmm_long_kernel + spmm_rows_kernel (the exact SpMM, one plan run)",
@@ -865,6 +878,9 @@ def main() -> int:
             "gather_ceiling_GBs": round(b_exact / (probe["ms"] * 1e-3) / 1e9, 2),
             "frac_of_gather_ceiling": round(probe["ms"] / exact_ms, 4),
             "gather_ceiling": probe,
+            # gathers plus the product's output stream
+            "frac_of_gather_output_ceiling": round(probe_out["ms"] / exact_ms, 4),
+            "gather_output_ceiling": probe_out,
             "algorithmic_bytes_per_launch": b_exact,
             "avg_launch_ms": round(exact_ms, 4),
             "traffic": None,

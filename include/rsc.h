@@ -177,16 +177,21 @@ rsc_status_t rsc_spmm_plan_destroy(rsc_spmm_plan_t *plan);
  * when it has one) in stored order, 64 entries per wave, and loads each
  * referenced row of B with the lane layout, feature passes and cache policy
  * an unblocked run of the plan takes for this d (rows are not walked, no
- * values are read, no Y is written); the loaded values are summed and one
- * float per 64 entries is written to sink (sink_count >= ceil(nnz / 64)),
- * only so that no load is dropped. inflight (4, 8 or 16): loads each wave
- * issues before consuming any. Its duration bounds how fast the product's
- * own gather pattern can run, the "gather ceiling" of the product.
- * *slice_out (nullable) receives the feature-pass width used. Runs are
- * tracked for rsc_spmm_plan_destroy like rsc_spmm_plan_run. */
+ * values are read); the loaded values are summed and one float per 64
+ * entries is written to sink (sink_count >= ceil(nnz / 64)), only so that no
+ * load is dropped. inflight (4, 8 or 16): loads each wave issues before
+ * consuming any. Its duration bounds how fast the product's own gather
+ * pattern can run, the "gather ceiling" of the product.
+ * Y (nullable; n_rows x d, ldy, checked like rsc_spmm's Y): also write an
+ * output of the product's size with the product's store pattern, the rows
+ * shared evenly over the waves, each wave's after its gathers. Y's contents
+ * afterwards are unspecified (not the product); nothing is written when A
+ * has no entries. The duration then bounds the gathers plus the output
+ * stream. *slice_out (nullable) receives the feature-pass width used. Runs
+ * are tracked for rsc_spmm_plan_destroy like rsc_spmm_plan_run. */
 rsc_status_t rsc_spmm_plan_gather_probe(rsc_spmm_plan_t *plan, const float *B, int32_t d, int64_t ldb,
-                                        int32_t inflight, float *sink, int64_t sink_count,
-                                        int32_t *slice_out, hipStream_t stream);
+                                        int32_t inflight, float *sink, int64_t sink_count, float *Y,
+                                        int64_t ldy, int32_t *slice_out, hipStream_t stream);
 
 /* MEAN aggregator operand (appendix A.3: SpMM_MEAN(A, H) = D^-1 A H, D the
  * degree matrix of A, D_ii = stored entries of row i). Writes A's values
@@ -358,12 +363,13 @@ rsc_status_t rsc_spmm_sampled(rsc_cache_t *cache, const float *B, int32_t d, int
 /* Measurement helper, not a step of the method: the gather-only pass of
  * rsc_spmm_sampled on the cached slice, as rsc_spmm_plan_gather_probe is for
  * a plan (the slice's column stream, the feature passes the sampled product
- * takes, no hint; rows not walked, no values, no Y; one float per 64 kept
- * entries into sink, sink_count >= ceil(nnz' / 64)). Needs a refreshed
+ * takes, no hint; rows not walked, no values; one float per 64 kept
+ * entries into sink, sink_count >= ceil(nnz' / 64); Y nullable, the
+ * product's n_rows x d output stream as for a plan). Needs a refreshed
  * cache; reads nnz' like rsc_cache_get. */
 rsc_status_t rsc_cache_gather_probe(rsc_cache_t *cache, const float *B, int32_t d, int64_t ldb,
-                                    int32_t inflight, float *sink, int64_t sink_count,
-                                    int32_t *slice_out, hipStream_t stream);
+                                    int32_t inflight, float *sink, int64_t sink_count, float *Y,
+                                    int64_t ldy, int32_t *slice_out, hipStream_t stream);
 /* Device arrays owned by the cache: cn2 (fp64) and colnnz (int32), n_cols
  * entries each; keys (uint64) and row square-norms rn2 (fp64) of the last
  * scored operand; mask (ceil(n_cols/32) words) of the last selection. Any

@@ -116,7 +116,8 @@ def lib():
             "rsc_spmm_plan_create": ([csrp, vp, ctypes.POINTER(vp)], ctypes.c_int),
             "rsc_spmm_plan_run": ([vp, vp, i32, i64, vp, i64, vp], ctypes.c_int),
             "rsc_spmm_plan_destroy": ([vp], ctypes.c_int),
-            "rsc_spmm_plan_gather_probe": ([vp, vp, i32, i64, i32, vp, i64, ctypes.POINTER(i32), vp], ctypes.c_int),
+            "rsc_spmm_plan_gather_probe": ([vp, vp, i32, i64, i32, vp, i64, vp, i64, ctypes.POINTER(i32), vp],
+                                          ctypes.c_int),
             "rsc_col_sqnorms": ([csrp, vp, vp, vp], ctypes.c_int),
             "rsc_degree_scale": ([csrp, vp, i32, vp, vp], ctypes.c_int),
             "rsc_pair_scores": ([vp, vp, i32, i32, i64, vp, vp, vp, vp], ctypes.c_int),
@@ -140,7 +141,8 @@ def lib():
             "rsc_cache_buffers": ([vp, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
                                    ctypes.POINTER(vp), ctypes.POINTER(vp)], ctypes.c_int),
             "rsc_cache_destroy": ([vp], ctypes.c_int),
-            "rsc_cache_gather_probe": ([vp, vp, i32, i64, i32, vp, i64, ctypes.POINTER(i32), vp], ctypes.c_int),
+            "rsc_cache_gather_probe": ([vp, vp, i32, i64, i32, vp, i64, vp, i64, ctypes.POINTER(i32), vp],
+                                      ctypes.c_int),
             "rsc_cache_norms": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), vp],
                                 ctypes.c_int),
             "rsc_k_from_fraction": ([i32, i32, i32], i32),
@@ -208,6 +210,28 @@ def _ld(t: torch.Tensor) -> int:
     return t.stride(0)
 
 
+def _dense(t: torch.Tensor, rows: int, d: int, name: str) -> tuple[int, int]:
+    """(device address, leading dimension) of a float32 operand that holds at
+    least rows x d elements: the library reads or writes that many through
+    the pointer, so a smaller or differently typed tensor is refused here."""
+    if t.dtype != torch.float32:
+        raise ValueError(f"{name}: dtype {t.dtype}, float32 expected")
+    ld = _ld(t)
+    if t.shape[0] < rows or t.shape[1] < d:
+        raise ValueError(f"{name}: shape {tuple(t.shape)} holds less than {rows} x {d}")
+    return _dp(t), ld
+
+
+def _vec(t: torch.Tensor | None, count: int, dtype, name: str) -> int | None:
+    """Device address of an optional 1-D-contiguous array of at least count
+    elements of dtype."""
+    if t is None:
+        return None
+    if t.dtype != dtype or not t.is_contiguous() or t.numel() < count:
+        raise ValueError(f"{name}: {t.dtype}[{t.numel()}], contiguous {dtype}[>= {count}] expected")
+    return _dp(t)
+
+
 def _new_out(rows: int, d: int, device) -> torch.Tensor:
     """rows x d output view with a leading dimension rounded up to 4 floats."""
     ld = (d + 3) // 4 * 4
@@ -241,9 +265,10 @@ class DeviceCsr:
         return cls(len(rowptr) - 1, int(n_cols), rp, c, v)
 
     def struct(self) -> CsrStruct:
-        return CsrStruct(self.n_rows, self.n_cols, self.nnz, _dp(self.rowptr),
-                         _dp(self.col) if self.nnz else None,
-                         _dp(self.val) if self.nnz else None)
+        return CsrStruct(self.n_rows, self.n_cols, self.nnz,
+                         _vec(self.rowptr, self.n_rows + 1, torch.int32, "rowptr"),
+                         _vec(self.col, self.nnz, torch.int32, "col") if self.nnz else None,
+                         _vec(self.val, self.nnz, torch.float32, "val") if self.nnz else None)
 
 
 # ---------------------------------------------------------------- A1
@@ -259,8 +284,9 @@ def spmm(A: DeviceCsr, B: torch.Tensor, d: int | None = None, out: torch.Tensor 
     s = A.struct()
     need = lib().rsc_spmm_workspace_bytes(ctypes.byref(s))
     ws = _workspace(need, B.device) if ws is None else ws
-    _check(lib().rsc_spmm(ctypes.byref(s), _dp(B), d, _ld(B), _dp(Y), _ld(Y),
-                          _dp(ws), ws.numel(), _stream()))
+    pb, ldb = _dense(B, A.n_cols, d, "B")
+    py, ldy = _dense(Y, A.n_rows, d, "Y")
+    _check(lib().rsc_spmm(ctypes.byref(s), pb, d, ldb, py, ldy, _dp(ws), ws.numel(), _stream()))
     return Y
 
 
@@ -270,7 +296,9 @@ def spmm_noalloc(A: DeviceCsr, B: torch.Tensor, d: int | None = None, out: torch
     nothing is allocated here either."""
     d = B.shape[1] if d is None else d
     Y = _new_out(A.n_rows, d, B.device) if out is None else out
-    _check(lib().rsc_spmm_noalloc(ctypes.byref(A.struct()), _dp(B), d, _ld(B), _dp(Y), _ld(Y), _stream()))
+    pb, ldb = _dense(B, A.n_cols, d, "B")
+    py, ldy = _dense(Y, A.n_rows, d, "Y")
+    _check(lib().rsc_spmm_noalloc(ctypes.byref(A.struct()), pb, d, ldb, py, ldy, _stream()))
     return Y
 
 
@@ -289,19 +317,25 @@ class SpmmPlan:
     def run(self, B: torch.Tensor, d: int | None = None, out: torch.Tensor | None = None) -> torch.Tensor:
         d = B.shape[1] if d is None else d
         Y = _new_out(self.A.n_rows, d, B.device) if out is None else out
-        _check(lib().rsc_spmm_plan_run(self._h, _dp(B), d, _ld(B), _dp(Y), _ld(Y), _stream()))
+        pb, ldb = _dense(B, self.A.n_cols, d, "B")
+        py, ldy = _dense(Y, self.A.n_rows, d, "Y")
+        _check(lib().rsc_spmm_plan_run(self._h, pb, d, ldb, py, ldy, _stream()))
         return Y
 
     def gather_probe(self, B: torch.Tensor, d: int | None = None, inflight: int = 8,
-                     sink: torch.Tensor | None = None) -> int:
+                     sink: torch.Tensor | None = None, out: torch.Tensor | None = None) -> int:
         """The gather-only pass of this plan's product (rsc_spmm_plan_gather_probe,
-        a measurement helper); returns the feature-pass width it used."""
+        a measurement helper), with `out` (n_rows x d) also the product's
+        output stream (out's contents are then unspecified); returns the
+        feature-pass width it used."""
         d = B.shape[1] if d is None else d
         need = (self.A.nnz + 63) // 64
         sink = torch.empty(max(need, 1), dtype=torch.float32, device=B.device) if sink is None else sink
         sl = ctypes.c_int32(0)
-        _check(lib().rsc_spmm_plan_gather_probe(self._h, _dp(B), d, _ld(B), inflight, _dp(sink), sink.numel(),
-                                                ctypes.byref(sl), _stream()))
+        pb, ldb = _dense(B, self.A.n_cols, d, "B")
+        py, ldy = _dense(out, self.A.n_rows, d, "out") if out is not None else (None, 0)
+        _check(lib().rsc_spmm_plan_gather_probe(self._h, pb, d, ldb, inflight, _vec(sink, 0, torch.float32, "sink"),
+                                                sink.numel(), py, ldy, ctypes.byref(sl), _stream()))
         return sl.value
 
     def close(self) -> None:
@@ -344,7 +378,8 @@ def pair_scores(cn2: torch.Tensor, B: torch.Tensor, d: int | None = None, with_s
     key = torch.empty(n, dtype=torch.int64, device=B.device)
     score = torch.empty(n, dtype=torch.float32, device=B.device) if with_score else None
     rn2 = torch.empty(n, dtype=torch.float64, device=B.device) if with_rn2 else None
-    _check(lib().rsc_pair_scores(_dp(cn2), _dp(B), n, d, _ld(B), _dp(key),
+    pb, ldb = _dense(B, n, d, "B")
+    _check(lib().rsc_pair_scores(_vec(cn2, n, torch.float64, "cn2"), pb, n, d, ldb, _dp(key),
                                  _ptr(score), _ptr(rn2), _stream()))
     out = [key] + ([score] if with_score else []) + ([rn2] if with_rn2 else [])
     return out[0] if len(out) == 1 else tuple(out)
@@ -378,7 +413,9 @@ def slice_csr(A: DeviceCsr, mask: torch.Tensor, capacity: int | None = None,
     s = A.struct()
     need = lib().rsc_slice_workspace_bytes(ctypes.byref(s))
     ws = _workspace(need, dev) if ws is None else ws
-    _check(lib().rsc_slice_csr(ctypes.byref(s), _ptr(mask), _ptr(colw), _dp(rp), _dp(co),
+    pm = _vec(mask, (A.n_cols + 31) // 32, torch.int32, "mask")
+    pw = _vec(colw, A.n_cols, torch.float64, "colw")
+    _check(lib().rsc_slice_csr(ctypes.byref(s), pm, pw, _dp(rp), _dp(co),
                                _dp(vo), cap, _dp(nnz_out), _dp(ws), ws.numel(), _stream()))
     return DeviceCsr(A.n_rows, A.n_cols, rp, co, vo, nnz=cap), nnz_out
 
@@ -424,18 +461,23 @@ class Cache:
 
     def refresh(self, B: torch.Tensor, k: int, step: int, d: int | None = None) -> None:
         d = B.shape[1] if d is None else d
-        _check(lib().rsc_cache_refresh(self._h, _dp(B), d, _ld(B), k, step, _stream()))
+        _check(lib().rsc_cache_refresh(self._h, *self._b(B, d), k, step, _stream()))
 
     def score(self, B: torch.Tensor, d: int | None = None) -> None:
         d = B.shape[1] if d is None else d
-        _check(lib().rsc_cache_score(self._h, _dp(B), d, _ld(B), _stream()))
+        _check(lib().rsc_cache_score(self._h, *self._b(B, d), _stream()))
+
+    def _b(self, B: torch.Tensor, d: int):
+        # (pointer, d, ld) of an operand with a row per column of X
+        pb, ldb = _dense(B, self.X.n_cols, d, "B")
+        return pb, d, ldb
 
     def select(self, k: int, step: int) -> None:
         _check(lib().rsc_cache_select(self._h, k, step, _stream()))
 
     def refresh_random(self, B: torch.Tensor, k_draws: int, seed: int, step: int, d: int | None = None) -> None:
         d = B.shape[1] if d is None else d
-        _check(lib().rsc_cache_refresh_random(self._h, _dp(B), d, _ld(B), k_draws, seed, step, _stream()))
+        _check(lib().rsc_cache_refresh_random(self._h, *self._b(B, d), k_draws, seed, step, _stream()))
 
     def get(self, step: int, with_slice: bool = True):
         """dict(slice=CsrStruct or None, idx_ptr, k, needs_refresh, version).
@@ -454,21 +496,23 @@ class Cache:
     def spmm_sampled(self, B: torch.Tensor, d: int | None = None, out: torch.Tensor | None = None):
         d = B.shape[1] if d is None else d
         Y = _new_out(self.X.n_rows, d, B.device) if out is None else out
-        _check(lib().rsc_spmm_sampled(self._h, _dp(B), d, _ld(B), _dp(Y), _ld(Y), _stream()))
+        py, ldy = _dense(Y, self.X.n_rows, d, "Y")
+        _check(lib().rsc_spmm_sampled(self._h, *self._b(B, d), py, ldy, _stream()))
         return Y
 
     def gather_probe(self, B: torch.Tensor, d: int | None = None, inflight: int = 8,
-                     sink: torch.Tensor | None = None) -> int:
+                     sink: torch.Tensor | None = None, out: torch.Tensor | None = None) -> int:
         """The gather-only pass of spmm_sampled on the cached slice
-        (rsc_cache_gather_probe, a measurement helper); returns the
-        feature-pass width it used."""
+        (rsc_cache_gather_probe, a measurement helper), with `out` also the
+        product's output stream; returns the feature-pass width it used."""
         d = B.shape[1] if d is None else d
         if sink is None:
             nnz = self.get(0)["slice"].nnz
             sink = torch.empty(max((nnz + 63) // 64, 1), dtype=torch.float32, device=B.device)
         sl = ctypes.c_int32(0)
-        _check(lib().rsc_cache_gather_probe(self._h, _dp(B), d, _ld(B), inflight, _dp(sink), sink.numel(),
-                                            ctypes.byref(sl), _stream()))
+        py, ldy = _dense(out, self.X.n_rows, d, "out") if out is not None else (None, 0)
+        _check(lib().rsc_cache_gather_probe(self._h, *self._b(B, d), inflight, _vec(sink, 0, torch.float32, "sink"),
+                                            sink.numel(), py, ldy, ctypes.byref(sl), _stream()))
         return sl.value
 
     def norms(self, scored: bool = True):

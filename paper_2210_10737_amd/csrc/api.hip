@@ -482,10 +482,12 @@ rsc_status_t rsc_spmm_plan_run(rsc_spmm_plan_t *p, const float *B, int32_t d, in
 }
 
 rsc_status_t rsc_spmm_plan_gather_probe(rsc_spmm_plan_t *p, const float *B, int32_t d, int64_t ldb, int32_t inflight,
-                                       float *sink, int64_t sink_count, int32_t *slice_out, hipStream_t stream) {
+                                       float *sink, int64_t sink_count, float *Y, int64_t ldy, int32_t *slice_out,
+                                       hipStream_t stream) {
     if (!p) return fail(RSC_ERR_INVALID_ARGUMENT, "plan is NULL");
     const rsc_csr_t *A = &p->A;
     RSC_TRY(check_dense(B, A->n_cols, d, ldb, "B"));
+    if (Y) RSC_TRY(check_dense(Y, A->n_rows, d, ldy, "Y"));
     if (inflight != 4 && inflight != 8 && inflight != 16)
         return fail(RSC_ERR_INVALID_ARGUMENT, "inflight = %d (4, 8 or 16)", inflight);
     const int64_t need = rsc::gather_probe_sink_count(A->nnz);
@@ -497,8 +499,8 @@ rsc_status_t rsc_spmm_plan_gather_probe(rsc_spmm_plan_t *p, const float *B, int3
     const int32_t slice = rsc::spmm_slice_width(A->n_rows, A->nnz, A->n_cols, d);
     const bool hint = p->colf != nullptr && rsc::spmm_hint_taken(A->n_cols, d, slice);
     if (slice_out) *slice_out = slice;
-    RSC_HIP(rsc::gather_probe_launch(p->colf ? p->colf : A->col, A->nnz, B, ldb, d, slice, hint, inflight, sink,
-                                     stream),
+    RSC_HIP(rsc::gather_probe_launch(p->colf ? p->colf : A->col, A->nnz, B, ldb, d, slice, hint, inflight, sink, Y,
+                                     ldy, A->n_rows, stream),
             "gather probe launch");
     RSC_HIP(p->fence.record(stream), "gather probe event");
     return RSC_OK;
@@ -902,10 +904,12 @@ rsc_status_t rsc_spmm_sampled(rsc_cache_t *c, const float *B, int32_t d, int64_t
 }
 
 rsc_status_t rsc_cache_gather_probe(rsc_cache_t *c, const float *B, int32_t d, int64_t ldb, int32_t inflight,
-                                    float *sink, int64_t sink_count, int32_t *slice_out, hipStream_t stream) {
+                                    float *sink, int64_t sink_count, float *Y, int64_t ldy, int32_t *slice_out,
+                                    hipStream_t stream) {
     if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
     if (c->version == 0) return fail(RSC_ERR_INVALID_ARGUMENT, "cache was never refreshed");
     RSC_TRY(check_dense(B, c->X.n_cols, d, ldb, "B"));
+    if (Y) RSC_TRY(check_dense(Y, c->X.n_rows, d, ldy, "Y"));
     if (inflight != 4 && inflight != 8 && inflight != 16)
         return fail(RSC_ERR_INVALID_ARGUMENT, "inflight = %d (4, 8 or 16)", inflight);
     RSC_TRY(check_same_device(c->device, "cache"));
@@ -920,7 +924,7 @@ rsc_status_t rsc_cache_gather_probe(rsc_cache_t *c, const float *B, int32_t d, i
     const int64_t nnz_hint = c->n > 0 ? c->X.nnz * kk / c->n : 0;
     const int32_t slice = rsc::spmm_slice_width(c->X.n_rows, nnz_hint, kk, d);
     if (slice_out) *slice_out = slice;
-    RSC_HIP(rsc::gather_probe_launch(s.col, s.nnz, B, ldb, d, slice, false, inflight, sink, stream),
+    RSC_HIP(rsc::gather_probe_launch(s.col, s.nnz, B, ldb, d, slice, false, inflight, sink, Y, ldy, s.n_rows, stream),
             "gather probe launch");
     RSC_HIP(c->fence.record(stream), "gather probe event");
     return RSC_OK;

@@ -11,8 +11,17 @@
 // with the SpMM's lane layout (LPE lanes per entry, one float4 per lane, two
 // for 512-wide rows), `kInflight` loads issued before any is consumed. The
 // loaded values are added into a register sum; one float per wave goes to
-// `sink`, so no load can be dropped. No values, no row pointers, no output
-// rows: only the col stream (4 bytes per entry) besides the gathers.
+// `sink`, so no load can be dropped. No values and no row pointers: only the
+// col stream (4 bytes per entry) besides the gathers.
+//
+// With Y, the probe also writes an output of the product's size (n_rows rows
+// of the pass's slice, the same non-temporal float4 stores as the SpMM's row
+// store), shared evenly over the waves: wave w writes rows
+// [w n_rows / W, (w + 1) n_rows / W) of W waves after its gathers, each
+// element its wave's sum. That is the gather pattern plus the output stream,
+// the product's whole compulsory traffic bar values and row pointers; where
+// the output is a large share of it (sampled products of sparse slices)
+// it bounds the product more tightly than the gathers alone.
 #include "rsc_internal.h"
 
 namespace rsc {
@@ -27,7 +36,9 @@ __device__ __forceinline__ vf4 load_nt(const vf4 *p) { return __builtin_nontempo
 template <int LPE, int NV, int kInflight, bool kHint>
 __global__ __launch_bounds__(kProbeWaves * 64) void gather_probe_kernel(const int32_t *__restrict__ col, int64_t nnz,
                                                                        const float *__restrict__ B, int64_t ldb,
-                                                                       int32_t d, float *__restrict__ sink) {
+                                                                       int32_t d, float *__restrict__ sink,
+                                                                       float *__restrict__ Y, int64_t ldy,
+                                                                       int32_t n_rows) {
     constexpr int G = kWave / LPE;  // entries per load instruction
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t w = (int64_t)blockIdx.x * kProbeWaves + (threadIdx.x >> 6);
@@ -67,31 +78,55 @@ __global__ __launch_bounds__(kProbeWaves * 64) void gather_probe_kernel(const in
 #pragma unroll
     for (int m = 1; m < kWave; m <<= 1) s += __shfl_xor(s, m);
     if (lane == 0) sink[w] = s;
+    if (Y == nullptr) return;  // kernel-uniform
+    const int64_t n_waves = (nnz + kWave - 1) / kWave;
+    const int64_t r1 = (w + 1) * n_rows / n_waves;  // <= n_rows since w < n_waves
+    const vf4 o = {s, s, s, s};
+    for (int64_t r = w * n_rows / n_waves + g; r < r1; r += G) {
+        float *yrow = Y + r * ldy;
+#pragma unroll
+        for (int q = 0; q < NV; ++q) {
+            const int32_t f = 4 * sl + 4 * kWave * q;
+            if (f + 4 <= d) {
+                __builtin_nontemporal_store(o, reinterpret_cast<vf4 *>(yrow + f));
+            } else if (f < d) {
+                for (int32_t x = f; x < d; ++x) yrow[x] = s;
+            }
+        }
+    }
 }
+
+struct ProbeOut {
+    float *Y;  // nullptr: no output stream
+    int64_t ldy;
+    int32_t n_rows;
+};
 
 template <int LPE, int NV, int U>
 void launch_one(const int32_t *col, int64_t nnz, const float *B, int64_t ldb, int32_t dl, bool hint, float *sink,
-                hipStream_t stream) {
+                ProbeOut out, hipStream_t stream) {
     const unsigned grid = (unsigned)ceil_div(ceil_div(nnz, kWave), kProbeWaves);
     if (hint)
-        gather_probe_kernel<LPE, NV, U, true><<<grid, kProbeWaves * 64, 0, stream>>>(col, nnz, B, ldb, dl, sink);
+        gather_probe_kernel<LPE, NV, U, true>
+            <<<grid, kProbeWaves * 64, 0, stream>>>(col, nnz, B, ldb, dl, sink, out.Y, out.ldy, out.n_rows);
     else
-        gather_probe_kernel<LPE, NV, U, false><<<grid, kProbeWaves * 64, 0, stream>>>(col, nnz, B, ldb, dl, sink);
+        gather_probe_kernel<LPE, NV, U, false>
+            <<<grid, kProbeWaves * 64, 0, stream>>>(col, nnz, B, ldb, dl, sink, out.Y, out.ldy, out.n_rows);
 }
 
 template <int U>
 void launch_width(const int32_t *col, int64_t nnz, const float *B, int64_t ldb, int32_t dl, int32_t slice, bool hint,
-                  float *sink, hipStream_t stream) {
+                  float *sink, ProbeOut out, hipStream_t stream) {
     switch (slice) {
-        case 16: launch_one<4, 1, U>(col, nnz, B, ldb, dl, hint, sink, stream); break;
-        case 32: launch_one<8, 1, U>(col, nnz, B, ldb, dl, hint, sink, stream); break;
-        case 64: launch_one<16, 1, U>(col, nnz, B, ldb, dl, hint, sink, stream); break;
-        case 128: launch_one<32, 1, U>(col, nnz, B, ldb, dl, hint, sink, stream); break;
+        case 16: launch_one<4, 1, U>(col, nnz, B, ldb, dl, hint, sink, out, stream); break;
+        case 32: launch_one<8, 1, U>(col, nnz, B, ldb, dl, hint, sink, out, stream); break;
+        case 64: launch_one<16, 1, U>(col, nnz, B, ldb, dl, hint, sink, out, stream); break;
+        case 128: launch_one<32, 1, U>(col, nnz, B, ldb, dl, hint, sink, out, stream); break;
         default:
             if (dl <= 4 * kWave)
-                launch_one<64, 1, U>(col, nnz, B, ldb, dl, hint, sink, stream);
+                launch_one<64, 1, U>(col, nnz, B, ldb, dl, hint, sink, out, stream);
             else
-                launch_one<64, 2, U>(col, nnz, B, ldb, dl, hint, sink, stream);
+                launch_one<64, 2, U>(col, nnz, B, ldb, dl, hint, sink, out, stream);
     }
 }
 
@@ -100,14 +135,16 @@ void launch_width(const int32_t *col, int64_t nnz, const float *B, int64_t ldb, 
 int64_t gather_probe_sink_count(int64_t nnz) { return ceil_div(nnz, kWave); }
 
 hipError_t gather_probe_launch(const int32_t *col, int64_t nnz, const float *B, int64_t ldb, int32_t d, int32_t slice,
-                               bool hint, int32_t inflight, float *sink, hipStream_t stream) {
+                               bool hint, int32_t inflight, float *sink, float *Y, int64_t ldy, int32_t n_rows,
+                               hipStream_t stream) {
     if (nnz <= 0) return hipSuccess;
     for (int32_t f0 = 0; f0 < d; f0 += slice) {
         const int32_t dl = std::min<int32_t>(d - f0, slice);
+        const ProbeOut out{Y ? Y + f0 : nullptr, ldy, n_rows};
         switch (inflight) {
-            case 4: launch_width<4>(col, nnz, B + f0, ldb, dl, slice, hint, sink, stream); break;
-            case 16: launch_width<16>(col, nnz, B + f0, ldb, dl, slice, hint, sink, stream); break;
-            default: launch_width<8>(col, nnz, B + f0, ldb, dl, slice, hint, sink, stream);
+            case 4: launch_width<4>(col, nnz, B + f0, ldb, dl, slice, hint, sink, out, stream); break;
+            case 16: launch_width<16>(col, nnz, B + f0, ldb, dl, slice, hint, sink, out, stream); break;
+            default: launch_width<8>(col, nnz, B + f0, ldb, dl, slice, hint, sink, out, stream);
         }
     }
     return hipGetLastError();

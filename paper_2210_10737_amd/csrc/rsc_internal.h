@@ -61,8 +61,10 @@ const int32_t *spmm_long_count_of(const void *ws);
 
 // ---- gather-ceiling probe (measurement helper) ---------------------------
 int64_t gather_probe_sink_count(int64_t nnz);
+// Y (nullable, n_rows x d, ldy): also write an output of the product's size
 hipError_t gather_probe_launch(const int32_t *col, int64_t nnz, const float *B, int64_t ldb, int32_t d, int32_t slice,
-                               bool hint, int32_t inflight, float *sink, hipStream_t stream);
+                               bool hint, int32_t inflight, float *sink, float *Y, int64_t ldy, int32_t n_rows,
+                               hipStream_t stream);
 
 // ---- scores ------------------------------------------------------------
 hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,

@@ -294,3 +294,74 @@ def test_cache_gather_probe_gathers_the_slice_rows(d):
         mag = np.concatenate([np.abs(part).sum(axis=1)[co], pad]).reshape(chunks, 64).sum(axis=1)
         assert np.all(np.abs(got - want) <= 1e-4 * mag + 1e-30), (d, inflight, slice_w)
     cache.close()
+
+
+def _probe_out_expected(B, col, n_rows, d, slice_w):
+    # row r of the probe's output, pass [f0, f0 + slice_w): the sum over the
+    # 64-entry chunk w(r) of the gathered rows' slice, w(r) the chunk whose
+    # share [w n_rows / W, (w + 1) n_rows / W) holds r
+    nnz = len(col)
+    W = (nnz + 63) // 64
+    starts = (np.arange(W, dtype=np.int64) * n_rows) // W
+    owner = np.searchsorted(starts, np.arange(n_rows), side="right") - 1
+    want = np.empty((n_rows, d))
+    mag = np.empty((n_rows, d))
+    pad = np.zeros(W * 64 - nnz)
+    for f0 in range(0, d, slice_w):
+        part = B[:, f0:f0 + slice_w].astype(np.float64)
+        s = np.concatenate([part.sum(axis=1)[col], pad]).reshape(W, 64).sum(axis=1)
+        m = np.concatenate([np.abs(part).sum(axis=1)[col], pad]).reshape(W, 64).sum(axis=1)
+        want[:, f0:f0 + slice_w] = s[owner][:, None]
+        mag[:, f0:f0 + slice_w] = m[owner][:, None]
+    return want, mag
+
+
+@pytest.mark.parametrize("d", [66, 100, 256, 512])
+@pytest.mark.parametrize("n_rows", [3000, 40])
+def test_gather_probe_output_stream(d, n_rows):
+    # With an output, the probe writes every element of the n_rows x d rows
+    # (each its chunk's pass sum, so the stores follow the gathers), into a
+    # padded view, leaving the padding alone; fewer rows than 64-entry chunks
+    # (40 rows) leaves some chunks without rows.
+    A = synth.random_csr(n_rows, 2500, 60000 // n_rows, seed=28, hub_rows=2, hub_len=2000)
+    B = synth.dense_normal(2500, d, seed=29)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, 2500)
+    plan = rsc.SpmmPlan(X)
+    ld = (d + 3) // 4 * 4 + 8
+    Bd = torch.zeros((2500, ld), device="cuda")
+    Bd[:, :d] = torch.from_numpy(B).cuda()
+    Bd = Bd[:, :d]
+    for inflight in (4, 16):
+        wide = torch.full((n_rows, ld), 7777.0, device="cuda")
+        out = wide[:, :d]
+        slice_w = plan.gather_probe(Bd, inflight=inflight, out=out)
+        got = wide.cpu().numpy()
+        assert np.all(got[:, d:] == 7777.0)
+        want, mag = _probe_out_expected(B, A.col, n_rows, d, slice_w)
+        g = got[:, :d].astype(np.float64)
+        assert np.all(np.abs(g - want) <= 1e-4 * mag + 1e-30), (d, n_rows, inflight, slice_w)
+    with pytest.raises(ValueError, match="holds less"):   # refused before any launch
+        plan.gather_probe(Bd, out=torch.empty((n_rows - 1, d), device="cuda"))
+    with pytest.raises(rsc.RscError):                        # ld not a multiple of 4
+        plan.gather_probe(Bd, out=torch.empty((n_rows, d + 1), device="cuda")[:, :d])
+    plan.close()
+
+
+@pytest.mark.parametrize("d", [64, 256])
+def test_cache_gather_probe_output_stream(d):
+    A = synth.random_csr(3000, 2500, 400, seed=38, hub_rows=5, hub_len=2400)
+    AT = synth.transpose(A, 2500)
+    B = synth.dense_normal(2500, d, seed=39)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, 2500)
+    cache = rsc.Cache(X, rsc.DeviceCsr.from_host(AT.rowptr, AT.col, AT.val, 3000))
+    Bd = torch.from_numpy(B).cuda()
+    cache.refresh(Bd, 700, step=0)
+    cn2, _ = oracle.col_sqnorms(AT.rowptr, AT.val)
+    _, mask = oracle.topk(oracle.pair_keys(cn2, B)["key"], 700)
+    _, co, _ = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+    out = torch.full((3000, d), float("nan"), device="cuda")
+    slice_w = cache.gather_probe(Bd, inflight=8, out=out)
+    want, mag = _probe_out_expected(B, co, 3000, d, slice_w)
+    g = out.cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(g - want) <= 1e-4 * mag + 1e-30), (d, slice_w)
+    cache.close()
