@@ -158,10 +158,11 @@ def _oracle_ops(A, Hh, Gh, k, rows):
 
 def cpu_baseline(A, Hh, Gh, k, pct, refresh_interval, step_bytes_full, n_rows_sample,
                  min_s: float = 10.0, max_reps: int = 5):
-    """Oracle timing on the GPU machine's host cores: every operation of the hot
-    path timed separately (exact SpMM, cn2, keys, select, slice, sampled
-    SpMM), repeated until about min_s seconds of CPU work (at most max_reps),
-    median per operation, with all the oracle's threads; the SpMMs on the
+    """Oracle timing on the host cores of the machine the bench runs on:
+    every operation of the hot path timed separately (exact SpMM, cn2, keys,
+    select, slice, sampled SpMM), repeated until about min_s seconds of CPU
+    work (at most max_reps), median per operation, with all the oracle's
+    threads; the SpMMs on the
     first n_rows_sample rows (scaled linearly to the whole graph when that is
     fewer than all). The step time is exact + sampled SpMM plus one refresh
     (keys, select, slice) per refresh_interval steps; cn2 is computed once per
