@@ -222,13 +222,17 @@ def _dense(t: torch.Tensor, rows: int, d: int, name: str) -> tuple[int, int]:
     return _dp(t), ld
 
 
+def _vec_check(t: torch.Tensor, count: int, dtype, name: str) -> None:
+    if t.dtype != dtype or not t.is_contiguous() or t.numel() < count:
+        raise ValueError(f"{name}: {t.dtype}[{t.numel()}], contiguous {dtype}[>= {count}] expected")
+
+
 def _vec(t: torch.Tensor | None, count: int, dtype, name: str) -> int | None:
-    """Device address of an optional 1-D-contiguous array of at least count
+    """Device address of an optional contiguous array of at least count
     elements of dtype."""
     if t is None:
         return None
-    if t.dtype != dtype or not t.is_contiguous() or t.numel() < count:
-        raise ValueError(f"{name}: {t.dtype}[{t.numel()}], contiguous {dtype}[>= {count}] expected")
+    _vec_check(t, count, dtype, name)
     return _dp(t)
 
 
@@ -265,6 +269,10 @@ class DeviceCsr:
         return cls(len(rowptr) - 1, int(n_cols), rp, c, v)
 
     def struct(self) -> CsrStruct:
+        _vec_check(self.rowptr, self.n_rows + 1, torch.int32, "rowptr")
+        if self.nnz:
+            _vec_check(self.col, self.nnz, torch.int32, "col")
+            _vec_check(self.val, self.nnz, torch.float32, "val")
         return CsrStruct(self.n_rows, self.n_cols, self.nnz,
                          _vec(self.rowptr, self.n_rows + 1, torch.int32, "rowptr"),
                          _vec(self.col, self.nnz, torch.int32, "col") if self.nnz else None,

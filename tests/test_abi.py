@@ -313,3 +313,35 @@ def test_plan_argument_checks():
     assert out.value is None
     assert L.rsc_spmm_plan_run(None, None, 4, 4, None, 4, None) == 1
     assert L.rsc_spmm_plan_destroy(None) == 0
+
+
+def test_binding_refuses_operands_smaller_than_the_call():
+    # The library reads and writes rows x d elements through each pointer, so
+    # the binding refuses a dense operand with fewer rows or columns, another
+    # dtype or a non-unit column stride, and index arrays shorter than the
+    # call needs, before any launch (host tensors: the checks come first).
+    import torch
+    B = torch.zeros((10, 8), dtype=torch.float32)
+    with pytest.raises(ValueError, match="holds less"):
+        rsc._dense(B, 11, 8, "B")
+    with pytest.raises(ValueError, match="holds less"):
+        rsc._dense(B, 10, 9, "B")
+    with pytest.raises(ValueError, match="float32 expected"):
+        rsc._dense(B.double(), 10, 8, "B")
+    with pytest.raises(ValueError, match="unit column stride"):
+        rsc._dense(B.t(), 8, 10, "B")
+    with pytest.raises(ValueError, match="contiguous"):
+        rsc._vec(torch.zeros(3, dtype=torch.int32), 4, torch.int32, "mask")
+    with pytest.raises(ValueError, match="contiguous"):
+        rsc._vec(torch.zeros(4, dtype=torch.int64), 4, torch.int32, "mask")
+    with pytest.raises(ValueError, match="contiguous"):
+        rsc._vec(torch.zeros(8, dtype=torch.int32)[::2], 4, torch.int32, "mask")
+    assert rsc._vec(None, 4, torch.int32, "mask") is None
+    A = rsc.DeviceCsr(4, 4, torch.zeros(4, dtype=torch.int32), torch.zeros(0, dtype=torch.int32),
+                      torch.zeros(0, dtype=torch.float32))
+    with pytest.raises(ValueError, match="rowptr"):
+        A.struct()                                   # 4 row pointers for 4 rows
+    A = rsc.DeviceCsr(2, 4, torch.zeros(3, dtype=torch.int32), torch.zeros(5, dtype=torch.int32),
+                      torch.zeros(4, dtype=torch.float32), nnz=5)
+    with pytest.raises(ValueError, match="val"):
+        A.struct()                                   # 4 values for 5 entries
