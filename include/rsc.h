@@ -388,6 +388,26 @@ rsc_status_t rsc_cache_buffers(rsc_cache_t *cache, const double **cn2, const int
  * `stream`, on which the scores were enqueued. Either pointer may be NULL. */
 rsc_status_t rsc_cache_norms(rsc_cache_t *cache, double *fro_x2_host, double *fro_b2_host,
                              hipStream_t stream);
+/* Staleness of a cached selection (section 3.3.1 and Fig. 4: how well the
+ * columns chosen at one refresh still match the top pairs of a later
+ * gradient). The cache keeps the selection that its latest select, refresh
+ * or randomized refresh replaced ("previous", S_prev; its k_prev pairs) and
+ * the current one (S_new). `order` (device, int32[n], n = columns of X)
+ * ranks the n pairs best first, e.g. the ranking rsc_greedy_profile writes
+ * for the newly scored keys. Writes, each pointer nullable:
+ *   *auc_host     = the share of (selected, unselected) pairs of S_prev that
+ *                   `order` ranks selected-first: the count of such ordered
+ *                   pairs over k_prev (n - k_prev), in fp64; NaN when S_prev
+ *                   is empty or holds all n pairs (an exact integer count
+ *                   and one division, so equal bit for bit to any exact
+ *                   evaluation of that definition);
+ *   *overlap_host = |S_prev & S_new|;  *prev_k_host = k_prev.
+ * RSC_ERR_INVALID_ARGUMENT before the second selection or when `order` is
+ * not a ranking of 0..n-1 (an entry outside [0, n), or a selected pair
+ * ranked other than once). [sync]: waits for `stream`, on which the
+ * selections and the ranking were enqueued. */
+rsc_status_t rsc_cache_staleness(rsc_cache_t *cache, const int32_t *order, double *auc_host,
+                                 int64_t *overlap_host, int64_t *prev_k_host, hipStream_t stream);
 /* Waits (on the host) for the work this cache's own calls enqueued, on
  * every stream they used, then frees its buffers (stream-ordered, on a
  * library-owned stream of the cache's device; through the allocator for a

@@ -50,7 +50,7 @@ EXPORTED = [
     "rsc_cache_create", "rsc_cache_create_ex", "rsc_cache_refresh", "rsc_cache_score", "rsc_cache_select",
     "rsc_cache_refresh_random",
     "rsc_cache_get", "rsc_spmm_sampled",
-    "rsc_cache_buffers", "rsc_cache_norms", "rsc_cache_gather_probe", "rsc_cache_destroy",
+    "rsc_cache_buffers", "rsc_cache_norms", "rsc_cache_staleness", "rsc_cache_gather_probe", "rsc_cache_destroy",
     "rsc_k_from_fraction", "rsc_greedy_allocate",
     "rsc_greedy_profile_workspace_bytes", "rsc_greedy_blocks", "rsc_greedy_profile",
     "rsc_greedy_allocate_profiles",
@@ -145,6 +145,8 @@ def lib():
                                       ctypes.c_int),
             "rsc_cache_norms": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), vp],
                                 ctypes.c_int),
+            "rsc_cache_staleness": ([vp, vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64),
+                                     ctypes.POINTER(i64), vp], ctypes.c_int),
             "rsc_k_from_fraction": ([i32, i32, i32], i32),
             "rsc_greedy_allocate": ([i32, i32, i64, vp, vp, vp, ctypes.c_double, vp, i32, i32, i32,
                                      i32, vp, vp], ctypes.c_int),
@@ -529,6 +531,14 @@ class Cache:
         fx, fb = ctypes.c_double(), ctypes.c_double()
         _check(lib().rsc_cache_norms(self._h, ctypes.byref(fx), ctypes.byref(fb) if scored else None, _stream()))
         return fx.value, (fb.value if scored else None)
+
+    def staleness(self, order: torch.Tensor):
+        """(AUC of the previous selection under the ranking `order` (int32[n],
+        best first), |S_prev & S_new|, |S_prev|) from rsc_cache_staleness."""
+        auc, both, kp = ctypes.c_double(), ctypes.c_int64(), ctypes.c_int64()
+        _check(lib().rsc_cache_staleness(self._h, _vec(order, self.X.n_cols, torch.int32, "order"),
+                                         ctypes.byref(auc), ctypes.byref(both), ctypes.byref(kp), _stream()))
+        return auc.value, both.value, kp.value
 
     def buffers(self):
         """Device pointers [cn2, colnnz, key, rn2, mask]."""

@@ -263,6 +263,9 @@ struct rsc_cache {
     bool scored = false;       // keys have been computed at least once
     int32_t *idx = nullptr;
     uint32_t *mask = nullptr;
+    uint32_t *prev_mask = nullptr;          // the selection the latest one replaced
+    bool has_prev = false;                  // at least two selections were made
+    unsigned long long *stale_acc = nullptr;  // staleness counts
     int32_t *s_rowptr = nullptr;
     int32_t *s_col = nullptr;
     float *s_val = nullptr;
@@ -645,7 +648,7 @@ rsc_status_t rsc_slice_csr(const rsc_csr_t *A, const uint32_t *mask, const doubl
 static void cache_free(rsc_cache_t *c, hipStream_t s) {
     if (!c) return;
     void *dev[] = {c->cn2, c->colnnz, c->key, c->rn2, c->norms, c->sum_ws, c->count, c->colw, c->idx, c->mask,
-                   c->s_rowptr, c->s_col, c->s_val, c->d_nnz, c->ws_topk, c->ws_slice, c->ws_spmm, c->ws_sample,
+                   c->prev_mask, c->stale_acc, c->s_rowptr, c->s_col, c->s_val, c->d_nnz, c->ws_topk, c->ws_slice, c->ws_spmm, c->ws_sample,
                    c->s_split};
     for (void *p : dev) {
         if (!p) continue;
@@ -706,6 +709,8 @@ rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_
         {(void **)&c->colw, sizeof(double) * n},
         {(void **)&c->idx, sizeof(int32_t) * n},
         {(void **)&c->mask, sizeof(uint32_t) * (size_t)rsc::ceil_div(n, 32)},
+        {(void **)&c->prev_mask, sizeof(uint32_t) * (size_t)rsc::ceil_div(n, 32)},
+        {(void **)&c->stale_acc, sizeof(unsigned long long) * (size_t)rsc::staleness_acc_count()},
         {(void **)&c->s_rowptr, sizeof(int32_t) * ((size_t)X->n_rows + 1)},
         {(void **)&c->s_col, sizeof(int32_t) * m},
         {(void **)&c->s_val, sizeof(float) * m},
@@ -760,6 +765,17 @@ rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_
     return RSC_OK;
 }
 
+// Before a new selection overwrites the mask: keep the current one (if any)
+// as the previous selection, for rsc_cache_staleness.
+static rsc_status_t keep_previous_selection(rsc_cache_t *c, hipStream_t stream) {
+    if (c->version == 0) return RSC_OK;
+    RSC_HIP(hipMemcpyAsync(c->prev_mask, c->mask, sizeof(uint32_t) * (size_t)rsc::ceil_div(c->n, 32),
+                           hipMemcpyDeviceToDevice, stream),
+            "cache previous selection");
+    c->has_prev = true;
+    return RSC_OK;
+}
+
 // After a new slice: what every sampled product would build first (split
 // bounds and long-piece list when blocked, else the long-row list or the
 // row order), built once into ws_spmm. Asynchronous (the list's length stays
@@ -803,6 +819,7 @@ rsc_status_t rsc_cache_select(rsc_cache_t *c, int32_t k, int64_t step, hipStream
     if (k < 0 || k > c->n) return fail(RSC_ERR_INVALID_ARGUMENT, "k = %d outside [0, %d]", k, c->n);
     if (!c->scored) return fail(RSC_ERR_INVALID_ARGUMENT, "cache select before any score");
     RSC_TRY(check_same_device(c->device, "cache"));
+    RSC_TRY(keep_previous_selection(c, stream));
     RSC_HIP(rsc::topk_launch(c->key, c->n, k, c->idx, c->mask, c->ws_topk, stream), "cache topk");
     RSC_HIP(rsc::slice_launch(c->X.n_rows, c->X.n_cols, c->X.nnz, c->X.rowptr, c->X.col, c->X.val, c->mask, c->s_rowptr,
                               c->s_col, c->s_val, c->X.nnz, c->d_nnz, c->ws_slice, stream),
@@ -826,6 +843,7 @@ rsc_status_t rsc_cache_refresh_random(rsc_cache_t *c, const float *B, int32_t d,
     if (k_draws < 0) return fail(RSC_ERR_INVALID_ARGUMENT, "k_draws < 0");
     RSC_TRY(check_same_device(c->device, "cache"));
     RSC_TRY(rsc_cache_score(c, B, d, ldb, stream));
+    RSC_TRY(keep_previous_selection(c, stream));
     RSC_HIP(rsc::sample_launch(c->key, c->n, k_draws, seed, c->count, c->colw, c->mask, c->ws_sample, stream),
             "cache sample");
     RSC_HIP(rsc::slice_launch(c->X.n_rows, c->X.n_cols, c->X.nnz, c->X.rowptr, c->X.col, c->X.val, c->mask, c->s_rowptr,
@@ -950,6 +968,33 @@ rsc_status_t rsc_cache_norms(rsc_cache_t *c, double *fro_x2_host, double *fro_b2
     RSC_HIP(hipStreamSynchronize(stream), "cache norms wait");
     if (fro_x2_host) *fro_x2_host = h[0];
     if (fro_b2_host) *fro_b2_host = h[1];
+    return RSC_OK;
+}
+
+rsc_status_t rsc_cache_staleness(rsc_cache_t *c, const int32_t *order, double *auc_host, int64_t *overlap_host,
+                                 int64_t *prev_k_host, hipStream_t stream) {
+    if (!c) return fail(RSC_ERR_INVALID_ARGUMENT, "cache is NULL");
+    if (!c->has_prev) return fail(RSC_ERR_INVALID_ARGUMENT, "cache staleness needs two selections");
+    if (c->n > 0 && !order) return fail(RSC_ERR_INVALID_ARGUMENT, "order is NULL");
+    if (!aligned(order, 4)) return fail(RSC_ERR_UNSUPPORTED, "order is not 4-byte aligned");
+    RSC_TRY(check_same_device(c->device, "cache"));
+    const int32_t n = c->n;
+    unsigned long long h[8] = {0};
+    RSC_HIP(rsc::staleness_launch(order, n, c->prev_mask, c->mask, c->stale_acc, stream), "staleness launch");
+    RSC_HIP(hipMemcpyAsync(h, c->stale_acc, sizeof(unsigned long long) * (size_t)rsc::staleness_acc_count(),
+                           hipMemcpyDeviceToHost, stream),
+            "staleness read");
+    RSC_HIP(hipStreamSynchronize(stream), "staleness wait");
+    const unsigned long long ranks_sum = h[0], k = h[1], bad = h[2], k_mask = h[3], both = h[4];
+    if (bad != 0 || k != k_mask)
+        return fail(RSC_ERR_INVALID_ARGUMENT, "order is not a ranking of the %d pairs", n);
+    // ordered (selected, unselected) pairs over all such pairs
+    const double auc = (k == 0 || k == (unsigned long long)n)
+                           ? NAN
+                           : (double)(ranks_sum - k * (k - 1) / 2) / ((double)k * (double)(n - (int64_t)k));
+    if (auc_host) *auc_host = auc;
+    if (overlap_host) *overlap_host = (int64_t)both;
+    if (prev_k_host) *prev_k_host = (int64_t)k;
     return RSC_OK;
 }
 

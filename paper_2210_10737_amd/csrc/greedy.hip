@@ -184,7 +184,82 @@ __global__ __launch_bounds__(64) void greedy_profile_kernel(const double *__rest
     }
 }
 
+// ---- staleness of a selection (section 3.3.1, Fig. 4) ---------------------
+// For a previous selection S (mask prev) and a new ranking `order` (pairs
+// best first): the matching score of S under the new ranking is the share of
+// (selected, unselected) pairs that the ranking puts in that order. With the
+// selected pairs at ranks r_1 < ... < r_k, the unselected pairs after rank
+// r_j number (n - 1 - r_j) - (k - j), so the count of ordered pairs is
+// sum_j (n - 1 - r_j) - k (k - 1) / 2: one pass over the ranks adds
+// n - 1 - r for every selected pair. Integer sums with integer atomics, so
+// the result does not depend on the order of the blocks.
+//   acc[0] = sum of (n - 1 - r) over ranks r whose pair is in prev
+//   acc[1] = number of those ranks
+//   acc[2] = ranks whose entry lies outside [0, n) (not a ranking)
+//   acc[3] = |prev| from the mask words, acc[4] = |prev & cur|
+constexpr int kStaleAcc = 5;
+
+__global__ __launch_bounds__(64) void stale_zero_kernel(unsigned long long *__restrict__ acc) {
+    if (threadIdx.x < kStaleAcc) acc[threadIdx.x] = 0;
+}
+
+__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
+#pragma unroll
+    for (int m = 1; m < kWave; m <<= 1) v += __shfl_xor(v, m);
+    return v;
+}
+
+__global__ __launch_bounds__(256) void stale_count_kernel(const int32_t *__restrict__ order, int32_t n,
+                                                          const uint32_t *__restrict__ prev,
+                                                          const uint32_t *__restrict__ cur,
+                                                          unsigned long long *__restrict__ acc) {
+    unsigned long long v[kStaleAcc] = {0, 0, 0, 0, 0};
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += stride) {
+        const int32_t i = order[r];
+        if ((uint32_t)i >= (uint32_t)n) {
+            v[2] += 1;
+        } else if ((prev[i >> 5] >> (i & 31)) & 1u) {
+            v[0] += (unsigned long long)(n - 1 - r);
+            v[1] += 1;
+        }
+    }
+    const int64_t words = ((int64_t)n + 31) / 32;
+    for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < words; w += stride) {
+        uint32_t p = prev[w];
+        if (w == words - 1 && (n & 31)) p &= (1u << (n & 31)) - 1u;  // bits past n are not pairs
+        v[3] += __popc(p);
+        v[4] += __popc(p & cur[w]);
+    }
+    __shared__ unsigned long long part[256 / kWave][kStaleAcc];
+    const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+#pragma unroll
+    for (int j = 0; j < kStaleAcc; ++j) {
+        const unsigned long long t = wave_sum_u64(v[j]);
+        if (lane == 0) part[wv][j] = t;
+    }
+    __syncthreads();
+    if (threadIdx.x < kStaleAcc) {
+        unsigned long long t = 0;
+        for (int q = 0; q < 256 / kWave; ++q) t += part[q][threadIdx.x];
+        if (t) atomicAdd(&acc[threadIdx.x], t);
+    }
+}
+
 }  // namespace
+
+int32_t staleness_acc_count() { return kStaleAcc; }
+
+hipError_t staleness_launch(const int32_t *order, int32_t n, const uint32_t *prev, const uint32_t *cur,
+                            unsigned long long *acc, hipStream_t stream) {
+    stale_zero_kernel<<<1, 64, 0, stream>>>(acc);
+    if (n > 0) {
+        const int64_t work = std::max<int64_t>(n, ceil_div(n, 32));
+        const unsigned g = (unsigned)std::min<int64_t>(ceil_div(work, 256), 1024);
+        stale_count_kernel<<<g, 256, 0, stream>>>(order, n, prev, cur, acc);
+    }
+    return hipGetLastError();
+}
 
 int32_t greedy_step(int32_t n, int32_t alpha_num, int32_t alpha_den) {
     // callers pass 0 <= alpha_num <= alpha_den, so 0 <= s <= n fits int32

@@ -118,6 +118,11 @@ hipError_t degree_scale_launch(int32_t n_rows, const int32_t *rowptr, const int3
 int32_t greedy_step(int32_t n, int32_t alpha_num, int32_t alpha_den);
 int32_t greedy_blocks(int32_t n, int32_t step);
 size_t greedy_profile_ws_bytes(int32_t n);
+// staleness counts of a previous selection under a ranking (acc: device,
+// staleness_acc_count() entries, cleared by the launch)
+int32_t staleness_acc_count();
+hipError_t staleness_launch(const int32_t *order, int32_t n, const uint32_t *prev, const uint32_t *cur,
+                            unsigned long long *acc, hipStream_t stream);
 hipError_t greedy_profile_launch(const uint64_t *key, const int32_t *colnnz, int32_t n, int32_t step,
                                  double *mass, int64_t *count, int32_t *order_out, void *ws,
                                  hipStream_t stream);

@@ -19,6 +19,11 @@ three modes, chosen per step by `RscController`:
 * "exact": plain exact backward (no approximation, or the final phase of
   training after switching back, section 3.3.2).
 
+With track_staleness, every refresh after the first also records, per
+layer, the AUC of the selection it replaced under the new ranking and the
+overlap of the two selections (section 3.3.1, Fig. 4), computed on the
+device by rsc_cache_staleness from rsc_greedy_profile's ranking.
+
 The dense update phase (MatMul, ReLU, loss, optimizer) uses torch; it is not
 part of the aggregation path.
 """
@@ -28,10 +33,9 @@ import math
 import time
 from dataclasses import dataclass, field
 
-import numpy as np
 import torch
 
-from . import Cache, DeviceCsr, SpmmPlan, _check, _stream, copy_to_host, greedy_allocate_profiles, lib
+from . import Cache, DeviceCsr, SpmmPlan, _check, _stream, greedy_allocate_profiles, lib
 
 
 class _Aggregate(torch.autograd.Function):
@@ -121,20 +125,6 @@ class StepRecord:
     overlap: list = field(default_factory=list)  # |S_prev & S_new| / |S_prev|
 
 
-def selection_auc(order: np.ndarray, selected: np.ndarray) -> float:
-    """AUC of a previous top-k selection under a new ranking (the matching
-    score of section 3.3.1 / Fig. 4): the probability that a previously
-    selected pair is ranked above a previously unselected one. `order` lists
-    the pairs from best to worst. NaN if the selection is empty or full."""
-    n, k = len(order), len(selected)
-    if k == 0 or k == n:
-        return float("nan")
-    pos = np.empty(n, dtype=np.int64)
-    pos[order] = np.arange(n)
-    above = float(np.sum(n - 1 - pos[selected])) - k * (k - 1) / 2.0
-    return above / (float(k) * (n - k))
-
-
 class RscController:
     """Decides each step's backward mode and, at refresh steps, allocates
     k_l with the greedy and refreshes every layer's slice."""
@@ -155,8 +145,9 @@ class RscController:
         self.nb = nb
         self.ws = torch.empty(max(lib().rsc_greedy_profile_workspace_bytes(self.n), 1), dtype=torch.uint8,
                               device=dev)
-        self.order = torch.empty(max(self.n, 1), dtype=torch.int32, device=dev) if cfg.track_staleness else None
-        self.prev_idx = [None] * len(layers)
+        # each layer's pair ranking at the latest refresh (for the staleness record)
+        self.order = torch.empty((len(layers), max(self.n, 1)), dtype=torch.int32, device=dev) \
+            if cfg.track_staleness else None
         self.last_refresh = None
         self.k = [self.n] * len(layers)
         self.history: list[StepRecord] = []
@@ -193,11 +184,9 @@ class RscController:
             _check(lib().rsc_greedy_profile(ptrs[2], self.colnnz_ptr, self.n, self.cfg.alpha[0],
                                             self.cfg.alpha[1], self.mass[l].data_ptr(),
                                             self.count[l].data_ptr(),
-                                            None if self.order is None else self.order.data_ptr(),
+                                            None if self.order is None else self.order[l].data_ptr(),
                                             self.ws.data_ptr(), self.ws.numel(), _stream()))
             fro_b2.append(layer.cache.norms()[1])   # ||grad H||_F^2 of the scored gradient (device sum)
-            if self.order is not None and self.prev_idx[l] is not None:
-                rec.auc.append(selection_auc(self.order.cpu().numpy(), self.prev_idx[l]))
         masses = self.mass[:, :self.nb].cpu().numpy()
         counts = self.count[:, :self.nb].cpu().numpy()
         widths = [layer.width for layer in self.layers]
@@ -208,14 +197,14 @@ class RscController:
             layer.cache.select(k, step)
             layer.k = k
         rec.greedy_s = time.perf_counter() - t0
-        if self.order is not None:
+        if self.order is not None and self.last_refresh is not None:
+            # the selection each cache just replaced, under the new ranking
+            # (section 3.3.1, Fig. 4), on the device
             for l, layer in enumerate(self.layers):
-                g = layer.cache.get(step, with_slice=False)
-                new_idx = copy_to_host(g["idx_ptr"], g["k"], np.int32) if g["k"] else np.zeros(0, np.int32)
-                if self.prev_idx[l] is not None and len(self.prev_idx[l]):
-                    rec.overlap.append(len(np.intersect1d(self.prev_idx[l], new_idx, assume_unique=True))
-                                       / len(self.prev_idx[l]))
-                self.prev_idx[l] = new_idx
+                auc, both, k_prev = layer.cache.staleness(self.order[l])
+                rec.auc.append(auc)
+                if k_prev:
+                    rec.overlap.append(both / k_prev)
         rec.k = list(self.k)
         self.last_refresh = step
 

@@ -116,6 +116,7 @@ def test_cache_argument_validation():
         "RSC_ERR_INVALID_ARGUMENT"
     assert _err(L.rsc_cache_refresh(None, 0x1000, 4, 4, 1, 0, None)) == "RSC_ERR_INVALID_ARGUMENT"
     assert _err(L.rsc_spmm_sampled(None, 0x1000, 4, 4, 0x2000, 4, None)) == "RSC_ERR_INVALID_ARGUMENT"
+    assert _err(L.rsc_cache_staleness(None, 0x1000, None, None, None, None)) == "RSC_ERR_INVALID_ARGUMENT"
     assert L.rsc_cache_destroy(None) == 0
     half = rsc.Allocator(rsc._ALLOC_FN(lambda n, s, c: None), rsc._FREE_FN(), None)  # no free
     assert _err(L.rsc_cache_create_ex(ctypes.byref(A), ctypes.byref(A), 10, ctypes.byref(half), None,
@@ -223,22 +224,6 @@ def test_greedy_profiles_match_oracle(C):
     k_o, b_o = oracle.greedy(keys, colnnz, A.nnz, ds, cn2.sum(), fb, C, alpha)
     assert k_p == k_o and b_p == b_o
     assert rsc.lib().rsc_greedy_blocks(A.n, 3, 100) == len(profs[0][0])
-
-
-def test_selection_auc_brute_force():
-    from paper_2210_10737_amd.gcn import selection_auc
-    rng = np.random.default_rng(5)
-    for n, k in ((10, 3), (50, 1), (64, 63), (200, 77)):
-        order = rng.permutation(n)
-        sel = rng.choice(n, size=k, replace=False)
-        pos = np.empty(n, int)
-        pos[order] = np.arange(n)
-        pairs = [(i, j) for i in sel for j in range(n) if j not in set(sel)]
-        want = sum(pos[i] < pos[j] for i, j in pairs) / len(pairs)
-        assert abs(selection_auc(order, sel) - want) < 1e-12
-    # identical ranking: the previous top-k is ranked first -> AUC 1
-    assert selection_auc(np.arange(20), np.arange(5)) == 1.0
-    assert selection_auc(np.arange(20)[::-1].copy(), np.arange(5)) == 0.0
 
 
 def test_greedy_budget_comparison_wide_range():

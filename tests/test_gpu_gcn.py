@@ -170,7 +170,7 @@ def test_staleness_tracking():
     previous selection is ranked first again (AUC 1, overlap 1)."""
     A, X, Y, model, _ = _setup((1, 4), refresh=2)
     model.controller.cfg.track_staleness = True
-    model.controller.order = torch.empty(A.n, dtype=torch.int32, device="cuda")
+    model.controller.order = torch.empty((2, A.n), dtype=torch.int32, device="cuda")
     Xd, Yd = torch.from_numpy(X).cuda(), torch.from_numpy(Y).cuda()
     for step in range(6):
         model.train_step(Xd, Yd, None, step)
