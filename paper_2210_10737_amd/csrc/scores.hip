@@ -9,40 +9,115 @@
 namespace rsc {
 namespace {
 
-// cn2[i] = sum of val^2 over row i of X^T, in stored order. One wave per
-// row: the wave loads 64 values at a time (coalesced) and adds their squares
-// one after another in stored order, each value broadcast with readlane, so
-// the sum is the sequential one while the loads stay wide. Products of fp32
-// values are exact in fp64, so fma(v, v, acc) equals acc + v * v.
-__global__ __launch_bounds__(256) void col_sqnorms_kernel(int32_t n, const int32_t *__restrict__ rowptr,
-                                                          const float *__restrict__ val,
-                                                          double *__restrict__ cn2,
-                                                          int32_t *__restrict__ colnnz) {
-    const int lane = threadIdx.x & 63;
-    const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (i >= n) return;
-    const int32_t s = __builtin_amdgcn_readfirstlane(rowptr[i]);
-    const int32_t e = __builtin_amdgcn_readfirstlane(rowptr[i + 1]);
+// cn2[i] = sum of val^2 over row i of X^T, in stored order: a sequential
+// fp64 chain per row. Products of fp32 values are exact in fp64, so
+// fma(v, v, acc) equals acc + v * v.
+//
+// One wave per 64 consecutive rows. Rows of at most kNormThreadMax entries
+// are walked by their own lane, 16 values per step through four aligned
+// float4 loads (the next step's loads in flight), so the chain costs no
+// memory operation or broadcast per value and the 64 lanes' chains advance
+// together. The wave then takes its longer rows one at a time: 64 values per
+// coalesced load (four more loads in flight), each value broadcast to the
+// chain with readlane. A wave-per-row form for every row kept 63 of 64 lanes
+// idle in the chain and took 3-5x longer on graphs of short rows.
+constexpr int32_t kNormThreadMax = 2048;
+
+__device__ __forceinline__ double sq_chain_thread(const float *__restrict__ val, int64_t s, int64_t e) {
     double acc = 0.0;
-    for (int64_t base = s; base < e; base += 64) {
-        const int32_t cnt = (int32_t)min<int64_t>(64, e - base);
-        const int vb = lane < cnt ? __float_as_int(__builtin_nontemporal_load(val + base + lane)) : 0;
-        if (cnt == 64) {
+    int64_t p = s;
+    while (p < e && (reinterpret_cast<uintptr_t>(val + p) & 15)) {  // up to 3 values to a 16-byte boundary
+        const double v = (double)val[p++];
+        acc = fma(v, v, acc);
+    }
+    if (p + 16 <= e) {
+        const float4 *q = reinterpret_cast<const float4 *>(val + p);
+        float4 a = q[0], b = q[1], c = q[2], d = q[3];
+        for (; p + 16 <= e; p += 16) {
+            float4 na = a, nb = b, nc = c, nd = d;
+            if (p + 32 <= e) {
+                const float4 *qn = reinterpret_cast<const float4 *>(val + p + 16);
+                na = qn[0];
+                nb = qn[1];
+                nc = qn[2];
+                nd = qn[3];
+            }
+            const float w[16] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w, c.x, c.y, c.z, c.w, d.x, d.y, d.z, d.w};
 #pragma unroll
-            for (int t = 0; t < 64; ++t) {
-                const double v = (double)__int_as_float(__builtin_amdgcn_readlane(vb, t));
+            for (int t = 0; t < 16; ++t) {
+                const double v = (double)w[t];
                 acc = fma(v, v, acc);
             }
-        } else {
-            for (int t = 0; t < cnt; ++t) {
-                const double v = (double)__int_as_float(__builtin_amdgcn_readlane(vb, t));
-                acc = fma(v, v, acc);
-            }
+            a = na;
+            b = nb;
+            c = nc;
+            d = nd;
         }
     }
-    if (lane == 0) {
-        cn2[i] = acc;
-        if (colnnz) colnnz[i] = e - s;
+    for (; p < e; ++p) {
+        const double v = (double)val[p];
+        acc = fma(v, v, acc);
+    }
+    return acc;
+}
+
+// adds the squares of the first cnt values of vb (lane t holds value t)
+__device__ __forceinline__ void chain64(int vb, int32_t cnt, double &acc) {
+    if (cnt >= 64) {
+#pragma unroll
+        for (int t = 0; t < 64; ++t) {
+            const double v = (double)__int_as_float(__builtin_amdgcn_readlane(vb, t));
+            acc = fma(v, v, acc);
+        }
+    } else {
+        for (int t = 0; t < cnt; ++t) {
+            const double v = (double)__int_as_float(__builtin_amdgcn_readlane(vb, t));
+            acc = fma(v, v, acc);
+        }
+    }
+}
+
+__device__ __forceinline__ double sq_chain_wave(const float *__restrict__ val, int64_t s, int64_t e, int lane) {
+    double acc = 0.0;
+    auto ld = [&](int64_t base) -> int {
+        return base + lane < e ? __float_as_int(__builtin_nontemporal_load(val + base + lane)) : 0;
+    };
+    int c0 = ld(s), c1 = ld(s + 64), c2 = ld(s + 128), c3 = ld(s + 192);
+    for (int64_t base = s; base < e; base += 256) {
+        const int n0 = ld(base + 256), n1 = ld(base + 320), n2 = ld(base + 384), n3 = ld(base + 448);
+        const int64_t left = e - base;
+        chain64(c0, (int32_t)min<int64_t>(64, left), acc);
+        if (left > 64) chain64(c1, (int32_t)min<int64_t>(64, left - 64), acc);
+        if (left > 128) chain64(c2, (int32_t)min<int64_t>(64, left - 128), acc);
+        if (left > 192) chain64(c3, (int32_t)min<int64_t>(64, left - 192), acc);
+        c0 = n0;
+        c1 = n1;
+        c2 = n2;
+        c3 = n3;
+    }
+    return acc;
+}
+
+__global__ __launch_bounds__(64) void col_sqnorms_kernel(int32_t n, const int32_t *__restrict__ rowptr,
+                                                         const float *__restrict__ val, double *__restrict__ cn2,
+                                                         int32_t *__restrict__ colnnz) {
+    const int lane = threadIdx.x;
+    const int64_t r = (int64_t)blockIdx.x * kWave + lane;
+    int32_t s = 0, e = 0;
+    if (r < n) {
+        s = rowptr[r];
+        e = rowptr[r + 1];
+        if (colnnz) colnnz[r] = e - s;
+    }
+    const bool is_long = r < n && e - s > kNormThreadMax;
+    if (r < n && !is_long) cn2[r] = sq_chain_thread(val, s, e);
+    uint64_t longs = __ballot(is_long);
+    while (longs) {  // wave-uniform
+        const int j = __builtin_ctzll(longs);
+        longs &= longs - 1;
+        const int32_t sj = __builtin_amdgcn_readlane(s, j), ej = __builtin_amdgcn_readlane(e, j);
+        const double acc = sq_chain_wave(val, sj, ej, lane);
+        if (lane == 0) cn2[r - lane + j] = acc;  // row r0 + j
     }
 }
 
@@ -167,7 +242,7 @@ hipError_t sum_fixed_order_launch(const double *x, int64_t n, double *ws, double
 hipError_t col_sqnorms_launch(int32_t n, const int32_t *rowptr_t, const float *val_t, double *cn2,
                               int32_t *colnnz, hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    col_sqnorms_kernel<<<(unsigned)ceil_div(n, 4), 256, 0, stream>>>(n, rowptr_t, val_t, cn2, colnnz);
+    col_sqnorms_kernel<<<(unsigned)ceil_div(n, kWave), kWave, 0, stream>>>(n, rowptr_t, val_t, cn2, colnnz);
     return hipGetLastError();
 }
 

@@ -265,6 +265,38 @@ def test_col_sqnorms_bitwise(gen_graph):
     assert np.array_equal(colnnz.cpu().numpy(), colnnz_o)
 
 
+@pytest.mark.parametrize("seed", range(4))
+def test_col_sqnorms_both_paths_bitwise(seed):
+    """Rows walked by their own lane (up to 2,048 entries: 16-byte alignment
+    head of 0-3 values, 16-value steps, ragged tails) and rows taken by the
+    whole wave (2,049 and more: 64-value loads, four in flight, ragged last
+    block), mixed in one 64-row group and alone, with empty rows, values
+    spanning many binades (so the sequential fp64 order shows in the last
+    bits) and a row starting at every offset modulo 4."""
+    rng = np.random.default_rng(100 + seed)
+    lens = [0, 1, 2, 3, 4, 15, 16, 17, 31, 32, 33, 47, 48, 2047, 2048, 2049, 2050, 4095, 4096, 4097,
+            255, 256, 257, 511, 512, 513, 70_001]
+    lens += list(rng.integers(0, 3000, 200)) + [0] * 7 + [int(x) for x in rng.integers(2049, 9000, 5)]
+    lens = np.array(lens if seed % 2 == 0 else lens[::-1], dtype=np.int64)
+    if seed >= 2:
+        lens = rng.permutation(lens)
+    rowptr = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    nnz = int(rowptr[-1])
+    val = (rng.standard_normal(nnz) * np.exp2(rng.integers(-40, 40, nnz))).astype(np.float32)
+    val[rng.random(nnz) < 0.01] = 0.0
+    n = len(lens)
+    col = np.zeros(nnz, np.int32)          # cn2 reads rowptr and val only
+    cn2_o, cnt_o = oracle.col_sqnorms(rowptr, val)
+    AT = rsc.DeviceCsr.from_host(rowptr, col, val, 1)
+    for shift in range(4):                # the rows' start offsets modulo 4
+        buf = torch.zeros(nnz + 4, dtype=torch.float32, device="cuda")
+        buf[shift:shift + nnz] = AT.val
+        X = rsc.DeviceCsr(n, 1, AT.rowptr, AT.col, buf[shift:shift + nnz], nnz=nnz)
+        cn2, cnt = rsc.col_sqnorms(X)
+        assert np.array_equal(cn2.cpu().numpy().view(np.uint64), cn2_o.view(np.uint64)), (seed, shift)
+        assert np.array_equal(cnt.cpu().numpy(), cnt_o)
+
+
 @pytest.mark.parametrize("d", [1, 5, 32, 33, 256, 300])
 def test_pair_scores_bitwise(d):
     n = 5000
