@@ -63,8 +63,19 @@ __global__ __launch_bounds__(256) void topk_hist_kernel(const uint64_t *__restri
     for (int b = threadIdx.x; b < kBins; b += blockDim.x) lh[b] = 0;
     __syncthreads();
     const uint64_t prefix = st->prefix, pmask = st->pmask;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    // eight keys per thread loaded before any is counted (the launch gives
+    // most threads eight), then the rest one at a time
+    for (; i + 7 * stride < n; i += 8 * stride) {
+        uint64_t k[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) k[u] = key[i + u * stride];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if ((k[u] & pmask) == prefix) atomicAdd(&lh[(k[u] >> shift) & dmask], 1u);
+    }
+    for (; i < n; i += stride) {
         const uint64_t k = key[i];
         if ((k & pmask) == prefix) atomicAdd(&lh[(k >> shift) & dmask], 1u);
     }
