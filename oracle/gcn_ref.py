@@ -71,13 +71,9 @@ class RscReference:
             return self.slices[l] @ g
         return self.AT @ g
 
-    def step(self, X, W1, W2, Y, step, score_inputs=None):
-        """One training step with weights W1, W2. score_inputs (optional,
-        used at refresh steps only): (keys per layer, ||grad H||_F^2 per layer,
-        ||A||_F^2) to take instead of the values this step computes, so that a
-        run can be followed on exactly the inputs another implementation
-        scored; the ones computed here are still returned as keys_own and
-        fro_b2_own."""
+    def step(self, X, W1, W2, Y, step):
+        """One training step with weights W1, W2. At a refresh step the keys
+        and ||grad H||_F^2 it scored are also returned (keys, fro_b2)."""
         mode = "score" if (self.last is None or step - self.last >= self.R) else "sampled"
         J1 = X @ W1
         P1 = self.A @ J1
@@ -98,11 +94,8 @@ class RscReference:
                 o = pair_keys(self.cn2, g.astype(np.float32))
                 keys.append(o["key"])
                 fro_b2.append(sum_sequential(o["rn2"]))     # ||grad H||_F^2 (Eq. 4a)
-            out["keys_own"], out["fro_b2_own"] = keys, fro_b2
-            fro_a2 = self.fro_a2
-            if score_inputs is not None:
-                keys, fro_b2, fro_a2 = score_inputs
-            self.k, _ = greedy(keys, self.colnnz, self.nnz, self.widths, fro_a2, fro_b2,
+            out["keys"], out["fro_b2"] = keys, fro_b2
+            self.k, _ = greedy(keys, self.colnnz, self.nnz, self.widths, self.fro_a2, fro_b2,
                                self.budget, self.alpha)
             rec = {"step": step, "k": list(self.k), "auc": [], "overlap": []}
             for l in range(2):

@@ -725,7 +725,7 @@ def test_gcn_reference_staleness_record():
                 assert rec["auc"] == [] and rec["overlap"] == []
             else:
                 for l in range(2):
-                    order = oracle.rank_order(out["keys_own"][l])
+                    order = oracle.rank_order(out["keys"][l])
                     assert rec["auc"][l] == _brute_auc(order, set(int(i) for i in prev_idx[l]))
                     inter = len(set(prev_idx[l].tolist()) & set(out["idx"][l].tolist()))
                     assert rec["overlap"][l] == inter / len(prev_idx[l])
