@@ -147,9 +147,9 @@ __global__ __launch_bounds__(256) void rank_values_kernel(const uint64_t *__rest
 
 // Block j (counted from the lowest rank) covers ranks
 // [max(0, n - (j+1) step), n - j step); one wave per block. The wave loads 64
-// ranks at a time; the fp64 mass is added one rank after another in
-// ascending rank order (the order that defines it), the integer count by a
-// wave reduction (exact in any order).
+// ranks at a time (the next 64 in flight meanwhile); the fp64 mass is added
+// one rank after another in ascending rank order (the order that defines
+// it), the integer count by a wave reduction (exact in any order).
 __global__ __launch_bounds__(64) void greedy_profile_kernel(const double *__restrict__ rv,
                                                             const int32_t *__restrict__ rc, int32_t n,
                                                             int32_t step, int32_t n_blocks,
@@ -160,23 +160,37 @@ __global__ __launch_bounds__(64) void greedy_profile_kernel(const double *__rest
     const int lane = threadIdx.x;
     const int64_t hi = (int64_t)n - (int64_t)j * step;
     const int64_t lo = std::max<int64_t>(0, hi - step);
-    double s = 0.0;
     int64_t c = 0;
+    for (int64_t b = lo + lane; b < hi; b += 64) c += rc[b];
+    for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+    // the chain reads its values from LDS at one address for all lanes (a
+    // broadcast read into a vector register), so no broadcast instruction
+    // sits between two adds; two 64-value buffers, the next one filled
+    // while the current one is summed
+    __shared__ double buf[2][64];
+    double s = 0.0;
+    double x = lo + lane < hi ? rv[lo + lane] : 0.0;
+    int cur = 0;
     for (int64_t base = lo; base < hi; base += 64) {
         const int32_t cnt = (int32_t)std::min<int64_t>(64, hi - base);
-        const double x = lane < cnt ? rv[base + lane] : 0.0;
-        int64_t y = lane < cnt ? rc[base + lane] : 0;
-        for (int off = 32; off > 0; off >>= 1) y += __shfl_xor(y, off);
-        c += y;
-        const int lo_bits = __double2loint(x), hi_bits = __double2hiint(x);
+        buf[cur][lane] = x;
+        const double xn = base + 64 + lane < hi ? rv[base + 64 + lane] : 0.0;  // the next 64, in flight
+        __syncthreads();  // one-wave block: the buffer is written
+        const double *bp = buf[cur];
         if (cnt == 64) {
 #pragma unroll
-            for (int t = 0; t < 64; ++t)
-                s += __hiloint2double(__builtin_amdgcn_readlane(hi_bits, t), __builtin_amdgcn_readlane(lo_bits, t));
+            for (int t0 = 0; t0 < 64; t0 += 8) {
+                double w[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) w[u] = bp[t0 + u];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) s += w[u];
+            }
         } else {
-            for (int t = 0; t < cnt; ++t)
-                s += __hiloint2double(__builtin_amdgcn_readlane(hi_bits, t), __builtin_amdgcn_readlane(lo_bits, t));
+            for (int t = 0; t < cnt; ++t) s += bp[t];
         }
+        cur ^= 1;
+        x = xn;
     }
     if (lane == 0) {
         mass[j] = s;

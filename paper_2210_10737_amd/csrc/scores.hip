@@ -18,8 +18,8 @@ namespace {
 // float4 loads (the next step's loads in flight), so the chain costs no
 // memory operation or broadcast per value and the 64 lanes' chains advance
 // together. The wave then takes its longer rows one at a time: 64 values per
-// coalesced load (four more loads in flight), each value broadcast to the
-// chain with readlane. A wave-per-row form for every row kept 63 of 64 lanes
+// coalesced load (four more loads in flight), squared by the lanes and read
+// back by the chain from LDS. A wave-per-row form for every row kept 63 of 64 lanes
 // idle in the chain and took 3-5x longer on graphs of short rows.
 constexpr int32_t kNormThreadMax = 2048;
 
@@ -61,35 +61,43 @@ __device__ __forceinline__ double sq_chain_thread(const float *__restrict__ val,
     return acc;
 }
 
-// adds the squares of the first cnt values of vb (lane t holds value t)
-__device__ __forceinline__ void chain64(int vb, int32_t cnt, double &acc) {
+// Adds, in order, the squares of the first cnt values of a 64-value batch
+// (lane t holds value t): each lane squares its value exactly in fp64 and
+// stores it in LDS, and the chain reads the squares back at one address for
+// all lanes (a broadcast read into a vector register), so nothing but the
+// adds sits on the chain. buf alternates between two 64-entry halves so the
+// next batch can be stored while this one is read.
+__device__ __forceinline__ void chain64(float x, int32_t cnt, int lane, double *buf, double &acc) {
+    buf[lane] = (double)x * (double)x;  // exact: fma(v, v, acc) == acc + v * v
+    __syncthreads();                    // one-wave block
     if (cnt >= 64) {
 #pragma unroll
-        for (int t = 0; t < 64; ++t) {
-            const double v = (double)__int_as_float(__builtin_amdgcn_readlane(vb, t));
-            acc = fma(v, v, acc);
+        for (int t0 = 0; t0 < 64; t0 += 8) {
+            double w[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) w[u] = buf[t0 + u];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) acc += w[u];
         }
     } else {
-        for (int t = 0; t < cnt; ++t) {
-            const double v = (double)__int_as_float(__builtin_amdgcn_readlane(vb, t));
-            acc = fma(v, v, acc);
-        }
+        for (int t = 0; t < cnt; ++t) acc += buf[t];
     }
 }
 
-__device__ __forceinline__ double sq_chain_wave(const float *__restrict__ val, int64_t s, int64_t e, int lane) {
+__device__ __forceinline__ double sq_chain_wave(const float *__restrict__ val, int64_t s, int64_t e, int lane,
+                                                double (*buf)[64]) {
     double acc = 0.0;
-    auto ld = [&](int64_t base) -> int {
-        return base + lane < e ? __float_as_int(__builtin_nontemporal_load(val + base + lane)) : 0;
+    auto ld = [&](int64_t base) -> float {
+        return base + lane < e ? __builtin_nontemporal_load(val + base + lane) : 0.f;
     };
-    int c0 = ld(s), c1 = ld(s + 64), c2 = ld(s + 128), c3 = ld(s + 192);
+    float c0 = ld(s), c1 = ld(s + 64), c2 = ld(s + 128), c3 = ld(s + 192);
     for (int64_t base = s; base < e; base += 256) {
-        const int n0 = ld(base + 256), n1 = ld(base + 320), n2 = ld(base + 384), n3 = ld(base + 448);
+        const float n0 = ld(base + 256), n1 = ld(base + 320), n2 = ld(base + 384), n3 = ld(base + 448);
         const int64_t left = e - base;
-        chain64(c0, (int32_t)min<int64_t>(64, left), acc);
-        if (left > 64) chain64(c1, (int32_t)min<int64_t>(64, left - 64), acc);
-        if (left > 128) chain64(c2, (int32_t)min<int64_t>(64, left - 128), acc);
-        if (left > 192) chain64(c3, (int32_t)min<int64_t>(64, left - 192), acc);
+        chain64(c0, (int32_t)min<int64_t>(64, left), lane, buf[0], acc);
+        if (left > 64) chain64(c1, (int32_t)min<int64_t>(64, left - 64), lane, buf[1], acc);
+        if (left > 128) chain64(c2, (int32_t)min<int64_t>(64, left - 128), lane, buf[0], acc);
+        if (left > 192) chain64(c3, (int32_t)min<int64_t>(64, left - 192), lane, buf[1], acc);
         c0 = n0;
         c1 = n1;
         c2 = n2;
@@ -101,6 +109,7 @@ __device__ __forceinline__ double sq_chain_wave(const float *__restrict__ val, i
 __global__ __launch_bounds__(64) void col_sqnorms_kernel(int32_t n, const int32_t *__restrict__ rowptr,
                                                          const float *__restrict__ val, double *__restrict__ cn2,
                                                          int32_t *__restrict__ colnnz) {
+    __shared__ double buf[2][64];
     const int lane = threadIdx.x;
     const int64_t r = (int64_t)blockIdx.x * kWave + lane;
     int32_t s = 0, e = 0;
@@ -116,7 +125,7 @@ __global__ __launch_bounds__(64) void col_sqnorms_kernel(int32_t n, const int32_
         const int j = __builtin_ctzll(longs);
         longs &= longs - 1;
         const int32_t sj = __builtin_amdgcn_readlane(s, j), ej = __builtin_amdgcn_readlane(e, j);
-        const double acc = sq_chain_wave(val, sj, ej, lane);
+        const double acc = sq_chain_wave(val, sj, ej, lane, buf);
         if (lane == 0) cn2[r - lane + j] = acc;  // row r0 + j
     }
 }
