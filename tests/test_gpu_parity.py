@@ -256,6 +256,48 @@ def test_degenerate_shapes():
     cache.close()
 
 
+@pytest.mark.parametrize("d", [64, 256])
+def test_spmm_nonfinite_operands_propagate(d):
+    """NaN and +-Inf entries of B reach exactly the output elements whose
+    sums contain them (IEEE: NaN spreads, Inf of one sign stays Inf, +Inf
+    and -Inf meet as NaN, 0 * Inf is NaN), in the exact product (plan and
+    plain call) and the sampled one; the finite elements stay within the
+    usual tolerance."""
+    n = 3000
+    A = synth.random_csr(n, n, 60, seed=77, hub_rows=3, hub_len=2500)
+    B = synth.dense_normal(n, d, seed=78)
+    rng = np.random.default_rng(79)
+    rows = rng.choice(n, 30, replace=False)
+    B[rows[:10], rng.integers(0, d, 10)] = np.nan
+    B[rows[10:20], rng.integers(0, d, 10)] = np.inf
+    B[rows[20:], rng.integers(0, d, 10)] = -np.inf
+    B[rows[12], 3] = np.inf                    # the same feature +Inf and -Inf in two rows
+    B[rows[22], 3] = -np.inf
+    X = to_dev(A)
+    Bd = dense_dev(B)
+    Yo, S = oracle.spmm(A.rowptr, A.col, A.val, B, with_mag=True)
+    plan = rsc.SpmmPlan(X)
+    cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)
+    with np.errstate(invalid="ignore"):
+        key = oracle.pair_keys(cn2, synth.dense_normal(n, d, seed=80))["key"]
+    _, mask = oracle.topk(key, n // 2)
+    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+    Yso, Ss = oracle.spmm(ro, co, vo, B, with_mag=True)
+    cache = rsc.Cache(X, X)
+    cache.refresh(dense_dev(synth.dense_normal(n, d, seed=80)), n // 2, step=0)
+    for Y, Yr, Sr, tol in ((rsc.spmm(X, Bd), Yo, S, 1e-5), (plan.run(Bd), Yo, S, 1e-5),
+                           (cache.spmm_sampled(Bd), Yso, Ss, 1e-4)):
+        Y = Y.cpu().numpy().astype(np.float64)
+        assert np.array_equal(np.isnan(Y), np.isnan(Yr))
+        assert np.array_equal(np.isposinf(Y), np.isposinf(Yr)) and np.array_equal(np.isneginf(Y), np.isneginf(Yr))
+        fin = np.isfinite(Yr) & np.isfinite(Sr)
+        assert fin.sum() > Y.size // 2
+        assert np.max(np.abs(Y[fin] - Yr[fin]) / np.maximum(Sr[fin], FLT_MIN)) <= tol
+    assert np.isnan(Yo).any() and np.isposinf(Yo).any() and np.isneginf(Yo).any()
+    plan.close()
+    cache.close()
+
+
 # ------------------------------------------------------------------ scores
 def test_col_sqnorms_bitwise(gen_graph):
     AT = synth.transpose(gen_graph, 2500)
