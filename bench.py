@@ -18,7 +18,7 @@ peak. `cpu_baseline` times the oracle (all its OpenMP threads) on a bounded
 sample of the same step. `vendor_baseline` times rocSPARSE's SpMM on the
 exact product's operands beside the library's (context only).
 
-usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload copurchase]
+usage: python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload copurchase]
                        [--budget-pct 30] [--aggregator gcn|mean] [--selector topk|random]
                        [--no-cpu-baseline] [--no-vendor-baseline]
        python bench.py --workload gcn2-train [--budget-pct 10]   (training-step comparison)
