@@ -65,15 +65,30 @@ __global__ __launch_bounds__(256) void topk_hist_kernel(const uint64_t *__restri
     const uint64_t prefix = st->prefix, pmask = st->pmask;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    // eight keys per thread loaded before any is counted (the launch gives
-    // most threads eight), then the rest one at a time
+    // eight keys per thread loaded before any is counted, then the rest one
+    // at a time
     for (; i + 7 * stride < n; i += 8 * stride) {
         uint64_t k[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) k[u] = key[i + u * stride];
+        if (pass == 0) {  // block-uniform
+            // the top digit is nearly constant over the keys: a wave whose
+            // keys all share one digit adds them with one LDS atomic
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if ((k[u] & pmask) == prefix) atomicAdd(&lh[(k[u] >> shift) & dmask], 1u);
+            for (int u = 0; u < 8; ++u) {
+                const uint32_t dg = (uint32_t)((k[u] >> shift) & dmask);
+                const uint32_t d0 = __shfl(dg, 0);
+                if (__ballot(dg == d0) == ~0ull) {
+                    if ((threadIdx.x & 63) == 0) atomicAdd(&lh[d0], 64u);
+                } else {
+                    atomicAdd(&lh[dg], 1u);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if ((k[u] & pmask) == prefix) atomicAdd(&lh[(k[u] >> shift) & dmask], 1u);
+        }
     }
     for (; i < n; i += stride) {
         const uint64_t k = key[i];
@@ -365,9 +380,18 @@ hipError_t topk_launch(const uint64_t *key, int32_t n, int32_t k, int32_t *idx, 
     uint32_t *sel_before = reinterpret_cast<uint32_t *>(p + 3 * tb);
 
     topk_init_kernel<<<1, 256, 0, stream>>>(&h->st, h->hist[0], k);
-    const unsigned hgrid = (unsigned)std::min<int64_t>(ceil_div(n, 256 * 8), 2048);
+    // Each block flushes its non-empty bins with one global atomic each. The
+    // first two passes count every key, into a few bins (pass 0) or into
+    // most of them (pass 1), so they run on 256 and 128 blocks to keep those
+    // atomics few (measured on 2.45M keys: 12.4 and 9.5 us, against 18.9 and
+    // 29.6 with eight keys per thread); later passes count only the keys
+    // under the chosen prefix and take eight keys per thread, for more loads
+    // in flight.
+    const unsigned hgrid_wide = (unsigned)std::min<int64_t>(ceil_div(n, 256 * 8), 2048);
+    const unsigned hgrid_pass[2] = {std::min(hgrid_wide, 256u), std::min(hgrid_wide, 128u)};
     for (int pass = 0; pass < kPasses; ++pass) {
-        topk_hist_kernel<<<hgrid, 256, 0, stream>>>(key, n, &h->st, h->hist[pass & 1], pass);
+        topk_hist_kernel<<<pass < 2 ? hgrid_pass[pass] : hgrid_wide, 256, 0, stream>>>(key, n, &h->st,
+                                                                                        h->hist[pass & 1], pass);
         topk_pick_kernel<<<1, 256, 0, stream>>>(&h->st, h->hist[pass & 1], h->hist[(pass + 1) & 1], pass);
     }
     topk_tile_count_kernel<<<nt, 256, 0, stream>>>(key, n, &h->st, tile_eq, tile_gt);
