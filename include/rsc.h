@@ -251,14 +251,14 @@ rsc_status_t rsc_topk_select(const uint64_t *key, int32_t n, int32_t k, int32_t 
  * colw (nullable, fp64[n_cols]): per-column scale; when given, each kept
  * value becomes fl32(val * colw[col]) (fp64 product, one rounding), as the
  * randomized sampler's 1/(k p) weighting needs.
- * nnz_out: device int64 receiving nnz'. For n_cols up to about 410,000 (a
- * mask that fits on-chip memory several times per compute unit) the slice
- * runs as one fused kernel (count, a decoupled look-back scan over tiles
- * taken in ticket order, compaction), otherwise as three launches (count,
- * scan, emit); RSC_SLICE_FUSED = 0 / 1 forces either. Both give the same
- * bytes. The fused kernel's waits are bounded: if one ever ran out, *nnz_out
- * would be -1 and rsc_slice_csr's synchronous form and rsc_cache_get would
- * return RSC_ERR_INTERNAL.
+ * nnz_out: device int64 receiving nnz'. The slice runs as a stream
+ * compaction in four launches (a tile-to-row table, count, scan, emit);
+ * with the environment variable RSC_SLICE_FUSED=1 it runs as one fused
+ * kernel instead (count, a decoupled look-back scan over tiles taken in
+ * ticket order, compaction). Both give the same bytes. The fused kernel's
+ * waits are bounded: if one ever ran out, *nnz_out would be -1 and
+ * rsc_slice_csr's synchronous form and rsc_cache_get would return
+ * RSC_ERR_INTERNAL.
  * capacity: entries available in col_out / val_out. If capacity >= A->nnz
  * the call is asynchronous. Otherwise it is [sync]: entries beyond capacity
  * are not written, and RSC_ERR_CAPACITY is returned when nnz' > capacity

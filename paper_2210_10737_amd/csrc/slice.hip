@@ -6,18 +6,19 @@
 // stay in their original order, the output position of a kept entry is the
 // number of kept entries before it, and Rowptr'[i] is that count at position
 // Rowptr[i]. So the slice is one stream compaction over the nnz entries:
-//   1. per tile of 4096 entries: the kept flags as 64 wave ballots (reads
-//      col; the n-bit mask is tested from LDS, loaded piece by piece), stored
-//      for step 3, and their count;
+//   0. per tile of 4096 entries: the first row whose Rowptr lies in it (a
+//      table built from Rowptr; it also clears the tile counts);
+//   1. per tile: the kept flags as 64 wave ballots (reads col; the n-bit mask
+//      is tested from LDS, loaded piece by piece), stored for step 3, and
+//      their count;
 //   2. one block scans the tile counts (and stores nnz');
 //   3. per tile: load col/val into registers, scan the tile's ballot counts,
 //      compact the kept entries in LDS and write them out coalesced at their
 //      global positions, and write Rowptr'[i] for every row whose Rowptr[i]
 //      falls in the tile.
-// When the mask fits LDS with room for several blocks per CU (up to about
-// 410,000 columns) the three steps run fused in one kernel instead (count,
-// decoupled look-back scan over ticketed tiles, compaction; below); both
-// forms give the same bytes.
+// A single-pass form (count, decoupled look-back scan over ticketed tiles,
+// compaction in one kernel; below) gives the same bytes and is available on
+// request; the launches above measured faster.
 // Integer-only and deterministic. With a per-column scale (the randomized
 // sampler's 1/(k p)), each kept value becomes fl32(val * colw[col]).
 #include <cstdlib>
@@ -42,11 +43,13 @@ static_assert(kGroups == 64, "one wave scans the (chunk, wave) ballots of a tile
 // few cycles. Persistent blocks of 1024 threads (one per CU, 156 KB of LDS
 // each) walk the column range in pieces of 1,277,952 columns: load that
 // piece of the mask, then test every tile's entries against it, taking
-// kTilesPerIter tiles per step with the next step's 16 column loads per
-// thread already in flight.
-// A tile's ballots and count from later pieces are OR-ed / added by the same
-// threads that wrote them (the tile-to-block assignment is the same in every
-// piece).
+// kTilesPerIter tiles per step with the next step's column loads already in
+// flight. Each wave publishes its ballots and its kept count without waiting
+// for anything: the first piece stores the ballots, later pieces OR theirs in
+// (an entry is kept by at most one piece; the same lane wrote the stored
+// value), and every piece adds the wave's count of each tile to tile_cnt
+// (cleared beforehand) with an integer atomic. No result depends on the order
+// of the atomics, and the steps need no barrier.
 constexpr int kMaskLdsWords = 39936;  // 156 KB of LDS: 1,277,952 columns per piece
 constexpr int kCountThreads = 1024;
 constexpr int kTilesPerIter = 4;
@@ -59,24 +62,32 @@ __global__ __launch_bounds__(kCountThreads) void slice_count_kernel(const int32_
                                                                     uint32_t *__restrict__ tile_cnt,
                                                                     uint64_t *__restrict__ tile_bits) {
     __shared__ uint32_t s_mask[kMaskLdsWords];
-    __shared__ uint32_t s_cnt[kTilesPerIter][kCountWaves];
     const int T = threadIdx.x, lane = T & 63, wv = T >> 6;
     for (int32_t w0 = 0; w0 == 0 || w0 < n_words; w0 += kMaskLdsWords) {
         const int32_t words = max(0, min(kMaskLdsWords, n_words - w0));
         __syncthreads();  // the previous piece's lookups are done
         for (int i = T; i < words; i += kCountThreads) s_mask[i] = mask[w0 + i];
         __syncthreads();
-        const int64_t lo = (int64_t)w0 * 32, hi = lo + (int64_t)words * 32;
+        // column v is in this piece iff 0 <= v - lo < span (32-bit: both are
+        // below 2^31, and the padding value -1 falls outside)
+        const int32_t lo = w0 * 32;
+        const uint32_t span = (uint32_t)words * 32u;
         const int32_t stride = gridDim.x * kTilesPerIter;
         // the next step's column loads are issued before this step's tests
+        // (a step's tiles are consecutive: value (u, i) is entry
+        // T + kCountThreads * (4 u + i) from the step's first entry)
         int32_t nx[kTilesPerIter][4];
         auto load = [&](int32_t t0) {
+            const int64_t base = (int64_t)t0 * kTile;
+            const int64_t left = nnz - base;
+            const int32_t rem = left < (int64_t)kTilesPerIter * kTile ? (int32_t)left : kTilesPerIter * kTile;
+            const int32_t *src = col + base;
 #pragma unroll
             for (int u = 0; u < kTilesPerIter; ++u)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int64_t p = (int64_t)(t0 + u) * kTile + T + kCountThreads * i;
-                    nx[u][i] = (t0 + u < nt && p < nnz) ? __builtin_nontemporal_load(col + p) : -1;
+                    const int32_t q = T + kCountThreads * (4 * u + i);
+                    nx[u][i] = q < rem ? __builtin_nontemporal_load(src + q) : -1;
                 }
         };
         load(blockIdx.x * kTilesPerIter);
@@ -87,30 +98,55 @@ __global__ __launch_bounds__(kCountThreads) void slice_count_kernel(const int32_
 #pragma unroll
                 for (int i = 0; i < 4; ++i) cv[u][i] = nx[u][i];
             if (t0 + stride < nt) load(t0 + stride);
+            // lane 4 u + i keeps ballot (u, i) and lane u the wave's count of
+            // tile u, so the step's 16 ballots and 4 counts leave in one store
+            // (or atomic) instruction each
+            uint64_t my_ball = 0;
+            uint32_t my_cnt = 0;
 #pragma unroll
             for (int u = 0; u < kTilesPerIter; ++u) {
                 uint32_t c = 0;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int64_t v = cv[u][i];
-                    const bool k = v >= lo && v < hi && ((s_mask[(v - lo) >> 5] >> (v & 31)) & 1u);
+                    const uint32_t off = (uint32_t)(cv[u][i] - lo);
+                    const bool k = off < span && ((s_mask[off >> 5] >> (off & 31)) & 1u);
                     const uint64_t b = __ballot(k);
                     c += __popcll(b);
-                    if (lane == 0 && t0 + u < nt) {
-                        const int64_t g = (int64_t)(t0 + u) * 64 + wv + kCountWaves * i;  // (o >> 6) of the entries
-                        tile_bits[g] = w0 == 0 ? b : (tile_bits[g] | b);
-                    }
+                    if (lane == 4 * u + i) my_ball = b;
                 }
-                if (lane == 0) s_cnt[u][wv] = c;
+                if (lane == u) my_cnt = c;
             }
-            __syncthreads();
-            if (T < kTilesPerIter && t0 + T < nt) {
-                uint32_t c = 0;
-                for (int v = 0; v < kCountWaves; ++v) c += s_cnt[T][v];
-                tile_cnt[t0 + T] = w0 == 0 ? c : tile_cnt[t0 + T] + c;
+            if (lane < 4 * kTilesPerIter && t0 + (lane >> 2) < nt) {
+                // group (o >> 6) of tile t0 + u for entries T + kCountThreads * i
+                uint64_t *g = tile_bits + (int64_t)(t0 + (lane >> 2)) * 64 + wv + kCountWaves * (lane & 3);
+                if (w0 == 0)
+                    *g = my_ball;
+                else if (my_ball)
+                    atomicOr(reinterpret_cast<unsigned long long *>(g), (unsigned long long)my_ball);
             }
-            __syncthreads();  // s_cnt is reused by the next step
+            if (lane < kTilesPerIter && my_cnt && t0 + lane < nt) atomicAdd(&tile_cnt[t0 + lane], my_cnt);
         }
+    }
+}
+
+// tile_row[t] = the first row i with rowptr[i] >= t * kTile, for every tile
+// t < nt: row i takes the tiles whose first entry lies in
+// (rowptr[i - 1], rowptr[i]] (rowptr[-1] read as -1), so for a well-formed
+// row pointer each tile is written exactly once. The emit reads its rows'
+// range from here instead of two binary searches per tile. The same launch
+// clears the tile counts the count pass adds into.
+__global__ __launch_bounds__(256) void slice_tile_rows_kernel(const int32_t *__restrict__ rowptr, int32_t n_rows,
+                                                              int32_t nt, int32_t *__restrict__ tile_row,
+                                                              uint32_t *__restrict__ tile_cnt) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t first = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (int64_t t = first; t < nt; t += stride) tile_cnt[t] = 0;
+    for (int64_t i = first; i <= n_rows; i += stride) {
+        const int64_t a = i == 0 ? -1 : (int64_t)rowptr[i - 1];
+        const int64_t b = rowptr[i];
+        const int64_t t0 = a < 0 ? 0 : a / kTile + 1;  // first tile starting above a
+        const int64_t t1 = min<int64_t>(b / kTile, (int64_t)nt - 1);
+        for (int64_t t = t0; t <= t1; ++t) tile_row[t] = (int32_t)i;
     }
 }
 
@@ -158,6 +194,7 @@ __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restri
                                                          const float *__restrict__ val, int64_t nnz,
                                                          const uint64_t *__restrict__ tile_bits,
                                                          const uint32_t *__restrict__ tile_off,
+                                                         const int32_t *__restrict__ tile_row,
                                                          int32_t *__restrict__ rowptr_out,
                                                          int32_t *__restrict__ col_out,
                                                          float *__restrict__ val_out, int64_t capacity,
@@ -171,8 +208,10 @@ __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restri
     const int64_t ts = (int64_t)blockIdx.x * kTile;
     const int64_t te = min<int64_t>(ts + kTile, nnz);
     const bool last = blockIdx.x == gridDim.x - 1;
-    if (t == 0) s_rows[0] = lower_bound_rowptr(rowptr, n_rows, ts);
-    if (t == 1) s_rows[1] = last ? n_rows + 1 : lower_bound_rowptr(rowptr, n_rows, te);
+    // the rows whose Rowptr[i] lies in the tile (clamped to [0, n_rows + 1],
+    // so a malformed row pointer cannot send the stores below out of range)
+    if (t == 0) s_rows[0] = min(max(tile_row[blockIdx.x], 0), n_rows + 1);
+    if (t == 1) s_rows[1] = last ? n_rows + 1 : min(max(tile_row[blockIdx.x + 1], 0), n_rows + 1);
     int32_t rc[kPer];
     float rv[kPer];
     uint64_t ball[kPer];
@@ -223,7 +262,9 @@ __global__ __launch_bounds__(256) void slice_emit_kernel(const int32_t *__restri
     for (int64_t i = (int64_t)r0 + t; i < r1; i += 256) {
         const int64_t off = (int64_t)rowptr[i] - ts;
         uint32_t c;
-        if (off >= kTile || ts + off >= te) {
+        if (off < 0) {  // only for a malformed row pointer
+            c = 0;
+        } else if (off >= kTile || ts + off >= te) {
             c = total;
         } else {
             const int g = (int)(off >> 6), l = (int)(off & 63);  // g = chunk * 4 + wave
@@ -421,22 +462,23 @@ bool mask_in_lds(int32_t n_words) {
     return sizeof(uint32_t) * (size_t)n_words + 2048 <= (size_t)kLdsPerCu / 3;
 }
 
-// The single-pass form is taken when its mask goes to LDS (up to about
-// 410,000 columns): measured there it beats the three launches (social's
-// refresh 0.540 against 0.570 ms, protein's 0.427 against 0.436 ms); with
-// the mask in global memory the lookups cost more than the saved read of col
-// (gcn2 0.485 against 0.469 ms, copurchase 1.41 against 1.35 ms).
-// RSC_SLICE_FUSED = 0 / 1 forces the three-launch / fused form.
-bool use_fused(int32_t n_words) {
+// The three launches are the default: with the count's ballots and counts
+// published by atomics and the emit's row ranges read from a table, they
+// measured faster than the single pass on every workload (slice kernels,
+// three launches against single pass: tiny 21 / 26 us, social 344-393 /
+// 372-403 us, protein 250 / 281 us, gcn2 72 / 114 us, copurchase 503 /
+// 787 us). RSC_SLICE_FUSED = 1 / 0 forces the single-pass / three-launch form.
+bool use_fused() {
     if (const char *env = getenv("RSC_SLICE_FUSED")) return atoi(env) != 0;
-    return mask_in_lds(n_words);
+    return false;
 }
 
 }  // namespace
 
 size_t slice_ws_bytes(int64_t nnz) {
     const size_t nt = (size_t)ceil_div(std::max<int64_t>(nnz, 1), kTile);
-    return 2 * align_up(nt * sizeof(uint32_t), 256) + align_up(nt * kGroups * sizeof(uint64_t), 256);
+    return 2 * align_up(nt * sizeof(uint32_t), 256) + align_up(nt * kGroups * sizeof(uint64_t), 256) +
+           align_up((nt + 1) * sizeof(int32_t), 256);
 }
 
 hipError_t slice_launch(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32_t *rowptr, const int32_t *col,
@@ -453,11 +495,13 @@ hipError_t slice_launch(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
     uint32_t *tile_cnt = static_cast<uint32_t *>(ws);
     uint32_t *tile_off = reinterpret_cast<uint32_t *>(static_cast<char *>(ws) + tb);
     uint64_t *tile_bits = reinterpret_cast<uint64_t *>(static_cast<char *>(ws) + 2 * tb);
+    int32_t *tile_row = reinterpret_cast<int32_t *>(static_cast<char *>(ws) + 2 * tb +
+                                                    align_up((size_t)nt * kGroups * sizeof(uint64_t), 256));
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess)
         (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     const int32_t n_words = (int32_t)ceil_div((int64_t)n_cols, 32);
-    if (use_fused(n_words)) {
+    if (use_fused()) {
         // ws: [ticket, failure flag | pad to 256 B][status word per tile]
         int32_t *ticket = static_cast<int32_t *>(ws);
         uint64_t *status = reinterpret_cast<uint64_t *>(static_cast<char *>(ws) + 256);
@@ -480,11 +524,14 @@ hipError_t slice_launch(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
                 capacity, nnz_out, ticket + 1, colw);
         return hipGetLastError();
     }
+    slice_tile_rows_kernel<<<(unsigned)std::min<int64_t>(ceil_div(std::max<int64_t>((int64_t)n_rows + 1, nt), 256),
+                                                         4096),
+                             256, 0, stream>>>(rowptr, n_rows, nt, tile_row, tile_cnt);
     const unsigned cgrid = (unsigned)std::max<int64_t>(1, std::min<int64_t>(cus, ceil_div(nt, kTilesPerIter)));
     slice_count_kernel<<<cgrid, kCountThreads, 0, stream>>>(col, nnz, mask, n_words, nt, tile_cnt, tile_bits);
     slice_scan_kernel<<<1, 1024, 0, stream>>>(nt, tile_cnt, tile_off, nnz_out);
-    slice_emit_kernel<<<nt, 256, 0, stream>>>(rowptr, n_rows, col, val, nnz, tile_bits, tile_off, rowptr_out,
-                                              col_out, val_out, capacity, colw);
+    slice_emit_kernel<<<nt, 256, 0, stream>>>(rowptr, n_rows, col, val, nnz, tile_bits, tile_off, tile_row,
+                                              rowptr_out, col_out, val_out, capacity, colw);
     return hipGetLastError();
 }
 
