@@ -1,6 +1,6 @@
 """The single-pass CSR column slice (count, decoupled look-back scan over
 ticketed tiles, compaction in one kernel; taken with RSC_SLICE_FUSED=1)
-against the three-launch form and the oracle: rowptr', col', val' and nnz'
+against the default multi-launch form and the oracle: rowptr', col', val' and nnz'
 byte for byte, with the mask in LDS (up to 1,179,648 columns) and in global
 memory (above that), with a per-column scale, ragged tails, empty rows,
 k = 0 and k = n, and the capacity error."""
@@ -134,3 +134,39 @@ def test_fused_full_size_copurchase_against_three_launch():
     for a, b in zip(f[:3], t[:3]):
         assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
     assert f[3] == t[3]
+
+
+def _tile_edge_lengths(case):
+    """Row lengths whose row boundaries sit on 4096-entry tile edges (both
+    slice forms cut the entries into such tiles): rows ending exactly on an
+    edge, runs of empty rows at an edge and at both ends, rows spanning
+    several tiles, and nnz a whole number of tiles or one entry past it."""
+    T = 4096
+    if case == "edges":
+        return [0, 0, T, 0, 0, 0, T - 1, 1, 0, 2 * T, 0, T, 0, 0]
+    if case == "spans":
+        return [1, 5 * T + 7, 0, T - 8, 3, 0, 0, 3 * T, 0]
+    if case == "one_past":
+        return [T] * 5 + [0, 1, 0]
+    if case == "all_empty_tail":
+        return [2 * T - 1, 1] + [0] * 9000
+    raise ValueError(case)
+
+
+@pytest.mark.parametrize("case", ["edges", "spans", "one_past", "all_empty_tail"])
+@pytest.mark.parametrize("form", [0, 1])
+def test_rows_on_tile_edges(case, form):
+    rng = np.random.default_rng(["edges", "spans", "one_past", "all_empty_tail"].index(case) + 900)
+    lens = np.array(_tile_edge_lengths(case), dtype=np.int64)
+    n_cols = int(max(lens.max(), 1)) + 3
+    A = synth.bucket_csr(lens, n_cols, seed=11)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
+    for keep in (0, n_cols // 2, n_cols):
+        mask = _mask(n_cols, keep, rng)
+        mask_d = torch.from_numpy(mask.view(np.int32)).cuda()
+        ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+        with fused(form):
+            r, c, v, k = _slice(X, mask_d)
+        assert k == len(co), (case, form, keep)
+        assert np.array_equal(r, ro), (case, form, keep)
+        assert np.array_equal(c, co) and np.array_equal(v.view(np.uint32), vo.view(np.uint32)), (case, form, keep)
