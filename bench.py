@@ -565,6 +565,7 @@ def train_bench(args) -> int:
         "exact": results["exact"], "rsc": results["rsc"],
         "ablation": ablation,
         "staleness": staleness,
+        "paper_context": PAPER_CONTEXT,
     }
     print(json.dumps(out), flush=True)
     return 0
