@@ -405,6 +405,29 @@ def test_topk_single_block_boundary(n):
     _topk_case(np.arange(1, n + 1).astype(np.uint64), 777)
 
 
+@pytest.mark.parametrize("m", [16384, 16385])
+def test_topk_candidates_at_the_cap(m):
+    """Above 16,384 keys the first two radix passes (22 bits) leave the keys
+    of the threshold's bin as candidates for one block, which holds up to
+    16,384 of them and otherwise reads every key: exactly m keys share the
+    threshold's 22-bit prefix (with ties among them), the rest lie above and
+    below it."""
+    n = 100_000
+    rng = np.random.default_rng(m)
+    low = np.uint64((1 << 42) - 1)
+    prefix = np.uint64(0x1234A5) << np.uint64(42)
+    mid = prefix | (rng.integers(0, 1 << 20, size=m).astype(np.uint64) << np.uint64(22))  # ties in the low bits
+    mid[: m // 4] = mid[0]
+    rest = n - m
+    above = (np.uint64(0x1234A6) + rng.integers(0, 1000, size=rest // 2).astype(np.uint64)) << np.uint64(42)
+    below = (np.uint64(0x1234A4) - rng.integers(0, 1000, size=rest - rest // 2).astype(np.uint64)) << np.uint64(42)
+    key = np.concatenate([above | (rng.integers(0, 1 << 40, size=rest // 2).astype(np.uint64) & low),
+                          mid, below]).astype(np.uint64)
+    key = key[rng.permutation(n)]
+    for k in (rest // 2 + 1, rest // 2 + m // 8, rest // 2 + m // 2, rest // 2 + m):
+        _topk_case(key, k)
+
+
 def test_topk_on_real_keys():
     A = synth.make_graph("tiny", 0)
     cn2, _ = oracle.col_sqnorms(A.rowptr, A.val)
