@@ -136,6 +136,7 @@ __global__ __launch_bounds__(64) void col_sqnorms_kernel(int32_t n, const int32_
 // in ascending feature order.
 constexpr int kRows = 256;
 constexpr int kTileF = 32;
+typedef float vf4 __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(256) void pair_scores_kernel(const double *__restrict__ cn2,
                                                           const float *__restrict__ B, int32_t n,
@@ -157,8 +158,12 @@ __global__ __launch_bounds__(256) void pair_scores_kernel(const double *__restri
             const int64_t row = row0 + rl;
             const int32_t f = f0 + 4 * fq;
             v[it] = make_float4(0.f, 0.f, 0.f, 0.f);
-            // ld % 4 == 0 and ld >= d, so a float4 starting below d stays in the row
-            if (row < n && f < d) v[it] = *reinterpret_cast<const float4 *>(B + row * ldb + f);
+            // ld % 4 == 0 and ld >= d, so a float4 starting below d stays in the row;
+            // B is read once, so its lines are streamed past the caches
+            if (row < n && f < d) {
+                const vf4 x = __builtin_nontemporal_load(reinterpret_cast<const vf4 *>(B + row * ldb + f));
+                v[it] = make_float4(x.x, x.y, x.z, x.w);
+            }
         }
     };
     double acc = 0.0;
