@@ -52,10 +52,17 @@ static_assert(kGroups == 64, "one wave scans the (chunk, wave) ballots of a tile
 // of the atomics, and the steps need no barrier.
 constexpr int kMaskLdsWords = 39936;  // 156 KB of LDS: 1,277,952 columns per piece
 constexpr int kCountThreads = 1024;
-constexpr int kTilesPerIter = 4;
+constexpr int kTilesPerIterSingle = 4;  // tiles per step, one block per CU
+constexpr int kTilesPerIterPaired = 4;  // tiles per step, paired blocks (8 measured the same)
 constexpr int kCountWaves = kCountThreads / 64;
 static_assert(kTile == kCountThreads * 4, "four entries per thread per tile");
 
+// kPaired (a mask of exactly two pieces): blocks 16 g + x and 16 g + 8 + x
+// (x < 8) form pair 8 g + x; the first holds piece 0, the second piece 1,
+// and both walk the pair's tiles at the same time. Blocks are dispatched to
+// the 8 XCDs round-robin, so the two share an L2 and col is mostly fetched
+// from HBM once; both OR their ballots into tile_bits, which starts cleared.
+template <bool kPaired, int kTilesPerIter>
 __global__ __launch_bounds__(kCountThreads) void slice_count_kernel(const int32_t *__restrict__ col, int64_t nnz,
                                                                     const uint32_t *__restrict__ mask,
                                                                     int32_t n_words, int32_t nt,
@@ -63,7 +70,11 @@ __global__ __launch_bounds__(kCountThreads) void slice_count_kernel(const int32_
                                                                     uint64_t *__restrict__ tile_bits) {
     __shared__ uint32_t s_mask[kMaskLdsWords];
     const int T = threadIdx.x, lane = T & 63, wv = T >> 6;
-    for (int32_t w0 = 0; w0 == 0 || w0 < n_words; w0 += kMaskLdsWords) {
+    const int32_t piece = kPaired ? (int32_t)((blockIdx.x >> 3) & 1) : 0;
+    const int32_t group = kPaired ? (int32_t)((blockIdx.x >> 4) * 8 + (blockIdx.x & 7)) : (int32_t)blockIdx.x;
+    const int32_t groups = kPaired ? (int32_t)(gridDim.x / 2) : (int32_t)gridDim.x;
+    for (int32_t w0 = piece * kMaskLdsWords; w0 == piece * kMaskLdsWords || (!kPaired && w0 < n_words);
+         w0 += kMaskLdsWords) {
         const int32_t words = max(0, min(kMaskLdsWords, n_words - w0));
         __syncthreads();  // the previous piece's lookups are done
         for (int i = T; i < words; i += kCountThreads) s_mask[i] = mask[w0 + i];
@@ -72,7 +83,7 @@ __global__ __launch_bounds__(kCountThreads) void slice_count_kernel(const int32_
         // below 2^31, and the padding value -1 falls outside)
         const int32_t lo = w0 * 32;
         const uint32_t span = (uint32_t)words * 32u;
-        const int32_t stride = gridDim.x * kTilesPerIter;
+        const int32_t stride = groups * kTilesPerIter;
         // the next step's column loads are issued before this step's tests
         // (a step's tiles are consecutive: value (u, i) is entry
         // T + kCountThreads * (4 u + i) from the step's first entry)
@@ -87,11 +98,12 @@ __global__ __launch_bounds__(kCountThreads) void slice_count_kernel(const int32_
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int32_t q = T + kCountThreads * (4 * u + i);
-                    nx[u][i] = q < rem ? __builtin_nontemporal_load(src + q) : -1;
+                    // paired: the partner block reads the same lines from L2
+                    nx[u][i] = q < rem ? (kPaired ? src[q] : __builtin_nontemporal_load(src + q)) : -1;
                 }
         };
-        load(blockIdx.x * kTilesPerIter);
-        for (int32_t t0 = blockIdx.x * kTilesPerIter; t0 < nt; t0 += stride) {
+        load(group * kTilesPerIter);
+        for (int32_t t0 = group * kTilesPerIter; t0 < nt; t0 += stride) {
             int32_t cv[kTilesPerIter][4];
 #pragma unroll
             for (int u = 0; u < kTilesPerIter; ++u)
@@ -119,7 +131,7 @@ __global__ __launch_bounds__(kCountThreads) void slice_count_kernel(const int32_
             if (lane < 4 * kTilesPerIter && t0 + (lane >> 2) < nt) {
                 // group (o >> 6) of tile t0 + u for entries T + kCountThreads * i
                 uint64_t *g = tile_bits + (int64_t)(t0 + (lane >> 2)) * 64 + wv + kCountWaves * (lane & 3);
-                if (w0 == 0)
+                if (w0 == 0 && !kPaired)
                     *g = my_ball;
                 else if (my_ball)
                     atomicOr(reinterpret_cast<unsigned long long *>(g), (unsigned long long)my_ball);
@@ -134,13 +146,17 @@ __global__ __launch_bounds__(kCountThreads) void slice_count_kernel(const int32_
 // (rowptr[i - 1], rowptr[i]] (rowptr[-1] read as -1), so for a well-formed
 // row pointer each tile is written exactly once. The emit reads its rows'
 // range from here instead of two binary searches per tile. The same launch
-// clears the tile counts the count pass adds into.
+// clears the tile counts the count pass adds into (and, for the paired count
+// pass, the ballots).
 __global__ __launch_bounds__(256) void slice_tile_rows_kernel(const int32_t *__restrict__ rowptr, int32_t n_rows,
                                                               int32_t nt, int32_t *__restrict__ tile_row,
-                                                              uint32_t *__restrict__ tile_cnt) {
+                                                              uint32_t *__restrict__ tile_cnt,
+                                                              uint64_t *__restrict__ tile_bits_to_clear) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t first = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     for (int64_t t = first; t < nt; t += stride) tile_cnt[t] = 0;
+    if (tile_bits_to_clear)
+        for (int64_t t = first; t < (int64_t)nt * kGroups; t += stride) tile_bits_to_clear[t] = 0;
     for (int64_t i = first; i <= n_rows; i += stride) {
         const int64_t a = i == 0 ? -1 : (int64_t)rowptr[i - 1];
         const int64_t b = rowptr[i];
@@ -468,6 +484,13 @@ bool mask_in_lds(int32_t n_words) {
 // three launches against single pass: tiny 21 / 26 us, social 344-393 /
 // 372-403 us, protein 250 / 281 us, gcn2 72 / 114 us, copurchase 503 /
 // 787 us). RSC_SLICE_FUSED = 1 / 0 forces the single-pass / three-launch form.
+// RSC_SLICE_PAIRED = 0 makes a two-piece mask walk col twice with one block
+// per CU instead of in pairs.
+bool paired_count() {
+    if (const char *env = getenv("RSC_SLICE_PAIRED")) return atoi(env) != 0;
+    return true;
+}
+
 bool use_fused() {
     if (const char *env = getenv("RSC_SLICE_FUSED")) return atoi(env) != 0;
     return false;
@@ -524,11 +547,23 @@ hipError_t slice_launch(int32_t n_rows, int32_t n_cols, int64_t nnz, const int32
                 capacity, nnz_out, ticket + 1, colw);
         return hipGetLastError();
     }
+    // a mask of two LDS pieces is tested by pairs of blocks (one piece each,
+    // the same tiles at the same time), given whole groups of 16 blocks
+    const int32_t n_pieces = (int32_t)ceil_div(std::max<int32_t>(n_words, 1), kMaskLdsWords);
+    const int64_t pair_grid = std::min<int64_t>(cus, 2 * ceil_div(nt, kTilesPerIterPaired)) / 16 * 16;
+    const bool paired = n_pieces == 2 && pair_grid >= 16 && paired_count();
     slice_tile_rows_kernel<<<(unsigned)std::min<int64_t>(ceil_div(std::max<int64_t>((int64_t)n_rows + 1, nt), 256),
                                                          4096),
-                             256, 0, stream>>>(rowptr, n_rows, nt, tile_row, tile_cnt);
-    const unsigned cgrid = (unsigned)std::max<int64_t>(1, std::min<int64_t>(cus, ceil_div(nt, kTilesPerIter)));
-    slice_count_kernel<<<cgrid, kCountThreads, 0, stream>>>(col, nnz, mask, n_words, nt, tile_cnt, tile_bits);
+                             256, 0, stream>>>(rowptr, n_rows, nt, tile_row, tile_cnt, paired ? tile_bits : nullptr);
+    if (paired) {
+        slice_count_kernel<true, kTilesPerIterPaired><<<(unsigned)pair_grid, kCountThreads, 0, stream>>>(
+            col, nnz, mask, n_words, nt, tile_cnt, tile_bits);
+    } else {
+        const unsigned cgrid =
+            (unsigned)std::max<int64_t>(1, std::min<int64_t>(cus, ceil_div(nt, kTilesPerIterSingle)));
+        slice_count_kernel<false, kTilesPerIterSingle><<<cgrid, kCountThreads, 0, stream>>>(
+            col, nnz, mask, n_words, nt, tile_cnt, tile_bits);
+    }
     slice_scan_kernel<<<1, 1024, 0, stream>>>(nt, tile_cnt, tile_off, nnz_out);
     slice_emit_kernel<<<nt, 256, 0, stream>>>(rowptr, n_rows, col, val, nnz, tile_bits, tile_off, tile_row,
                                               rowptr_out, col_out, val_out, capacity, colw);
