@@ -252,7 +252,9 @@ rsc_status_t rsc_topk_select(const uint64_t *key, int32_t n, int32_t k, int32_t 
  * value becomes fl32(val * colw[col]) (fp64 product, one rounding), as the
  * randomized sampler's 1/(k p) weighting needs.
  * nnz_out: device int64 receiving nnz'. The slice runs as a stream
- * compaction in four launches (a tile-to-row table, count, scan, emit);
+ * compaction in four launches (a tile-to-row table, count, scan, emit;
+ * RSC_SLICE_PAIRED=0 turns off the count's block pairing for masks of
+ * 1.28M to 2.56M columns, which changes only its speed);
  * with the environment variable RSC_SLICE_FUSED=1 it runs as one fused
  * kernel instead (count, a decoupled look-back scan over tiles taken in
  * ticket order, compaction). Both give the same bytes. The fused kernel's
