@@ -170,3 +170,41 @@ def test_rows_on_tile_edges(case, form):
         assert k == len(co), (case, form, keep)
         assert np.array_equal(r, ro), (case, form, keep)
         assert np.array_equal(c, co) and np.array_equal(v.view(np.uint32), vo.view(np.uint32)), (case, form, keep)
+
+
+class paired:
+    def __init__(self, value):
+        self.value = value
+
+    def __enter__(self):
+        self.old = os.environ.get("RSC_SLICE_PAIRED")
+        os.environ["RSC_SLICE_PAIRED"] = str(self.value)
+
+    def __exit__(self, *exc):
+        if self.old is None:
+            os.environ.pop("RSC_SLICE_PAIRED", None)
+        else:
+            os.environ["RSC_SLICE_PAIRED"] = self.old
+
+
+@pytest.mark.parametrize("n_rows,mean_len", [(60_000, 40), (500, 20)])
+def test_two_piece_mask_paired_and_unpaired(n_rows, mean_len):
+    """A mask of two LDS pieces (2,000,003 columns): the count pass by pairs
+    of blocks (one piece each; the default when the tiles fill 16 blocks)
+    and by one block per CU walking col twice give the same bytes as the
+    oracle; the small case has too few tiles to pair."""
+    n_cols = 2_000_003
+    rng = np.random.default_rng(n_rows)
+    A = synth.bucket_csr(rng.integers(0, 2 * mean_len, n_rows), n_cols, seed=21)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
+    mask = np.zeros((n_cols + 31) // 32, np.uint32)
+    keep = rng.choice(n_cols, n_cols * 3 // 10, replace=False)
+    np.bitwise_or.at(mask, keep >> 5, (np.uint32(1) << (keep & 31).astype(np.uint32)))
+    mask_d = torch.from_numpy(mask.view(np.int32)).cuda()
+    ro, co, vo = oracle.slice_csr(A.rowptr, A.col, A.val, mask)
+    for p in (1, 0):
+        with paired(p):
+            r, c, v, k = _slice(X, mask_d)
+        assert k == len(co), p
+        assert np.array_equal(r, ro) and np.array_equal(c, co), p
+        assert np.array_equal(v.view(np.uint32), vo.view(np.uint32)), p
