@@ -3,23 +3,19 @@
 //
 // 1. Radix select of the threshold T = the k-th largest key, most significant
 //    digit first: 6 passes of 11/11/11/11/10/10 bits. Each pass builds a
-//    histogram of the digit over the keys that match the prefix chosen so
-//    far and picks the digit that holds the k-th key. The first two passes
-//    run grid-wide (LDS histograms, then integer atomics into global bins; a
-//    one-block kernel picks the first digit). After them, the keys that
-//    match the 22-bit prefix are few for any spread of values (the count is
-//    the picked bin's): one kernel compacts each 2048-key chunk's matches
-//    into a segment of its own, and a single block gathers them into LDS and
-//    finishes the last four passes there. If more
-//    than kCandCap keys share the prefix (heavy ties), the same block runs
-//    the four passes over all keys instead. After the last pass T is known,
-//    and r = the number of keys equal to T that must be kept (G = k - r keys
-//    are strictly above T).
-// 2. Tiles of 4096 keys count (== T) and (> T); one block scans the tile
-//    counts; a third kernel keeps key i iff key > T, or key == T and fewer
-//    than r equal keys precede it, writing mask words from wave ballots and
-//    idx at the running count of kept keys. Everything is integer, so the
-//    result is exact and deterministic.
+//    grid-wide histogram of the digit over the keys that match the prefix
+//    chosen so far (LDS histograms, then integer atomics into global bins).
+//    The digit that holds the k-th key is picked at the start of the next
+//    kernel: every block reads the finished histogram and makes the same
+//    pick (a wave-shuffle scan over the bins), and its first block records
+//    the state after it, one slot per pass, so no kernel of its own is
+//    needed. After the last pass T is known, and r = the number of keys
+//    equal to T that must be kept (G = k - r keys are strictly above T).
+// 2. Tiles of 4096 keys count (== T) and (> T) (their kernel makes the last
+//    pick); one block scans the tile counts; a third kernel keeps key i iff
+//    key > T, or key == T and fewer than r equal keys precede it, writing
+//    mask words from wave ballots and idx at the running count of kept keys.
+//    Everything is integer, so the result is exact and deterministic.
 // Up to 16,384 keys the whole selection runs in one block with the keys in
 // LDS (one launch; the small graphs are launch-bound).
 #include "rsc_internal.h"
@@ -44,51 +40,113 @@ struct TopkState {
     uint64_t prefix;  // digits of T fixed so far
     uint64_t pmask;   // which bits of prefix are fixed
     int64_t k_rem;    // how many keys among those matching prefix remain to be taken
-    int64_t count;    // keys matching prefix (the picked bin's count)
-    int64_t pad[28];
+    int64_t pad;
 };
 
-// Keys sharing the 22-bit prefix of the first two passes that the finishing
-// block takes into LDS; more than this and it reads all keys instead.
-constexpr int kCandCap = 16384;
-
+// st[p] = the state after p picks (st[0] initial, st[kPasses] final: prefix
+// = T, k_rem = r); the histogram of pass p is hist[p % 3] (pass p reads
+// pass p - 1's and clears pass p + 1's, three distinct buffers).
 struct TopkWs {
-    TopkState st;
-    uint32_t hist[2][kBins];
+    TopkState st[kPasses + 1];
+    uint32_t hist[3][kBins];
 };
-// After the header (workspace layout, each part 256-byte aligned): the
-// candidate segments (one slot per key: chunk c's matches sit compacted at
-// the start of [c * kChunk, (c + 1) * kChunk)), the per-chunk match counts,
-// then the tile arrays of step 2.
-constexpr int kChunk = 2048;  // keys per collect block: 256 threads x 8
 
-__global__ __launch_bounds__(256) void topk_init_kernel(TopkState *st, uint32_t *hist0, int64_t k) {
-    for (int b = threadIdx.x; b < kBins; b += blockDim.x) hist0[b] = 0;
+struct PickOut {
+    uint64_t prefix, pmask;
+    int64_t k_rem, count;
+};
+
+// One block of 256 threads picks the digit of `pass` from histogram h,
+// starting from state *sp: thread t owns the bins nb-1-t*per .. nb-per-t*per
+// (descending), and an exclusive scan over threads (within each wave by
+// shuffles, then over the four wave totals) gives the count of keys in
+// higher bins. Every thread gets the new state.
+__device__ void block_pick_256(const TopkState *sp, const uint32_t *h, int pass, uint64_t &prefix, uint64_t &pmask,
+                               int64_t &k_rem, int64_t *wsum, PickOut *s_out) {
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    const int shift = kShift[pass];
+    const int nb = 1 << kWidth[pass];
+    const int per = nb / 256;  // 8 or 4
+    uint32_t hv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) hv[j] = j < per ? h[nb - 1 - (t * per + j)] : 0u;
+    prefix = sp->prefix;
+    pmask = sp->pmask;
+    k_rem = sp->k_rem;
+    int64_t s = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s += hv[j];
+    int64_t incl = s;
+    for (int off = 1; off < 64; off <<= 1) {
+        const int64_t x = __shfl_up(incl, off);
+        if (lane >= off) incl += x;
+    }
+    if (lane == 63) wsum[w] = incl;
+    __syncthreads();
+    int64_t run = incl - s;  // keys in bins above this thread's range
+    for (int u = 0; u < w; ++u) run += wsum[u];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int64_t c = hv[j];
+        if (j < per && run < k_rem && run + c >= k_rem) {  // exactly one (thread, bin) satisfies this
+            const int b = nb - 1 - (t * per + j);
+            s_out->prefix = prefix | ((uint64_t)b << shift);
+            s_out->pmask = pmask | ((uint64_t)(nb - 1) << shift);
+            s_out->k_rem = k_rem - run;
+        }
+        run += c;
+    }
+    __syncthreads();
+    prefix = s_out->prefix;
+    pmask = s_out->pmask;
+    k_rem = s_out->k_rem;
+}
+
+__global__ __launch_bounds__(256) void topk_init_kernel(TopkWs *h, int64_t k) {
+    for (int b = threadIdx.x; b < kBins; b += blockDim.x) h->hist[0][b] = 0;
     if (threadIdx.x == 0) {
-        st->prefix = 0;
-        st->pmask = 0;
-        st->k_rem = k;
-        st->count = 0;
+        h->st[0].prefix = 0;
+        h->st[0].pmask = 0;
+        h->st[0].k_rem = k;
     }
 }
 
-__global__ __launch_bounds__(256) void topk_hist_kernel(const uint64_t *__restrict__ key, int32_t n,
-                                                        const TopkState *__restrict__ st,
-                                                        uint32_t *__restrict__ hist, int pass) {
+// Pass p: the pick of pass p - 1 (from its finished histogram; the first
+// block records the state in st[p]), the clearing of pass p + 1's histogram,
+// then this pass's histogram over the keys that match the prefix.
+__global__ __launch_bounds__(256) void topk_hist_kernel(const uint64_t *__restrict__ key, int32_t n, TopkWs *ws,
+                                                        int pass) {
     __shared__ uint32_t lh[kBins];
+    __shared__ int64_t wsum[4];
+    __shared__ PickOut s_out;
     const int shift = kShift[pass];
     const uint64_t dmask = (1ull << kWidth[pass]) - 1ull;
     for (int b = threadIdx.x; b < kBins; b += blockDim.x) lh[b] = 0;
-    __syncthreads();
-    const uint64_t prefix = st->prefix, pmask = st->pmask;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    // eight keys per thread loaded before any is counted, then the rest one
-    // at a time
-    for (; i + 7 * stride < n; i += 8 * stride) {
-        uint64_t k[8];
+    // eight keys per thread loaded before any is counted (the first eight
+    // before the pick, so the two waits overlap), then the rest one at a time
+    uint64_t k[8];
+    bool more = i + 7 * stride < n;
+    if (more) {
 #pragma unroll
         for (int u = 0; u < 8; ++u) k[u] = key[i + u * stride];
+    }
+    uint64_t prefix = ws->st[0].prefix, pmask = ws->st[0].pmask;
+    if (pass > 0) {
+        int64_t k_rem;
+        block_pick_256(&ws->st[pass - 1], ws->hist[(pass - 1) % 3], pass - 1, prefix, pmask, k_rem, wsum, &s_out);
+        if (blockIdx.x == 0 && threadIdx.x == 0) {
+            ws->st[pass].prefix = prefix;
+            ws->st[pass].pmask = pmask;
+            ws->st[pass].k_rem = k_rem;
+        }
+    }
+    if (blockIdx.x == 0)
+        for (int b = threadIdx.x; b < kBins; b += blockDim.x) ws->hist[(pass + 1) % 3][b] = 0;
+    __syncthreads();  // lh cleared
+    uint32_t *hist = ws->hist[pass % 3];
+    while (more) {
         if (pass == 0) {  // block-uniform
             // the top digit is nearly constant over the keys: a wave whose
             // keys all share one digit adds them with one LDS atomic
@@ -107,6 +165,12 @@ __global__ __launch_bounds__(256) void topk_hist_kernel(const uint64_t *__restri
             for (int u = 0; u < 8; ++u)
                 if ((k[u] & pmask) == prefix) atomicAdd(&lh[(k[u] >> shift) & dmask], 1u);
         }
+        i += 8 * stride;
+        more = i + 7 * stride < n;
+        if (more) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) k[u] = key[i + u * stride];
+        }
     }
     for (; i < n; i += stride) {
         const uint64_t k = key[i];
@@ -117,60 +181,37 @@ __global__ __launch_bounds__(256) void topk_hist_kernel(const uint64_t *__restri
         if (lh[b]) atomicAdd(&hist[b], lh[b]);
 }
 
-// One block of 256 threads. Thread t owns the bins nb-1-t*per .. nb-per-t*per
-// (descending); an exclusive scan over threads (within each wave by
-// shuffles, then over the four wave totals) gives the count of keys in
-// higher bins.
-__global__ __launch_bounds__(256) void topk_pick_kernel(TopkState *st, const uint32_t *__restrict__ hist,
-                                                        uint32_t *__restrict__ hist_next, int pass) {
-    __shared__ int64_t wsum[4];
-    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-    // read before any thread updates the state (the scan's barrier orders it)
-    const int64_t k_rem = st->k_rem;
-    const int shift = kShift[pass];
-    const int nb = 1 << kWidth[pass];
-    const int per = nb / 256;
-    int64_t s = 0;
-    for (int j = 0; j < per; ++j) s += hist[nb - 1 - (t * per + j)];
-    int64_t incl = s;
-    for (int off = 1; off < 64; off <<= 1) {
-        const int64_t x = __shfl_up(incl, off);
-        if (lane >= off) incl += x;
-    }
-    if (lane == 63) wsum[w] = incl;
-    __syncthreads();
-    int64_t run = incl - s;  // keys in bins above this thread's range
-    for (int u = 0; u < w; ++u) run += wsum[u];
-    for (int j = 0; j < per; ++j) {
-        const int b = nb - 1 - (t * per + j);
-        const int64_t c = hist[b];
-        if (run < k_rem && run + c >= k_rem) {  // exactly one (thread, bin) satisfies this
-            st->prefix |= (uint64_t)b << shift;
-            st->pmask |= (uint64_t)(nb - 1) << shift;
-            st->k_rem = k_rem - run;
-            st->count = c;
-        }
-        run += c;
-    }
-    for (int b = t; b < kBins; b += 256) hist_next[b] = 0;
-}
-
+// Also makes the last pass's pick (every block; the first records the final
+// state, T and r, for the scan and the emit).
 __global__ __launch_bounds__(256) void topk_tile_count_kernel(const uint64_t *__restrict__ key,
-                                                              int32_t n,
-                                                              const TopkState *__restrict__ st,
+                                                              int32_t n, TopkWs *ws,
                                                               uint32_t *__restrict__ tile_eq,
                                                               uint32_t *__restrict__ tile_gt) {
     __shared__ uint32_t s_eq[4], s_gt[4];
-    const uint64_t T = st->prefix;
+    __shared__ int64_t wsum[4];
+    __shared__ PickOut s_out;
+    // the tile's keys are loaded before the pick, so the two waits overlap
     const int64_t ts = (int64_t)blockIdx.x * kTile;
-    uint32_t eq = 0, gt = 0;
+    uint64_t kv[kTile / 256];
+#pragma unroll
     for (int j = 0; j < kTile / 256; ++j) {
         const int64_t i = ts + threadIdx.x + 256 * j;
-        if (i < n) {
-            const uint64_t k = key[i];
-            eq += k == T;
-            gt += k > T;
-        }
+        kv[j] = i < n ? key[i] : 0ull;
+    }
+    uint64_t T, pmask;
+    int64_t r;
+    block_pick_256(&ws->st[kPasses - 1], ws->hist[(kPasses - 1) % 3], kPasses - 1, T, pmask, r, wsum, &s_out);
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        ws->st[kPasses].prefix = T;
+        ws->st[kPasses].pmask = pmask;
+        ws->st[kPasses].k_rem = r;
+    }
+    uint32_t eq = 0, gt = 0;
+#pragma unroll
+    for (int j = 0; j < kTile / 256; ++j) {
+        const bool in = ts + threadIdx.x + 256 * j < n;
+        eq += in && kv[j] == T;
+        gt += in && kv[j] > T;
     }
     for (int off = 32; off > 0; off >>= 1) {
         eq += __shfl_down(eq, off);
@@ -211,11 +252,6 @@ __device__ int64_t block_exclusive_scan_1024(int64_t v, int64_t *sh, int64_t *to
 // (nb bins; LDS or global): thread t owns bins nb-1-(t*per+j), descending,
 // and the exclusive scan gives the keys in all higher bins. Updates
 // prefix/pmask/k_rem for every thread and returns the picked bin's count.
-struct PickOut {
-    uint64_t prefix, pmask;
-    int64_t k_rem, count;
-};
-
 __device__ int64_t block_pick_1024(const uint32_t *h, int pass, uint64_t &prefix, uint64_t &pmask, int64_t &k_rem,
                                    int64_t *s_scan, PickOut *s_out) {
     const int t = threadIdx.x;
@@ -386,113 +422,6 @@ __global__ __launch_bounds__(kSmallThreads) void topk_small_kernel(const uint64_
     if ((t & 1) == 0 && word < ((int64_t)n + 31) / 32) mask[word] = bits | (hi16 << 16);
 }
 
-// Block c takes keys [c * kChunk, (c + 1) * kChunk) and, if the keys that
-// match the 22-bit prefix of the first two passes number at most kCandCap
-// (the picked bin's count, recorded by the second pick), writes its matches
-// compacted at the start of its segment and their number to chunk_cnt[c].
-// No atomics: the finishing block scans the counts and gathers.
-__global__ __launch_bounds__(256) void topk_collect_kernel(const uint64_t *__restrict__ key, int32_t n,
-                                                           const TopkState *__restrict__ st,
-                                                           uint64_t *__restrict__ seg,
-                                                           uint32_t *__restrict__ chunk_cnt) {
-    __shared__ uint32_t s_wave[4];
-    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-    if (st->count > kCandCap) return;  // grid-uniform: the finishing block reads all keys
-    const uint64_t prefix = st->prefix, pmask = st->pmask;
-    const int64_t base = (int64_t)blockIdx.x * kChunk;
-    constexpr int kPer = kChunk / 256;
-    uint64_t kv[kPer];
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {  // all loads before any test
-        const int64_t i = base + t + 256 * u;
-        kv[u] = i < n ? key[i] : 0ull;
-    }
-    uint64_t bal[kPer];
-    uint32_t wtot = 0;
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-        bal[u] = __ballot(base + t + 256 * u < n && (kv[u] & pmask) == prefix);
-        wtot += (uint32_t)__popcll(bal[u]);
-    }
-    if (lane == 0) s_wave[w] = wtot;
-    __syncthreads();
-    if (t == 0) chunk_cnt[blockIdx.x] = s_wave[0] + s_wave[1] + s_wave[2] + s_wave[3];
-    uint32_t pos = 0;
-    for (int v = 0; v < w; ++v) pos += s_wave[v];
-    const uint64_t below = (1ull << lane) - 1ull;
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-        if ((bal[u] >> lane) & 1ull) seg[base + pos + (uint32_t)__popcll(bal[u] & below)] = kv[u];
-        pos += (uint32_t)__popcll(bal[u]);
-    }
-}
-
-// One block of 1024 threads: passes 2-5 over the candidate list in LDS (or,
-// with more than kCandCap candidates, over all keys), and the final state:
-// T = prefix, r = k_rem.
-__global__ __launch_bounds__(kSmallThreads) void topk_finish_kernel(const uint64_t *__restrict__ key, int32_t n,
-                                                                    TopkState *st,
-                                                                    const uint64_t *__restrict__ seg,
-                                                                    const uint32_t *__restrict__ chunk_cnt) {
-    __shared__ uint64_t s_key[kCandCap];
-    __shared__ uint32_t s_hist[kBins];
-    __shared__ int64_t s_scan[kSmallThreads / 64];
-    __shared__ PickOut s_out;
-    const int t = threadIdx.x;
-    uint64_t prefix = st->prefix, pmask = st->pmask;
-    int64_t k_rem = st->k_rem;
-    const int64_t c1 = st->count;
-    const bool in_lds = c1 <= kCandCap;  // block-uniform
-    if (in_lds) {
-        // thread t gathers the matches of chunks [t * per, (t + 1) * per) to
-        // their place in the list: an exclusive scan of the chunk counts
-        const int32_t chunks = (n + kChunk - 1) / kChunk;
-        const int32_t per = (chunks + kSmallThreads - 1) / kSmallThreads;
-        const int32_t lo = min(chunks, t * per), hi = min(chunks, lo + per);
-        int64_t mine = 0;
-        for (int32_t c = lo; c < hi; ++c) mine += chunk_cnt[c];
-        int64_t total;
-        int64_t at = block_exclusive_scan_1024(mine, s_scan, &total);
-        for (int32_t c = lo; c < hi; ++c) {
-            const uint32_t m = chunk_cnt[c];
-            const uint64_t *src = seg + (int64_t)c * kChunk;
-            for (uint32_t j0 = 0; j0 < m; j0 += 8) {  // eight loads in flight
-                uint64_t v[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) v[u] = j0 + u < m ? src[j0 + u] : 0ull;
-#pragma unroll
-                for (int u = 0; u < 8; ++u)
-                    if (j0 + u < m && at + j0 + u < kCandCap) s_key[at + j0 + u] = v[u];
-            }
-            at += m;
-        }
-    }
-    for (int pass = 2; pass < kPasses; ++pass) {
-        const int shift = kShift[pass];
-        const uint64_t dmask = (1ull << kWidth[pass]) - 1ull;
-        for (int b = t; b < kBins; b += kSmallThreads) s_hist[b] = 0;
-        __syncthreads();  // candidates loaded (first pass), histogram cleared
-        if (in_lds) {
-            for (int64_t i = t; i < c1; i += kSmallThreads) {
-                const uint64_t kv = s_key[i];
-                if ((kv & pmask) == prefix) atomicAdd(&s_hist[(kv >> shift) & dmask], 1u);
-            }
-        } else {
-            for (int64_t i = t; i < n; i += kSmallThreads) {
-                const uint64_t kv = key[i];
-                if ((kv & pmask) == prefix) atomicAdd(&s_hist[(kv >> shift) & dmask], 1u);
-            }
-        }
-        __syncthreads();
-        block_pick_1024(s_hist, pass, prefix, pmask, k_rem, s_scan, &s_out);
-    }
-    if (t == 0) {
-        st->prefix = prefix;
-        st->pmask = pmask;
-        st->k_rem = k_rem;
-    }
-}
-
 __global__ __launch_bounds__(256) void fill_u32_kernel(uint32_t *p, int64_t count, uint32_t v) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
          i += (int64_t)gridDim.x * blockDim.x)
@@ -502,11 +431,8 @@ __global__ __launch_bounds__(256) void fill_u32_kernel(uint32_t *p, int64_t coun
 }  // namespace
 
 size_t topk_ws_bytes(int32_t n) {
-    const size_t nn = (size_t)std::max<int32_t>(n, 1);
-    const size_t nt = (size_t)ceil_div((int64_t)nn, kTile);
-    const size_t chunks = (size_t)ceil_div((int64_t)nn, kChunk);
-    return align_up(sizeof(TopkWs), 256) + align_up(nn * sizeof(uint64_t), 256) +
-           align_up(chunks * sizeof(uint32_t), 256) + 4 * align_up(nt * sizeof(uint32_t), 256);
+    const size_t nt = (size_t)ceil_div(std::max<int32_t>(n, 1), kTile);
+    return align_up(sizeof(TopkWs), 256) + 4 * align_up(nt * sizeof(uint32_t), 256);
 }
 
 hipError_t topk_launch(const uint64_t *key, int32_t n, int32_t k, int32_t *idx, uint32_t *mask,
@@ -524,35 +450,28 @@ hipError_t topk_launch(const uint64_t *key, int32_t n, int32_t k, int32_t *idx, 
     }
     TopkWs *h = static_cast<TopkWs *>(ws);
     const int32_t nt = (int32_t)ceil_div(n, kTile);
-    const int32_t chunks = (int32_t)ceil_div(n, kChunk);
     char *p = static_cast<char *>(ws) + align_up(sizeof(TopkWs), 256);
-    uint64_t *seg = reinterpret_cast<uint64_t *>(p);
-    p += align_up((size_t)n * sizeof(uint64_t), 256);
-    uint32_t *chunk_cnt = reinterpret_cast<uint32_t *>(p);
-    p += align_up((size_t)chunks * sizeof(uint32_t), 256);
     const size_t tb = align_up((size_t)nt * sizeof(uint32_t), 256);
     uint32_t *tile_eq = reinterpret_cast<uint32_t *>(p);
     uint32_t *tile_gt = reinterpret_cast<uint32_t *>(p + tb);
     uint32_t *eq_before = reinterpret_cast<uint32_t *>(p + 2 * tb);
     uint32_t *sel_before = reinterpret_cast<uint32_t *>(p + 3 * tb);
 
-    topk_init_kernel<<<1, 256, 0, stream>>>(&h->st, h->hist[0], k);
+    topk_init_kernel<<<1, 256, 0, stream>>>(h, k);
     // Each block flushes its non-empty bins with one global atomic each. The
-    // two grid-wide passes count every key, into a few bins (pass 0) or into
+    // first two passes count every key, into a few bins (pass 0) or into
     // most of them (pass 1), so they run on 256 and 128 blocks to keep those
     // atomics few (measured on 2.45M keys: 12.4 and 9.5 us, against 18.9 and
-    // 29.6 with eight keys per thread).
+    // 29.6 with eight keys per thread); later passes count only the keys
+    // under the chosen prefix and take eight keys per thread, for more loads
+    // in flight.
     const unsigned hgrid_wide = (unsigned)std::min<int64_t>(ceil_div(n, 256 * 8), 2048);
     const unsigned hgrid_pass[2] = {std::min(hgrid_wide, 256u), std::min(hgrid_wide, 128u)};
-    topk_hist_kernel<<<hgrid_pass[0], 256, 0, stream>>>(key, n, &h->st, h->hist[0], 0);
-    topk_pick_kernel<<<1, 256, 0, stream>>>(&h->st, h->hist[0], h->hist[1], 0);
-    topk_hist_kernel<<<hgrid_pass[1], 256, 0, stream>>>(key, n, &h->st, h->hist[1], 1);
-    topk_pick_kernel<<<1, 256, 0, stream>>>(&h->st, h->hist[1], h->hist[0], 1);
-    topk_collect_kernel<<<chunks, 256, 0, stream>>>(key, n, &h->st, seg, chunk_cnt);
-    topk_finish_kernel<<<1, kSmallThreads, 0, stream>>>(key, n, &h->st, seg, chunk_cnt);
-    topk_tile_count_kernel<<<nt, 256, 0, stream>>>(key, n, &h->st, tile_eq, tile_gt);
-    topk_tile_scan_kernel<<<1, 1024, 0, stream>>>(nt, &h->st, tile_eq, tile_gt, eq_before, sel_before);
-    topk_emit_kernel<<<nt, 256, 0, stream>>>(key, n, &h->st, eq_before, sel_before, idx, mask, k);
+    for (int pass = 0; pass < kPasses; ++pass)
+        topk_hist_kernel<<<pass < 2 ? hgrid_pass[pass] : hgrid_wide, 256, 0, stream>>>(key, n, h, pass);
+    topk_tile_count_kernel<<<nt, 256, 0, stream>>>(key, n, h, tile_eq, tile_gt);
+    topk_tile_scan_kernel<<<1, 1024, 0, stream>>>(nt, &h->st[kPasses], tile_eq, tile_gt, eq_before, sel_before);
+    topk_emit_kernel<<<nt, 256, 0, stream>>>(key, n, &h->st[kPasses], eq_before, sel_before, idx, mask, k);
     return hipGetLastError();
 }
 

@@ -407,10 +407,9 @@ def test_topk_single_block_boundary(n):
 
 @pytest.mark.parametrize("m", [16384, 16385])
 def test_topk_candidates_at_the_cap(m):
-    """Above 16,384 keys the first two radix passes (22 bits) leave the keys
-    of the threshold's bin as candidates for one block, which holds up to
-    16,384 of them and otherwise reads every key: exactly m keys share the
-    threshold's 22-bit prefix (with ties among them), the rest lie above and
+    """Keys crowded into the threshold's 22-bit bin after the first two
+    radix passes, so the last four passes resolve T among them: exactly m
+    keys share that prefix (with ties among them), the rest lie above and
     below it."""
     n = 100_000
     rng = np.random.default_rng(m)
