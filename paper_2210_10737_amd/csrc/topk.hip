@@ -173,8 +173,8 @@ __global__ __launch_bounds__(256) void topk_hist_kernel(const uint64_t *__restri
         }
     }
     for (; i < n; i += stride) {
-        const uint64_t k = key[i];
-        if ((k & pmask) == prefix) atomicAdd(&lh[(k >> shift) & dmask], 1u);
+        const uint64_t kv = key[i];
+        if ((kv & pmask) == prefix) atomicAdd(&lh[(kv >> shift) & dmask], 1u);
     }
     __syncthreads();
     for (int b = threadIdx.x; b < (1 << kWidth[pass]); b += blockDim.x)
