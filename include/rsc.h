@@ -106,10 +106,11 @@ rsc_status_t rsc_csr_validate(const rsc_csr_t *A, int64_t *bad_row_host, hipStre
  * summation order. Rows may be
  * taken longest first (when rows are long on average; RSC_SPMM_ORDER = 0/1
  * overrides), which never changes a result. Column-blocked mode: when a
- * 64-float slice of B spans 2..8 ranges of about 4.5 MiB and rows hold at
- * least 64 entries per range on average, the columns are cut into P equal
- * index ranges processed one after another (the gathered B rows then stay
- * in L2); each row's entries in one range are summed as above and rounded
+ * 64-float slice of B spans 2..16 ranges of about 4.5 MiB and rows hold at
+ * least 56 entries per range on average, the columns are cut into
+ * P = min(8, ranges) equal index ranges processed one after another (the
+ * gathered B rows then stay in L2, or mostly so for ranges of up to two L2
+ * sizes); each row's entries in one range are summed as above and rounded
  * to an fp32 partial, and the P partials are added in fp64 in range order
  * and rounded once (RSC_SPMM_BLOCKED = 0 switches it off, 2..8 forces that
  * P). Deterministic: equal arguments give bitwise equal Y, and

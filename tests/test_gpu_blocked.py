@@ -1,7 +1,8 @@
 """Column-blocked SpMM mode (the columns cut into P index ranges processed
 one after another, partial rows added in fixed range order). Forced with
 RSC_SPMM_BLOCKED = 2..8 on seeded random shapes, and chosen automatically on
-a graph whose B slice spans two L2-sized ranges: exact and sampled SpMM
+graphs whose B slice spans 2, 9 (capped to 8) and 17 (not blocked) L2-sized
+ranges: exact and sampled SpMM
 against the oracle, a full-budget slice equal to the exact product bit for
 bit, and the automatic choice equal to the forced one."""
 import os
@@ -135,6 +136,41 @@ def test_automatic_choice_on_long_rows():
     rows = np.arange(0, n, 97, dtype=np.int32)
     Yo, S = oracle.spmm(A.rowptr, A.col, A.val, B, rows=rows, with_mag=True)
     assert rel_err(Y.cpu().numpy()[rows], Yo, S) <= 1e-5
+
+
+@pytest.mark.parametrize("n_cols,P", [(160_000, 8), (300_000, 0)])
+def test_automatic_range_count_is_capped(n_cols, P):
+    # A 64-float slice of B over 160,000 columns (41 MB) spans 9 ranges of
+    # 4.5 MiB: the rule takes P = 8 (rows of 500 entries hold 62 per range).
+    # Over 300,000 columns it spans 17, beyond the cap of 16: not blocked.
+    # The automatic choice equals the forced one bit for bit; a plan and a
+    # full-budget slice reproduce it.
+    n_rows, d = 2000, 96
+    A = synth.bucket_csr(np.full(n_rows, 500), n_cols, seed=31)
+    AT = synth.transpose(A, n_cols)
+    B = synth.dense_normal(n_cols, d, seed=32)
+    Bd = torch.from_numpy(B).cuda()
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
+    XT = rsc.DeviceCsr.from_host(AT.rowptr, AT.col, AT.val, n_rows)
+    with blocked(None):
+        Y = rsc.spmm(X, Bd)
+        plan = rsc.SpmmPlan(X)
+        Yp = plan.run(Bd)
+        plan.close()
+        cache = rsc.Cache(X, XT)
+        cache.refresh(Bd, n_cols, step=0)
+        Yk = cache.spmm_sampled(Bd)
+        cache.close()
+    with blocked(P):
+        Yf = rsc.spmm(X, Bd)
+    with blocked(0 if P else 8):
+        Yo_mode = rsc.spmm(X, Bd)
+    torch.cuda.synchronize()
+    assert torch.equal(Y, Yf), P               # the automatic mode took this P
+    assert not torch.equal(Y, Yo_mode), P      # and not the other mode
+    assert torch.equal(Yp, Y) and torch.equal(Yk, Y)
+    Yo, S = oracle.spmm(A.rowptr, A.col, A.val, B, with_mag=True)
+    assert rel_err(Y.cpu().numpy(), Yo, S) <= 1e-5
 
 
 @pytest.mark.parametrize("n_rows,n_cols,row_len,d", [
