@@ -105,12 +105,14 @@ rsc_status_t rsc_csr_validate(const rsc_csr_t *A, int64_t *bad_row_host, hipStre
  * RSC_SPMM_SLICE = 16/32/64/128/256 as an override); the layout sets the
  * summation order. Rows may be
  * taken longest first (when rows are long on average; RSC_SPMM_ORDER = 0/1
- * overrides), which never changes a result. Column-blocked mode: when a
- * 64-float slice of B spans 2..16 ranges of about 4.5 MiB and rows hold at
- * least 56 entries per range on average, the columns are cut into
- * P = min(8, ranges) equal index ranges processed one after another (the
- * gathered B rows then stay in L2, or mostly so for ranges of up to two L2
- * sizes); each row's entries in one range are summed as above and rounded
+ * overrides), which never changes a result. Column-blocked mode: the
+ * features are taken in passes of 16, 32 or 64 floats (the narrowest that
+ * holds d; wider d in 64-float passes); when that slice of the referenced B
+ * rows spans 2..16 ranges of about 4.5 MiB and rows hold at least 56, 112 or
+ * 224 entries per range on average (64-, 32-, 16-float passes), the columns
+ * are cut into P = min(8, ranges) equal index ranges processed one after
+ * another (the gathered B rows then stay in L2, or mostly so for ranges of
+ * up to two L2 sizes); each row's entries in one range are summed as above and rounded
  * to an fp32 partial, and the P partials are added in fp64 in range order
  * and rounded once (RSC_SPMM_BLOCKED = 0 switches it off, 2..8 forces that
  * P). Deterministic: equal arguments give bitwise equal Y, and
@@ -145,7 +147,10 @@ rsc_status_t rsc_spmm_noalloc(const rsc_csr_t *A, const float *B, int32_t d, int
  * buffers runs unblocked). What the plan adds is per-matrix preparation,
  * done once:
  *   - its own workspace, so runs need none;
- *   - when the product runs column-blocked, the split bounds of the rows;
+ *   - when the product runs column-blocked, the split bounds of the rows
+ *     (for the range count of feature widths above 32; a run at a width
+ *     whose range count differs builds its own, as rsc_spmm does, and so
+ *     does every later run of the plan);
  *   - the long-row list (or the length-class row order) and its length,
  *     which every rsc_spmm call builds first;
  *   - for operands with more than 262,144 columns, a copy of col whose bit
@@ -326,7 +331,11 @@ rsc_status_t rsc_sample_columns(const uint64_t *key, int32_t n, int32_t k, uint6
  *     stay valid until the next refresh or destroy.
  *   rsc_spmm_sampled: Y' = X[:, S] * B on the cached slice (Eq. 2 with the
  *     top-k rule: kept pairs summed with scale 1), the same kernels as
- *     rsc_spmm; every row of Y' is written. Needs a refreshed cache. */
+ *     rsc_spmm; every row of Y' is written. Needs a refreshed cache. Each
+ *     selection prepares the products for the feature width of the operand
+ *     last scored (row list, or split bounds when column-blocked); a
+ *     product of another width whose preparation differs builds its own,
+ *     and so does every later product until the next selection. */
 typedef struct rsc_cache rsc_cache_t;
 rsc_status_t rsc_cache_create(const rsc_csr_t *X, const rsc_csr_t *XT, int32_t refresh_interval,
                               hipStream_t stream, rsc_cache_t **out);

@@ -261,6 +261,7 @@ struct rsc_cache {
     size_t ws_sample_bytes = 0;
     bool random = false;       // the current slice comes from rsc_cache_refresh_random
     bool scored = false;       // keys have been computed at least once
+    int32_t score_d = 64;      // feature width of the last scored operand
     int32_t *idx = nullptr;
     uint32_t *mask = nullptr;
     uint32_t *prev_mask = nullptr;          // the selection the latest one replaced
@@ -404,7 +405,9 @@ rsc_status_t rsc_spmm_plan_create(const rsc_csr_t *A, hipStream_t stream, rsc_sp
     }
     // the per-call preparation of the product, done once: split bounds and
     // long-piece list (column-blocked), or the long-row list / row order
-    const int32_t P = std::max(1, rsc::spmm_column_blocks(A->n_rows, A->nnz, A->n_cols));
+    // (prepared for feature widths of 33 and more; a narrower product whose
+    // range count differs prepares for itself on every run)
+    const int32_t P = std::max(1, rsc::spmm_column_blocks(A->n_rows, A->nnz, A->n_cols, 64));
     {
         hipError_t e = hipSuccess;
         if (P > 1) {
@@ -693,8 +696,12 @@ rsc_status_t rsc_cache_create_ex(const rsc_csr_t *X, const rsc_csr_t *XT, int32_
     c->ws_slice_bytes = rsc::slice_ws_bytes(X->nnz);
     c->ws_spmm_bytes = rsc::spmm_ws_bytes(X->n_rows, X->nnz, X->n_cols);
     c->ws_sample_bytes = rsc::sample_ws_bytes(c->n);
-    // a slice's product is column-blocked with at most the full product's ranges
-    c->split_P = std::max(1, rsc::spmm_column_blocks(X->n_rows, X->nnz, X->n_cols));
+    // split bounds for as many ranges as the full product takes at any of
+    // the blocked layouts' widths; a slice's product that would take more
+    // runs unblocked
+    c->split_P = 1;
+    for (const int32_t w : {16, 32, 64})
+        c->split_P = std::max(c->split_P, rsc::spmm_column_blocks(X->n_rows, X->nnz, X->n_cols, w));
     struct {
         void **p;
         size_t bytes;
@@ -776,17 +783,18 @@ static rsc_status_t keep_previous_selection(rsc_cache_t *c, hipStream_t stream) 
     return RSC_OK;
 }
 
-// After a new slice: what every sampled product would build first (split
-// bounds and long-piece list when blocked, else the long-row list or the
-// row order), built once into ws_spmm. Asynchronous (the list's length stays
-// on the device; launches use its bound).
-static hipError_t cache_prepare(rsc_cache_t *c, hipStream_t stream) {
+// After a new slice: what every sampled product of feature width d (the
+// last scored operand's) would build first (split bounds and long-piece list
+// when blocked, else the long-row list or the row order), built once into
+// ws_spmm. Asynchronous (the list's length stays on the device; launches use
+// its bound).
+static hipError_t cache_prepare(rsc_cache_t *c, int32_t d, hipStream_t stream) {
     c->prep = rsc::SpmmPrepared{};
     const rsc_csr_t &X = c->X;
     if (X.n_rows == 0) return hipSuccess;
     const int64_t kk = std::min<int64_t>(c->k, c->n);
     const int64_t nnz_hint = c->n > 0 ? X.nnz * kk / c->n : 0;
-    const int32_t P = std::max(1, rsc::spmm_column_blocks(X.n_rows, nnz_hint, kk));
+    const int32_t P = std::max(1, rsc::spmm_column_blocks(X.n_rows, nnz_hint, kk, d));
     hipError_t e;
     if (P > 1) {
         if (P > c->split_P || rsc::spmm_blocked_fits(X.n_rows, X.nnz, P) > c->ws_spmm_bytes) return hipSuccess;
@@ -810,6 +818,7 @@ rsc_status_t rsc_cache_score(rsc_cache_t *c, const float *B, int32_t d, int64_t 
     RSC_HIP(rsc::pair_scores_launch(c->cn2, B, c->n, d, ldb, c->key, nullptr, c->rn2, stream), "cache scores");
     RSC_HIP(rsc::sum_fixed_order_launch(c->rn2, c->n, c->sum_ws, c->norms + 1, stream), "cache norm sum");
     c->scored = true;
+    c->score_d = d;
     RSC_HIP(c->fence.record(stream), "cache event");
     return RSC_OK;
 }
@@ -831,7 +840,7 @@ rsc_status_t rsc_cache_select(rsc_cache_t *c, int32_t k, int64_t step, hipStream
     c->version += 1;
     c->nnz_known = false;
     c->random = false;
-    RSC_HIP(cache_prepare(c, stream), "cache slice preparation");
+    RSC_HIP(cache_prepare(c, c->score_d, stream), "cache slice preparation");
     RSC_HIP(c->fence.record(stream), "cache event");
     return RSC_OK;
 }
@@ -856,7 +865,7 @@ rsc_status_t rsc_cache_refresh_random(rsc_cache_t *c, const float *B, int32_t d,
     c->version += 1;
     c->nnz_known = false;
     c->random = true;
-    RSC_HIP(cache_prepare(c, stream), "cache slice preparation");
+    RSC_HIP(cache_prepare(c, c->score_d, stream), "cache slice preparation");
     RSC_HIP(c->fence.record(stream), "cache event");
     return RSC_OK;
 }

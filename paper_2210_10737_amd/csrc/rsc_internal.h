@@ -42,7 +42,7 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
 // its split bounds S[(P + 1) * n_rows]; the row-order decision; and the
 // preparation a launch would do, run once into a plan's workspace (then
 // *spmm_long_count_of(ws) holds the list's length on the device).
-int32_t spmm_column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src);
+int32_t spmm_column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d);
 hipError_t spmm_split_launch(int32_t n_rows, int32_t n_cols, const int32_t *rowptr, const int32_t *col, int32_t P,
                              int32_t *S, hipStream_t stream);
 bool spmm_use_order(int32_t n_rows, int64_t nnz);

@@ -447,32 +447,43 @@ inline bool use_order(int32_t n_rows, int64_t nnz) {
 // rows (a few MB, resident in each XCD's L2) instead of from all of them.
 // Each virtual row writes a partial row; a combine pass adds the P partials
 // of row r in fixed order b = 0..P-1 in fp64 and rounds once.
-constexpr int kBlockW = 64;                         // features per blocked pass
+constexpr int kBlockW = 64;                         // features per blocked pass, the widest layout
 constexpr double kBlockBytes = 4.5 * 1024 * 1024;   // B bytes per column range (~ one XCD's L2)
 constexpr int kMaxBlocks = 8;                       // partial outputs at most 8 x Y per pass
 constexpr int kPieceMin = 56;                       // mean entries per piece of a row for blocking
 
+// Features per blocked pass for feature width d: the narrowest of the 16-,
+// 32- and 64-float layouts that holds d (wider d in several 64-float
+// passes), so no lane of a narrow product idles.
+inline int32_t blocked_width(int32_t d) { return d <= 16 ? 16 : d <= 32 ? 32 : kBlockW; }
+
 // Number of column ranges P for a product with n_rows rows, about nnz
-// entries and n_src distinct B rows referenced; 1 = not blocked. Blocked when
-// the referenced 64-float slice of B spans 2..16 L2-sized ranges and rows are
-// long enough that each piece still holds most of a 64-entry run on average
-// (kPieceMin entries). Beyond 8 ranges P stays 8: ranges of up to two L2
-// sizes still keep most gathers on chip (on a 233K-node graph with 489
-// entries per row, 8 ranges of 7.5 MB measured 6 % faster than unblocked
-// passes, while 32-float passes over ranges that do fit L2 were slower:
-// twice the passes over the row structure, more and shorter pieces).
+// entries, n_src distinct B rows referenced and d features; 1 = not blocked.
+// Blocked when the referenced slice of B one pass gathers from (the
+// blocked_width(d) floats of each row) spans 2..16 L2-sized ranges and rows
+// are long enough that each piece still fills about 14 load instructions on
+// average: kPieceMin entries in the 64-float layout (4 entries per
+// instruction), twice and four times that in the 32- and 16-float layouts
+// (8 and 16 per instruction; shorter pieces made a power-law graph with
+// 489 entries per row slower at d = 16 and 32, while a uniform one with
+// 600 per row gained 16-33 %). Beyond 8 ranges P stays 8: ranges of up to
+// two L2 sizes still keep most gathers on chip (on a 233K-node graph with
+// 489 entries per row, 8 ranges of 7.5 MB measured 5 % faster than
+// unblocked passes at d = 256, while 32-float passes over ranges that do
+// fit L2 were slower: twice the passes over the row structure).
 // RSC_SPMM_BLOCKED=0 switches the mode off, =2..8 forces that P.
-inline int32_t column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src) {
+inline int32_t column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) {
     if (n_rows <= 0 || (int64_t)(kMaxBlocks + 1) * n_rows > INT32_MAX) return 1;  // virtual rows are int32
     if (const char *env = getenv("RSC_SPMM_BLOCKED")) {
         const int v = atoi(env);
         if (v == 0) return 1;
         if (v >= 2 && v <= kMaxBlocks) return v;
     }
-    int64_t P = (int64_t)std::ceil((double)n_src * kBlockW * 4 / kBlockBytes);
+    const int32_t W = blocked_width(d);
+    int64_t P = (int64_t)std::ceil((double)n_src * W * 4 / kBlockBytes);
     if (P < 2 || P > 2 * kMaxBlocks) return 1;
     P = std::min<int64_t>(P, kMaxBlocks);
-    if (nnz < (int64_t)kPieceMin * P * n_rows) return 1;
+    if (nnz < (int64_t)kPieceMin * (kBlockW / W) * P * n_rows) return 1;
     return (int32_t)P;
 }
 
@@ -560,7 +571,9 @@ size_t blocked_bytes(int32_t n_rows, int32_t P) {
 }
 }  // namespace
 
-int32_t spmm_column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src) { return column_blocks(n_rows, nnz, n_src); }
+int32_t spmm_column_blocks(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) {
+    return column_blocks(n_rows, nnz, n_src, d);
+}
 
 hipError_t spmm_split_launch(int32_t n_rows, int32_t n_cols, const int32_t *rowptr, const int32_t *col, int32_t P,
                              int32_t *S, hipStream_t stream) {
@@ -572,7 +585,10 @@ hipError_t spmm_split_launch(int32_t n_rows, int32_t n_cols, const int32_t *rowp
 size_t spmm_ws_bytes(int32_t n_rows, int64_t nnz, int32_t n_cols) {
     // header, the row list, then the blocked mode's buffers when the full
     // product would be blocked (a slice of it never needs more ranges)
-    return sizeof(SpmmWs) + list_bytes(n_rows, nnz) + blocked_bytes(n_rows, column_blocks(n_rows, nnz, n_cols));
+    size_t blocked = 0;
+    for (const int32_t d : {16, 32, kBlockW})  // the three blocked layouts' range counts
+        blocked = std::max(blocked, blocked_bytes(n_rows, column_blocks(n_rows, nnz, n_cols, d)));
+    return sizeof(SpmmWs) + list_bytes(n_rows, nnz) + blocked;
 }
 
 int32_t spmm_slice_width(int32_t n_rows, int64_t nnz, int64_t n_src, int32_t d) {
@@ -657,7 +673,7 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
     // The blocked mode is chosen from the expected entries and referenced B
     // rows (the same for the exact product and a full-budget slice of it);
     // it runs only when the workspace holds its buffers.
-    const int32_t P = column_blocks(n_rows, nnz_hint, n_src_hint);
+    const int32_t P = column_blocks(n_rows, nnz_hint, n_src_hint, d);
     const size_t head = sizeof(SpmmWs) + list_bytes(n_rows, nnz_bound);
     if (P > 1 && head + blocked_bytes(n_rows, P) <= ws_bytes) {
         // the long-piece list must hold every piece the collect pass can find
@@ -689,18 +705,29 @@ hipError_t spmm_launch(int32_t n_rows, int32_t n_cols, int64_t nnz_bound, const 
             }
         }
         const unsigned vgrid = (unsigned)ceil_div(nv, kSpmmRowWaves);
-        for (int32_t f0 = 0; f0 < d; f0 += kBlockW) {
-            const int32_t dl = std::min<int32_t>(d - f0, kBlockW);
-            if (n_long > 0) {
-                if (f0 > 0 || pre) zero_next_kernel<<<1, 1, 0, stream>>>(&h->long_next);
-                spmm_long_kernel<16, 1, false><<<n_long, kSpmmLongWaves * 64, 0, stream>>>(
-                    S, n_rows, col, val, B + f0, ldb, part, kBlockW, dl, &h->long_count, &h->long_next, list);
-            }
-            spmm_rows_kernel<16, 1, false, false><<<vgrid, kSpmmRowWaves * 64, 0, stream>>>(
-                S, n_rows, col, val, B + f0, ldb, part, kBlockW, nv, dl, n_long > 0 ? 1 : 0, nullptr,
-                &h->long_count);
+        // partial rows are W floats apart (the workspace holds kBlockW)
+        const int32_t W = blocked_width(d);
+        for (int32_t f0 = 0; f0 < d; f0 += W) {
+            const int32_t dl = std::min<int32_t>(d - f0, W);
+#define RSC_SPMM_BLOCKED_LAUNCH(LPE_)                                                                         \
+    do {                                                                                                      \
+        if (n_long > 0) {                                                                                     \
+            if (f0 > 0 || pre) zero_next_kernel<<<1, 1, 0, stream>>>(&h->long_next);                          \
+            spmm_long_kernel<LPE_, 1, false><<<n_long, kSpmmLongWaves * 64, 0, stream>>>(                     \
+                S, n_rows, col, val, B + f0, ldb, part, W, dl, &h->long_count, &h->long_next, list);          \
+        }                                                                                                     \
+        spmm_rows_kernel<LPE_, 1, false, false><<<vgrid, kSpmmRowWaves * 64, 0, stream>>>(                    \
+            S, n_rows, col, val, B + f0, ldb, part, W, nv, dl, n_long > 0 ? 1 : 0, nullptr, &h->long_count);  \
+    } while (0)
+            if (W == 16)
+                RSC_SPMM_BLOCKED_LAUNCH(4);
+            else if (W == 32)
+                RSC_SPMM_BLOCKED_LAUNCH(8);
+            else
+                RSC_SPMM_BLOCKED_LAUNCH(16);
+#undef RSC_SPMM_BLOCKED_LAUNCH
             const int64_t nc = (int64_t)n_rows * ((dl + 3) / 4);
-            combine_blocks_kernel<<<(unsigned)ceil_div(nc, 256), 256, 0, stream>>>(part, kBlockW, n_rows, P, dl,
+            combine_blocks_kernel<<<(unsigned)ceil_div(nc, 256), 256, 0, stream>>>(part, W, n_rows, P, dl,
                                                                                   Y + f0, ldy);
         }
         return hipGetLastError();

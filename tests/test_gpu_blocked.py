@@ -1,8 +1,9 @@
 """Column-blocked SpMM mode (the columns cut into P index ranges processed
 one after another, partial rows added in fixed range order). Forced with
 RSC_SPMM_BLOCKED = 2..8 on seeded random shapes, and chosen automatically on
-graphs whose B slice spans 2, 9 (capped to 8) and 17 (not blocked) L2-sized
-ranges: exact and sampled SpMM
+graphs whose B slice (16, 32 or 64 floats per row, by feature width) spans
+2 to 9 (capped to 8) and 17 (not blocked) L2-sized ranges, with plans and
+caches used at several widths: exact and sampled SpMM
 against the oracle, a full-budget slice equal to the exact product bit for
 bit, and the automatic choice equal to the forced one."""
 import os
@@ -138,15 +139,22 @@ def test_automatic_choice_on_long_rows():
     assert rel_err(Y.cpu().numpy()[rows], Yo, S) <= 1e-5
 
 
-@pytest.mark.parametrize("n_cols,P", [(160_000, 8), (300_000, 0)])
-def test_automatic_range_count_is_capped(n_cols, P):
-    # A 64-float slice of B over 160,000 columns (41 MB) spans 9 ranges of
-    # 4.5 MiB: the rule takes P = 8 (rows of 500 entries hold 62 per range).
-    # Over 300,000 columns it spans 17, beyond the cap of 16: not blocked.
-    # The automatic choice equals the forced one bit for bit; a plan and a
-    # full-budget slice reproduce it.
-    n_rows, d = 2000, 96
-    A = synth.bucket_csr(np.full(n_rows, 500), n_cols, seed=31)
+@pytest.mark.parametrize("n_cols,d,row_len,P", [
+    (160_000, 96, 500, 8),    # 64-float passes: 9 ranges of 4.5 MiB, capped to 8
+    (160_000, 32, 1000, 5),   # the 32-float layout: 4.3 ranges
+    (160_000, 16, 1000, 3),   # the 16-float layout: 2.2 ranges
+    (300_000, 96, 500, 0),    # 17 ranges, beyond the cap of 16: not blocked
+    (300_000, 32, 1000, 8),   # 8.1 ranges at 32 floats: capped to 8 (125 entries per piece)
+    (300_000, 16, 1200, 5),   # 240 entries per piece, at least 224 in the 16-float layout
+    (300_000, 16, 500, 0),    # 100 entries per piece: too short for it, not blocked
+])
+def test_automatic_range_count(n_cols, d, row_len, P):
+    # The range count follows the slice of B one pass gathers from (the
+    # blocked layout's 16, 32 or 64 floats of each row), and the pieces must
+    # hold 56, 112 or 224 entries on average. The automatic choice equals
+    # the forced one bit for bit; a plan and a full-budget slice reproduce it.
+    n_rows = 2000
+    A = synth.bucket_csr(np.full(n_rows, row_len), n_cols, seed=31)
     AT = synth.transpose(A, n_cols)
     B = synth.dense_normal(n_cols, d, seed=32)
     Bd = torch.from_numpy(B).cuda()
@@ -171,6 +179,33 @@ def test_automatic_range_count_is_capped(n_cols, P):
     assert torch.equal(Yp, Y) and torch.equal(Yk, Y)
     Yo, S = oracle.spmm(A.rowptr, A.col, A.val, B, with_mag=True)
     assert rel_err(Y.cpu().numpy(), Yo, S) <= 1e-5
+
+
+def test_plan_and_cache_across_feature_widths():
+    # A plan prepares for 64-float passes (8 ranges here); a run at d = 16
+    # takes 3 ranges (d = 32: 5) and prepares for itself, and later runs at
+    # any width still equal rsc_spmm bit for bit. A cache refreshed at one
+    # width and used at another does the same.
+    n_rows, n_cols = 2000, 160_000
+    A = synth.bucket_csr(np.full(n_rows, 1000), n_cols, seed=33)
+    AT = synth.transpose(A, n_cols)
+    X = rsc.DeviceCsr.from_host(A.rowptr, A.col, A.val, n_cols)
+    XT = rsc.DeviceCsr.from_host(AT.rowptr, AT.col, AT.val, n_rows)
+    Bs = {d: torch.from_numpy(synth.dense_normal(n_cols, d, seed=34 + d)).cuda() for d in (16, 32, 96)}
+    with blocked(None):
+        ref = {d: rsc.spmm(X, B) for d, B in Bs.items()}
+        plan = rsc.SpmmPlan(X)
+        for d in (96, 16, 96, 32, 16):
+            assert torch.equal(plan.run(Bs[d]), ref[d]), d
+        plan.close()
+        cache = rsc.Cache(X, XT)
+        for d_ref, order in ((16, (16, 96, 32)), (96, (96, 16))):
+            cache.refresh(Bs[d_ref], n_cols, step=0)
+            for d in order:
+                assert torch.equal(cache.spmm_sampled(Bs[d]), ref[d]), (d_ref, d)
+        cache.close()
+    Yo, S = oracle.spmm(A.rowptr, A.col, A.val, Bs[16].cpu().numpy(), with_mag=True)
+    assert rel_err(ref[16].cpu().numpy(), Yo, S) <= 1e-5
 
 
 @pytest.mark.parametrize("n_rows,n_cols,row_len,d", [
