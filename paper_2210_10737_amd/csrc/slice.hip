@@ -112,16 +112,24 @@ __global__ __launch_bounds__(kCountThreads) void slice_count_kernel(const int32_
             if (t0 + stride < nt) load(t0 + stride);
             // lane 4 u + i keeps ballot (u, i) and lane u the wave's count of
             // tile u, so the step's 16 ballots and 4 counts leave in one store
-            // (or atomic) instruction each
+            // (or atomic) instruction each. A tile's four lookups read LDS
+            // unconditionally (an index outside the piece is clamped and its
+            // word ignored), so they issue together and share one wait
+            // instead of each one branching and waiting on its own.
             uint64_t my_ball = 0;
             uint32_t my_cnt = 0;
 #pragma unroll
             for (int u = 0; u < kTilesPerIter; ++u) {
+                uint32_t off[4], word[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    off[i] = (uint32_t)(cv[u][i] - lo);
+                    word[i] = s_mask[min(off[i] >> 5, (uint32_t)(kMaskLdsWords - 1))];
+                }
                 uint32_t c = 0;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const uint32_t off = (uint32_t)(cv[u][i] - lo);
-                    const bool k = off < span && ((s_mask[off >> 5] >> (off & 31)) & 1u);
+                    const bool k = off[i] < span && ((word[i] >> (off[i] & 31)) & 1u);
                     const uint64_t b = __ballot(k);
                     c += __popcll(b);
                     if (lane == 4 * u + i) my_ball = b;
