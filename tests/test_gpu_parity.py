@@ -543,12 +543,15 @@ def full_rel_err(Yd, rowptr, col, val, Bh, chunk=250_000):
 
 @pytest.mark.parametrize("name,d,pcts", [("copurchase", 256, (10, 30, 50)), ("social", 256, (10, 30, 50)),
                                          ("protein", 256, (10, 30, 50)), ("gcn2", 100, (10, 30)),
-                                         ("gcn2", 512, (10, 50))])
+                                         ("gcn2", 512, (10, 50)), ("protein", 32, (30,)),
+                                         ("protein", 16, (30,)), ("social", 32, (30,))])
 def test_full_workload(name, d, pcts):
     """The benchmark workloads at full size, in the configurations the
     benchmark times and at 10 / 30 / 50 % budgets (which change the sampled
     products' layouts: feature-slice width, column blocking; gcn2 also at the
-    training step's d = 100): every element of the exact and the sampled products
+    training step's d = 100; protein at d = 16 and 32, whose exact products
+    run column-blocked in the 16- and 32-float layouts, and social at d = 32,
+    which the blocking rule leaves unblocked): every element of the exact and the sampled products
     against the oracle; keys, selected indices, mask and slice bit-exact over
     the whole graph; the plan's product bitwise equal to rsc_spmm."""
     A = synth.make_graph(name, 0)
