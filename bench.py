@@ -19,7 +19,7 @@ sample of the same step. `vendor_baseline` times rocSPARSE's SpMM on the
 exact product's operands beside the library's (context only).
 
 usage: python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload copurchase]
-                       [--budget-pct 30] [--aggregator gcn|mean] [--selector topk|random]
+                       [--budget-pct 30] [--features D] [--aggregator gcn|mean] [--selector topk|random]
                        [--no-cpu-baseline] [--no-vendor-baseline]
        python bench.py --workload gcn2-train [--budget-pct 10]   (training-step comparison)
 """
@@ -578,6 +578,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="copurchase")
     ap.add_argument("--budget-pct", type=int, default=None)
+    ap.add_argument("--features", type=int, default=None,
+                    help="feature width d of the dense operands (default: the workload's)")
     ap.add_argument("--refresh", type=int, default=10)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -629,7 +631,9 @@ def main() -> int:
     torch.cuda.set_device(0)
     w = synth.WORKLOADS[args.workload]
     pct = args.budget_pct if args.budget_pct is not None else w.budgets_pct[-1 if args.workload != "social" else 1]
-    d = w.d
+    d = args.features if args.features else w.d
+    if d < 1:
+        raise SystemExit("--features must be at least 1")
     t_gen = time.perf_counter()
     A = synth.make_graph(args.workload, args.seed)
     Hh = synth.dense_normal(A.n, d, seed=args.seed + 1)
